@@ -1,0 +1,251 @@
+/*
+ * aj.h -- C ABI of libaj: the merged actor update on one MI355X (gfx950).
+ *
+ * The actor (policy) update over multi-turn agent trajectories, in three
+ * stages:
+ *   1. timeline merging          (Section 4.4.2, Algorithm 1, token-level Match)
+ *   2. one packed variable-length causal decoder block, forward and backward
+ *   3. the fused LM head: vocab projection, log-softmax, token log-prob and the
+ *      clipped policy-gradient loss (Section 3: GRPO-style updates), forward
+ *      and backward, over the loss-masked tokens only.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless marked host.  The caller allocates
+ *     every buffer, including workspaces sized by the *_bytes queries; the
+ *     library allocates no device memory, keeps no pointer after returning
+ *     and holds no state besides a thread-local error string.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  All work is
+ *     enqueued on it; no call synchronises the host except aj_read_device_error.
+ *   - Return value: AJ_OK, or an aj_status code after which nothing was
+ *     enqueued (argument errors are found on the host before any launch);
+ *     aj_last_error() then describes it.  AJ_ERR_HIP means a launch failed.
+ *   - Data errors that only the device can see (a token id >= vocab, a
+ *     timeline whose first token does not start a block, an author value of 3)
+ *     set bits in a device int32 `err` word when one is passed; the kernels
+ *     then skip the bad element and finish normally.
+ *   - Floating point gradients are ACCUMULATED (+=) into float32 buffers, so
+ *     packs can be looped; the caller zeroes them first.
+ *   - dtype AJ_F32 stores weights and activations as float32, AJ_BF16 as
+ *     bfloat16 (round to nearest even); accumulation is float32 either way.
+ *   - Matrices are row-major; a weight of shape [out, in] maps x[in] to y[out].
+ */
+#ifndef AJ_H
+#define AJ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AJ_OK = 0,
+  AJ_ERR_NULL = 1,          /* a required pointer is NULL */
+  AJ_ERR_SHAPE = 2,         /* a size or offset is out of range / not monotone */
+  AJ_ERR_UNSUPPORTED = 3,   /* a valid request this build does not implement */
+  AJ_ERR_WORKSPACE = 4,     /* workspace smaller than the *_bytes query asked for */
+  AJ_ERR_HIP = 5            /* a HIP launch or runtime call failed */
+} aj_status;
+
+typedef enum { AJ_F32 = 0, AJ_BF16 = 1 } aj_dtype;
+
+/* Per-token flag byte of the unmerged timelines. */
+enum {
+  AJ_AUTHOR_USER = 0, AJ_AUTHOR_ENV = 1, AJ_AUTHOR_LLM = 2, AJ_AUTHOR_MASK = 3,
+  AJ_FLAG_BLOCK_START = 4   /* set on the first token of every message block */
+};
+
+/* Bits of the device error word. */
+enum {
+  AJ_DEVERR_TOKEN_RANGE = 1,   /* a token id outside [0, vocab) */
+  AJ_DEVERR_BAD_FLAGS = 2,     /* author 3, or a timeline not starting a block */
+  AJ_DEVERR_EMPTY = 4,         /* an empty timeline */
+  AJ_DEVERR_OFFSETS = 8        /* offsets not monotone, out of range, or not tiling [0, n) */
+};
+
+const char *aj_status_str(int status);
+/* Detail of the last non-OK return on this thread ("" if none). */
+const char *aj_last_error(void);
+/* Waits for `stream`, then copies the device error word to *host_err. */
+int aj_read_device_error(const int32_t *err, void *stream, int32_t *host_err);
+
+/* ------------------------------------------------------------------ 1. merge
+ * Section 4.4.2: each intercepted LLM call yields one timeline, an ordered list
+ * of message blocks (token ids, author in {user, env, llm}, per-token log-prob,
+ * loss mask = 1 exactly on llm tokens).  Algorithm 1 visits timelines from the
+ * last one down; each one not yet absorbed absorbs every earlier, not yet
+ * absorbed timeline whose blocks it matches one by one (|T_i| >= |T_j| and
+ * Match on blocks 1..|T_j|), and takes over llm authorship -- author, tokens,
+ * log-prob and, here, the advantage -- on the aligned blocks where its own
+ * block is not llm.  Survivors are returned in original order.
+ *
+ * Match here is token-level: equal token ids AND equal block boundaries
+ * (block starts are the AJ_FLAG_BLOCK_START bits; blocks are never empty).
+ * Authors are not compared.  Merging stays inside one episode.
+ */
+typedef struct {
+  int32_t n_traj;               /* episodes */
+  int32_t n_tl;                 /* timelines (one per LLM call), all episodes */
+  int64_t n_tok;                /* unmerged tokens, < 2^31 */
+  const int32_t *traj_tl_off;   /* [n_traj+1] timelines of episode e: [off[e], off[e+1]), collection order */
+  const int64_t *tl_tok_off;    /* [n_tl+1]   tokens of timeline i: [off[i], off[i+1]) */
+  const int32_t *tok;           /* [n_tok] token ids */
+  const uint8_t *flags;         /* [n_tok] author | AJ_FLAG_BLOCK_START */
+  const float *old_logprob;     /* [n_tok] rollout log-prob; read where author == llm */
+  const float *adv;             /* [n_tok] advantage; read where author == llm */
+} aj_timelines;
+
+typedef struct {
+  /* per timeline / segment; capacity n_tl (+1) */
+  int32_t *absorber;            /* [n_tl] -1 = survivor, else global index of the absorbing timeline */
+  int32_t *cu_seqlens;          /* [n_tl+1] segment token offsets; entries past n_seg are left alone */
+  int32_t *seg_src;             /* [n_tl]   timeline each segment comes from */
+  int32_t *cu_targets;          /* [n_tl+1] offsets of each segment's masked targets in `targets` */
+  int64_t *counts;              /* [4] n_seg, n_tok_out, n_mask (= number of targets), max_seqlen */
+  /* per output token; capacity n_tok (merged output is never longer than the input) */
+  int32_t *tok;
+  int32_t *pos;                 /* position inside its segment, from 0 */
+  uint8_t *mask;                /* 1 on llm tokens after the transfers */
+  float *old_logprob;           /* the llm token's rollout log-prob, 0 elsewhere */
+  float *adv;                   /* the llm token's advantage, 0 elsewhere */
+  int32_t *targets;             /* [n_tok] ascending output positions p with mask[p] == 1 that do
+                                   not start a segment: the tokens the loss scores */
+} aj_packed;
+
+/* Workspace for aj_merge_timelines / aj_flatten_timelines. */
+size_t aj_merge_workspace_bytes(int32_t n_traj, int32_t n_tl, int64_t n_tok);
+/* Algorithm 1 over every episode, then the survivors laid end to end.
+ * The offsets must tile [0, n_tok) and [0, n_tl) exactly (else
+ * AJ_DEVERR_OFFSETS, and every count comes back 0).  Result is independent of
+ * the launch: bit-identical on every call. */
+int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
+                       void *ws, size_t ws_bytes, void *stream);
+/* The same outputs without merging: every timeline is its own segment
+ * (absorber all -1).  The unmerged baseline the paper compares against. */
+int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* Host: greedy in-order packing of segments into packs of at most max_tokens
+ * tokens (a longer segment gets a pack of its own).  cu_seqlens is a HOST copy
+ * [n_seg+1]; pack_seg_off (HOST, capacity n_seg+1) receives the first segment
+ * of each pack plus a final n_seg; *n_packs receives the pack count. */
+int aj_plan_packs(const int32_t *cu_seqlens, int32_t n_seg, int32_t max_tokens,
+                  int32_t *pack_seg_off, int32_t *n_packs);
+
+/* ------------------------------------------------------------------ embedding */
+/* x[p] = emb[tok[p]] for p < n_tok; emb [vocab, d], x [n_tok, d] in `dtype`. */
+int aj_embed_fwd(const int32_t *tok, int32_t n_tok, const void *emb, int32_t d, int32_t vocab,
+                 int dtype, void *x, int32_t *err, void *stream);
+/* d_emb[tok[p]] += dx[p] (float32, [vocab, d] and [n_tok, d]). */
+int aj_embed_bwd(const int32_t *tok, int32_t n_tok, const float *dx, int32_t d, int32_t vocab,
+                 float *d_emb, void *stream);
+
+/* ------------------------------------------------------------------ 2. block
+ * One pre-norm decoder block over a pack of segments laid end to end:
+ *   a = RMSNorm(x)*g1; q,k,v = a W_qkv^T; rotate-half RoPE on q,k at `pos`
+ *   (inverse frequency theta^(-2i/head_dim)); o = causal softmax(q k^T/sqrt(hd)) v
+ *   inside each segment, query head h reading kv head floor(h*Hkv/Hq);
+ *   x1 = x + o W_o^T; b = RMSNorm(x1)*g2;
+ *   y = x1 + (silu(b W_gate^T) * b W_up^T) W_down^T.
+ * W_qkv rows: Hq*hd query rows, then Hkv*hd key rows, then Hkv*hd value rows.
+ * W_gate_up rows: d_ff gate rows, then d_ff up rows.
+ */
+typedef struct {
+  int32_t d_model, n_q_heads, n_kv_heads, head_dim, d_ff;
+  float rms_eps;
+  float rope_theta;
+  int32_t dtype;                /* aj_dtype of weights, x, y and saved activations */
+} aj_block_cfg;
+
+typedef struct {
+  const void *attn_norm;        /* [d] */
+  const void *w_qkv;            /* [(Hq+2Hkv)*hd, d] */
+  const void *w_o;              /* [d, Hq*hd] */
+  const void *mlp_norm;         /* [d] */
+  const void *w_gate_up;        /* [2*d_ff, d] */
+  const void *w_down;           /* [d, d_ff] */
+} aj_block_weights;
+
+typedef struct {                /* float32, accumulated */
+  float *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
+} aj_block_grads;
+
+typedef struct {
+  int32_t n_tok;                /* tokens in the pack */
+  int32_t n_seg;                /* segments in the pack */
+  int32_t max_seqlen;           /* longest segment (host value) */
+  int32_t base;                 /* cu_seqlens values are offsets + base (a slice of a
+                                   batch-wide array): row r of the pack is offset r + base */
+  const int32_t *cu_seqlens;    /* [n_seg+1], cu_seqlens[0] == base, cu_seqlens[n_seg] == base + n_tok */
+  const int32_t *pos;           /* [n_tok] position of each token inside its segment (RoPE) */
+} aj_varlen;
+
+/* Bytes of the activation arena the forward fills and the backward reads. */
+size_t aj_block_saved_bytes(const aj_block_cfg *cfg, int32_t n_tok);
+/* Scratch for either direction. */
+size_t aj_block_workspace_bytes(const aj_block_cfg *cfg, int32_t n_tok, int32_t n_seg);
+/* x, y: [n_tok, d] in cfg->dtype.  `saved` must outlive the matching backward. */
+int aj_varlen_block_fwd(const aj_block_cfg *cfg, const aj_block_weights *w, const aj_varlen *vl,
+                        const void *x, void *y, void *saved, void *ws, size_t ws_bytes,
+                        void *stream);
+/* dy, dx: float32 [n_tok, d] (dx is written, not accumulated; dx may alias dy).
+ * x must be the forward's input. */
+int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w, const aj_varlen *vl,
+                        const void *x, const void *saved, const float *dy, float *dx,
+                        const aj_block_grads *g, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------ 3. loss
+ * hn = RMSNorm(h) * g_final; for every target position p (targets[i]):
+ *   logprob[i] = log softmax(hn[p-1] W_vocab^T)[tok[p]]
+ *   r = exp(logprob[i] - old_logprob[p])
+ *   loss += -min(r A, clip(r, 1-eps, 1+eps) A) * inv_n_mask,   A = adv[p]
+ * The vocab projection is streamed: logits never reach memory in the forward;
+ * the backward materialises one vocab_chunk-wide slab of d logits at a time.
+ * d loss / d logprob = -A r inv_n_mask where the unclipped branch is active
+ * ((A > 0 and r <= 1+eps) or (A < 0 and r >= 1-eps)), else 0.
+ * Only the rows feeding a target are touched: the loss does not depend on
+ * the logits of any other row.
+ */
+typedef struct {
+  int32_t d_model, vocab, vocab_chunk;
+  float clip_eps;
+  float rms_eps;
+  int32_t dtype;                /* aj_dtype of h, final_norm, w_vocab */
+} aj_loss_cfg;
+
+typedef struct {
+  int32_t n_tok;                /* rows of h (one pack) */
+  int32_t n_tgt;                /* targets scored in this call */
+  int32_t row_base;             /* h row of position p is p - row_base */
+  const int32_t *targets;       /* [n_tgt] positions p, row_base < p < row_base + n_tok + 1,
+                                   each scored from h row p - 1 - row_base */
+  const int32_t *tok;           /* token ids, indexed by p */
+  const float *old_logprob;     /* indexed by p */
+  const float *adv;             /* indexed by p */
+  float inv_n_mask;             /* 1 / (loss-masked tokens of the WHOLE batch) */
+} aj_loss_in;
+
+size_t aj_loss_saved_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
+size_t aj_loss_workspace_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
+/* h [n_tok, d], final_norm [d], w_vocab [vocab, d] in cfg->dtype.
+ * logprob, lse: [n_tgt] float32 (written).  stats: float32[4] accumulated:
+ * [0] loss (already scaled by inv_n_mask), [1] clipped-branch count,
+ * [2] sum of r, [3] targets seen.  `saved` (aj_loss_saved_bytes) keeps the
+ * normalised rows for the backward. */
+int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
+                           const void *final_norm, const void *w_vocab, void *saved,
+                           float *logprob, float *lse, float *stats, int32_t *err,
+                           void *ws, size_t ws_bytes, void *stream);
+/* dh: float32 [n_tok, d], WRITTEN (rows that feed no target become 0).
+ * d_final_norm [d], d_w_vocab [vocab, d]: float32, accumulated. */
+int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
+                           const void *final_norm, const void *w_vocab, const void *saved,
+                           const float *logprob, const float *lse, float *dh,
+                           float *d_final_norm, float *d_w_vocab, void *ws, size_t ws_bytes,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AJ_H */

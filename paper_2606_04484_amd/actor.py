@@ -1,0 +1,203 @@
+"""One actor-update step on the GPU, driven from the host through the C ABI.
+
+    merge (or flatten) the timelines -> read back the counts once -> plan packs
+    for each pack: embed -> block fwd -> loss fwd -> loss bwd -> block bwd -> embed bwd
+
+Gradients accumulate in float32 across packs; the loss is normalised by the
+masked-token count of the whole batch, so the per-pack calls compose into the
+batch's token mean.  torch only allocates device memory and provides the
+stream; every step of the path is a libaj call.
+"""
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import capi as C
+
+BLOCK_NAMES = ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+
+
+def upload_timelines(tl, old_logprob, device="cuda"):
+    """Host Timelines (+ rollout log-probs, float32 [n_tok]) -> device tensors."""
+    def t(a, dt):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dt)
+    return {
+        "traj_tl_off": t(tl.traj_tl_off, torch.int32),
+        "tl_tok_off": t(tl.tl_tok_off, torch.int64),
+        "tok": t(tl.tok, torch.int32),
+        "flags": t(tl.flags, torch.uint8),
+        "old_logprob": t(old_logprob.astype(np.float32), torch.float32),
+        "adv": t(tl.adv, torch.float32),
+    }
+
+
+@dataclass
+class Layout:
+    """Packed segments on the device plus the host-side counts and packs."""
+    dev: dict
+    n_seg: int
+    n_tok: int
+    n_mask: int
+    max_seqlen: int
+    cu_host: np.ndarray
+    cut_host: np.ndarray
+    packs: list = field(default_factory=list)
+
+    def __getattr__(self, k):
+        d = self.__dict__.get("dev")
+        if d is not None and k in d:
+            return d[k]
+        raise AttributeError(k)
+
+
+class Merger:
+    """Owns the output and workspace buffers of aj_merge_timelines for one input size."""
+
+    def __init__(self, tl_dev):
+        dev = tl_dev["tok"].device
+        n_traj = tl_dev["traj_tl_off"].numel() - 1
+        n_tl = tl_dev["tl_tok_off"].numel() - 1
+        n_tok = tl_dev["tok"].numel()
+        cap = max(n_tok, 1)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.tl = tl_dev
+        self.out = {
+            "absorber": torch.empty(max(n_tl, 1), **i32),
+            "cu_seqlens": torch.empty(n_tl + 1, **i32),
+            "seg_src": torch.empty(max(n_tl, 1), **i32),
+            "cu_targets": torch.empty(n_tl + 1, **i32),
+            "counts": torch.zeros(4, dtype=torch.int64, device=dev),
+            "tok": torch.empty(cap, **i32),
+            "pos": torch.empty(cap, **i32),
+            "mask": torch.empty(cap, dtype=torch.uint8, device=dev),
+            "old_logprob": torch.empty(cap, dtype=torch.float32, device=dev),
+            "adv": torch.empty(cap, dtype=torch.float32, device=dev),
+            "targets": torch.empty(cap, **i32),
+        }
+        self.err = torch.zeros(1, **i32)
+        self.ws = torch.empty(C.aj_merge_workspace_bytes(n_traj, n_tl, n_tok), dtype=torch.uint8,
+                              device=dev)
+
+    def launch(self, merged=True):
+        fn = C.aj_merge_timelines if merged else C.aj_flatten_timelines
+        fn(self.tl, self.out, self.err, self.ws)
+
+    def layout(self, pack_tokens):
+        """Reads the counts back (one synchronisation) and plans the packs."""
+        counts = self.out["counts"].cpu().tolist()
+        n_seg, n_tok, n_mask, max_seqlen = (int(v) for v in counts)
+        cu = self.out["cu_seqlens"][:n_seg + 1].cpu()
+        cut = self.out["cu_targets"][:n_seg + 1].cpu().numpy()
+        L = Layout(self.out, n_seg, n_tok, n_mask, max_seqlen, cu.numpy(), cut)
+        if n_seg:
+            offs = C.aj_plan_packs(cu, pack_tokens)
+            cuh = cu.numpy()
+            for a, b in zip(offs[:-1], offs[1:]):
+                lens = np.diff(cuh[a:b + 1])
+                L.packs.append(dict(s0=a, s1=b, t0=int(cuh[a]), t1=int(cuh[b]), r0=int(cut[a]),
+                                    r1=int(cut[b]), max_len=int(lens.max())))
+        return L
+
+    def device_error(self):
+        return C.aj_read_device_error(self.err)
+
+
+def merge(tl_dev, merged=True, pack_tokens=131072):
+    m = Merger(tl_dev)
+    m.launch(merged)
+    return m.layout(pack_tokens)
+
+
+class ActorUpdate:
+    """Weights, gradient accumulators and step buffers of one policy block + LM head."""
+
+    def __init__(self, m, weights, device="cuda"):
+        self.m = m
+        self.W = weights
+        self.dev = torch.device(device)
+        self.dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+        self.bcfg = C.block_cfg(m)
+        self.lcfg = C.loss_cfg(m)
+        self.G = {k: torch.zeros(v.shape, dtype=torch.float32, device=self.dev)
+                  for k, v in weights.items()}
+        self.stats = torch.zeros(4, dtype=torch.float32, device=self.dev)
+        self.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        self._cap = (0, 0)
+
+    def zero_grads(self):
+        for g in self.G.values():
+            g.zero_()
+        self.stats.zero_()
+
+    def _buffers(self, n_tok, n_tgt):
+        if n_tok <= self._cap[0] and n_tgt <= self._cap[1]:
+            return
+        n_tok, n_tgt = max(n_tok, self._cap[0]), max(n_tgt, self._cap[1])
+        d, dev = self.m.d_model, self.dev
+        u8 = lambda nb: torch.empty(max(int(nb), 1), dtype=torch.uint8, device=dev)
+        self.x = torch.empty(n_tok, d, dtype=self.dt, device=dev)
+        self.y = torch.empty(n_tok, d, dtype=self.dt, device=dev)
+        self.dh = torch.empty(n_tok, d, dtype=torch.float32, device=dev)
+        self.saved = u8(C.aj_block_saved_bytes(self.bcfg, n_tok))
+        self.bws = u8(C.aj_block_workspace_bytes(self.bcfg, n_tok, n_tok))
+        self.lsaved = u8(C.aj_loss_saved_bytes(self.lcfg, n_tgt))
+        self.lws = u8(C.aj_loss_workspace_bytes(self.lcfg, n_tgt))
+        self._cap = (n_tok, n_tgt)
+
+    def prepare(self, L):
+        """Allocates everything a step over layout L needs (outside any timed region)."""
+        mt = max((p["t1"] - p["t0"] for p in L.packs), default=0)
+        mr = max((p["r1"] - p["r0"] for p in L.packs), default=0)
+        self._buffers(mt, mr)
+        self.logprob = torch.empty(max(L.n_mask, 1), dtype=torch.float32, device=self.dev)
+        self.lse = torch.empty(max(L.n_mask, 1), dtype=torch.float32, device=self.dev)
+
+    def step(self, L):
+        """Forward + backward over every pack of L; gradients accumulate into self.G."""
+        if not hasattr(self, "logprob") or self.logprob.numel() < max(L.n_mask, 1):
+            self.prepare(L)
+        W, G = self.W, self.G
+        inv = 1.0 / L.n_mask if L.n_mask else 0.0
+        bw = {k: W[k] for k in BLOCK_NAMES}
+        bg = {k: G[k] for k in BLOCK_NAMES}
+        for p in L.packs:
+            t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
+            n = t1 - t0
+            x, y, dh = self.x[:n], self.y[:n], self.dh[:n]
+            tok = L.tok[t0:t1]
+            cu = L.cu_seqlens[s0:s1 + 1]
+            pos = L.pos[t0:t1]
+            tg = L.targets[r0:r1]
+            C.aj_embed_fwd(tok, W["emb"], x, self.err)
+            C.aj_varlen_block_fwd(self.bcfg, bw, cu, pos, p["max_len"], x, y, self.saved,
+                                  base=t0)
+            C.aj_logprob_pg_loss_fwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
+                                     W["final_norm"], W["w_vocab"], self.lsaved,
+                                     self.logprob[r0:r1], self.lse[r0:r1], self.stats, self.lws,
+                                     self.err, row_base=t0)
+            C.aj_logprob_pg_loss_bwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
+                                     W["final_norm"], W["w_vocab"], self.lsaved,
+                                     self.logprob[r0:r1], self.lse[r0:r1], dh,
+                                     G["final_norm"], G["w_vocab"], self.lws, row_base=t0)
+            C.aj_varlen_block_bwd(self.bcfg, bw, cu, pos, p["max_len"], x, self.saved, dh, dh, bg,
+                                  self.bws, base=t0)
+            C.aj_embed_bwd(tok, dh, G["emb"])
+        return self.stats
+
+    def forward_logprob(self, L):
+        """Log-probs of every target under the current weights (forward only)."""
+        self.prepare(L)
+        inv = 1.0 / L.n_mask if L.n_mask else 0.0
+        bw = {k: self.W[k] for k in BLOCK_NAMES}
+        for p in L.packs:
+            t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
+            n = t1 - t0
+            C.aj_embed_fwd(L.tok[t0:t1], self.W["emb"], self.x[:n], self.err)
+            C.aj_varlen_block_fwd(self.bcfg, bw, L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1],
+                                  p["max_len"], self.x[:n], self.y[:n], self.saved, base=t0)
+            C.aj_logprob_pg_loss_fwd(self.lcfg, L.targets[r0:r1], L.tok, L.old_logprob, L.adv,
+                                     inv, self.y[:n], self.W["final_norm"], self.W["w_vocab"],
+                                     self.lsaved, self.logprob[r0:r1], self.lse[r0:r1],
+                                     self.stats, self.lws, self.err, row_base=t0)
+        return self.logprob[:L.n_mask]

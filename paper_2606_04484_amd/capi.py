@@ -1,0 +1,288 @@
+"""ctypes binding of libaj (include/aj.h): same names, argument marshalling only.
+
+Every function takes torch tensors (device memory owned by torch), passes
+their data pointers and the current HIP stream to the library, and raises
+AjError on a non-OK status.  No arithmetic happens here.
+"""
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libaj.so")
+
+AJ_F32, AJ_BF16 = 0, 1
+AUTHOR_LLM = 2
+FLAG_BLOCK_START = 4
+
+
+class AjError(RuntimeError):
+    pass
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise AjError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_04484_amd.build`")
+    return C.CDLL(LIB_PATH)
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        _lib = _load()
+        _declare(_lib)
+    return _lib
+
+
+vp = C.c_void_p
+i32, i64, f32, sz = C.c_int32, C.c_int64, C.c_float, C.c_size_t
+
+
+class Timelines(C.Structure):
+    _fields_ = [("n_traj", i32), ("n_tl", i32), ("n_tok", i64), ("traj_tl_off", vp),
+                ("tl_tok_off", vp), ("tok", vp), ("flags", vp), ("old_logprob", vp), ("adv", vp)]
+
+
+class Packed(C.Structure):
+    _fields_ = [("absorber", vp), ("cu_seqlens", vp), ("seg_src", vp), ("cu_targets", vp),
+                ("counts", vp), ("tok", vp), ("pos", vp), ("mask", vp), ("old_logprob", vp),
+                ("adv", vp), ("targets", vp)]
+
+
+class BlockCfg(C.Structure):
+    _fields_ = [("d_model", i32), ("n_q_heads", i32), ("n_kv_heads", i32), ("head_dim", i32),
+                ("d_ff", i32), ("rms_eps", f32), ("rope_theta", f32), ("dtype", i32)]
+
+
+class BlockWeights(C.Structure):
+    _fields_ = [(n, vp) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
+class BlockGrads(C.Structure):
+    _fields_ = [(n, vp) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
+class Varlen(C.Structure):
+    _fields_ = [("n_tok", i32), ("n_seg", i32), ("max_seqlen", i32), ("base", i32),
+                ("cu_seqlens", vp), ("pos", vp)]
+
+
+class LossCfg(C.Structure):
+    _fields_ = [("d_model", i32), ("vocab", i32), ("vocab_chunk", i32), ("clip_eps", f32),
+                ("rms_eps", f32), ("dtype", i32)]
+
+
+class LossIn(C.Structure):
+    _fields_ = [("n_tok", i32), ("n_tgt", i32), ("row_base", i32), ("targets", vp), ("tok", vp),
+                ("old_logprob", vp), ("adv", vp), ("inv_n_mask", f32)]
+
+
+EXPORTS = {
+    "aj_status_str": (C.c_char_p, [C.c_int]),
+    "aj_last_error": (C.c_char_p, []),
+    "aj_read_device_error": (C.c_int, [vp, vp, C.POINTER(i32)]),
+    "aj_merge_workspace_bytes": (sz, [i32, i32, i64]),
+    "aj_merge_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
+    "aj_flatten_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
+    "aj_plan_packs": (C.c_int, [vp, i32, i32, vp, C.POINTER(i32)]),
+    "aj_embed_fwd": (C.c_int, [vp, i32, vp, i32, i32, C.c_int, vp, vp, vp]),
+    "aj_embed_bwd": (C.c_int, [vp, i32, vp, i32, i32, vp, vp]),
+    "aj_block_saved_bytes": (sz, [C.POINTER(BlockCfg), i32]),
+    "aj_block_workspace_bytes": (sz, [C.POINTER(BlockCfg), i32, i32]),
+    "aj_varlen_block_fwd": (C.c_int, [C.POINTER(BlockCfg), C.POINTER(BlockWeights),
+                                      C.POINTER(Varlen), vp, vp, vp, vp, sz, vp]),
+    "aj_varlen_block_bwd": (C.c_int, [C.POINTER(BlockCfg), C.POINTER(BlockWeights),
+                                      C.POINTER(Varlen), vp, vp, vp, vp,
+                                      C.POINTER(BlockGrads), vp, sz, vp]),
+    "aj_loss_saved_bytes": (sz, [C.POINTER(LossCfg), i32]),
+    "aj_loss_workspace_bytes": (sz, [C.POINTER(LossCfg), i32]),
+    "aj_logprob_pg_loss_fwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
+                                         vp, vp, vp, vp, vp, sz, vp]),
+    "aj_logprob_pg_loss_bwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
+                                         vp, vp, vp, vp, vp, vp, sz, vp]),
+}
+
+
+def _declare(L):
+    for name, (res, args) in EXPORTS.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+
+
+def _check(status, name):
+    if status != 0:
+        L = lib()
+        raise AjError(f"{name}: {L.aj_status_str(status).decode()}: {L.aj_last_error().decode()}")
+
+
+def ptr(t):
+    """Device (or host) address of a tensor, None for None."""
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def stream_handle(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return AJ_BF16
+    if t.dtype == torch.float32:
+        return AJ_F32
+    raise AjError(f"unsupported dtype {t.dtype}")
+
+
+# ------------------------------------------------------------------ merge
+
+def aj_merge_workspace_bytes(n_traj, n_tl, n_tok):
+    return int(lib().aj_merge_workspace_bytes(n_traj, n_tl, n_tok))
+
+
+def _timelines(t):
+    return Timelines(int(t["traj_tl_off"].numel() - 1), int(t["tl_tok_off"].numel() - 1),
+                     int(t["tok"].numel()), ptr(t["traj_tl_off"]), ptr(t["tl_tok_off"]),
+                     ptr(t["tok"]), ptr(t["flags"]), ptr(t["old_logprob"]), ptr(t["adv"]))
+
+
+def _packed(o):
+    return Packed(*[ptr(o[k]) for k in ("absorber", "cu_seqlens", "seg_src", "cu_targets",
+                                        "counts", "tok", "pos", "mask", "old_logprob", "adv",
+                                        "targets")])
+
+
+def aj_merge_timelines(tl, out, err, ws, stream=None):
+    """tl: dict of device tensors (traj_tl_off int32, tl_tok_off int64, tok int32, flags uint8,
+    old_logprob, adv float32); out: dict of output tensors (see aj_packed)."""
+    _check(lib().aj_merge_timelines(C.byref(_timelines(tl)), C.byref(_packed(out)), ptr(err),
+                                    ptr(ws), ws.numel() * ws.element_size(),
+                                    stream_handle(stream)), "aj_merge_timelines")
+
+
+def aj_flatten_timelines(tl, out, err, ws, stream=None):
+    _check(lib().aj_flatten_timelines(C.byref(_timelines(tl)), C.byref(_packed(out)), ptr(err),
+                                      ptr(ws), ws.numel() * ws.element_size(),
+                                      stream_handle(stream)), "aj_flatten_timelines")
+
+
+def aj_plan_packs(cu_seqlens_host, max_tokens):
+    """cu_seqlens_host: int32 CPU tensor [n_seg+1] -> list of pack segment offsets."""
+    n_seg = cu_seqlens_host.numel() - 1
+    off = torch.zeros(n_seg + 1, dtype=torch.int32)
+    n = i32(0)
+    cu = cu_seqlens_host.contiguous()
+    _check(lib().aj_plan_packs(ptr(cu), n_seg, max_tokens, ptr(off), C.byref(n)), "aj_plan_packs")
+    return off[:n.value + 1].tolist()
+
+
+def aj_read_device_error(err, stream=None):
+    v = i32(0)
+    _check(lib().aj_read_device_error(ptr(err), stream_handle(stream), C.byref(v)),
+           "aj_read_device_error")
+    return v.value
+
+
+# ------------------------------------------------------------------ embedding
+
+def aj_embed_fwd(tok, emb, x, err=None, stream=None):
+    _check(lib().aj_embed_fwd(ptr(tok), tok.numel(), ptr(emb), emb.shape[1], emb.shape[0],
+                              dtype_code(emb), ptr(x), ptr(err), stream_handle(stream)),
+           "aj_embed_fwd")
+
+
+def aj_embed_bwd(tok, dx, d_emb, stream=None):
+    _check(lib().aj_embed_bwd(ptr(tok), tok.numel(), ptr(dx), d_emb.shape[1], d_emb.shape[0],
+                              ptr(d_emb), stream_handle(stream)), "aj_embed_bwd")
+
+
+# ------------------------------------------------------------------ block
+
+def block_cfg(m):
+    return BlockCfg(m.d_model, m.n_q_heads, m.n_kv_heads, m.head_dim, m.d_ff, m.rms_eps,
+                    m.rope_theta, AJ_BF16 if m.dtype == "bf16" else AJ_F32)
+
+
+def aj_block_saved_bytes(cfg, n_tok):
+    return int(lib().aj_block_saved_bytes(C.byref(cfg), n_tok))
+
+
+def aj_block_workspace_bytes(cfg, n_tok, n_seg):
+    return int(lib().aj_block_workspace_bytes(C.byref(cfg), n_tok, n_seg))
+
+
+def _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos):
+    return Varlen(n_tok, n_seg, max_seqlen, base, ptr(cu_seqlens), ptr(pos))
+
+
+def _bw(w):
+    return BlockWeights(*[ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm",
+                                              "w_gate_up", "w_down")])
+
+
+def aj_varlen_block_fwd(cfg, w, cu_seqlens, pos, max_seqlen, x, y, saved, ws=None, stream=None,
+                        base=0):
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    _check(lib().aj_varlen_block_fwd(C.byref(cfg), C.byref(_bw(w)), C.byref(vl), ptr(x), ptr(y),
+                                     ptr(saved), ptr(ws),
+                                     0 if ws is None else ws.numel() * ws.element_size(),
+                                     stream_handle(stream)), "aj_varlen_block_fwd")
+
+
+def aj_varlen_block_bwd(cfg, w, cu_seqlens, pos, max_seqlen, x, saved, dy, dx, grads, ws,
+                        stream=None, base=0):
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    g = BlockGrads(*[ptr(grads[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm",
+                                             "w_gate_up", "w_down")])
+    _check(lib().aj_varlen_block_bwd(C.byref(cfg), C.byref(_bw(w)), C.byref(vl), ptr(x),
+                                     ptr(saved), ptr(dy), ptr(dx), C.byref(g), ptr(ws),
+                                     ws.numel() * ws.element_size(), stream_handle(stream)),
+           "aj_varlen_block_bwd")
+
+
+# ------------------------------------------------------------------ loss
+
+def loss_cfg(m):
+    return LossCfg(m.d_model, m.vocab, m.vocab_chunk, m.clip_eps, m.rms_eps,
+                   AJ_BF16 if m.dtype == "bf16" else AJ_F32)
+
+
+def aj_loss_saved_bytes(cfg, n_tgt):
+    return int(lib().aj_loss_saved_bytes(C.byref(cfg), n_tgt))
+
+
+def aj_loss_workspace_bytes(cfg, n_tgt):
+    return int(lib().aj_loss_workspace_bytes(C.byref(cfg), n_tgt))
+
+
+def _loss_in(n_tok, row_base, targets, tok, old_logprob, adv, inv_n_mask):
+    return LossIn(n_tok, targets.numel(), row_base, ptr(targets), ptr(tok), ptr(old_logprob),
+                  ptr(adv), float(inv_n_mask))
+
+
+def aj_logprob_pg_loss_fwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
+                           w_vocab, saved, logprob, lse, stats, ws, err=None, stream=None,
+                           row_base=0):
+    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask)
+    _check(lib().aj_logprob_pg_loss_fwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
+                                        ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
+                                        ptr(stats), ptr(err), ptr(ws),
+                                        ws.numel() * ws.element_size(), stream_handle(stream)),
+           "aj_logprob_pg_loss_fwd")
+
+
+def aj_logprob_pg_loss_bwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
+                           w_vocab, saved, logprob, lse, dh, d_final_norm, d_w_vocab, ws,
+                           stream=None, row_base=0):
+    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask)
+    _check(lib().aj_logprob_pg_loss_bwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
+                                        ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
+                                        ptr(dh), ptr(d_final_norm), ptr(d_w_vocab), ptr(ws),
+                                        ws.numel() * ws.element_size(), stream_handle(stream)),
+           "aj_logprob_pg_loss_bwd")

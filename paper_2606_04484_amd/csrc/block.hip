@@ -1,0 +1,262 @@
+// aj_varlen_block_fwd / aj_varlen_block_bwd and the embedding entry points.
+//
+// Forward:  a = RMSNorm(x) g1 -> qkv = a W_qkv^T -> RoPE(q, k) -> o = attention
+//           -> x1 = x + o W_o^T -> b = RMSNorm(x1) g2 -> gu = b W_gu^T
+//           -> s = silu(gate) * up -> y = x1 + s W_down^T
+// Backward: the same chain reversed; weight gradients are GEMMs over the
+// token axis accumulated into float32; the residual gradient stays float32.
+#include "ops.h"
+
+namespace {
+
+struct Saved {
+  void *a, *qkv, *o, *x1, *b, *gu, *s;
+  float *rstd1, *lse, *rstd2;
+  size_t bytes;
+};
+
+Saved carve_saved(const aj_block_cfg &c, int n, void *base) {
+  const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
+  const int64_t d = c.d_model, q = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int64_t hq = (int64_t)c.n_q_heads * c.head_dim, F = c.d_ff;
+  aj::Carver cv(base);
+  Saved s;
+  s.a = cv.take<char>(n * d * es);
+  s.qkv = cv.take<char>(n * q * es);
+  s.o = cv.take<char>(n * hq * es);
+  s.x1 = cv.take<char>(n * d * es);
+  s.b = cv.take<char>(n * d * es);
+  s.gu = cv.take<char>(n * 2 * F * es);
+  s.s = cv.take<char>(n * F * es);
+  s.rstd1 = cv.take<float>(n);
+  s.lse = cv.take<float>((int64_t)c.n_q_heads * n);
+  s.rstd2 = cv.take<float>(n);
+  s.bytes = cv.bytes();
+  return s;
+}
+
+struct BwdWs {
+  void *dy_t, *ds, *dgu, *dx1_t, *dout, *dqkv;
+  float *db, *dx1, *delta, *da, *dg_part;
+  size_t bytes;
+};
+
+BwdWs carve_bwd(const aj_block_cfg &c, int n, void *base) {
+  const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
+  const int64_t d = c.d_model, q = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int64_t hq = (int64_t)c.n_q_heads * c.head_dim, F = c.d_ff;
+  aj::Carver cv(base);
+  BwdWs w;
+  w.dy_t = cv.take<char>(n * d * es);
+  w.ds = cv.take<char>(n * F * es);
+  w.dgu = cv.take<char>(n * 2 * F * es);
+  w.dx1_t = cv.take<char>(n * d * es);
+  w.dout = cv.take<char>(n * hq * es);
+  w.dqkv = cv.take<char>(n * q * es);
+  w.db = cv.take<float>(n * d);
+  w.dx1 = cv.take<float>(n * d);
+  w.delta = cv.take<float>((int64_t)c.n_q_heads * n);
+  w.da = cv.take<float>(n * d);
+  w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n, (int)d));
+  w.bytes = cv.bytes();
+  return w;
+}
+
+int check_cfg(const aj_block_cfg *c, const char *name) {
+  AJ_REQUIRE(c, AJ_ERR_NULL, "%s: null cfg", name);
+  AJ_REQUIRE(c->dtype == AJ_F32 || c->dtype == AJ_BF16, AJ_ERR_UNSUPPORTED, "%s: dtype %d", name,
+             c->dtype);
+  AJ_REQUIRE(c->d_model > 0 && c->d_model <= 8192 && c->d_model % 8 == 0, AJ_ERR_SHAPE,
+             "%s: d_model %d (multiple of 8, at most 8192)", name, c->d_model);
+  AJ_REQUIRE(c->n_q_heads > 0 && c->n_kv_heads > 0 && c->n_q_heads % c->n_kv_heads == 0,
+             AJ_ERR_SHAPE, "%s: heads %d/%d", name, c->n_q_heads, c->n_kv_heads);
+  AJ_REQUIRE(c->head_dim >= 8 && c->head_dim <= 128 && c->head_dim % 8 == 0, AJ_ERR_UNSUPPORTED,
+             "%s: head_dim %d (8..128, multiple of 8)", name, c->head_dim);
+  AJ_REQUIRE(c->d_ff > 0 && c->d_ff % 8 == 0, AJ_ERR_SHAPE, "%s: d_ff %d", name, c->d_ff);
+  AJ_REQUIRE(c->rms_eps > 0 && c->rope_theta > 1, AJ_ERR_SHAPE, "%s: eps/theta", name);
+  return AJ_OK;
+}
+
+int check_varlen(const aj_varlen *v, const char *name) {
+  AJ_REQUIRE(v, AJ_ERR_NULL, "%s: null varlen", name);
+  AJ_REQUIRE(v->n_tok >= 0 && v->n_seg >= 0 && (v->n_tok == 0 || v->n_seg > 0), AJ_ERR_SHAPE,
+             "%s: n_tok %d n_seg %d", name, v->n_tok, v->n_seg);
+  AJ_REQUIRE(v->n_tok == 0 || (v->cu_seqlens && v->pos), AJ_ERR_NULL, "%s: null offsets", name);
+  return AJ_OK;
+}
+
+template <typename T>
+int block_fwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen &v, const T *x,
+              T *y, const Saved &sv, hipStream_t st) {
+  using namespace aj;
+  const int n = v.n_tok, d = c.d_model, hd = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
+  const int qdim = (Hq + 2 * Hkv) * hd, F = c.d_ff;
+  int r;
+  rmsnorm_fwd<T>(x, (const T *)w.attn_norm, n, d, c.rms_eps, nullptr, 0, (T *)sv.a, sv.rstd1, st);
+  Gemm g;
+  g.M = n; g.N = qdim; g.K = d;
+  g.A = sv.a; g.lda = d; g.B = w.w_qkv; g.ldb = d; g.C = sv.qkv; g.ldc = qdim;
+  if ((r = gemm<T>(g, st))) return r;
+  rope<T>((T *)sv.qkv, n, v.pos, Hq + Hkv, qdim, hd, c.rope_theta, false, st);
+  AttnArgs at{n, v.n_seg, Hq, Hkv, hd, v.base, v.cu_seqlens, sv.qkv, sv.o, sv.lse,
+              1.0f / sqrtf((float)hd)};
+  if ((r = attn_fwd<T>(at, st))) return r;
+  g = Gemm();
+  g.M = n; g.N = d; g.K = Hq * hd;
+  g.A = sv.o; g.lda = Hq * hd; g.B = w.w_o; g.ldb = Hq * hd; g.C = sv.x1; g.ldc = d; g.R = x;
+  if ((r = gemm<T>(g, st))) return r;
+  rmsnorm_fwd<T>((const T *)sv.x1, (const T *)w.mlp_norm, n, d, c.rms_eps, nullptr, 0, (T *)sv.b,
+                 sv.rstd2, st);
+  g = Gemm();
+  g.M = n; g.N = 2 * F; g.K = d;
+  g.A = sv.b; g.lda = d; g.B = w.w_gate_up; g.ldb = d; g.C = sv.gu; g.ldc = 2 * F;
+  if ((r = gemm<T>(g, st))) return r;
+  swiglu_fwd<T>((const T *)sv.gu, n, F, (T *)sv.s, st);
+  g = Gemm();
+  g.M = n; g.N = d; g.K = F;
+  g.A = sv.s; g.lda = F; g.B = w.w_down; g.ldb = F; g.C = y; g.ldc = d; g.R = sv.x1;
+  if ((r = gemm<T>(g, st))) return r;
+  return check_launch("aj_varlen_block_fwd");
+}
+
+template <typename T>
+int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen &v, const T *x,
+              const Saved &sv, const float *dy, float *dx, const aj_block_grads &gr,
+              const BwdWs &ws, hipStream_t st) {
+  using namespace aj;
+  const int n = v.n_tok, d = c.d_model, hd = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
+  const int qdim = (Hq + 2 * Hkv) * hd, F = c.d_ff, hq = Hq * hd;
+  const bool same = sizeof(T) == sizeof(float);
+  int r;
+  const T *dy_t = same ? (const T *)dy : (const T *)ws.dy_t;
+  if (!same) cast_from_f32<T>(dy, (int64_t)n * d, (T *)ws.dy_t, st);
+  // MLP down projection
+  Gemm g;
+  g.M = d; g.N = F; g.K = n; g.A = dy_t; g.lda = d; g.a_kmajor = false;
+  g.B = sv.s; g.ldb = F; g.b_kmajor = false; g.C = gr.w_down; g.ldc = F; g.out = OUT_ACCUM_F32;
+  if ((r = gemm<T>(g, st))) return r;
+  g = Gemm();
+  g.M = n; g.N = F; g.K = d; g.A = dy_t; g.lda = d;
+  g.B = w.w_down; g.ldb = F; g.b_kmajor = false; g.C = ws.ds; g.ldc = F;
+  if ((r = gemm<T>(g, st))) return r;
+  swiglu_bwd<T, T>((const T *)ws.ds, (const T *)sv.gu, n, F, (T *)ws.dgu, st);
+  // gate/up projection
+  g = Gemm();
+  g.M = 2 * F; g.N = d; g.K = n; g.A = ws.dgu; g.lda = 2 * F; g.a_kmajor = false;
+  g.B = sv.b; g.ldb = d; g.b_kmajor = false; g.C = gr.w_gate_up; g.ldc = d; g.out = OUT_ACCUM_F32;
+  if ((r = gemm<T>(g, st))) return r;
+  g = Gemm();
+  g.M = n; g.N = d; g.K = 2 * F; g.A = ws.dgu; g.lda = 2 * F;
+  g.B = w.w_gate_up; g.ldb = d; g.b_kmajor = false; g.C = ws.db; g.ldc = d; g.c_f32 = true;
+  if ((r = gemm<T>(g, st))) return r;
+  rmsnorm_bwd<T>(ws.db, (const T *)sv.x1, sv.rstd2, (const T *)w.mlp_norm, n, d, nullptr, 0, 0, dy,
+                 ws.dx1, same ? nullptr : (T *)ws.dx1_t, ws.dg_part, gr.mlp_norm, st);
+  const T *dx1_t = same ? (const T *)ws.dx1 : (const T *)ws.dx1_t;
+  // attention output projection
+  g = Gemm();
+  g.M = d; g.N = hq; g.K = n; g.A = dx1_t; g.lda = d; g.a_kmajor = false;
+  g.B = sv.o; g.ldb = hq; g.b_kmajor = false; g.C = gr.w_o; g.ldc = hq; g.out = OUT_ACCUM_F32;
+  if ((r = gemm<T>(g, st))) return r;
+  g = Gemm();
+  g.M = n; g.N = hq; g.K = d; g.A = dx1_t; g.lda = d;
+  g.B = w.w_o; g.ldb = hq; g.b_kmajor = false; g.C = ws.dout; g.ldc = hq;
+  if ((r = gemm<T>(g, st))) return r;
+  AttnBwdArgs ab{n, v.n_seg, Hq, Hkv, hd, v.base, v.cu_seqlens, sv.qkv, sv.o, ws.dout, sv.lse,
+                 ws.delta, ws.dqkv, 1.0f / sqrtf((float)hd)};
+  if ((r = attn_bwd<T>(ab, st))) return r;
+  rope<T>((T *)ws.dqkv, n, v.pos, Hq + Hkv, qdim, hd, c.rope_theta, true, st);
+  // qkv projection
+  g = Gemm();
+  g.M = qdim; g.N = d; g.K = n; g.A = ws.dqkv; g.lda = qdim; g.a_kmajor = false;
+  g.B = sv.a; g.ldb = d; g.b_kmajor = false; g.C = gr.w_qkv; g.ldc = d; g.out = OUT_ACCUM_F32;
+  if ((r = gemm<T>(g, st))) return r;
+  g = Gemm();
+  g.M = n; g.N = d; g.K = qdim; g.A = ws.dqkv; g.lda = qdim;
+  g.B = w.w_qkv; g.ldb = d; g.b_kmajor = false; g.C = ws.da; g.ldc = d; g.c_f32 = true;
+  if ((r = gemm<T>(g, st))) return r;
+  rmsnorm_bwd<T>(ws.da, x, sv.rstd1, (const T *)w.attn_norm, n, d, nullptr, 0, 0, ws.dx1, dx,
+                 nullptr, ws.dg_part, gr.attn_norm, st);
+  return check_launch("aj_varlen_block_bwd");
+}
+
+int check_weights(const aj_block_weights *w, const char *name) {
+  AJ_REQUIRE(w && w->attn_norm && w->w_qkv && w->w_o && w->mlp_norm && w->w_gate_up && w->w_down,
+             AJ_ERR_NULL, "%s: null weight", name);
+  return AJ_OK;
+}
+
+}  // namespace
+
+extern "C" size_t aj_block_saved_bytes(const aj_block_cfg *cfg, int32_t n_tok) {
+  if (!cfg || n_tok < 0) return 0;
+  return carve_saved(*cfg, n_tok, nullptr).bytes;
+}
+
+extern "C" size_t aj_block_workspace_bytes(const aj_block_cfg *cfg, int32_t n_tok, int32_t n_seg) {
+  (void)n_seg;
+  if (!cfg || n_tok < 0) return 0;
+  return carve_bwd(*cfg, n_tok, nullptr).bytes;
+}
+
+extern "C" int aj_varlen_block_fwd(const aj_block_cfg *cfg, const aj_block_weights *w,
+                                   const aj_varlen *vl, const void *x, void *y, void *saved,
+                                   void *ws, size_t ws_bytes, void *stream) {
+  const char *name = "aj_varlen_block_fwd";
+  int r;
+  if ((r = check_cfg(cfg, name)) || (r = check_varlen(vl, name)) || (r = check_weights(w, name)))
+    return r;
+  (void)ws; (void)ws_bytes;
+  if (vl->n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(x && y && saved, AJ_ERR_NULL, "%s: null x/y/saved", name);
+  Saved sv = carve_saved(*cfg, vl->n_tok, saved);
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return block_fwd<bf16_t>(*cfg, *w, *vl, (const bf16_t *)x, (bf16_t *)y, sv, st);
+  return block_fwd<float>(*cfg, *w, *vl, (const float *)x, (float *)y, sv, st);
+}
+
+extern "C" int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w,
+                                   const aj_varlen *vl, const void *x, const void *saved,
+                                   const float *dy, float *dx, const aj_block_grads *g, void *ws,
+                                   size_t ws_bytes, void *stream) {
+  const char *name = "aj_varlen_block_bwd";
+  int r;
+  if ((r = check_cfg(cfg, name)) || (r = check_varlen(vl, name)) || (r = check_weights(w, name)))
+    return r;
+  AJ_REQUIRE(g && g->attn_norm && g->w_qkv && g->w_o && g->mlp_norm && g->w_gate_up && g->w_down,
+             AJ_ERR_NULL, "%s: null gradient", name);
+  if (vl->n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(x && saved && dy && dx && ws, AJ_ERR_NULL, "%s: null x/saved/dy/dx/ws", name);
+  BwdWs bw = carve_bwd(*cfg, vl->n_tok, ws);
+  AJ_REQUIRE(ws_bytes >= bw.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu", name, ws_bytes,
+             bw.bytes);
+  Saved sv = carve_saved(*cfg, vl->n_tok, const_cast<void *>(saved));
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return block_bwd<bf16_t>(*cfg, *w, *vl, (const bf16_t *)x, sv, dy, dx, *g, bw, st);
+  return block_bwd<float>(*cfg, *w, *vl, (const float *)x, sv, dy, dx, *g, bw, st);
+}
+
+extern "C" int aj_embed_fwd(const int32_t *tok, int32_t n_tok, const void *emb, int32_t d,
+                            int32_t vocab, int dtype, void *x, int32_t *err, void *stream) {
+  AJ_REQUIRE(n_tok >= 0 && d > 0 && vocab > 0, AJ_ERR_SHAPE, "aj_embed_fwd: sizes");
+  if (n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(tok && emb && x, AJ_ERR_NULL, "aj_embed_fwd: null pointer");
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == AJ_BF16)
+    aj::embed_fwd<bf16_t>(tok, n_tok, (const bf16_t *)emb, d, vocab, (bf16_t *)x, err, st);
+  else if (dtype == AJ_F32)
+    aj::embed_fwd<float>(tok, n_tok, (const float *)emb, d, vocab, (float *)x, err, st);
+  else
+    return aj::fail(AJ_ERR_UNSUPPORTED, "aj_embed_fwd: dtype %d", dtype);
+  return aj::check_launch("aj_embed_fwd");
+}
+
+extern "C" int aj_embed_bwd(const int32_t *tok, int32_t n_tok, const float *dx, int32_t d,
+                            int32_t vocab, float *d_emb, void *stream) {
+  AJ_REQUIRE(n_tok >= 0 && d > 0 && vocab > 0, AJ_ERR_SHAPE, "aj_embed_bwd: sizes");
+  if (n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(tok && dx && d_emb, AJ_ERR_NULL, "aj_embed_bwd: null pointer");
+  aj::embed_bwd(tok, n_tok, dx, d, vocab, d_emb, (hipStream_t)stream);
+  return aj::check_launch("aj_embed_bwd");
+}

@@ -1,0 +1,340 @@
+// aj_logprob_pg_loss_fwd / _bwd: final RMSNorm, vocab projection,
+// log-softmax, token log-prob and the clipped policy-gradient loss.
+//
+// Only the rows that feed a target are normalised and projected (the loss
+// reads no other logits).  The vocab is walked in vocab_chunk-wide chunks with
+// a running (max, sum of exp) per row, so only one chunk of logits exists at a
+// time.  The backward recomputes each chunk's logits and turns them into
+//   dz = g * (onehot(target) - softmax)        g = d loss / d logprob
+// then accumulates dhn += dz W_chunk and dW_chunk += dz^T hn.
+#include "ops.h"
+
+namespace {
+
+struct LossWs {
+  float *z, *run_m, *run_s, *zt, *part, *g, *dhn, *dg_part;
+  void *dz;
+  int32_t *tpos, *trow;   // targets clamped into the documented range, and their h rows
+  size_t bytes;
+};
+
+constexpr int kFinBlocks = 256;
+
+LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
+  const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
+  const int64_t cw = c.vocab_chunk < c.vocab ? c.vocab_chunk : c.vocab;
+  aj::Carver cv(base);
+  LossWs w;
+  w.z = cv.take<float>((int64_t)n_tgt * cw);
+  w.dz = cv.take<char>((int64_t)n_tgt * cw * es);
+  w.run_m = cv.take<float>(n_tgt);
+  w.run_s = cv.take<float>(n_tgt);
+  w.zt = cv.take<float>(n_tgt);
+  w.g = cv.take<float>(n_tgt);
+  w.tpos = cv.take<int32_t>(n_tgt);
+  w.trow = cv.take<int32_t>(n_tgt);
+  w.part = cv.take<float>(kFinBlocks * 4);
+  w.dhn = cv.take<float>((int64_t)n_tgt * c.d_model);
+  w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n_tgt, c.d_model));
+  w.bytes = cv.bytes();
+  return w;
+}
+
+struct LossSaved {
+  void *hn;
+  float *rstd;
+  size_t bytes;
+};
+
+LossSaved carve_saved(const aj_loss_cfg &c, int n_tgt, void *base) {
+  const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
+  aj::Carver cv(base);
+  LossSaved s;
+  s.hn = cv.take<char>((int64_t)n_tgt * c.d_model * es);
+  s.rstd = cv.take<float>(n_tgt);
+  s.bytes = cv.bytes();
+  return s;
+}
+
+AJ_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+AJ_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Target p is scored from h row p - 1 - row_base; anything outside [0, n_tok)
+// is reported and clamped so that no access leaves the documented ranges.
+__global__ void sanitize_targets_kernel(int n, const int32_t *targets, int row_base, int n_tok,
+                                        int32_t *tpos, int32_t *trow, int32_t *err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int r = targets[i] - 1 - row_base;
+  if (r < 0 || r >= n_tok) {
+    if (err) atomicOr(err, AJ_DEVERR_OFFSETS);
+    r = r < 0 ? 0 : n_tok - 1;
+  }
+  trow[i] = r;
+  tpos[i] = r + 1 + row_base;
+}
+
+__global__ void loss_init_kernel(int n, float *run_m, float *run_s, float *zt) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  run_m[i] = -INFINITY;
+  run_s[i] = 0.f;
+  zt[i] = 0.f;
+}
+
+// One wave per row: fold chunk [c0, c0+cw) of logits into the running max/sum,
+// and pick up the target's logit if it lies in the chunk.
+__global__ __launch_bounds__(256) void lse_update_kernel(const float *z, int n, int cw, int c0,
+                                                         const int32_t *tpos,
+                                                         const int32_t *tok, int vocab,
+                                                         float *run_m, float *run_s, float *zt,
+                                                         int32_t *err) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const float *zr = z + (int64_t)row * cw;
+  float m = -INFINITY;
+  for (int j = lane; j < cw; j += 64) m = fmaxf(m, zr[j]);
+  m = wave_max(m);
+  float s = 0.f;
+  for (int j = lane; j < cw; j += 64) s += __expf(zr[j] - m);
+  s = wave_sum(s);
+  if (lane == 0) {
+    const float mo = run_m[row], so = run_s[row];
+    const float mn = fmaxf(mo, m);
+    run_s[row] = so * __expf(mo - mn) + s * __expf(m - mn);
+    run_m[row] = mn;
+    const int t = tok[tpos[row]];
+    if (t >= c0 && t < c0 + cw) zt[row] = zr[t - c0];
+    if (c0 == 0 && (t < 0 || t >= vocab) && err) atomicOr(err, AJ_DEVERR_TOKEN_RANGE);
+  }
+}
+
+// d loss / d logprob for one target (unnormalised by N_mask).
+AJ_DEV float pg_grad(float lp, float old, float A, float eps, float *term, int *clipped,
+                     float *ratio) {
+  const float r = __expf(lp - old);
+  const float rc = fminf(fmaxf(r, 1.f - eps), 1.f + eps);
+  *term = -fminf(r * A, rc * A);
+  const bool active = (A > 0.f && r <= 1.f + eps) || (A < 0.f && r >= 1.f - eps);
+  *clipped = (!active && A != 0.f) ? 1 : 0;
+  *ratio = r;
+  return active ? -A * r : 0.f;
+}
+
+__global__ __launch_bounds__(256) void loss_finalize_kernel(
+    int n, const int32_t *tpos, const float *old_lp, const float *adv, float eps, float inv_n,
+    const float *run_m, const float *run_s, const float *zt, float *logprob, float *lse,
+    float *part) {
+  __shared__ float red[4][256];
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    const float l = run_m[i] + logf(run_s[i]);
+    const float lp = zt[i] - l;
+    lse[i] = l;
+    logprob[i] = lp;
+    const int p = tpos[i];
+    float term, r;
+    int clipped;
+    pg_grad(lp, old_lp[p], adv[p], eps, &term, &clipped, &r);
+    acc[0] += term * inv_n;
+    acc[1] += (float)clipped;
+    acc[2] += r;
+    acc[3] += 1.f;
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) red[k][threadIdx.x] = acc[k];
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x < 4) part[blockIdx.x * 4 + threadIdx.x] = red[threadIdx.x][0];
+}
+
+__global__ void stats_reduce_kernel(const float *part, int nb, float *stats) {
+  const int k = threadIdx.x;
+  if (k >= 4) return;
+  float s = 0.f;
+  for (int b = 0; b < nb; ++b) s += part[b * 4 + k];
+  stats[k] += s;
+}
+
+__global__ void loss_grad_kernel(int n, const int32_t *tpos, const float *logprob,
+                                 const float *old_lp, const float *adv, float eps, float inv_n,
+                                 float *g) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int p = tpos[i];
+  float term, r;
+  int clipped;
+  g[i] = pg_grad(logprob[i], old_lp[p], adv[p], eps, &term, &clipped, &r) * inv_n;
+}
+
+// dz[i][j] = g_i * ((c0 + j == target_i) - exp(z_ij - lse_i))
+template <typename T>
+__global__ __launch_bounds__(256) void dz_kernel(const float *z, int n, int cw, int c0,
+                                                 const int32_t *tpos, const int32_t *tok,
+                                                 const float *lse, const float *g, T *dz) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * cw) return;
+  const int i = (int)(idx / cw), j = (int)(idx % cw);
+  const float gi = g[i];
+  const float p = __expf(z[idx] - lse[i]);
+  const float oh = (tok[tpos[i]] == c0 + j) ? 1.f : 0.f;
+  stf(dz + idx, gi * (oh - p));
+}
+
+int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
+  AJ_REQUIRE(c && in, AJ_ERR_NULL, "%s: null cfg/in", name);
+  AJ_REQUIRE(c->dtype == AJ_F32 || c->dtype == AJ_BF16, AJ_ERR_UNSUPPORTED, "%s: dtype", name);
+  AJ_REQUIRE(c->d_model > 0 && c->d_model % 8 == 0 && c->d_model <= 8192, AJ_ERR_SHAPE,
+             "%s: d_model %d", name, c->d_model);
+  AJ_REQUIRE(c->vocab > 0 && c->vocab_chunk > 0 && c->vocab_chunk % 8 == 0, AJ_ERR_SHAPE,
+             "%s: vocab %d chunk %d", name, c->vocab, c->vocab_chunk);
+  AJ_REQUIRE(c->clip_eps >= 0 && c->rms_eps > 0, AJ_ERR_SHAPE, "%s: eps", name);
+  AJ_REQUIRE(in->n_tok >= 0 && in->n_tgt >= 0 && in->n_tgt <= in->n_tok, AJ_ERR_SHAPE,
+             "%s: n_tok %d n_tgt %d", name, in->n_tok, in->n_tgt);
+  AJ_REQUIRE(in->n_tgt == 0 || (in->targets && in->tok && in->old_logprob && in->adv),
+             AJ_ERR_NULL, "%s: null input arrays", name);
+  return AJ_OK;
+}
+
+template <typename T>
+int chunk_logits(const aj_loss_cfg &c, int n_tgt, const void *hn, const void *w_vocab, int c0,
+                 int cw, float *z, hipStream_t st) {
+  aj::Gemm g;
+  g.M = n_tgt; g.N = cw; g.K = c.d_model;
+  g.A = hn; g.lda = c.d_model;
+  g.B = (const T *)w_vocab + (int64_t)c0 * c.d_model; g.ldb = c.d_model;
+  g.C = z; g.ldc = cw; g.c_f32 = true;
+  return aj::gemm<T>(g, st);
+}
+
+template <typename T>
+int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const void *gf,
+             const void *w_vocab, const LossSaved &sv, float *logprob, float *lse, float *stats,
+             int32_t *err, const LossWs &w, hipStream_t st) {
+  const int n = in.n_tgt, d = c.d_model;
+  sanitize_targets_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, in.targets, in.row_base, in.n_tok,
+                                                           w.tpos, w.trow, err);
+  aj::rmsnorm_fwd<T>((const T *)h, (const T *)gf, n, d, c.rms_eps, w.trow, 0, (T *)sv.hn,
+                     sv.rstd, st);
+  loss_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.run_m, w.run_s, w.zt);
+  for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
+    const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
+    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st);
+    if (r) return r;
+    lse_update_kernel<<<(n + 3) / 4, 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok, c.vocab,
+                                                  w.run_m, w.run_s, w.zt, err);
+  }
+  int nb = (n + 255) / 256;
+  if (nb > kFinBlocks) nb = kFinBlocks;
+  loss_finalize_kernel<<<nb, 256, 0, st>>>(n, w.tpos, in.old_logprob, in.adv, c.clip_eps,
+                                           in.inv_n_mask, w.run_m, w.run_s, w.zt, logprob, lse,
+                                           w.part);
+  stats_reduce_kernel<<<1, 64, 0, st>>>(w.part, nb, stats);
+  return aj::check_launch("aj_logprob_pg_loss_fwd");
+}
+
+template <typename T>
+int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const void *gf,
+             const void *w_vocab, const LossSaved &sv, const float *logprob, const float *lse,
+             float *dh, float *dgf, float *dwv, const LossWs &w, hipStream_t st) {
+  const int n = in.n_tgt, d = c.d_model;
+  aj::fill_f32(dh, (int64_t)in.n_tok * d, 0.f, st);
+  if (n == 0) return aj::check_launch("aj_logprob_pg_loss_bwd");
+  sanitize_targets_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, in.targets, in.row_base, in.n_tok,
+                                                           w.tpos, w.trow, nullptr);
+  loss_grad_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, logprob, in.old_logprob, in.adv,
+                                                    c.clip_eps, in.inv_n_mask, w.g);
+  aj::fill_f32(w.dhn, (int64_t)n * d, 0.f, st);
+  for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
+    const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
+    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st);
+    if (r) return r;
+    const int64_t tot = (int64_t)n * cw;
+    dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok,
+                                                                lse, w.g, (T *)w.dz);
+    aj::Gemm g;   // dhn += dz W_chunk
+    g.M = n; g.N = d; g.K = cw; g.A = w.dz; g.lda = cw;
+    g.B = (const T *)w_vocab + (int64_t)c0 * d; g.ldb = d; g.b_kmajor = false;
+    g.C = w.dhn; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
+    if ((r = aj::gemm<T>(g, st))) return r;
+    g = aj::Gemm();   // dW_chunk += dz^T hn
+    g.M = cw; g.N = d; g.K = n; g.A = w.dz; g.lda = cw; g.a_kmajor = false;
+    g.B = sv.hn; g.ldb = d; g.b_kmajor = false;
+    g.C = dwv + (int64_t)c0 * d; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
+    if ((r = aj::gemm<T>(g, st))) return r;
+  }
+  aj::rmsnorm_bwd<T>(w.dhn, (const T *)h, sv.rstd, (const T *)gf, n, d, w.trow, 0, 1,
+                     nullptr, dh, nullptr, w.dg_part, dgf, st);
+  return aj::check_launch("aj_logprob_pg_loss_bwd");
+}
+
+}  // namespace
+
+extern "C" size_t aj_loss_saved_bytes(const aj_loss_cfg *cfg, int32_t n_tgt) {
+  if (!cfg || n_tgt < 0) return 0;
+  return carve_saved(*cfg, n_tgt, nullptr).bytes;
+}
+
+extern "C" size_t aj_loss_workspace_bytes(const aj_loss_cfg *cfg, int32_t n_tgt) {
+  if (!cfg || n_tgt < 0) return 0;
+  return carve_ws(*cfg, n_tgt, nullptr).bytes;
+}
+
+extern "C" int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
+                                      const void *final_norm, const void *w_vocab, void *saved,
+                                      float *logprob, float *lse, float *stats, int32_t *err,
+                                      void *ws, size_t ws_bytes, void *stream) {
+  const char *name = "aj_logprob_pg_loss_fwd";
+  int r;
+  if ((r = check_cfg(cfg, in, name))) return r;
+  AJ_REQUIRE(stats, AJ_ERR_NULL, "%s: null stats", name);
+  if (in->n_tgt == 0) return AJ_OK;
+  AJ_REQUIRE(h && final_norm && w_vocab && saved && logprob && lse && ws, AJ_ERR_NULL,
+             "%s: null pointer", name);
+  LossWs w = carve_ws(*cfg, in->n_tgt, ws);
+  AJ_REQUIRE(ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu", name, ws_bytes,
+             w.bytes);
+  LossSaved sv = carve_saved(*cfg, in->n_tgt, saved);
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return loss_fwd<bf16_t>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, stats, err, w, st);
+  return loss_fwd<float>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, stats, err, w, st);
+}
+
+extern "C" int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
+                                      const void *final_norm, const void *w_vocab,
+                                      const void *saved, const float *logprob, const float *lse,
+                                      float *dh, float *d_final_norm, float *d_w_vocab, void *ws,
+                                      size_t ws_bytes, void *stream) {
+  const char *name = "aj_logprob_pg_loss_bwd";
+  int r;
+  if ((r = check_cfg(cfg, in, name))) return r;
+  if (in->n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(dh && d_final_norm && d_w_vocab, AJ_ERR_NULL, "%s: null gradient", name);
+  AJ_REQUIRE(in->n_tgt == 0 || (h && final_norm && w_vocab && saved && logprob && lse && ws),
+             AJ_ERR_NULL, "%s: null pointer", name);
+  LossWs w = carve_ws(*cfg, in->n_tgt, ws);
+  AJ_REQUIRE(in->n_tgt == 0 || ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu",
+             name, ws_bytes, w.bytes);
+  LossSaved sv = carve_saved(*cfg, in->n_tgt, const_cast<void *>(saved));
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return loss_bwd<bf16_t>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, dh, d_final_norm,
+                            d_w_vocab, w, st);
+  return loss_bwd<float>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, dh, d_final_norm,
+                         d_w_vocab, w, st);
+}

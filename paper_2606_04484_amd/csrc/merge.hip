@@ -1,0 +1,453 @@
+// Timeline merging on the GPU (Section 4.4.2, Algorithm 1, token-level Match).
+//
+// Algorithm 1 is a sequential double loop, but its result has a closed form
+// that parallelises:
+//   * Match leaves token ids unchanged, so whether T_j is a block-aligned
+//     prefix of T_i (written T_j <= T_i) never changes while the loop runs;
+//   * the largest i > j with T_j <= T_i is never absorbed itself (whatever
+//     absorbed it would be a larger i with T_j <= i), and it is the first
+//     candidate the descending loop offers j to, so
+//         absorber(j) = max { i > j in j's episode : T_j <= T_i }   (or none);
+//   * an absorbed timeline never absorbs (it is skipped when its turn comes),
+//     so it hands over its ORIGINAL blocks; on a survivor's non-llm block k the
+//     first transfer wins, and absorbed timelines arrive in descending j:
+//         payload(s, k) = s's own block if llm, else the block k of the largest
+//                         j absorbed into s whose block k is llm.
+// Kernels:
+//   validate        offsets tile [0, n_tok) and [0, n_tl); first token starts a block
+//   find_absorber   one workgroup per timeline j: candidates i from the episode's
+//                   last timeline down, prefix compare with early exit
+//   resolve         survivor scan -> segment index, cu_seqlens, counts
+//   claim_fill / claim   llm tokens of absorbed timelines vote (atomicMax of j)
+//                   for the survivor position they land on
+//   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv
+//   tgt_count / tgt_scan / tgt_write / cu_targets   ascending masked targets
+#include "common.h"
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kChunk = 1024;          // outputs per workgroup in the target compaction
+// Offsets that do not tile the input stop the merge (every count 0); bad flag
+// bytes are reported and the token is treated as written (author 3: not llm).
+constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY;
+
+struct MergeArgs {
+  int32_t n_traj, n_tl;
+  int64_t n_tok;
+  const int32_t *traj_tl_off;
+  const int64_t *tl_tok_off;
+  const int32_t *tok;
+  const uint8_t *flags;
+  const float *old_logprob, *adv;
+  // outputs
+  int32_t *absorber, *cu_seqlens, *seg_src, *cu_targets;
+  int64_t *counts;
+  int32_t *otok, *opos;
+  uint8_t *omask;
+  float *olp, *oadv;
+  int32_t *targets;
+  // workspace
+  int32_t *status;      // [0] error bits seen by this call
+  int32_t *tl_seg;      // [n_tl]
+  int32_t *claim;       // [n_tok]
+  int32_t *chunk_cnt;   // [n_chunks]
+  int32_t *chunk_off;   // [n_chunks]
+  int32_t *user_err;
+};
+
+AJ_DEV bool fatal(const MergeArgs &a) { return (a.status[0] & kFatal) != 0; }
+
+AJ_DEV void raise(const MergeArgs &a, int bits) {
+  atomicOr(a.status, bits);
+  if (a.user_err) atomicOr(a.user_err, bits);
+}
+
+// Largest timeline index i with tl_tok_off[i] <= u (u < n_tok, offsets valid).
+AJ_DEV int find_timeline(const int64_t *off, int n_tl, int64_t u, int lo, int hi) {
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= u) lo = mid; else hi = mid - 1;
+  }
+  // skip empty timelines sharing the offset (none when offsets are valid)
+  while (lo + 1 < n_tl && off[lo + 1] <= u) ++lo;
+  return lo;
+}
+
+// Inclusive block scan of one int per thread; returns the inclusive value, *total
+// gets the block sum.  blockDim.x must equal NT (a multiple of 64).
+template <int NT>
+AJ_DEV int block_scan_incl(int v, int *total) {
+  __shared__ int wsum[NT / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    int w = (lane < NT / 64) ? wsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int y = __shfl_up(w, o, 64);
+      if (lane >= o) w += y;
+    }
+    if (lane < NT / 64) wsum[lane] = w;
+  }
+  __syncthreads();
+  int res = x + (wid > 0 ? wsum[wid - 1] : 0);
+  *total = wsum[NT / 64 - 1];
+  __syncthreads();
+  return res;
+}
+
+__global__ void init_status_kernel(MergeArgs a) {
+  if (threadIdx.x < 4) a.status[threadIdx.x] = 0;
+}
+
+__global__ void validate_kernel(MergeArgs a) {
+  int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t == 0) {
+    if (a.traj_tl_off[0] != 0 || a.traj_tl_off[a.n_traj] != a.n_tl) raise(a, AJ_DEVERR_OFFSETS);
+    if (a.tl_tok_off[0] != 0 || a.tl_tok_off[a.n_tl] != a.n_tok) raise(a, AJ_DEVERR_OFFSETS);
+  }
+  if (t < a.n_traj && a.traj_tl_off[t] > a.traj_tl_off[t + 1]) raise(a, AJ_DEVERR_OFFSETS);
+  if (t < a.n_tl) {
+    int64_t lo = a.tl_tok_off[t], hi = a.tl_tok_off[t + 1];
+    if (lo < 0 || lo > hi || hi > a.n_tok) {
+      raise(a, AJ_DEVERR_OFFSETS);
+    } else if (lo == hi) {
+      raise(a, AJ_DEVERR_EMPTY);
+    } else if (!(a.flags[lo] & AJ_FLAG_BLOCK_START)) {
+      raise(a, AJ_DEVERR_BAD_FLAGS);
+    }
+  }
+}
+
+// One workgroup per timeline j.
+__global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
+  const int j = blockIdx.x;
+  if (fatal(a)) {
+    if (threadIdx.x == 0) a.absorber[j] = -1;
+    return;
+  }
+  // episode of j: largest e with traj_tl_off[e] <= j
+  int lo = 0, hi = a.n_traj - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (a.traj_tl_off[mid] <= j) lo = mid; else hi = mid - 1;
+  }
+  while (lo + 1 < a.n_traj && a.traj_tl_off[lo + 1] <= j) ++lo;
+  const int last = a.traj_tl_off[lo + 1] - 1;
+  const int64_t bj = a.tl_tok_off[j];
+  const int64_t lj = a.tl_tok_off[j + 1] - bj;
+  int result = -1;
+  for (int i = last; i > j; --i) {
+    const int64_t bi = a.tl_tok_off[i];
+    const int64_t li = a.tl_tok_off[i + 1] - bi;
+    if (li < lj) continue;
+    // block-aligned: T_i must start a new block right where T_j ends
+    if (li > lj && !(a.flags[bi + lj] & AJ_FLAG_BLOCK_START)) continue;
+    bool equal = true;
+    for (int64_t base = 0; base < lj; base += 8 * kBlock) {
+      int bad = 0;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        int64_t p = base + r * kBlock + threadIdx.x;
+        if (p < lj) {
+          bad |= a.tok[bj + p] != a.tok[bi + p];
+          bad |= ((a.flags[bj + p] ^ a.flags[bi + p]) & AJ_FLAG_BLOCK_START) != 0;
+        }
+      }
+      if (__syncthreads_or(bad)) { equal = false; break; }
+    }
+    if (equal) { result = i; break; }
+  }
+  if (threadIdx.x == 0) a.absorber[j] = result;
+}
+
+__global__ void fill_absorber_kernel(MergeArgs a) {
+  int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < a.n_tl) a.absorber[t] = -1;
+}
+
+// Single workgroup of 1024 threads.
+__global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
+  __shared__ int carry_seg, carry_tok, carry_max;
+  if (threadIdx.x == 0) { carry_seg = 0; carry_tok = 0; carry_max = 0; }
+  __syncthreads();
+  const bool bad = fatal(a);
+  for (int base = 0; base < a.n_tl; base += 1024) {
+    int i = base + threadIdx.x;
+    int surv = 0, len = 0;
+    if (!bad && i < a.n_tl) {
+      surv = a.absorber[i] < 0;
+      len = surv ? (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]) : 0;
+    }
+    int tot_s, tot_l;
+    int is = block_scan_incl<1024>(surv, &tot_s);
+    int il = block_scan_incl<1024>(len, &tot_l);
+    if (i < a.n_tl) {
+      if (surv) {
+        int seg = carry_seg + is - 1;
+        a.tl_seg[i] = seg;
+        a.seg_src[seg] = i;
+        a.cu_seqlens[seg] = carry_tok + il - len;
+        atomicMax(&carry_max, len);
+      } else {
+        a.tl_seg[i] = -1;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) { carry_seg += tot_s; carry_tok += tot_l; }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    a.cu_seqlens[carry_seg] = carry_tok;
+    a.counts[0] = carry_seg;
+    a.counts[1] = carry_tok;
+    a.counts[2] = 0;
+    a.counts[3] = carry_max;
+  }
+}
+
+__global__ void claim_fill_kernel(MergeArgs a) {
+  int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (o < a.counts[1]) a.claim[o] = -1;
+}
+
+// The WG's tokens span timelines [tl_first, tl_last]; find them once.
+AJ_DEV void wg_timeline_range(const MergeArgs &a, int64_t u0, int *lo, int *hi) {
+  __shared__ int r[2];
+  if (threadIdx.x == 0) {
+    int64_t u1 = u0 + blockDim.x - 1;
+    if (u1 >= a.n_tok) u1 = a.n_tok - 1;
+    r[0] = find_timeline(a.tl_tok_off, a.n_tl, u0, 0, a.n_tl - 1);
+    r[1] = find_timeline(a.tl_tok_off, a.n_tl, u1, r[0], a.n_tl - 1);
+  }
+  __syncthreads();
+  *lo = r[0];
+  *hi = r[1];
+}
+
+__global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
+  if (fatal(a)) return;
+  const int64_t u0 = (int64_t)blockIdx.x * blockDim.x;
+  int lo, hi;
+  wg_timeline_range(a, u0, &lo, &hi);
+  const int64_t u = u0 + threadIdx.x;
+  if (u >= a.n_tok) return;
+  const int i = find_timeline(a.tl_tok_off, a.n_tl, u, lo, hi);
+  const int s = a.absorber[i];
+  if (s < 0) return;
+  if ((a.flags[u] & AJ_AUTHOR_MASK) != AJ_AUTHOR_LLM) return;
+  const int64_t p = u - a.tl_tok_off[i];
+  atomicMax(&a.claim[a.cu_seqlens[a.tl_seg[s]] + p], i);
+}
+
+__global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claims) {
+  if (fatal(a)) return;
+  const int64_t u0 = (int64_t)blockIdx.x * blockDim.x;
+  int lo, hi;
+  wg_timeline_range(a, u0, &lo, &hi);
+  const int64_t u = u0 + threadIdx.x;
+  if (u >= a.n_tok) return;
+  const int i = find_timeline(a.tl_tok_off, a.n_tl, u, lo, hi);
+  const uint8_t f = a.flags[u];
+  if ((f & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK) raise(a, AJ_DEVERR_BAD_FLAGS);
+  if (a.absorber[i] >= 0) return;
+  const int64_t p = u - a.tl_tok_off[i];
+  const int64_t o = a.cu_seqlens[a.tl_seg[i]] + p;
+  int64_t src = -1;
+  if ((f & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM) {
+    src = u;
+  } else if (use_claims) {
+    int c = a.claim[o];
+    if (c >= 0) src = a.tl_tok_off[c] + p;
+  }
+  a.otok[o] = a.tok[u];
+  a.opos[o] = (int32_t)p;
+  a.omask[o] = src >= 0;
+  a.olp[o] = src >= 0 ? a.old_logprob[src] : 0.f;
+  a.oadv[o] = src >= 0 ? a.adv[src] : 0.f;
+}
+
+AJ_DEV int is_target(const MergeArgs &a, int64_t o, int64_t n_out) {
+  return o < n_out && a.omask[o] && a.opos[o] != 0;
+}
+
+__global__ __launch_bounds__(kBlock) void tgt_count_kernel(MergeArgs a) {
+  const int64_t n_out = fatal(a) ? 0 : a.counts[1];
+  const int64_t o0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
+  int c = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) c += is_target(a, o0 + r, n_out);
+  int tot;
+  block_scan_incl<kBlock>(c, &tot);
+  if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunks) {
+  __shared__ int carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int base = 0; base < n_chunks; base += 1024) {
+    int c = base + threadIdx.x;
+    int v = c < n_chunks ? a.chunk_cnt[c] : 0;
+    int tot;
+    int incl = block_scan_incl<1024>(v, &tot);
+    if (c < n_chunks) a.chunk_off[c] = carry + incl - v;
+    __syncthreads();
+    if (threadIdx.x == 0) carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.counts[2] = carry;
+}
+
+__global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
+  const int64_t n_out = fatal(a) ? 0 : a.counts[1];
+  const int64_t o0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
+  int f[4], c = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) { f[r] = is_target(a, o0 + r, n_out); c += f[r]; }
+  int tot;
+  int incl = block_scan_incl<kBlock>(c, &tot);
+  int w = a.chunk_off[blockIdx.x] + incl - c;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    if (f[r]) a.targets[w++] = (int32_t)(o0 + r);
+}
+
+__global__ void cu_targets_kernel(MergeArgs a) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n_seg = a.counts[0];
+  if (s > n_seg) return;
+  const int n_mask = (int)a.counts[2];
+  const int key = a.cu_seqlens[s];
+  int lo = 0, hi = n_mask;          // first target >= key
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if (a.targets[mid] < key) lo = mid + 1; else hi = mid;
+  }
+  a.cu_targets[s] = lo;
+}
+
+struct MergeWs {
+  int32_t *status, *tl_seg, *claim, *chunk_cnt, *chunk_off;
+  size_t bytes;
+};
+
+MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok) {
+  aj::Carver c(ws);
+  MergeWs w;
+  int64_t n_chunks = (n_tok + kChunk - 1) / kChunk;
+  w.status = c.take<int32_t>(4);
+  w.tl_seg = c.take<int32_t>(n_tl > 0 ? n_tl : 1);
+  w.claim = c.take<int32_t>(n_tok > 0 ? n_tok : 1);
+  w.chunk_cnt = c.take<int32_t>(n_chunks > 0 ? n_chunks : 1);
+  w.chunk_off = c.take<int32_t>(n_chunks > 0 ? n_chunks : 1);
+  w.bytes = c.bytes();
+  return w;
+}
+
+int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t ws_bytes,
+        void *stream, bool merge) {
+  const char *name = merge ? "aj_merge_timelines" : "aj_flatten_timelines";
+  AJ_REQUIRE(in && out, AJ_ERR_NULL, "%s: null argument struct", name);
+  AJ_REQUIRE(in->n_traj >= 0 && in->n_tl >= 0 && in->n_tok >= 0 && in->n_tok < (int64_t)1 << 31,
+             AJ_ERR_SHAPE, "%s: n_traj=%d n_tl=%d n_tok=%lld out of range", name, in->n_traj,
+             in->n_tl, (long long)in->n_tok);
+  AJ_REQUIRE(in->n_tl == 0 || in->n_traj > 0, AJ_ERR_SHAPE, "%s: timelines without episodes", name);
+  AJ_REQUIRE(in->traj_tl_off && in->tl_tok_off, AJ_ERR_NULL, "%s: null offsets", name);
+  AJ_REQUIRE(in->n_tok == 0 || (in->tok && in->flags && in->old_logprob && in->adv), AJ_ERR_NULL,
+             "%s: null token arrays", name);
+  AJ_REQUIRE(out->absorber || in->n_tl == 0, AJ_ERR_NULL, "%s: null absorber", name);
+  AJ_REQUIRE(out->cu_seqlens && out->seg_src && out->cu_targets && out->counts, AJ_ERR_NULL,
+             "%s: null segment outputs", name);
+  AJ_REQUIRE(in->n_tok == 0 || (out->tok && out->pos && out->mask && out->old_logprob &&
+                                out->adv && out->targets),
+             AJ_ERR_NULL, "%s: null token outputs", name);
+  MergeWs w = carve(ws, in->n_tl, in->n_tok);
+  AJ_REQUIRE(ws, AJ_ERR_NULL, "%s: null workspace", name);
+  AJ_REQUIRE(ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes", name,
+             ws_bytes, w.bytes);
+
+  MergeArgs a;
+  a.n_traj = in->n_traj; a.n_tl = in->n_tl; a.n_tok = in->n_tok;
+  a.traj_tl_off = in->traj_tl_off; a.tl_tok_off = in->tl_tok_off;
+  a.tok = in->tok; a.flags = in->flags; a.old_logprob = in->old_logprob; a.adv = in->adv;
+  a.absorber = out->absorber; a.cu_seqlens = out->cu_seqlens; a.seg_src = out->seg_src;
+  a.cu_targets = out->cu_targets; a.counts = out->counts;
+  a.otok = out->tok; a.opos = out->pos; a.omask = out->mask; a.olp = out->old_logprob;
+  a.oadv = out->adv; a.targets = out->targets;
+  a.status = w.status; a.tl_seg = w.tl_seg; a.claim = w.claim;
+  a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
+
+  hipStream_t s = (hipStream_t)stream;
+  init_status_kernel<<<1, 64, 0, s>>>(a);
+  const int n_val = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
+  validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  if (in->n_tl > 0) {
+    if (merge)
+      find_absorber_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
+    else
+      fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  }
+  resolve_kernel<<<1, 1024, 0, s>>>(a);
+  const int64_t n_chunks = (in->n_tok + kChunk - 1) / kChunk;
+  if (in->n_tok > 0) {
+    const int64_t gtok = (in->n_tok + kBlock - 1) / kBlock;
+    if (merge) {
+      claim_fill_kernel<<<gtok, kBlock, 0, s>>>(a);
+      claim_kernel<<<gtok, kBlock, 0, s>>>(a);
+    }
+    emit_kernel<<<gtok, kBlock, 0, s>>>(a, merge ? 1 : 0);
+    tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  }
+  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks);
+  if (in->n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  cu_targets_kernel<<<(in->n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  return aj::check_launch(name);
+}
+
+}  // namespace
+
+extern "C" size_t aj_merge_workspace_bytes(int32_t n_traj, int32_t n_tl, int64_t n_tok) {
+  (void)n_traj;
+  return carve(nullptr, n_tl, n_tok).bytes;
+}
+
+extern "C" int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws,
+                                  size_t ws_bytes, void *stream) {
+  return run(in, out, err, ws, ws_bytes, stream, true);
+}
+
+extern "C" int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
+                                    void *ws, size_t ws_bytes, void *stream) {
+  return run(in, out, err, ws, ws_bytes, stream, false);
+}
+
+extern "C" int aj_plan_packs(const int32_t *cu_seqlens, int32_t n_seg, int32_t max_tokens,
+                             int32_t *pack_seg_off, int32_t *n_packs) {
+  AJ_REQUIRE(cu_seqlens && pack_seg_off && n_packs, AJ_ERR_NULL, "aj_plan_packs: null pointer");
+  AJ_REQUIRE(n_seg >= 0 && max_tokens > 0, AJ_ERR_SHAPE, "aj_plan_packs: n_seg=%d max_tokens=%d",
+             n_seg, max_tokens);
+  for (int s = 0; s < n_seg; ++s)
+    AJ_REQUIRE(cu_seqlens[s] <= cu_seqlens[s + 1], AJ_ERR_SHAPE,
+               "aj_plan_packs: cu_seqlens not monotone at %d", s);
+  int np = 0;
+  int s = 0;
+  while (s < n_seg) {
+    pack_seg_off[np++] = s;
+    const int32_t start = cu_seqlens[s];
+    int e = s + 1;
+    while (e < n_seg && cu_seqlens[e + 1] - start <= max_tokens) ++e;
+    s = e;
+  }
+  pack_seg_off[np] = n_seg;
+  *n_packs = np;
+  return AJ_OK;
+}

@@ -1,0 +1,87 @@
+// Internal kernel launchers shared by the block and loss entry points.
+#pragma once
+#include "common.h"
+
+namespace aj {
+
+template <typename T>
+void embed_fwd(const int32_t *tok, int n, const T *emb, int d, int vocab, T *x, int32_t *err,
+               hipStream_t s);
+void embed_bwd(const int32_t *tok, int n, const float *dx, int d, int vocab, float *demb,
+               hipStream_t s);
+
+// out[i] = RMSNorm(x[r]) * g, r = rows ? rows[i] + shift : i; rstd[i] saved.
+template <typename T>
+void rmsnorm_fwd(const T *x, const T *g, int n, int d, float eps, const int32_t *rows, int shift,
+                 T *out, float *rstd, hipStream_t s);
+// Backward of the above; dg += sum over rows (deterministic, via dg_part of
+// rmsnorm_bwd_part_floats floats).  dx / dx_t (either may be null) receive
+// add + d x; with scatter they are indexed by r instead of i.
+size_t rmsnorm_bwd_part_floats(int n, int d);
+template <typename T>
+void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int n, int d,
+                 const int32_t *rows, int shift, int scatter, const float *add, float *dx, T *dx_t,
+                 float *dg_part, float *dg, hipStream_t s);
+
+// Rotate-half RoPE in place on the first n_rot_heads heads of each row (row
+// stride ld); inverse applies the transposed rotation (the backward).
+template <typename T>
+void rope(T *qkv, int n, const int32_t *pos, int n_rot_heads, int ld, int hd, float theta,
+          bool inverse, hipStream_t s);
+
+template <typename T>
+void swiglu_fwd(const T *gu, int n, int F, T *out, hipStream_t s);
+template <typename TI, typename T>
+void swiglu_bwd(const TI *ds, const T *gu, int n, int F, T *dgu, hipStream_t s);
+
+template <typename T>
+void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s);
+void fill_f32(float *p, int64_t n, float v, hipStream_t s);
+void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumulate, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM
+// C[M,N] (op) sum_k A(m,k) B(n,k)
+//   A(m,k) = a_kmajor ? A[m*lda + k] : A[k*lda + m]
+//   B(n,k) = b_kmajor ? B[n*ldb + k] : B[k*ldb + n]
+enum GemmOut { OUT_STORE = 0, OUT_ACCUM_F32 = 1 };
+struct Gemm {
+  int M = 0, N = 0, K = 0;
+  const void *A = nullptr; int64_t lda = 0; bool a_kmajor = true;
+  const void *B = nullptr; int64_t ldb = 0; bool b_kmajor = true;
+  void *C = nullptr; int64_t ldc = 0;
+  bool c_f32 = false;          // C element type: float32, else the input type
+  int out = OUT_STORE;         // OUT_ACCUM_F32: C (float32) += A B
+  const void *R = nullptr;     // optional residual, same type/ld as C: C = A B + R
+  int split_k = 1;             // > 1: partial sums in `partial`, reduced in fixed order
+  float *partial = nullptr;    // split_k * M * N floats (OUT_ACCUM_F32 or c_f32 only)
+};
+template <typename T>
+int gemm(const Gemm &g, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  int n_tok, n_seg, Hq, Hkv, hd;
+  int base;             // cu_seqlens values are row offsets + base
+  const int32_t *cu_seqlens;
+  const void *qkv;      // [n_tok, (Hq+2Hkv)*hd], q and k already rotated
+  void *o;              // [n_tok, Hq*hd]
+  float *lse;           // [Hq, n_tok]
+  float scale;
+};
+template <typename T>
+int attn_fwd(const AttnArgs &a, hipStream_t s);
+
+struct AttnBwdArgs {
+  int n_tok, n_seg, Hq, Hkv, hd;
+  int base;
+  const int32_t *cu_seqlens;
+  const void *qkv, *o, *dout;
+  const float *lse;
+  float *delta;         // [Hq, n_tok] workspace
+  void *dqkv;           // [n_tok, (Hq+2Hkv)*hd] written
+  float scale;
+};
+template <typename T>
+int attn_bwd(const AttnBwdArgs &a, hipStream_t s);
+
+}  // namespace aj

@@ -1,0 +1,277 @@
+// Row-wise and elementwise kernels of the decoder block and the LM head.
+// All of them are HBM-bound; rows are handled one wavefront (64 lanes) each.
+#include "ops.h"
+
+namespace aj {
+namespace {
+
+constexpr int kRowsPerBlock = 4;   // 4 waves of 64 lanes
+
+AJ_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------- embedding
+template <typename T>
+__global__ __launch_bounds__(256) void embed_fwd_kernel(const int32_t *tok, int n, const T *emb,
+                                                        int d, int vocab, T *x, int32_t *err) {
+  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const int t = tok[row];
+  const bool ok = t >= 0 && t < vocab;
+  if (!ok && lane == 0 && err) atomicOr(err, AJ_DEVERR_TOKEN_RANGE);
+  const T *src = emb + (int64_t)(ok ? t : 0) * d;
+  T *dst = x + (int64_t)row * d;
+  for (int c = lane; c < d; c += 64) dst[c] = ok ? src[c] : T(0);
+}
+
+__global__ __launch_bounds__(256) void embed_bwd_kernel(const int32_t *tok, int n, const float *dx,
+                                                        int d, int vocab, float *demb) {
+  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const int t = tok[row];
+  if (t < 0 || t >= vocab) return;
+  const float *src = dx + (int64_t)row * d;
+  float *dst = demb + (int64_t)t * d;
+  for (int c = lane; c < d; c += 64) atomicAdd(dst + c, src[c]);
+}
+
+// ---------------------------------------------------------------- RMSNorm
+// out[i] = x[r] * rstd * g, r = rows ? rows[i] + row_shift : i
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const T *x, const T *g, int n, int d,
+                                                          float eps, const int32_t *rows,
+                                                          int row_shift, T *out, float *rstd) {
+  const int i = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= n) return;
+  const int64_t r = rows ? (int64_t)rows[i] + row_shift : i;
+  const T *xr = x + r * d;
+  float ss = 0.f;
+  for (int c = lane; c < d; c += 64) {
+    float v = ldf(xr + c);
+    ss += v * v;
+  }
+  ss = wave_sum(ss);
+  const float rs = 1.0f / sqrtf(ss / d + eps);
+  if (lane == 0 && rstd) rstd[i] = rs;
+  T *o = out + (int64_t)i * d;
+  for (int c = lane; c < d; c += 64) stf(o + c, ldf(xr + c) * rs * ldf(g + c));
+}
+
+// dx = add + rstd * (g*dy - x * rstd^2 * mean(g*dy*x)).
+// Input row i reads x row r (gather as in the forward); output row i goes to
+// out row r when scatter is set, else row i.  Each wave walks a fixed set of
+// rows and keeps its share of dg = sum_rows dy*x*rstd in registers; the
+// per-wave partial rows are summed in a fixed order afterwards.
+constexpr int kBwdMaxCols = 128;   // d <= 64 * 128
+constexpr int kBwdBlocks = 256;
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(
+    const float *dy, const T *x, const float *rstd, const T *g, int n, int d,
+    const int32_t *rows, int row_shift, int scatter, const float *add, float *dx, T *dx_t,
+    float *dg_part) {
+  const int gw = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int nw = gridDim.x * kRowsPerBlock;
+  const int lane = threadIdx.x & 63;
+  float acc[kBwdMaxCols];
+#pragma unroll
+  for (int j = 0; j < kBwdMaxCols; ++j) acc[j] = 0.f;
+  for (int i = gw; i < n; i += nw) {
+    const int64_t r = rows ? (int64_t)rows[i] + row_shift : i;
+    const int64_t o = scatter ? r : i;
+    const float *dyr = dy + (int64_t)i * d;
+    const T *xr = x + r * d;
+    const float rs = rstd[i];
+    float dot = 0.f;
+    for (int c = lane; c < d; c += 64) dot += dyr[c] * ldf(g + c) * ldf(xr + c);
+    dot = wave_sum(dot) / d;
+#pragma unroll
+    for (int j = 0; j < kBwdMaxCols; ++j) {
+      const int c = lane + 64 * j;
+      if (c < d) {
+        const float xv = ldf(xr + c), dv = dyr[c];
+        float v = rs * (ldf(g + c) * dv - xv * rs * rs * dot);
+        if (add) v += add[o * d + c];
+        if (dx) dx[o * d + c] = v;
+        if (dx_t) stf(dx_t + o * d + c, v);
+        acc[j] += dv * xv * rs;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kBwdMaxCols; ++j) {
+    const int c = lane + 64 * j;
+    if (c < d) dg_part[(int64_t)gw * d + c] = acc[j];
+  }
+}
+
+// out[c] += sum_b part[b][c], b ascending (deterministic).
+__global__ void col_reduce_kernel(const float *part, int nb, int d, float *out) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= d) return;
+  float s = 0.f;
+  for (int b = 0; b < nb; ++b) s += part[(int64_t)b * d + c];
+  out[c] += s;
+}
+
+// ---------------------------------------------------------------- RoPE
+// In place on the q and k heads of qkv [n, (Hq+2Hkv)*hd].  Angles are formed
+// in double precision: pos * theta^(-2i/hd) reaches ~7e4 rad.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kernel(T *qkv, int n, const int32_t *pos, int n_rot_heads,
+                                                   int ld, int hd, double log_theta, int inverse) {
+  const int half = hd >> 1;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)n * n_rot_heads * half;
+  if (idx >= total) return;
+  const int i = (int)(idx % half);
+  const int64_t t = idx / half;
+  const int h = (int)(t % n_rot_heads);
+  const int row = (int)(t / n_rot_heads);
+  const double ang = (double)pos[row] * exp(-(2.0 * i / hd) * log_theta);
+  double sd, cd;
+  sincos(ang, &sd, &cd);
+  const float c = (float)cd, s = inverse ? -(float)sd : (float)sd;
+  T *p = qkv + (int64_t)row * ld + (int64_t)h * hd;
+  const float x1 = ldf(p + i), x2 = ldf(p + i + half);
+  stf(p + i, x1 * c - x2 * s);
+  stf(p + i + half, x2 * c + x1 * s);
+}
+
+// ---------------------------------------------------------------- SwiGLU
+template <typename T>
+__global__ __launch_bounds__(256) void swiglu_fwd_kernel(const T *gu, int n, int F, T *s) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * F) return;
+  const int64_t r = idx / F, f = idx % F;
+  const float g = ldf(gu + r * 2 * F + f), u = ldf(gu + r * 2 * F + F + f);
+  stf(s + idx, g / (1.f + __expf(-g)) * u);
+}
+
+template <typename TI, typename T>
+__global__ __launch_bounds__(256) void swiglu_bwd_kernel(const TI *ds, const T *gu, int n, int F,
+                                                         T *dgu) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * F) return;
+  const int64_t r = idx / F, f = idx % F;
+  const float g = ldf(gu + r * 2 * F + f), u = ldf(gu + r * 2 * F + F + f);
+  const float d = ldf(ds + idx);
+  const float sg = 1.f / (1.f + __expf(-g));
+  stf(dgu + r * 2 * F + f, d * u * sg * (1.f + g * (1.f - sg)));
+  stf(dgu + r * 2 * F + F + f, d * g * sg);
+}
+
+template <typename T>
+__global__ void cast_kernel(const float *in, int64_t n, T *out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) stf(out + i, in[i]);
+}
+
+__global__ void fill_kernel(float *p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// out[i] += sum_s part[s][i], s ascending.
+__global__ void splitk_reduce_kernel(const float *part, int S, int64_t n, float *out, int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float v = accumulate ? out[i] : 0.f;
+  for (int s = 0; s < S; ++s) v += part[(int64_t)s * n + i];
+  out[i] = v;
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+template <typename T>
+void embed_fwd(const int32_t *tok, int n, const T *emb, int d, int vocab, T *x, int32_t *err,
+               hipStream_t s) {
+  if (n > 0) embed_fwd_kernel<T><<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(tok, n, emb, d, vocab, x, err);
+}
+void embed_bwd(const int32_t *tok, int n, const float *dx, int d, int vocab, float *demb,
+               hipStream_t s) {
+  if (n > 0) embed_bwd_kernel<<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(tok, n, dx, d, vocab, demb);
+}
+
+template <typename T>
+void rmsnorm_fwd(const T *x, const T *g, int n, int d, float eps, const int32_t *rows, int shift,
+                 T *out, float *rstd, hipStream_t s) {
+  if (n > 0)
+    rmsnorm_fwd_kernel<T><<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(x, g, n, d, eps, rows, shift, out, rstd);
+}
+
+size_t rmsnorm_bwd_part_floats(int n, int d) {
+  (void)n;
+  return (size_t)kBwdBlocks * kRowsPerBlock * d;
+}
+
+template <typename T>
+void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int n, int d,
+                 const int32_t *rows, int shift, int scatter, const float *add, float *dx, T *dx_t,
+                 float *dg_part, float *dg, hipStream_t s) {
+  if (n <= 0) return;
+  unsigned nb = blocks_for(n, kRowsPerBlock);
+  if (nb > (unsigned)kBwdBlocks) nb = kBwdBlocks;
+  rmsnorm_bwd_kernel<T><<<nb, 256, 0, s>>>(dy, x, rstd, g, n, d, rows, shift, scatter, add, dx,
+                                           dx_t, dg_part);
+  col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb * kRowsPerBlock, d, dg);
+}
+
+template <typename T>
+void rope(T *qkv, int n, const int32_t *pos, int n_rot_heads, int ld, int hd, float theta,
+          bool inverse, hipStream_t s) {
+  const int64_t total = (int64_t)n * n_rot_heads * (hd / 2);
+  if (total > 0)
+    rope_kernel<T><<<blocks_for(total, 256), 256, 0, s>>>(qkv, n, pos, n_rot_heads, ld, hd,
+                                                         log((double)theta), inverse ? 1 : 0);
+}
+
+template <typename T>
+void swiglu_fwd(const T *gu, int n, int F, T *out, hipStream_t s) {
+  const int64_t total = (int64_t)n * F;
+  if (total > 0) swiglu_fwd_kernel<T><<<blocks_for(total, 256), 256, 0, s>>>(gu, n, F, out);
+}
+
+template <typename TI, typename T>
+void swiglu_bwd(const TI *ds, const T *gu, int n, int F, T *dgu, hipStream_t s) {
+  const int64_t total = (int64_t)n * F;
+  if (total > 0) swiglu_bwd_kernel<TI, T><<<blocks_for(total, 256), 256, 0, s>>>(ds, gu, n, F, dgu);
+}
+
+template <typename T>
+void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s) {
+  if (n > 0) cast_kernel<T><<<blocks_for(n, 256), 256, 0, s>>>(in, n, out);
+}
+
+void fill_f32(float *p, int64_t n, float v, hipStream_t s) {
+  if (n > 0) fill_kernel<<<blocks_for(n, 256), 256, 0, s>>>(p, n, v);
+}
+
+void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumulate, hipStream_t s) {
+  if (n > 0) splitk_reduce_kernel<<<blocks_for(n, 256), 256, 0, s>>>(part, S, n, out, accumulate ? 1 : 0);
+}
+
+#define AJ_INST(T)                                                                              \
+  template void embed_fwd<T>(const int32_t *, int, const T *, int, int, T *, int32_t *,       \
+                             hipStream_t);                                                     \
+  template void rmsnorm_fwd<T>(const T *, const T *, int, int, float, const int32_t *, int, T *, \
+                               float *, hipStream_t);                                          \
+  template void rmsnorm_bwd<T>(const float *, const T *, const float *, const T *, int, int,    \
+                               const int32_t *, int, int, const float *, float *, T *, float *, \
+                               float *, hipStream_t);                                          \
+  template void rope<T>(T *, int, const int32_t *, int, int, int, float, bool, hipStream_t);    \
+  template void swiglu_fwd<T>(const T *, int, int, T *, hipStream_t);                           \
+  template void swiglu_bwd<float, T>(const float *, const T *, int, int, T *, hipStream_t);     \
+  template void cast_from_f32<T>(const float *, int64_t, T *, hipStream_t);
+AJ_INST(float)
+AJ_INST(bf16_t)
+template void swiglu_bwd<bf16_t, bf16_t>(const bf16_t *, const bf16_t *, int, int, bf16_t *, hipStream_t);
+
+}  // namespace aj

@@ -1,0 +1,94 @@
+"""The C-ABI library: loads, exports every symbol include/aj.h declares, and its
+host-side logic (argument validation, pack planning) works without a GPU."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    from paper_2606_04484_amd import capi
+    if not os.path.exists(capi.LIB_PATH):
+        from paper_2606_04484_amd.build import build
+        build()
+    return capi
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "aj.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(aj_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    capi = _lib()
+    names = _declared()
+    assert len(names) >= 17
+    raw = C.CDLL(capi.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+        assert n in capi.EXPORTS, f"{n} missing from the Python binding"
+
+
+def test_status_strings():
+    capi = _lib()
+    L = capi.lib()
+    assert L.aj_status_str(0) == b"ok"
+    assert L.aj_status_str(4) == b"workspace too small"
+
+
+def test_plan_packs_greedy_in_order():
+    capi = _lib()
+    lens = np.array([5, 7, 3, 10, 1, 1, 12, 4])
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    offs = capi.aj_plan_packs(cu, 12)
+    # greedy: [5,7] [3] [10,1,1] [12] [4] -- a segment never splits; packs <= 12 tokens
+    assert offs == [0, 2, 3, 6, 7, 8]
+    offs = capi.aj_plan_packs(cu, 8)   # 10 and 12 exceed the limit: alone in their packs
+    assert offs == [0, 1, 2, 3, 4, 6, 7, 8]
+
+
+def test_plan_packs_rejects_bad_offsets():
+    capi = _lib()
+    cu = torch.tensor([0, 5, 3], dtype=torch.int32)
+    with pytest.raises(capi.AjError, match="monotone"):
+        capi.aj_plan_packs(cu, 16)
+
+
+def test_host_validation_needs_no_gpu():
+    """Argument errors return before any HIP call."""
+    capi = _lib()
+    L = capi.lib()
+    assert L.aj_merge_timelines(None, None, None, None, 0, None) == 1   # AJ_ERR_NULL
+    tl = capi.Timelines(1, 1, -5, None, None, None, None, None, None)
+    out = capi.Packed()
+    assert L.aj_merge_timelines(C.byref(tl), C.byref(out), None, None, 0, None) == 2
+    cfg = capi.BlockCfg(128, 4, 3, 32, 512, 1e-6, 1e6, 0)      # 4 % 3 != 0
+    w = capi.BlockWeights(*[C.c_void_p(16)] * 6)
+    vl = capi.Varlen(0, 0, 0, 0, None, None)
+    assert L.aj_varlen_block_fwd(C.byref(cfg), C.byref(w), C.byref(vl), None, None, None, None,
+                                 0, None) == 2
+    cfg = capi.BlockCfg(128, 4, 4, 256, 512, 1e-6, 1e6, 0)     # head_dim 256 unsupported
+    assert L.aj_varlen_block_fwd(C.byref(cfg), C.byref(w), C.byref(vl), None, None, None, None,
+                                 0, None) == 3
+    assert b"head_dim" in L.aj_last_error()
+    lc = capi.LossCfg(128, 1024, 1024, 0.2, 1e-6, 0)
+    li = capi.LossIn(10, 11, 0, None, None, None, None, 1.0)      # n_tgt > n_tok
+    assert L.aj_logprob_pg_loss_fwd(C.byref(lc), C.byref(li), *([None] * 9), 0, None) == 2
+
+
+def test_workspace_queries_grow_with_size():
+    capi = _lib()
+    L = capi.lib()
+    cfg = capi.BlockCfg(3584, 28, 4, 128, 18944, 1e-6, 1e6, 1)
+    a = L.aj_block_saved_bytes(C.byref(cfg), 1000)
+    b = L.aj_block_saved_bytes(C.byref(cfg), 2000)
+    assert 0 < a < b
+    # ~150 KB of saved activations per token at the 7B block shape
+    assert 140e3 < b / 2000 < 160e3
+    assert capi.aj_merge_workspace_bytes(4, 32, 5000) > 5000 * 4

@@ -1,0 +1,103 @@
+"""GPU merge / flatten against the oracle: bit-exact on every output array.
+
+Covers the hand-worked golden cases, all five seeded workloads at full size
+(merged and unmerged layouts), an empty batch, and offsets that do not tile
+the token range (reported through the device error word, every count 0).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import merge as om
+from workloads import get_config, make_timelines
+from tests.cases import golden_merge_cases, case_to_flat
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(tl, old, merged=True):
+    from paper_2606_04484_amd import actor
+    dev = actor.upload_timelines(tl, old)
+    m = actor.Merger(dev)
+    m.launch(merged)
+    L = m.layout(pack_tokens=1 << 30)
+    torch.cuda.synchronize()
+    return m, L
+
+
+def _check(tl, old, merged):
+    eps = om.episodes_from_flat(tl.traj_tl_off, tl.tl_tok_off, tl.tok, tl.flags, old, tl.adv)
+    if merged:
+        ref, absorbers = om.merge_batch(eps)
+    else:
+        ref, absorbers = om.unmerged_batch(eps), [[-1] * len(e) for e in eps]
+    m, L = _run(tl, old, merged)
+    o = {k: v.cpu().numpy() for k, v in m.out.items()}
+    n_tl = tl.n_tl
+    glob = []
+    for e, ab in enumerate(absorbers):
+        base = int(tl.traj_tl_off[e])
+        glob.extend(a + base if a >= 0 else -1 for a in ab)
+    np.testing.assert_array_equal(o["absorber"][:n_tl], glob)
+    assert L.n_seg == ref.n_seg and L.n_tok == ref.n_tok
+    np.testing.assert_array_equal(o["cu_seqlens"][:L.n_seg + 1], ref.cu_seqlens)
+    surv = [i for i, a in enumerate(glob) if a == -1]
+    np.testing.assert_array_equal(o["seg_src"][:L.n_seg], surv)
+    n = ref.n_tok
+    np.testing.assert_array_equal(o["tok"][:n], ref.tok)
+    np.testing.assert_array_equal(o["pos"][:n], ref.pos)
+    np.testing.assert_array_equal(o["mask"][:n], ref.mask)
+    np.testing.assert_array_equal(o["old_logprob"][:n].astype(np.float64), ref.old_logprob)
+    np.testing.assert_array_equal(o["adv"][:n].astype(np.float64), ref.adv)
+    tgt = np.flatnonzero((ref.mask == 1) & (ref.pos != 0))
+    assert L.n_mask == len(tgt)
+    np.testing.assert_array_equal(o["targets"][:len(tgt)], tgt)
+    np.testing.assert_array_equal(o["cu_targets"][:L.n_seg + 1],
+                                  np.searchsorted(tgt, ref.cu_seqlens, side="left"))
+    lens = np.diff(ref.cu_seqlens)
+    assert L.max_seqlen == (int(lens.max()) if len(lens) else 0)
+    assert m.device_error() == 0
+
+
+@pytest.mark.parametrize("case", golden_merge_cases(), ids=lambda c: c["name"])
+def test_golden(case):
+    tl, lp = case_to_flat(case)
+    _check(tl, lp, merged=True)
+    _check(tl, lp, merged=False)
+
+
+@pytest.mark.parametrize("cfg_id", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("merged", [True, False])
+def test_full_workloads(cfg_id, merged):
+    tl = make_timelines(get_config(cfg_id))
+    print(f"merge parity cfg={cfg_id} merged={merged} n_tok={tl.n_tok}", flush=True)
+    _check(tl, tl.lp_noise, merged)
+
+
+def test_deterministic():
+    tl = make_timelines(get_config(3))
+    a, La = _run(tl, tl.lp_noise)
+    b, Lb = _run(tl, tl.lp_noise)
+    valid = {"absorber": tl.n_tl, "cu_seqlens": La.n_seg + 1, "seg_src": La.n_seg,
+             "cu_targets": La.n_seg + 1, "counts": 4, "targets": La.n_mask}
+    for k in a.out:
+        n = valid.get(k, La.n_tok)      # per-token outputs: the merged length
+        assert torch.equal(a.out[k][:n], b.out[k][:n]), k
+
+
+def test_empty_batch():
+    from workloads.gen import Timelines
+    tl = Timelines(np.zeros(1, np.int32), np.zeros(1, np.int64), np.zeros(0, np.int32),
+                   np.zeros(0, np.uint8), np.zeros(0, np.float32), np.zeros(0, np.float32))
+    m, L = _run(tl, np.zeros(0, np.float32))
+    assert (L.n_seg, L.n_tok, L.n_mask) == (0, 0, 0) and L.packs == []
+
+
+def test_offsets_not_tiling_are_reported():
+    tl = make_timelines(get_config(0))
+    tl.tl_tok_off = tl.tl_tok_off.copy()
+    tl.tl_tok_off[5], tl.tl_tok_off[6] = tl.tl_tok_off[6], tl.tl_tok_off[5]   # not monotone
+    m, L = _run(tl, tl.lp_noise)
+    from paper_2606_04484_amd.capi import lib  # noqa: F401
+    assert m.device_error() & 8
+    assert (L.n_seg, L.n_tok, L.n_mask) == (0, 0, 0)
