@@ -1,0 +1,206 @@
+#!/usr/bin/env python
+"""Merged actor-update benchmark on one MI355X.
+
+A step is one whole actor update over one batch of synthetic trajectories:
+timeline merging -> (per pack of <= 131072 tokens) embedding, decoder-block
+forward, fused LM-head / clipped policy-gradient loss forward and backward,
+block backward, embedding backward.  Inputs sit in HBM before timing starts.
+The same batch is also run unmerged (every LLM call its own sample) for the
+merged-vs-unmerged speedup.  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="1", help="workload index (0..4) or name")
+    ap.add_argument("--no-unmerged", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=0)
+    return ap.parse_args()
+
+
+def attention_flops(cu, m):
+    """Causal attention, fwd + bwd (bwd = 2.5 x fwd; recompute not credited)."""
+    L = np.diff(np.asarray(cu, np.float64))
+    fwd = 2.0 * m.head_dim * m.n_q_heads * np.sum(L * (L + 1))
+    return 3.5 * fwd, fwd
+
+
+def step_flops(L, m):
+    blk = 6.0 * m.block_params() * L.n_tok
+    lm = 6.0 * m.d_model * m.vocab * L.n_mask
+    att, att_fwd = attention_flops(L.cu_host, m)
+    return blk, lm, att, att_fwd
+
+
+def timed(A, merger, merged, steps, warmup, torch, capi, record=False):
+    L = None
+    for _ in range(warmup):
+        A.zero_grads()
+        merger.launch(merged)
+        L = merger.layout(A.m.pack_tokens)
+        A.step(L)
+    torch.cuda.synchronize()
+    if record:
+        capi.aj_timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        A.zero_grads()
+        merger.launch(merged)
+        L = merger.layout(A.m.pack_tokens)
+        A.step(L)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    rec = None
+    if record:
+        rec = capi.aj_timing_read()
+        capi.aj_timing_enable(False)
+    return L, dt, rec
+
+
+def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
+    """The oracle, as is, on a bounded sample of the same workload: the first
+    episode, merged by the oracle, its first segment cut to `sample_tokens`."""
+    from threadpoolctl import threadpool_info
+    from oracle import merge as om
+    from oracle import model as M
+    sub = tl.subset([0])
+    n0 = sub.n_tok
+    eps = om.episodes_from_flat(sub.traj_tl_off, sub.tl_tok_off, sub.tok, sub.flags, old[:n0],
+                                sub.adv)
+    t0 = time.perf_counter()
+    packed, _ = om.merge_batch(eps)
+    t_merge = time.perf_counter() - t0
+    L = min(sample_tokens, int(packed.cu_seqlens[1]))
+    cut = om.Packed([0, L], packed.tok[:L], packed.mask[:L], packed.old_logprob[:L],
+                    packed.adv[:L], packed.pos[:L])
+    W = {k: v.float().cpu().numpy() for k, v in W_dev.items()}
+    t0 = time.perf_counter()
+    M.actor_update(cut, W, cfg.model)
+    t_model = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": L / (t_model + t_merge * L / max(n0, 1)), "unit": "tokens/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"episode 0 of the same batch merged by the oracle ({n0} tokens, "
+                      f"{t_merge:.2f} s), then the float64 actor update on its first {L} "
+                      f"tokens ({t_model:.1f} s); merge time pro-rated to {L} tokens",
+            "host_cpus": os.cpu_count()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                          "(the multi-GPU layout is a design note, not a code path)"}))
+        sys.exit(2)
+    import torch
+    from paper_2606_04484_amd import actor, capi
+    if not os.path.exists(capi.LIB_PATH):
+        from paper_2606_04484_amd.build import build
+        build()
+    from workloads import get_config, make_timelines, make_weights_torch
+
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    m = cfg.model
+    torch.cuda.set_device(0)
+    tl = make_timelines(cfg)
+    W = make_weights_torch(m, seed=1000, device="cuda")
+    # rollout log-probs: the policy's own log-probs (untimed forward of this
+    # path on the unmerged layout) plus the generator's N(0, 0.05) noise
+    dev = actor.upload_timelines(tl, np.zeros(tl.n_tok, np.float32))
+    A = actor.ActorUpdate(m, W)
+    Lu = actor.merge(dev, merged=False, pack_tokens=m.pack_tokens)
+    cur = A.forward_logprob(Lu).float().cpu().numpy()
+    tg = Lu.targets[:Lu.n_mask].cpu().numpy()
+    old = np.zeros(tl.n_tok, np.float32)
+    old[tg] = cur + tl.lp_noise[tg]
+    dev["old_logprob"] = torch.from_numpy(old).cuda()
+    del Lu
+
+    merger = actor.Merger(dev)
+    merger.launch(True)
+    Lm = merger.layout(m.pack_tokens)
+    A.prepare(Lm)
+    Lm, t_m, rec = timed(A, merger, True, args.steps, args.warmup, torch, capi, record=False)
+    _, _, rec = timed(A, merger, True, 1, 0, torch, capi, record=True)
+    stats = A.stats.cpu().numpy()
+    res_u = None
+    if not args.no_unmerged:
+        mu = actor.Merger(dev)
+        mu.launch(False)
+        Lu = mu.layout(m.pack_tokens)
+        A.prepare(Lu)
+        Lu, t_u, _ = timed(A, mu, False, max(1, args.steps // 2), 1, torch, capi)
+        res_u = dict(ms_per_step=t_u * 1e3, tokens=Lu.n_tok, tokens_per_s=Lu.n_tok / t_u,
+                     packs=len(Lu.packs))
+
+    blk, lm, att, att_fwd = step_flops(Lm, m)
+    total = blk + lm + att
+    peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_F32_TFLOPS
+    # per-class kernel times of one timed step (HIP events on the launch stream)
+    classes = {}
+    for k, (ms, n, fl) in rec.items():
+        if k == "attn_fwd":
+            fl = att_fwd
+        elif k == "attn_bwd":
+            fl = att - att_fwd
+        classes[k] = dict(ms=ms, launches=n, tflops=(fl / (ms * 1e-3) / 1e12) if ms > 0 else 0.0)
+    dom = max((k for k in classes if k != "merge"), key=lambda k: classes[k]["ms"])
+    d = classes[dom]
+    fl_dom = {"attn_fwd": att_fwd, "attn_bwd": att - att_fwd}.get(dom, rec[dom][2])
+    roof = {"kernel": dom, "bound": "mfma", "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2),
+            "peak": peak, "unit": "TFLOP/s",
+            "frac": round(fl_dom / (d["ms"] * 1e-3) / 1e12 / peak, 4), "traffic": None,
+            "launches": d["launches"], "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}
+
+    out = {
+        "metric": "merged actor-update tokens/sec/GPU",
+        "value": round(Lm.n_tok / t_m, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t_m * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": m.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "merged_tokens": Lm.n_tok, "unmerged_tokens": tl.n_tok,
+                   "loss_tokens": Lm.n_mask, "segments": Lm.n_seg, "packs": len(Lm.packs),
+                   "pack_tokens": m.pack_tokens, "d_model": m.d_model, "heads": [m.n_q_heads, m.n_kv_heads],
+                   "head_dim": m.head_dim, "d_ff": m.d_ff, "vocab": m.vocab},
+        "effective_tokens_per_s": round(tl.n_tok / t_m, 1),
+        "loss_tokens_per_s": round(Lm.n_mask / t_m, 1),
+        "mfma_util": round(total / t_m / 1e12 / peak, 4),
+        "algorithmic_tflop_per_step": {"block": round(blk / 1e12, 3), "lm_head": round(lm / 1e12, 3),
+                                       "attention": round(att / 1e12, 3)},
+        "kernel_classes": {k: {kk: round(vv, 4) if isinstance(vv, float) else vv
+                               for kk, vv in v.items()} for k, v in classes.items()},
+        "roofline": roof,
+        "loss": float(stats[0]),
+    }
+    if res_u:
+        out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
+        out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)
+    if not args.no_cpu_baseline:
+        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 128)
+        out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -245,6 +245,25 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
                            float *d_final_norm, float *d_w_vocab, void *ws, size_t ws_bytes,
                            void *stream);
 
+/* ------------------------------------------------------------------ timing
+ * Benchmark instrumentation.  While enabled, every launch of the kernel
+ * classes below is bracketed by two hipEvents recorded on the launch's own
+ * stream.  The record is process-wide (the one piece of state the library
+ * keeps besides the error text) and meant for a single-threaded driver.
+ *   AJ_KC_MERGE      one aj_merge_timelines / aj_flatten_timelines call
+ *   AJ_KC_GEMM_*     the MFMA GEMM, by operand layout (NT: both K-major;
+ *                    NN: B N-major; TN: A M-major and B N-major)
+ *   AJ_KC_ATTN_FWD / AJ_KC_ATTN_BWD   the attention kernels of one call
+ * `flops` accumulates algorithmic flops where the library knows them
+ * (2*M*N*K per GEMM launch, 0 for launches that recompute a forward product,
+ * 0 for the other classes). */
+enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
+       AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_COUNT = 6 };
+/* on != 0 starts recording (clearing any earlier record); 0 stops. */
+int aj_timing_enable(int on);
+/* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */
+int aj_timing_read(double *ms, int64_t *launches, double *flops);
+
 #ifdef __cplusplus
 }
 #endif

@@ -104,7 +104,11 @@ EXPORTS = {
                                          vp, vp, vp, vp, vp, sz, vp]),
     "aj_logprob_pg_loss_bwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
                                          vp, vp, vp, vp, vp, vp, sz, vp]),
+    "aj_timing_enable": (C.c_int, [C.c_int]),
+    "aj_timing_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
 }
+
+KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd")
 
 
 def _declare(L):
@@ -286,3 +290,17 @@ def aj_logprob_pg_loss_bwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, f
                                         ptr(dh), ptr(d_final_norm), ptr(d_w_vocab), ptr(ws),
                                         ws.numel() * ws.element_size(), stream_handle(stream)),
            "aj_logprob_pg_loss_bwd")
+
+
+# ------------------------------------------------------------------ timing
+
+def aj_timing_enable(on=True):
+    _check(lib().aj_timing_enable(1 if on else 0), "aj_timing_enable")
+
+
+def aj_timing_read():
+    """{class: (ms, launches, flops)} summed over the launches recorded since enabling."""
+    n = len(KCLASSES)
+    ms, cnt, fl = (C.c_double * n)(), (i64 * n)(), (C.c_double * n)()
+    _check(lib().aj_timing_read(ms, cnt, fl), "aj_timing_read")
+    return {k: (ms[i], int(cnt[i]), fl[i]) for i, k in enumerate(KCLASSES)}

@@ -291,7 +291,9 @@ int attn_fwd(const AttnArgs &a, hipStream_t s) {
   if (a.n_tok <= 0) return AJ_OK;
   if (a.hd > kMaxHd || a.hd % 8) return fail(AJ_ERR_UNSUPPORTED, "attention: head_dim %d", a.hd);
   dim3 grid((a.n_tok + kRows - 1) / kRows, a.Hq);
+  const int tk = timing_begin(s, AJ_KC_ATTN_FWD, 0.0);
   attn_fwd_simple_kernel<T><<<grid, 256, 0, s>>>(a);
+  timing_end(s, tk);
   return check_launch("attention forward");
 }
 
@@ -300,9 +302,11 @@ int attn_bwd(const AttnBwdArgs &a, hipStream_t s) {
   if (a.n_tok <= 0) return AJ_OK;
   if (a.hd > kMaxHd || a.hd % 8) return fail(AJ_ERR_UNSUPPORTED, "attention: head_dim %d", a.hd);
   const int64_t nd = (int64_t)a.n_tok * a.Hq;
+  const int tk = timing_begin(s, AJ_KC_ATTN_BWD, 0.0);
   attn_delta_kernel<T><<<(unsigned)((nd + 3) / 4), 256, 0, s>>>(a);
   attn_dq_simple_kernel<T><<<dim3((a.n_tok + kRows - 1) / kRows, a.Hq), 256, 0, s>>>(a);
   attn_dkv_simple_kernel<T><<<dim3((a.n_tok + kRows - 1) / kRows, a.Hkv), 256, 0, s>>>(a);
+  timing_end(s, tk);
   return check_launch("attention backward");
 }
 

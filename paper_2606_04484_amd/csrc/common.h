@@ -33,6 +33,10 @@ int fail(int status, const char *fmt, ...);
 // Returns AJ_OK or AJ_ERR_HIP (with the HIP error text) after a launch.
 int check_launch(const char *what);
 
+// Benchmark timing (aj_timing_enable): returns a record index or -1 when off.
+int timing_begin(hipStream_t s, int kclass, double flops);
+void timing_end(hipStream_t s, int idx);
+
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Carves aligned sub-buffers out of a caller-provided workspace.

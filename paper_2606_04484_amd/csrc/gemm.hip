@@ -294,9 +294,12 @@ int gemm(const Gemm &g, hipStream_t s) {
            aligned16(g.A) && aligned16(g.B) && !(!g.a_kmajor && g.b_kmajor);
   }
   if (mfma) {
+    const int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
+    const int tk = timing_begin(s, kc, g.recompute ? 0.0 : 2.0 * g.M * g.N * (double)g.K);
     if (g.a_kmajor && g.b_kmajor) launch_mfma<CfgBig, true, true>(g, ep, kps, s);
     else if (g.a_kmajor) launch_mfma<CfgBig, true, false>(g, ep, kps, s);
     else launch_mfma<CfgBig, false, false>(g, ep, kps, s);
+    timing_end(s, tk);
   } else {
     dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, S);
     gemm_simple_kernel<T><<<grid, 256, 0, s>>>(g.M, g.N, g.K, kps, (const T *)g.A, g.lda,

@@ -212,8 +212,9 @@ int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
 
 template <typename T>
 int chunk_logits(const aj_loss_cfg &c, int n_tgt, const void *hn, const void *w_vocab, int c0,
-                 int cw, float *z, hipStream_t st) {
+                 int cw, float *z, hipStream_t st, bool recompute) {
   aj::Gemm g;
+  g.recompute = recompute;
   g.M = n_tgt; g.N = cw; g.K = c.d_model;
   g.A = hn; g.lda = c.d_model;
   g.B = (const T *)w_vocab + (int64_t)c0 * c.d_model; g.ldb = c.d_model;
@@ -233,7 +234,7 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   loss_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.run_m, w.run_s, w.zt);
   for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
-    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st);
+    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, false);
     if (r) return r;
     lse_update_kernel<<<(n + 3) / 4, 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok, c.vocab,
                                                   w.run_m, w.run_s, w.zt, err);
@@ -261,7 +262,7 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   aj::fill_f32(w.dhn, (int64_t)n * d, 0.f, st);
   for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
-    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st);
+    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true);
     if (r) return r;
     const int64_t tot = (int64_t)n * cw;
     dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok,

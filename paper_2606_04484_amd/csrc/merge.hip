@@ -387,6 +387,7 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
   a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
 
   hipStream_t s = (hipStream_t)stream;
+  const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
   init_status_kernel<<<1, 64, 0, s>>>(a);
   const int n_val = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
   validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
@@ -410,6 +411,7 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks);
   if (in->n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   cu_targets_kernel<<<(in->n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  aj::timing_end(s, tk);
   return aj::check_launch(name);
 }
 

@@ -54,6 +54,7 @@ struct Gemm {
   const void *R = nullptr;     // optional residual, same type/ld as C: C = A B + R
   int split_k = 1;             // > 1: partial sums in `partial`, reduced in fixed order
   float *partial = nullptr;    // split_k * M * N floats (OUT_ACCUM_F32 or c_f32 only)
+  bool recompute = false;      // recomputes a forward product: no algorithmic flops
 };
 template <typename T>
 int gemm(const Gemm &g, hipStream_t s);
