@@ -6,7 +6,8 @@
 //
 // These kernels use float FMA with 4 threads per query row (a quarter of the
 // head dimension each) and stream keys through LDS; they serve the float32
-// workload and every head_dim.
+// workload and head dims other than 64 and 128.  bfloat16 with head_dim 64 or
+// 128 goes to the MFMA kernels in attention_mfma.hip.
 #include "ops.h"
 
 namespace aj {
@@ -290,6 +291,7 @@ template <typename T>
 int attn_fwd(const AttnArgs &a, hipStream_t s) {
   if (a.n_tok <= 0) return AJ_OK;
   if (a.hd > kMaxHd || a.hd % 8) return fail(AJ_ERR_UNSUPPORTED, "attention: head_dim %d", a.hd);
+  if (sizeof(T) == 2 && attn_mfma_supported(a.hd, a.qkv, a.o, a.o)) return attn_fwd_mfma(a, s);
   dim3 grid((a.n_tok + kRows - 1) / kRows, a.Hq);
   const int tk = timing_begin(s, AJ_KC_ATTN_FWD, 0.0);
   attn_fwd_simple_kernel<T><<<grid, 256, 0, s>>>(a);
@@ -301,6 +303,7 @@ template <typename T>
 int attn_bwd(const AttnBwdArgs &a, hipStream_t s) {
   if (a.n_tok <= 0) return AJ_OK;
   if (a.hd > kMaxHd || a.hd % 8) return fail(AJ_ERR_UNSUPPORTED, "attention: head_dim %d", a.hd);
+  if (sizeof(T) == 2 && attn_mfma_supported(a.hd, a.qkv, a.dout, a.dqkv)) return attn_bwd_mfma(a, s);
   const int64_t nd = (int64_t)a.n_tok * a.Hq;
   const int tk = timing_begin(s, AJ_KC_ATTN_BWD, 0.0);
   attn_delta_kernel<T><<<(unsigned)((nd + 3) / 4), 256, 0, s>>>(a);

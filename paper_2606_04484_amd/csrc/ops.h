@@ -85,4 +85,9 @@ struct AttnBwdArgs {
 template <typename T>
 int attn_bwd(const AttnBwdArgs &a, hipStream_t s);
 
+// bfloat16 MFMA flash attention (head_dim 64 or 128, 16-byte aligned tensors)
+bool attn_mfma_supported(int hd, const void *p0, const void *p1, const void *p2);
+int attn_fwd_mfma(const AttnArgs &a, hipStream_t s);
+int attn_bwd_mfma(const AttnBwdArgs &a, hipStream_t s);
+
 }  // namespace aj

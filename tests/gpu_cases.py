@@ -22,9 +22,10 @@ def bf16_case_model(hd=64, d=256, hq=4, hkv=2, ff=512, vocab=2000, chunk=768):
                        vocab=vocab, dtype="bf16", vocab_chunk=chunk)
 
 
-def workload(model, n_traj=8, seed=0):
-    """The small trajectory recipe (8 x 4 calls, one rewrite each) on `model`."""
-    return dataclasses.replace(get_config(0), model=model, n_traj=n_traj, seed=seed)
+def workload(model, n_traj=8, seed=0, **kw):
+    """The small trajectory recipe (8 x 4 calls, one rewrite each) on `model`;
+    keyword arguments override fields of the recipe."""
+    return dataclasses.replace(get_config(0), model=model, n_traj=n_traj, seed=seed, **kw)
 
 
 def episodes(tl, old):

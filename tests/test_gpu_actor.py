@@ -74,16 +74,27 @@ def test_bf16(name, merged):
     check(case, run_gpu(case, merged), merged, 2e-2, 1e-2, 1e-2, 0.999)
 
 
+def test_bf16_long_segments():
+    """Segments of 2-4k tokens: many key tiles, GQA group of 4, causal edges mid-tile."""
+    m = bf16_case_model(hd=128, d=256, hq=4, hkv=1, ff=512, vocab=1000, chunk=512)
+    cfg = workload(m, n_traj=2, turns=(6, 6), prompt=(1500, 1500), resp=(100, 300),
+                   obs=(100, 300), one_rewrite=True)
+    case = Case(cfg, noise_std=0.3, margin=0.05)
+    print(f"bf16 long segments: {np.diff(case.merged.cu_seqlens)}", flush=True)
+    check(case, run_gpu(case, True), True, 2e-2, 1e-2, 1e-2, 0.999)
+
+
 def test_bf16_small_packs():
-    """Many packs (segments never split) give the same result as one."""
+    """Many packs (segments never split) give the same result as one, up to the
+    bfloat16 rounding that moves with where a segment's key tiles start."""
     m = bf16_case_model(**BF16_CASES["hd64_gqa2"])
     case = Case(workload(m), noise_std=0.3, margin=0.05)
     a = run_gpu(case, True, pack_tokens=131072)
     b = run_gpu(case, True, pack_tokens=700)
     assert len(b["L"].packs) > 3
-    np.testing.assert_allclose(a["lp"], b["lp"], atol=1e-6)
+    np.testing.assert_allclose(a["lp"], b["lp"], atol=1e-2)
     for k in GRADS:
-        assert rel_l2(b["grads"][k], a["grads"][k]) < 1e-5, k
+        assert rel_l2(b["grads"][k], a["grads"][k]) < 5e-3, k
 
 
 def test_merged_equals_unmerged_on_gpu():
