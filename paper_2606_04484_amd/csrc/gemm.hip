@@ -57,7 +57,9 @@ struct MfmaCfg {
 // through registers into LDS laid out [R][LDK].
 template <int R, int BK, int LDK, int NT, bool KMAJOR>
 struct Stager {
-  // K-major: 16-byte vectors of 8 k's; MN-major: 4 k-rows x 8 rows per slot.
+  // K-major: 16-byte vectors of 8 k's; MN-major: 4 k-rows x 8 rows per slot,
+  // k-blocks varying fastest across threads so that the transposed 8-byte LDS
+  // stores of a wave spread over all banks (2 lanes per bank pair).
   static constexpr int kSlots = KMAJOR ? R * BK / 8 : (R / 8) * (BK / 4);
   static constexpr int kPer = (kSlots + NT - 1) / NT;
   static constexpr int kVec = KMAJOR ? 1 : 4;
@@ -75,7 +77,7 @@ struct Stager {
         else
           v[i][0] = u32x4_t{0, 0, 0, 0};
       } else {
-        const int rb = slot % (R / 8), kb = slot / (R / 8);
+        const int kb = slot % (BK / 4), rb = slot / (BK / 4);
         const int r = r0 + rb * 8;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
@@ -98,7 +100,7 @@ struct Stager {
         const int row = slot / (BK / 8), kv = slot % (BK / 8);
         *(u32x4_t *)(lds + row * LDK + kv * 8) = v[i][0];
       } else {
-        const int rb = slot % (R / 8), kb = slot / (R / 8);
+        const int kb = slot % (BK / 4), rb = slot / (BK / 4);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const int w = e >> 1, sh = (e & 1) * 16;
@@ -112,7 +114,7 @@ struct Stager {
 };
 
 template <typename Cfg, bool A_K, bool B_K>
-__global__ __launch_bounds__(Cfg::NT) void gemm_mfma_kernel(
+__global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, LDK = Cfg::LDK, NT = Cfg::NT;
@@ -166,10 +168,12 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < Cfg::TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) {
-      sa.store(As[buf ^ 1]);
-      sb.store(Bs[buf ^ 1]);
+      // the other buffer was last read before the previous barrier: fill it
+      // while this one is still being consumed
+      if (kk == BK / 2 - 16 && kt + 1 < nk) {
+        sa.store(As[buf ^ 1]);
+        sb.store(Bs[buf ^ 1]);
+      }
     }
     __syncthreads();
   }
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(int M, int N, int K, i
     }
 }
 
-using CfgBig = MfmaCfg<128, 128, 64, 2, 2>;
+using CfgBig = MfmaCfg<256, 256, 64, 2, 4>;
 
 template <typename Cfg, bool A_K, bool B_K>
 void launch_mfma(const Gemm &g, const EpArgs &ep, int kps, hipStream_t s) {
