@@ -1,10 +1,11 @@
 // GEMMs of the block and the LM head.
 //
 // bfloat16: v_mfma_f32_32x32x16_bf16 tiles, float32 accumulation, LDS
-// double-buffered.  Both operands are kept in LDS as [row][k] (k contiguous):
-// a K-major operand is copied as is, an M/N-major one (the weight-gradient
-// GEMMs read activations [tokens, features]) is transposed in registers on
-// its way from HBM to LDS, 4 k-rows x 8 columns per thread.  Workgroup ids are
+// double-buffered, 256x256x64 workgroup tiles on 8 waves (128x64 per wave).
+// Operands are copied into LDS in their memory order: a K-major one as
+// [row][k], an M/N-major one (the weight-gradient GEMMs read activations
+// [tokens, features]) as [k][row], whose MFMA fragments come out of LDS
+// already transposed through ds_read_tr16_b64.  Workgroup ids are
 // remapped so that each XCD (ids are dealt round-robin over the 8 XCDs) walks
 // a contiguous, row-grouped run of tiles and its L2 sees the reuse.
 //
@@ -49,45 +50,33 @@ struct MfmaCfg {
   static constexpr int NT = WM * WN * 64;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int TM = WTM / 32, TN = WTN / 32;
-  static constexpr int LDK = BK + 8;            // padded LDS row (bf16 elements)
   static_assert(WTM % 32 == 0 && WTN % 32 == 0 && BK % 16 == 0, "tile shape");
 };
 
-// Stages one operand tile (rows [r0, r0+R) of the operand, k in [k0, k0+BK))
-// through registers into LDS laid out [R][LDK].
-template <int R, int BK, int LDK, int NT, bool KMAJOR>
+// Stages one operand tile through registers into LDS.
+//   K-major operand (rows r, k contiguous): LDS [R][BK + 8], 16-byte vectors.
+//   M/N-major operand (k rows, r contiguous): copied untransposed into LDS
+//   [BK][R + 32]; the MFMA fragments are then read with ds_read_tr16_b64.
+template <int R, int BK, int NT, bool KMAJOR>
 struct Stager {
-  // K-major: 16-byte vectors of 8 k's; MN-major: 4 k-rows x 8 rows per slot,
-  // k-blocks varying fastest across threads so that the transposed 8-byte LDS
-  // stores of a wave spread over all banks (2 lanes per bank pair).
-  static constexpr int kSlots = KMAJOR ? R * BK / 8 : (R / 8) * (BK / 4);
+  static constexpr int LD = KMAJOR ? BK + 8 : R + 32;    // LDS row pitch (bf16 elements)
+  static constexpr int kSlots = R * BK / 8;
   static constexpr int kPer = (kSlots + NT - 1) / NT;
-  static constexpr int kVec = KMAJOR ? 1 : 4;
-  u32x4_t v[kPer][kVec];
+  static constexpr int kBytes = (KMAJOR ? R * LD : BK * LD) * 2;
+  u32x4_t v[kPer];
 
   AJ_DEV void load(const bf16_t *X, int64_t ld, int r0, int rows, int k0, int K) {
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int slot = threadIdx.x + i * NT;
-      if (KMAJOR) {
-        const int row = slot / (BK / 8), kv = slot % (BK / 8);
-        const int r = r0 + row, k = k0 + kv * 8;
-        if (slot < kSlots && r < rows && k < K)
-          v[i][0] = *(const u32x4_t *)(X + (int64_t)r * ld + k);
-        else
-          v[i][0] = u32x4_t{0, 0, 0, 0};
-      } else {
-        const int kb = slot % (BK / 4), rb = slot / (BK / 4);
-        const int r = r0 + rb * 8;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int k = k0 + kb * 4 + kk;
-          if (slot < kSlots && r < rows && k < K)
-            v[i][kk] = *(const u32x4_t *)(X + (int64_t)k * ld + r);
-          else
-            v[i][kk] = u32x4_t{0, 0, 0, 0};
-        }
-      }
+      int r, k;
+      if (KMAJOR) { r = r0 + slot / (BK / 8); k = k0 + (slot % (BK / 8)) * 8; }
+      else { k = k0 + slot / (R / 8); r = r0 + (slot % (R / 8)) * 8; }
+      if (slot < kSlots && r < rows && k < K)
+        v[i] = KMAJOR ? *(const u32x4_t *)(X + (int64_t)r * ld + k)
+                      : *(const u32x4_t *)(X + (int64_t)k * ld + r);
+      else
+        v[i] = u32x4_t{0, 0, 0, 0};
     }
   }
 
@@ -96,20 +85,29 @@ struct Stager {
     for (int i = 0; i < kPer; ++i) {
       const int slot = threadIdx.x + i * NT;
       if (slot >= kSlots) continue;
-      if (KMAJOR) {
-        const int row = slot / (BK / 8), kv = slot % (BK / 8);
-        *(u32x4_t *)(lds + row * LDK + kv * 8) = v[i][0];
-      } else {
-        const int kb = slot % (BK / 4), rb = slot / (BK / 4);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int w = e >> 1, sh = (e & 1) * 16;
-          const uint32_t a0 = (v[i][0][w] >> sh) & 0xffffu, a1 = (v[i][1][w] >> sh) & 0xffffu;
-          const uint32_t a2 = (v[i][2][w] >> sh) & 0xffffu, a3 = (v[i][3][w] >> sh) & 0xffffu;
-          *(u32x2_t *)(lds + (rb * 8 + e) * LDK + kb * 4) = u32x2_t{a0 | (a1 << 16), a2 | (a3 << 16)};
-        }
-      }
+      if (KMAJOR) *(u32x4_t *)(lds + (slot / (BK / 8)) * LD + (slot % (BK / 8)) * 8) = v[i];
+      else *(u32x4_t *)(lds + (slot / (R / 8)) * LD + (slot % (R / 8)) * 8) = v[i];
     }
+  }
+
+  // MFMA 32x32x16 operand of rows [rb, rb+32), k [kk, kk+16): lane l gets row
+  // rb + l%32 and k = kk + 8*(l/32) + 0..7.
+  AJ_DEV bf16x8_t frag(const uint16_t *lds, int rb, int kk) const {
+    const int lane = threadIdx.x & 63;
+    if (KMAJOR) return *(const bf16x8_t *)(lds + (rb + (lane & 31)) * LD + kk + (lane >> 5) * 8);
+    // ds_read_tr16_b64: in each 16-lane group, lane j receives element j%4 of
+    // the 4-element run addressed by lane 4e + j/4 (e = 0..3).  Source lane s
+    // points at k row k0 + s/4, columns mb + 4*(s%4)..+3, so lane j receives
+    // row mb + j at k0..k0+3.
+    const int g = lane >> 4, s = lane & 15;
+    const int mb = rb + 16 * (g & 1), k0 = kk + 8 * (g >> 1);
+    const uint16_t *p = lds + (k0 + (s >> 2)) * LD + mb + 4 * (s & 3);
+    typedef short v4i16 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+    v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
+    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 4 * LD));
+    u32x2_t a = __builtin_bit_cast(u32x2_t, lo), b = __builtin_bit_cast(u32x2_t, hi);
+    return __builtin_bit_cast(bf16x8_t, u32x4_t{a[0], a[1], b[0], b[1]});
   }
 };
 
@@ -117,9 +115,11 @@ template <typename Cfg, bool A_K, bool B_K>
 __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, LDK = Cfg::LDK, NT = Cfg::NT;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDK];
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, NT = Cfg::NT;
+  using SA = Stager<BM, BK, NT, A_K>;
+  using SB = Stager<BN, BK, NT, B_K>;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][SA::kBytes / 2];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][SB::kBytes / 2];
 
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const TileIdx ti = tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
@@ -139,8 +139,8 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  Stager<BM, BK, LDK, NT, A_K> sa;
-  Stager<BN, BK, LDK, NT, B_K> sb;
+  SA sa;
+  SB sb;
   if (nk > 0) {
     sa.load(A, lda, m0, M, kbeg, kend);
     sb.load(B, ldb, n0, N, kbeg, kend);
@@ -154,15 +154,13 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
       sa.load(A, lda, m0, M, kbeg + (kt + 1) * BK, kend);
       sb.load(B, ldb, n0, N, kbeg + (kt + 1) * BK, kend);
     }
-    const uint16_t *as = As[buf] + (wm * Cfg::WTM + (lane & 31)) * LDK + (lane >> 5) * 8;
-    const uint16_t *bs = Bs[buf] + (wn * Cfg::WTN + (lane & 31)) * LDK + (lane >> 5) * 8;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8_t af[Cfg::TM], bfr[Cfg::TN];
 #pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i) af[i] = *(const bf16x8_t *)(as + i * 32 * LDK + kk);
+      for (int i = 0; i < Cfg::TM; ++i) af[i] = sa.frag(As[buf], wm * Cfg::WTM + i * 32, kk);
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) bfr[j] = *(const bf16x8_t *)(bs + j * 32 * LDK + kk);
+      for (int j = 0; j < Cfg::TN; ++j) bfr[j] = sb.frag(Bs[buf], wn * Cfg::WTN + j * 32, kk);
 #pragma unroll
       for (int i = 0; i < Cfg::TM; ++i)
 #pragma unroll
@@ -295,13 +293,14 @@ int gemm(const Gemm &g, hipStream_t s) {
     // vector loads need the contiguous dimension in whole 8-element groups
     const int a_contig = g.a_kmajor ? g.K : g.M, b_contig = g.b_kmajor ? g.K : g.N;
     mfma = a_contig % 8 == 0 && b_contig % 8 == 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
-           aligned16(g.A) && aligned16(g.B) && !(!g.a_kmajor && g.b_kmajor);
+           aligned16(g.A) && aligned16(g.B);
   }
   if (mfma) {
     const int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
     const int tk = timing_begin(s, kc, g.recompute ? 0.0 : 2.0 * g.M * g.N * (double)g.K);
     if (g.a_kmajor && g.b_kmajor) launch_mfma<CfgBig, true, true>(g, ep, kps, s);
     else if (g.a_kmajor) launch_mfma<CfgBig, true, false>(g, ep, kps, s);
+    else if (g.b_kmajor) launch_mfma<CfgBig, false, true>(g, ep, kps, s);
     else launch_mfma<CfgBig, false, false>(g, ep, kps, s);
     timing_end(s, tk);
   } else {
