@@ -166,12 +166,12 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < Cfg::TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-      // the other buffer was last read before the previous barrier: fill it
-      // while this one is still being consumed
-      if (kk == BK / 2 - 16 && kt + 1 < nk) {
-        sa.store(As[buf ^ 1]);
-        sb.store(Bs[buf ^ 1]);
-      }
+    }
+    // the other buffer was last read before the previous barrier; the loads
+    // for it had the whole step to arrive
+    if (kt + 1 < nk) {
+      sa.store(As[buf ^ 1]);
+      sb.store(Bs[buf ^ 1]);
     }
     __syncthreads();
   }
