@@ -163,10 +163,16 @@ def main():
         elif k == "attn_bwd":
             fl = att - att_fwd
         classes[k] = dict(ms=ms, launches=n, tflops=(fl / (ms * 1e-3) / 1e12) if ms > 0 else 0.0)
-    dom = max((k for k in classes if k != "merge"), key=lambda k: classes[k]["ms"])
+    # the roofline names one kernel with algorithmic flops: not the multi-kernel
+    # attention backward, not the logits recompute of the LM-head backward
+    dom = max((k for k in classes if k not in ("merge", "attn_bwd", "lm_dz")),
+              key=lambda k: classes[k]["ms"])
     d = classes[dom]
-    fl_dom = {"attn_fwd": att_fwd, "attn_bwd": att - att_fwd}.get(dom, rec[dom][2])
-    roof = {"kernel": dom, "bound": "mfma", "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2),
+    kernel_names = {"gemm_nt": "gemm_mfma_kernel<true, true>", "gemm_nn": "gemm_mfma_kernel<true, false>",
+                    "gemm_tn": "gemm_mfma_kernel<false, false>", "attn_fwd": "attn_fwd_mfma_kernel",
+                    "lm_fwd": "lm_fwd_fused_kernel", "lm_dz": "lm_dz_fused_kernel"}
+    fl_dom = {"attn_fwd": att_fwd}.get(dom, rec[dom][2])
+    roof = {"kernel": kernel_names.get(dom, dom), "bound": "mfma", "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2),
             "peak": peak, "unit": "TFLOP/s",
             "frac": round(fl_dom / (d["ms"] * 1e-3) / 1e12 / peak, 4), "traffic": None,
             "launches": d["launches"], "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}

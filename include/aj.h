@@ -254,11 +254,14 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
  *   AJ_KC_GEMM_*     the MFMA GEMM, by operand layout (NT: both K-major;
  *                    NN: B N-major; TN: A M-major and B N-major)
  *   AJ_KC_ATTN_FWD / AJ_KC_ATTN_BWD   the attention kernels of one call
+ *   AJ_KC_LM_FWD     the fused logits + log-sum-exp kernel of the LM head
+ *   AJ_KC_LM_DZ      the fused logits-recompute + d logits kernel (one per chunk)
  * `flops` accumulates algorithmic flops where the library knows them
- * (2*M*N*K per GEMM launch, 0 for launches that recompute a forward product,
- * 0 for the other classes). */
+ * (2*M*N*K per GEMM and LM_FWD launch; 0 for LM_DZ, which recomputes a
+ * forward product, and for the other classes). */
 enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
-       AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_COUNT = 6 };
+       AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_LM_FWD = 6, AJ_KC_LM_DZ = 7,
+       AJ_KC_COUNT = 8 };
 /* on != 0 starts recording (clearing any earlier record); 0 stops. */
 int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */

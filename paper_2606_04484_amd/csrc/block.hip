@@ -5,6 +5,7 @@
 //           -> s = silu(gate) * up -> y = x1 + s W_down^T
 // Backward: the same chain reversed; weight gradients are GEMMs over the
 // token axis accumulated into float32; the residual gradient stays float32.
+#include <algorithm>
 #include "ops.h"
 
 namespace {
@@ -37,7 +38,7 @@ Saved carve_saved(const aj_block_cfg &c, int n, void *base) {
 
 struct BwdWs {
   void *dy_t, *ds, *dgu, *dx1_t, *dout, *dqkv;
-  float *db, *dx1, *delta, *da, *dg_part;
+  float *db, *dx1, *delta, *da, *dg_part, *splitk;
   size_t bytes;
 };
 
@@ -58,6 +59,12 @@ BwdWs carve_bwd(const aj_block_cfg &c, int n, void *base) {
   w.delta = cv.take<float>((int64_t)c.n_q_heads * n);
   w.da = cv.take<float>(n * d);
   w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n, (int)d));
+  // split-K partials of the weight-gradient GEMMs (K = tokens)
+  size_t sk = aj::gemm_split_floats((int)d, (int)F, n);
+  sk = std::max(sk, aj::gemm_split_floats((int)(2 * F), (int)d, n));
+  sk = std::max(sk, aj::gemm_split_floats((int)d, (int)hq, n));
+  sk = std::max(sk, aj::gemm_split_floats((int)q, (int)d, n));
+  w.splitk = cv.take<float>(sk > 0 ? sk : 1);
   w.bytes = cv.bytes();
   return w;
 }
@@ -134,6 +141,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   Gemm g;
   g.M = d; g.N = F; g.K = n; g.A = dy_t; g.lda = d; g.a_kmajor = false;
   g.B = sv.s; g.ldb = F; g.b_kmajor = false; g.C = gr.w_down; g.ldc = F; g.out = OUT_ACCUM_F32;
+  g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
   if ((r = gemm<T>(g, st))) return r;
   g = Gemm();
   g.M = n; g.N = F; g.K = d; g.A = dy_t; g.lda = d;
@@ -144,6 +152,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   g = Gemm();
   g.M = 2 * F; g.N = d; g.K = n; g.A = ws.dgu; g.lda = 2 * F; g.a_kmajor = false;
   g.B = sv.b; g.ldb = d; g.b_kmajor = false; g.C = gr.w_gate_up; g.ldc = d; g.out = OUT_ACCUM_F32;
+  g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
   if ((r = gemm<T>(g, st))) return r;
   g = Gemm();
   g.M = n; g.N = d; g.K = 2 * F; g.A = ws.dgu; g.lda = 2 * F;
@@ -156,6 +165,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   g = Gemm();
   g.M = d; g.N = hq; g.K = n; g.A = dx1_t; g.lda = d; g.a_kmajor = false;
   g.B = sv.o; g.ldb = hq; g.b_kmajor = false; g.C = gr.w_o; g.ldc = hq; g.out = OUT_ACCUM_F32;
+  g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
   if ((r = gemm<T>(g, st))) return r;
   g = Gemm();
   g.M = n; g.N = hq; g.K = d; g.A = dx1_t; g.lda = d;
@@ -169,6 +179,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   g = Gemm();
   g.M = qdim; g.N = d; g.K = n; g.A = ws.dqkv; g.lda = qdim; g.a_kmajor = false;
   g.B = sv.a; g.ldb = d; g.b_kmajor = false; g.C = gr.w_qkv; g.ldc = d; g.out = OUT_ACCUM_F32;
+  g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
   if ((r = gemm<T>(g, st))) return r;
   g = Gemm();
   g.M = n; g.N = d; g.K = qdim; g.A = ws.dqkv; g.lda = qdim;

@@ -2,17 +2,25 @@
 // log-softmax, token log-prob and the clipped policy-gradient loss.
 //
 // Only the rows that feed a target are normalised and projected (the loss
-// reads no other logits).  The vocab is walked in vocab_chunk-wide chunks with
-// a running (max, sum of exp) per row, so only one chunk of logits exists at a
-// time.  The backward recomputes each chunk's logits and turns them into
+// reads no other logits).
+// bfloat16: the forward is one MFMA GEMM over the whole vocab whose epilogue
+// reduces each 256-column logit tile to a per-row (max, sum of exp) partial
+// and picks up the target's logit, so logits never reach memory; a small
+// kernel then combines the partials into the log-sum-exp.  The backward
+// recomputes each vocab_chunk-wide slab of logits and its epilogue writes
 //   dz = g * (onehot(target) - softmax)        g = d loss / d logprob
-// then accumulates dhn += dz W_chunk and dW_chunk += dz^T hn.
+// in bfloat16, then dhn += dz W_chunk and dW_chunk += dz^T hn are GEMMs.
+// float32 (the small workload): the same arithmetic with each chunk of logits
+// written to a float32 buffer and reduced by row kernels.
 #include "ops.h"
+#include "gemm_core.h"
 
 namespace {
 
 struct LossWs {
   float *z, *run_m, *run_s, *zt, *part, *g, *dhn, *dg_part;
+  float2 *tile_ms;        // fused forward: per (row, 256-column tile) (max, sum of exp), log2 units
+  float *splitk;          // split-K partials of the dW_vocab GEMM
   void *dz;
   int32_t *tpos, *trow;   // targets clamped into the documented range, and their h rows
   size_t bytes;
@@ -25,7 +33,8 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   const int64_t cw = c.vocab_chunk < c.vocab ? c.vocab_chunk : c.vocab;
   aj::Carver cv(base);
   LossWs w;
-  w.z = cv.take<float>((int64_t)n_tgt * cw);
+  w.z = cv.take<float>(c.dtype == AJ_BF16 ? 1 : (int64_t)n_tgt * cw);
+  w.tile_ms = cv.take<float2>(c.dtype == AJ_BF16 ? (int64_t)n_tgt * ((c.vocab + 255) / 256) : 1);
   w.dz = cv.take<char>((int64_t)n_tgt * cw * es);
   w.run_m = cv.take<float>(n_tgt);
   w.run_s = cv.take<float>(n_tgt);
@@ -36,6 +45,8 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   w.part = cv.take<float>(kFinBlocks * 4);
   w.dhn = cv.take<float>((int64_t)n_tgt * c.d_model);
   w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n_tgt, c.d_model));
+  const size_t sk = aj::gemm_split_floats((int)cw, c.d_model, n_tgt);
+  w.splitk = cv.take<float>(sk > 0 ? sk : 1);
   w.bytes = cv.bytes();
   return w;
 }
@@ -118,6 +129,14 @@ __global__ __launch_bounds__(256) void lse_update_kernel(const float *z, int n, 
   }
 }
 
+__global__ void token_check_kernel(int n, const int32_t *tpos, const int32_t *tok, int vocab,
+                                   int32_t *err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n || !err) return;
+  const int t = tok[tpos[i]];
+  if (t < 0 || t >= vocab) atomicOr(err, AJ_DEVERR_TOKEN_RANGE);
+}
+
 // d loss / d logprob for one target (unnormalised by N_mask).
 AJ_DEV float pg_grad(float lp, float old, float A, float eps, float *term, int *clipped,
                      float *ratio) {
@@ -130,6 +149,7 @@ AJ_DEV float pg_grad(float lp, float old, float A, float eps, float *term, int *
   return active ? -A * r : 0.f;
 }
 
+// run_m == nullptr: logprob (and lse) are already written.
 __global__ __launch_bounds__(256) void loss_finalize_kernel(
     int n, const int32_t *tpos, const float *old_lp, const float *adv, float eps, float inv_n,
     const float *run_m, const float *run_s, const float *zt, float *logprob, float *lse,
@@ -137,10 +157,15 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(
   __shared__ float red[4][256];
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    const float l = run_m[i] + logf(run_s[i]);
-    const float lp = zt[i] - l;
-    lse[i] = l;
-    logprob[i] = lp;
+    float lp;
+    if (run_m) {
+      const float l = run_m[i] + logf(run_s[i]);
+      lp = zt[i] - l;
+      lse[i] = l;
+      logprob[i] = lp;
+    } else {
+      lp = logprob[i];
+    }
     const int p = tpos[i];
     float term, r;
     int clipped;
@@ -195,6 +220,140 @@ __global__ __launch_bounds__(256) void dz_kernel(const float *z, int n, int cw, 
   stf(dz + idx, gi * (oh - p));
 }
 
+
+// ---------------------------------------------------------------- fused (bfloat16)
+namespace gemm_core = aj::gemm_core;
+using gemm_core::Cfg;
+using gemm_core::Smem;
+using gemm_core::f32x16_t;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+AJ_DEV float half_max(float v) {   // max over the 32 lanes of this half-wave
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+AJ_DEV float half_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// logits tile z = hn W^T (rows: targets, columns: 256 vocab ids) reduced in
+// registers: per row, the tile's max and sum of exp (log2 units) and, in the
+// tile that holds it, the target's logit.  Logits never leave the chip.
+__global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
+    int n, int V, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
+    const int32_t *tok, float2 *tile_ms, float *zt) {
+  __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
+  __shared__ int ttok[Cfg::BM];
+  __shared__ float2 red[Cfg::WN][Cfg::BM];
+  const int tiles_m = (n + Cfg::BM - 1) / Cfg::BM, tiles_n = (V + Cfg::BN - 1) / Cfg::BN;
+  const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
+  const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
+  if (threadIdx.x < Cfg::BM) {
+    const int m = m0 + threadIdx.x;
+    ttok[threadIdx.x] = m < n ? tok[tpos[m]] : -1;
+  }
+  f32x16_t acc[Cfg::TM][Cfg::TN];
+  gemm_core::mainloop<true, true>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+#pragma unroll
+  for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = gemm_core::acc_row(wm, i, r, lane);
+      float v[Cfg::TN], mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j) {
+        const int col = n0 + gemm_core::acc_col(wn, j, lane);
+        v[j] = col < V ? acc[i][j][r] * kLog2e : -INFINITY;
+        mx = fmaxf(mx, v[j]);
+        if (col == ttok[rl] && m0 + rl < n) zt[m0 + rl] = acc[i][j][r];
+      }
+      mx = half_max(mx);
+      float sm_ = 0.f;
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j) sm_ += v[j] == -INFINITY ? 0.f : exp2f(v[j] - mx);
+      sm_ = half_sum(sm_);
+      if ((lane & 31) == 0) red[wn][rl] = make_float2(mx, sm_);
+    }
+  __syncthreads();
+  if (threadIdx.x < Cfg::BM && m0 + (int)threadIdx.x < n) {
+    float M = -INFINITY, S = 0.f;
+#pragma unroll
+    for (int w = 0; w < Cfg::WN; ++w) M = fmaxf(M, red[w][threadIdx.x].x);
+#pragma unroll
+    for (int w = 0; w < Cfg::WN; ++w)   // a wave past the vocab end holds (-inf, 0)
+      S += red[w][threadIdx.x].x == -INFINITY ? 0.f
+                                               : red[w][threadIdx.x].y * exp2f(red[w][threadIdx.x].x - M);
+    tile_ms[(int64_t)(m0 + threadIdx.x) * tiles_n + ti.tn] = make_float2(M, S);
+  }
+}
+
+// One wave per row: combine the row's tile partials into its log-sum-exp.
+__global__ __launch_bounds__(256) void lm_combine_kernel(int n, int n_tiles, const float2 *tile_ms,
+                                                         const float *zt, float *lse,
+                                                         float *logprob) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const float2 *p = tile_ms + (int64_t)row * n_tiles;
+  float M = -INFINITY;
+  for (int t = lane; t < n_tiles; t += 64) M = fmaxf(M, p[t].x);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+  float S = 0.f;
+  for (int t = lane; t < n_tiles; t += 64) S += p[t].x == -INFINITY ? 0.f : p[t].y * exp2f(p[t].x - M);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
+  if (lane == 0) {
+    const float l = (M + log2f(S)) * kLn2;
+    lse[row] = l;
+    logprob[row] = zt[row] - l;
+  }
+}
+
+// dz = g (onehot(target) - softmax) for vocab columns [c0, c0 + cw), from the
+// recomputed logits, straight to bfloat16.
+__global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
+    int n, int cw, int c0, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
+    const int32_t *tok, const float *lse, const float *g, bf16_t *dz) {
+  __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
+  __shared__ int ttok[Cfg::BM];
+  __shared__ float tl[Cfg::BM], tg[Cfg::BM];
+  const int tiles_m = (n + Cfg::BM - 1) / Cfg::BM, tiles_n = (cw + Cfg::BN - 1) / Cfg::BN;
+  const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
+  const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
+  if (threadIdx.x < Cfg::BM) {
+    const int m = m0 + threadIdx.x;
+    ttok[threadIdx.x] = m < n ? tok[tpos[m]] - c0 : -1;
+    tl[threadIdx.x] = m < n ? lse[m] * kLog2e : 0.f;
+    tg[threadIdx.x] = m < n ? g[m] : 0.f;
+  }
+  f32x16_t acc[Cfg::TM][Cfg::TN];
+  gemm_core::mainloop<true, true>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+#pragma unroll
+  for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = gemm_core::acc_row(wm, i, r, lane);
+      const int m = m0 + rl;
+      if (m >= n) continue;
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j) {
+        const int col = n0 + gemm_core::acc_col(wn, j, lane);
+        if (col >= cw) continue;
+        const float p = exp2f(acc[i][j][r] * kLog2e - tl[rl]);
+        dz[(int64_t)m * cw + col] = f2bf(tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p));
+      }
+    }
+}
+
 int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
   AJ_REQUIRE(c && in, AJ_ERR_NULL, "%s: null cfg/in", name);
   AJ_REQUIRE(c->dtype == AJ_F32 || c->dtype == AJ_BF16, AJ_ERR_UNSUPPORTED, "%s: dtype", name);
@@ -231,19 +390,33 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
                                                            w.tpos, w.trow, err);
   aj::rmsnorm_fwd<T>((const T *)h, (const T *)gf, n, d, c.rms_eps, w.trow, 0, (T *)sv.hn,
                      sv.rstd, st);
-  loss_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.run_m, w.run_s, w.zt);
-  for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
-    const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
-    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, false);
-    if (r) return r;
-    lse_update_kernel<<<(n + 3) / 4, 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok, c.vocab,
-                                                  w.run_m, w.run_s, w.zt, err);
+  const bool fused = sizeof(T) == 2;
+  if (fused) {
+    loss_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.run_m, w.run_s, w.zt);
+    const int tiles_n = (c.vocab + Cfg::BN - 1) / Cfg::BN;
+    const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * tiles_n;
+    const int tk = aj::timing_begin(st, AJ_KC_LM_FWD, 2.0 * n * (double)c.vocab * d);
+    lm_fwd_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, c.vocab, d, (const bf16_t *)sv.hn,
+                                                   (const bf16_t *)w_vocab, w.tpos, in.tok,
+                                                   w.tile_ms, w.zt);
+    aj::timing_end(st, tk);
+    lm_combine_kernel<<<(n + 3) / 4, 256, 0, st>>>(n, tiles_n, w.tile_ms, w.zt, lse, logprob);
+    token_check_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, in.tok, c.vocab, err);
+  } else {
+    loss_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.run_m, w.run_s, w.zt);
+    for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
+      const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
+      int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, false);
+      if (r) return r;
+      lse_update_kernel<<<(n + 3) / 4, 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok, c.vocab,
+                                                    w.run_m, w.run_s, w.zt, err);
+    }
   }
   int nb = (n + 255) / 256;
   if (nb > kFinBlocks) nb = kFinBlocks;
   loss_finalize_kernel<<<nb, 256, 0, st>>>(n, w.tpos, in.old_logprob, in.adv, c.clip_eps,
-                                           in.inv_n_mask, w.run_m, w.run_s, w.zt, logprob, lse,
-                                           w.part);
+                                           in.inv_n_mask, fused ? nullptr : w.run_m, w.run_s,
+                                           w.zt, logprob, lse, w.part);
   stats_reduce_kernel<<<1, 64, 0, st>>>(w.part, nb, stats);
   return aj::check_launch("aj_logprob_pg_loss_fwd");
 }
@@ -262,11 +435,20 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   aj::fill_f32(w.dhn, (int64_t)n * d, 0.f, st);
   for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
-    int r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true);
-    if (r) return r;
-    const int64_t tot = (int64_t)n * cw;
-    dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok,
-                                                                lse, w.g, (T *)w.dz);
+    int r;
+    if (sizeof(T) == 2) {
+      const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
+      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
+      lm_dz_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, cw, c0, d, (const bf16_t *)sv.hn,
+                                                    (const bf16_t *)w_vocab, w.tpos, in.tok, lse,
+                                                    w.g, (bf16_t *)w.dz);
+      aj::timing_end(st, tk);
+    } else {
+      if ((r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true))) return r;
+      const int64_t tot = (int64_t)n * cw;
+      dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok,
+                                                                  lse, w.g, (T *)w.dz);
+    }
     aj::Gemm g;   // dhn += dz W_chunk
     g.M = n; g.N = d; g.K = cw; g.A = w.dz; g.lda = cw;
     g.B = (const T *)w_vocab + (int64_t)c0 * d; g.ldb = d; g.b_kmajor = false;
@@ -276,6 +458,7 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     g.M = cw; g.N = d; g.K = n; g.A = w.dz; g.lda = cw; g.a_kmajor = false;
     g.B = sv.hn; g.ldb = d; g.b_kmajor = false;
     g.C = dwv + (int64_t)c0 * d; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
+    g.split_k = aj::gemm_split_k(g.M, g.N, g.K); g.partial = w.splitk;
     if ((r = aj::gemm<T>(g, st))) return r;
   }
   aj::rmsnorm_bwd<T>(w.dhn, (const T *)h, sv.rstd, (const T *)gf, n, d, w.trow, 0, 1,

@@ -59,6 +59,23 @@ struct Gemm {
 template <typename T>
 int gemm(const Gemm &g, hipStream_t s);
 
+// Split-K factor for an M x N output over K: 1 when the 256x256 tiles already
+// cover the 256 CUs, else enough splits for ~1.5-2 waves with K/S >= 4096.
+inline int gemm_split_k(int M, int N, int K) {
+  const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  if (tiles >= 240 || K < 8192) return 1;
+  int S = (448 + tiles - 1) / tiles;
+  const int kmax = K / 4096;
+  if (S > kmax) S = kmax;
+  if (S > 16) S = 16;
+  return S < 1 ? 1 : S;
+}
+// Floats of split-K partials gemm() needs for such a GEMM (0 when no split).
+inline size_t gemm_split_floats(int M, int N, int K) {
+  const int S = gemm_split_k(M, N, K);
+  return S > 1 ? (size_t)S * M * N : 0;
+}
+
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
   int n_tok, n_seg, Hq, Hkv, hd;

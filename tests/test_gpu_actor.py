@@ -84,6 +84,17 @@ def test_bf16_long_segments():
     check(case, run_gpu(case, True), True, 2e-2, 1e-2, 1e-2, 0.999)
 
 
+def test_bf16_split_k():
+    """A pack of > 8192 tokens with few output tiles: the weight-gradient GEMMs
+    run split over K with partial sums reduced in a fixed order."""
+    m = bf16_case_model(**BF16_CASES["hd64_gqa2"])
+    case = Case(workload(m, n_traj=24), noise_std=0.3, margin=0.05)
+    assert case.unmerged.n_tok > 8192
+    got = run_gpu(case, False)
+    assert len(got["L"].packs) == 1
+    check(case, got, False, 2e-2, 1e-2, 1e-2, 0.999)
+
+
 def test_bf16_small_packs():
     """Many packs (segments never split) give the same result as one, up to the
     bfloat16 rounding that moves with where a segment's key tiles start."""
