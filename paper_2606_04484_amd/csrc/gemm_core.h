@@ -101,25 +101,30 @@ struct Stager {
 };
 
 
+// The plain GEMM: 8 waves as 2 x 4, each 128 rows x 64 columns.
 using Cfg = MfmaCfg<256, 256, 64, 2, 4>;
+// The LM-head kernels: 8 waves as 4 x 2, each 64 rows x 128 columns, so that a
+// lane holds 4 columns of each of its rows for the per-row epilogue reductions.
+using CfgWide = MfmaCfg<256, 256, 64, 4, 2>;
 
-template <bool A_K, bool B_K>
+template <bool A_K, bool B_K, typename C = Cfg>
 struct Smem {
-  using SA = Stager<Cfg::BM, Cfg::BK, Cfg::NT, A_K>;
-  using SB = Stager<Cfg::BN, Cfg::BK, Cfg::NT, B_K>;
+  using SA = Stager<C::BM, C::BK, C::NT, A_K>;
+  using SB = Stager<C::BN, C::BK, C::NT, B_K>;
   uint16_t a[2][SA::kBytes / 2];
   uint16_t b[2][SB::kBytes / 2];
 };
 
-// acc[i][j] (lane's share of the wave's 128x64 block) = sum over k in
-// [kbeg, kend) of A(m, k) B(n, k) for the 256x256 tile at (m0, n0).
-template <bool A_K, bool B_K>
-AJ_DEV void mainloop(f32x16_t (&acc)[Cfg::TM][Cfg::TN], const bf16_t *A, int64_t lda,
+// acc[i][j] (lane's share of the wave's block) = sum over k in [kbeg, kend)
+// of A(m, k) B(n, k) for the tile at (m0, n0).
+template <bool A_K, bool B_K, typename C = Cfg>
+AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda,
                      const bf16_t *B, int64_t ldb, int M, int N, int m0, int n0, int kbeg,
-                     int kend, Smem<A_K, B_K> &sm) {
+                     int kend, Smem<A_K, B_K, C> &sm) {
+  using Cfg = C;
   constexpr int BK = Cfg::BK;
-  using SA = typename Smem<A_K, B_K>::SA;
-  using SB = typename Smem<A_K, B_K>::SB;
+  using SA = typename Smem<A_K, B_K, C>::SA;
+  using SB = typename Smem<A_K, B_K, C>::SB;
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
@@ -169,10 +174,12 @@ AJ_DEV void mainloop(f32x16_t (&acc)[Cfg::TM][Cfg::TN], const bf16_t *A, int64_t
 
 // Row / column of accumulator element r of tile (i, j) for this lane: the
 // lane holds column lane%32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32.
+template <typename C = Cfg>
 AJ_DEV int acc_row(int wm, int i, int r, int lane) {
-  return wm * Cfg::WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  return wm * C::WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
-AJ_DEV int acc_col(int wn, int j, int lane) { return wn * Cfg::WTN + j * 32 + (lane & 31); }
+template <typename C = Cfg>
+AJ_DEV int acc_col(int wn, int j, int lane) { return wn * C::WTN + j * 32 + (lane & 31); }
 
 }  // namespace gemm_core
 }  // namespace aj

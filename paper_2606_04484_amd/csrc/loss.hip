@@ -223,8 +223,8 @@ __global__ __launch_bounds__(256) void dz_kernel(const float *z, int n, int cw, 
 
 // ---------------------------------------------------------------- fused (bfloat16)
 namespace gemm_core = aj::gemm_core;
-using gemm_core::Cfg;
-using gemm_core::Smem;
+using Cfg = gemm_core::CfgWide;
+template <bool A_K, bool B_K> using Smem = gemm_core::Smem<A_K, B_K, Cfg>;
 using gemm_core::f32x16_t;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -257,18 +257,18 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     ttok[threadIdx.x] = m < n ? tok[tpos[m]] : -1;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop<true, true>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
+  gemm_core::mainloop<true, true, Cfg>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = gemm_core::acc_row(wm, i, r, lane);
+      const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
       float v[Cfg::TN], mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < Cfg::TN; ++j) {
-        const int col = n0 + gemm_core::acc_col(wn, j, lane);
+        const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
         v[j] = col < V ? acc[i][j][r] * kLog2e : -INFINITY;
         mx = fmaxf(mx, v[j]);
         if (col == ttok[rl] && m0 + rl < n) zt[m0 + rl] = acc[i][j][r];
@@ -334,19 +334,19 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     tg[threadIdx.x] = m < n ? g[m] : 0.f;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop<true, true>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  gemm_core::mainloop<true, true, Cfg>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = gemm_core::acc_row(wm, i, r, lane);
+      const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
       const int m = m0 + rl;
       if (m >= n) continue;
 #pragma unroll
       for (int j = 0; j < Cfg::TN; ++j) {
-        const int col = n0 + gemm_core::acc_col(wn, j, lane);
+        const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
         if (col >= cw) continue;
         const float p = exp2f(acc[i][j][r] * kLog2e - tl[rl]);
         dz[(int64_t)m * cw + col] = f2bf(tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p));

@@ -41,8 +41,37 @@ __global__ __launch_bounds__(256) void embed_bwd_kernel(const int32_t *tok, int 
 }
 
 // ---------------------------------------------------------------- RMSNorm
+// One wave per row; lane handles columns 8*(lane + 64*v) + e, v < NV, e < 8,
+// so every access is a 16-byte (bf16) or 32-byte (float) vector.  NV is the
+// smallest instantiated value with 512*NV >= d; the row stays in registers
+// between the reduction and the output pass.
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+AJ_DEV void load8(const float *p, float (&v)[8]) {
+  const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+AJ_DEV void load8(const bf16_t *p, float (&v)[8]) {
+  const u32x4v u = *(const u32x4v *)p;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[2 * k] = __uint_as_float(u[k] << 16);
+    v[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
+  }
+}
+AJ_DEV void store8(float *p, const float (&v)[8]) {
+  *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4 *)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+AJ_DEV void store8(bf16_t *p, const float (&v)[8]) {
+  u32x4v u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) u[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+  *(u32x4v *)p = u;
+}
+
 // out[i] = x[r] * rstd * g, r = rows ? rows[i] + row_shift : i
-template <typename T>
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const T *x, const T *g, int n, int d,
                                                           float eps, const int32_t *rows,
                                                           int row_shift, T *out, float *rstd) {
@@ -51,63 +80,110 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const T *x, const T *g
   if (i >= n) return;
   const int64_t r = rows ? (int64_t)rows[i] + row_shift : i;
   const T *xr = x + r * d;
+  float xv[NV][8];
   float ss = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    float v = ldf(xr + c);
-    ss += v * v;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int c = 8 * (lane + 64 * v);
+    if (c < d) {
+      load8(xr + c, xv[v]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += xv[v][e] * xv[v][e];
+    }
   }
   ss = wave_sum(ss);
   const float rs = 1.0f / sqrtf(ss / d + eps);
   if (lane == 0 && rstd) rstd[i] = rs;
   T *o = out + (int64_t)i * d;
-  for (int c = lane; c < d; c += 64) stf(o + c, ldf(xr + c) * rs * ldf(g + c));
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int c = 8 * (lane + 64 * v);
+    if (c < d) {
+      float gv[8], y[8];
+      load8(g + c, gv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = xv[v][e] * rs * gv[e];
+      store8(o + c, y);
+    }
+  }
 }
 
 // dx = add + rstd * (g*dy - x * rstd^2 * mean(g*dy*x)).
 // Input row i reads x row r (gather as in the forward); output row i goes to
 // out row r when scatter is set, else row i.  Each wave walks a fixed set of
-// rows and keeps its share of dg = sum_rows dy*x*rstd in registers; the
-// per-wave partial rows are summed in a fixed order afterwards.
-constexpr int kBwdMaxCols = 128;   // d <= 64 * 128
-constexpr int kBwdBlocks = 256;
-template <typename T>
+// rows and keeps its share of dg = sum_rows dy*x*rstd in registers; the four
+// waves of a block then add theirs in a fixed order, and the per-block rows
+// are summed in order by col_reduce_kernel.
+constexpr int kBwdBlocks = 1024;
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(
     const float *dy, const T *x, const float *rstd, const T *g, int n, int d,
     const int32_t *rows, int row_shift, int scatter, const float *add, float *dx, T *dx_t,
     float *dg_part) {
-  const int gw = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  __shared__ float red[NV * 512];
+  const int w = threadIdx.x >> 6;
+  const int gw = blockIdx.x * kRowsPerBlock + w;
   const int nw = gridDim.x * kRowsPerBlock;
   const int lane = threadIdx.x & 63;
-  float acc[kBwdMaxCols];
+  float acc[NV][8];
 #pragma unroll
-  for (int j = 0; j < kBwdMaxCols; ++j) acc[j] = 0.f;
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[v][e] = 0.f;
   for (int i = gw; i < n; i += nw) {
     const int64_t r = rows ? (int64_t)rows[i] + row_shift : i;
     const int64_t o = scatter ? r : i;
     const float *dyr = dy + (int64_t)i * d;
     const T *xr = x + r * d;
     const float rs = rstd[i];
+    float dv[NV][8], xv[NV][8];
     float dot = 0.f;
-    for (int c = lane; c < d; c += 64) dot += dyr[c] * ldf(g + c) * ldf(xr + c);
-    dot = wave_sum(dot) / d;
 #pragma unroll
-    for (int j = 0; j < kBwdMaxCols; ++j) {
-      const int c = lane + 64 * j;
+    for (int v = 0; v < NV; ++v) {
+      const int c = 8 * (lane + 64 * v);
       if (c < d) {
-        const float xv = ldf(xr + c), dv = dyr[c];
-        float v = rs * (ldf(g + c) * dv - xv * rs * rs * dot);
-        if (add) v += add[o * d + c];
-        if (dx) dx[o * d + c] = v;
-        if (dx_t) stf(dx_t + o * d + c, v);
-        acc[j] += dv * xv * rs;
+        float gv[8];
+        load8(dyr + c, dv[v]);
+        load8(xr + c, xv[v]);
+        load8(g + c, gv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot += gv[e] * dv[v][e] * xv[v][e];
+      }
+    }
+    dot = wave_sum(dot) / d;
+    const float k2 = rs * rs * dot;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = 8 * (lane + 64 * v);
+      if (c < d) {
+        float y[8], gv[8];
+        load8(g + c, gv);
+        if (add) load8(add + o * d + c, y);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float val = rs * (gv[e] * dv[v][e] - xv[v][e] * k2);
+          y[e] = add ? y[e] + val : val;
+          acc[v][e] += dv[v][e] * xv[v][e] * rs;
+        }
+        if (dx) store8(dx + o * d + c, y);
+        if (dx_t) store8(dx_t + o * d + c, y);
       }
     }
   }
+  // fixed-order combine of the four waves' dg shares
+  for (int ww = 0; ww < kRowsPerBlock; ++ww) {
+    if (w == ww) {
 #pragma unroll
-  for (int j = 0; j < kBwdMaxCols; ++j) {
-    const int c = lane + 64 * j;
-    if (c < d) dg_part[(int64_t)gw * d + c] = acc[j];
+      for (int v = 0; v < NV; ++v) {
+        const int c = 8 * (lane + 64 * v);
+        if (c < d)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) red[c + e] = (ww == 0 ? 0.f : red[c + e]) + acc[v][e];
+      }
+    }
+    __syncthreads();
   }
+  for (int c = threadIdx.x; c < d; c += blockDim.x) dg_part[(int64_t)blockIdx.x * d + c] = red[c];
 }
 
 // out[c] += sum_b part[b][c], b ascending (deterministic).
@@ -144,32 +220,52 @@ __global__ __launch_bounds__(256) void rope_kernel(T *qkv, int n, const int32_t 
 }
 
 // ---------------------------------------------------------------- SwiGLU
+// 8 features per thread (d_ff is a multiple of 8): 16-byte bf16 vectors.
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_fwd_kernel(const T *gu, int n, int F, T *s) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)n * F) return;
-  const int64_t r = idx / F, f = idx % F;
-  const float g = ldf(gu + r * 2 * F + f), u = ldf(gu + r * 2 * F + F + f);
-  stf(s + idx, g / (1.f + __expf(-g)) * u);
+  const int F8 = F >> 3;
+  if (idx >= (int64_t)n * F8) return;
+  const int64_t r = idx / F8, f = (idx % F8) * 8;
+  float g[8], u[8], y[8];
+  load8(gu + r * 2 * F + f, g);
+  load8(gu + r * 2 * F + F + f, u);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) y[e] = g[e] / (1.f + __expf(-g[e])) * u[e];
+  store8(s + r * F + f, y);
 }
 
 template <typename TI, typename T>
 __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const TI *ds, const T *gu, int n, int F,
                                                          T *dgu) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)n * F) return;
-  const int64_t r = idx / F, f = idx % F;
-  const float g = ldf(gu + r * 2 * F + f), u = ldf(gu + r * 2 * F + F + f);
-  const float d = ldf(ds + idx);
-  const float sg = 1.f / (1.f + __expf(-g));
-  stf(dgu + r * 2 * F + f, d * u * sg * (1.f + g * (1.f - sg)));
-  stf(dgu + r * 2 * F + F + f, d * g * sg);
+  const int F8 = F >> 3;
+  if (idx >= (int64_t)n * F8) return;
+  const int64_t r = idx / F8, f = (idx % F8) * 8;
+  float g[8], u[8], dv[8], dg[8], du[8];
+  load8(gu + r * 2 * F + f, g);
+  load8(gu + r * 2 * F + F + f, u);
+  load8(ds + r * F + f, dv);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float sg = 1.f / (1.f + __expf(-g[e]));
+    dg[e] = dv[e] * u[e] * sg * (1.f + g[e] * (1.f - sg));
+    du[e] = dv[e] * g[e] * sg;
+  }
+  store8(dgu + r * 2 * F + f, dg);
+  store8(dgu + r * 2 * F + F + f, du);
 }
 
 template <typename T>
 __global__ void cast_kernel(const float *in, int64_t n, T *out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) stf(out + i, in[i]);
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (i + 8 <= n) {
+    float v[8];
+    load8(in + i, v);
+    store8(out + i, v);
+  } else {
+    for (int64_t k = i; k < n; ++k) stf(out + k, in[k]);
+  }
 }
 
 __global__ void fill_kernel(float *p, int64_t n, float v) {
@@ -200,16 +296,30 @@ void embed_bwd(const int32_t *tok, int n, const float *dx, int d, int vocab, flo
   if (n > 0) embed_bwd_kernel<<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(tok, n, dx, d, vocab, demb);
 }
 
+// Dispatch on the number of 512-column groups per row (d <= 8192).
+#define AJ_NV_DISPATCH(d, CALL)                      \
+  do {                                               \
+    const int nv_ = ((d) + 511) / 512;               \
+    if (nv_ <= 1) { constexpr int NV = 1; CALL; }     \
+    else if (nv_ <= 2) { constexpr int NV = 2; CALL; } \
+    else if (nv_ <= 3) { constexpr int NV = 3; CALL; } \
+    else if (nv_ <= 4) { constexpr int NV = 4; CALL; } \
+    else if (nv_ <= 7) { constexpr int NV = 7; CALL; } \
+    else if (nv_ <= 10) { constexpr int NV = 10; CALL; } \
+    else { constexpr int NV = 16; CALL; }             \
+  } while (0)
+
 template <typename T>
 void rmsnorm_fwd(const T *x, const T *g, int n, int d, float eps, const int32_t *rows, int shift,
                  T *out, float *rstd, hipStream_t s) {
-  if (n > 0)
-    rmsnorm_fwd_kernel<T><<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(x, g, n, d, eps, rows, shift, out, rstd);
+  if (n <= 0) return;
+  AJ_NV_DISPATCH(d, (rmsnorm_fwd_kernel<T, NV><<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(
+                        x, g, n, d, eps, rows, shift, out, rstd)));
 }
 
 size_t rmsnorm_bwd_part_floats(int n, int d) {
   (void)n;
-  return (size_t)kBwdBlocks * kRowsPerBlock * d;
+  return (size_t)kBwdBlocks * d;
 }
 
 template <typename T>
@@ -217,11 +327,11 @@ void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int
                  const int32_t *rows, int shift, int scatter, const float *add, float *dx, T *dx_t,
                  float *dg_part, float *dg, hipStream_t s) {
   if (n <= 0) return;
-  unsigned nb = blocks_for(n, kRowsPerBlock);
+  unsigned nb = blocks_for(n, 8 * kRowsPerBlock);     // ~8 rows per wave
   if (nb > (unsigned)kBwdBlocks) nb = kBwdBlocks;
-  rmsnorm_bwd_kernel<T><<<nb, 256, 0, s>>>(dy, x, rstd, g, n, d, rows, shift, scatter, add, dx,
-                                           dx_t, dg_part);
-  col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb * kRowsPerBlock, d, dg);
+  AJ_NV_DISPATCH(d, (rmsnorm_bwd_kernel<T, NV><<<nb, 256, 0, s>>>(
+                        dy, x, rstd, g, n, d, rows, shift, scatter, add, dx, dx_t, dg_part)));
+  col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb, d, dg);
 }
 
 template <typename T>
@@ -235,19 +345,19 @@ void rope(T *qkv, int n, const int32_t *pos, int n_rot_heads, int ld, int hd, fl
 
 template <typename T>
 void swiglu_fwd(const T *gu, int n, int F, T *out, hipStream_t s) {
-  const int64_t total = (int64_t)n * F;
+  const int64_t total = (int64_t)n * (F / 8);
   if (total > 0) swiglu_fwd_kernel<T><<<blocks_for(total, 256), 256, 0, s>>>(gu, n, F, out);
 }
 
 template <typename TI, typename T>
 void swiglu_bwd(const TI *ds, const T *gu, int n, int F, T *dgu, hipStream_t s) {
-  const int64_t total = (int64_t)n * F;
+  const int64_t total = (int64_t)n * (F / 8);
   if (total > 0) swiglu_bwd_kernel<TI, T><<<blocks_for(total, 256), 256, 0, s>>>(ds, gu, n, F, dgu);
 }
 
 template <typename T>
 void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s) {
-  if (n > 0) cast_kernel<T><<<blocks_for(n, 256), 256, 0, s>>>(in, n, out);
+  if (n > 0) cast_kernel<T><<<blocks_for((n + 7) / 8, 256), 256, 0, s>>>(in, n, out);
 }
 
 void fill_f32(float *p, int64_t n, float v, hipStream_t s) {

@@ -28,7 +28,7 @@ class ModelConfig:
     rope_theta: float = 1e6
     init_std: float = 0.02
     clip_eps: float = 0.2
-    vocab_chunk: int = 8192
+    vocab_chunk: int = 32768
     pack_tokens: int = 131072
 
     @property
@@ -86,7 +86,7 @@ LONG32B = WorkloadConfig(
     name="long32b-8x60", n_traj=8, turns=(60, 60), prompt=(8192, 8192), resp=(128, 512),
     obs=(128, 512), rewrite_p=0.0,
     model=ModelConfig(d_model=5120, n_q_heads=40, n_kv_heads=8, head_dim=128, d_ff=27648,
-                      vocab=152064))
+                      vocab=152064, vocab_chunk=8192))
 
 CONFIGS = {c.name: c for c in (TINY, B1P5, AGENT7B, MULTI7B, LONG32B)}
 ORDER = [TINY.name, B1P5.name, AGENT7B.name, MULTI7B.name, LONG32B.name]
