@@ -42,64 +42,76 @@ struct MfmaCfg {
   static_assert(WTM % 32 == 0 && WTN % 32 == 0 && BK % 16 == 0, "tile shape");
 };
 
-// Stages one operand tile through registers into LDS.
-//   K-major operand (rows r, k contiguous): LDS [R][BK + 8], 16-byte vectors.
-//   M/N-major operand (k rows, r contiguous): copied untransposed into LDS
-//   [BK][R + 32]; the MFMA fragments are then read with ds_read_tr16_b64.
-template <int R, int BK, int NT, bool KMAJOR>
-struct Stager {
-  static constexpr int LD = KMAJOR ? BK + 8 : R + 32;    // LDS row pitch (bf16 elements)
-  static constexpr int kSlots = R * BK / 8;
-  static constexpr int kPer = (kSlots + NT - 1) / NT;
-  static constexpr int kBytes = (KMAJOR ? R * LD : BK * LD) * 2;
-  u32x4_t v[kPer];
+// One operand tile of 256 rows (M or N) x 64 k, bfloat16, in LDS (32 KB), filled
+// by asynchronous direct-to-LDS global loads: a wave instruction moves 64 x 16
+// bytes and lane l's 16 bytes land at dst + 16*l, so the layout is chosen
+// through each lane's global address.  16-byte chunks are XOR-swizzled so that
+// the MFMA fragment reads hit all 64 banks:
+//   K-major operand (rows r, k contiguous): [256][64], chunk c of row r at
+//     r*128 + 16*(c ^ ((r >> 1) & 7))       (ds_read_b128 fragments)
+//   M/N-major operand (k rows, r contiguous): [64][256], chunk c of k row k at
+//     k*512 + 16*(c ^ (4 * (k & 3)))         (ds_read_tr16_b64 fragments)
+// Rows past the operand's end read row `rows - 1` (their products land in
+// output rows / columns that are never stored); k past K reads zeros.
+__device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0, 0, 0, 0};
 
-  AJ_DEV void load(const bf16_t *X, int64_t ld, int r0, int rows, int k0, int K) {
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int slot = threadIdx.x + i * NT;
-      int r, k;
-      if (KMAJOR) { r = r0 + slot / (BK / 8); k = k0 + (slot % (BK / 8)) * 8; }
-      else { k = k0 + slot / (R / 8); r = r0 + (slot % (R / 8)) * 8; }
-      if (slot < kSlots && r < rows && k < K)
-        v[i] = KMAJOR ? *(const u32x4_t *)(X + (int64_t)r * ld + k)
-                      : *(const u32x4_t *)(X + (int64_t)k * ld + r);
-      else
-        v[i] = u32x4_t{0, 0, 0, 0};
-    }
-  }
+template <int NT, bool KMAJOR>
+struct Tile {
+  static constexpr int R = 256, BK = 64;
+  static constexpr int kHalfs = R * BK;              // bf16 elements per stage
+  static constexpr int kInstr = R * BK * 2 / 1024 / (NT / 64);   // wave instructions per stage
 
-  AJ_DEV void store(uint16_t *lds) const {
+  AJ_DEV static void load(uint16_t *lds, const bf16_t *X, int64_t ld, int r0, int rows, int k0,
+                          int K) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int slot = threadIdx.x + i * NT;
-      if (slot >= kSlots) continue;
-      if (KMAJOR) *(u32x4_t *)(lds + (slot / (BK / 8)) * LD + (slot % (BK / 8)) * 8) = v[i];
-      else *(u32x4_t *)(lds + (slot / (R / 8)) * LD + (slot % (R / 8)) * 8) = v[i];
+    for (int q = 0; q < kInstr; ++q) {
+      const int blk = wave * kInstr + q;             // 1 KB block of the tile
+      const void *src;
+      if (KMAJOR) {
+        const int r = blk * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        const int k = k0 + 8 * c;
+        const int rr = min(r0 + r, rows - 1);
+        src = k < K ? (const void *)(X + (int64_t)rr * ld + k) : (const void *)kZero16;
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        const int c = (lane & 31) ^ (4 * (kr & 3));
+        const int k = k0 + kr;
+        const int rr = min(r0 + 8 * c, rows - 8);
+        src = k < K ? (const void *)(X + (int64_t)k * ld + rr) : (const void *)kZero16;
+      }
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(lds + blk * 512),
+                                       16, 0, 0);
     }
   }
 
   // MFMA 32x32x16 operand of rows [rb, rb+32), k [kk, kk+16): lane l gets row
   // rb + l%32 and k = kk + 8*(l/32) + 0..7.
-  AJ_DEV bf16x8_t frag(const uint16_t *lds, int rb, int kk) const {
+  AJ_DEV static bf16x8_t frag(const uint16_t *lds, int rb, int kk) {
     const int lane = threadIdx.x & 63;
-    if (KMAJOR) return *(const bf16x8_t *)(lds + (rb + (lane & 31)) * LD + kk + (lane >> 5) * 8);
+    if (KMAJOR) {
+      const int m = rb + (lane & 31);
+      const int c = (kk >> 3) + (lane >> 5);
+      return *(const bf16x8_t *)(lds + m * 64 + 8 * (c ^ ((m >> 1) & 7)));
+    }
     // ds_read_tr16_b64: in each 16-lane group, lane j receives element j%4 of
     // the 4-element run addressed by lane 4e + j/4 (e = 0..3).  Source lane s
     // points at k row k0 + s/4, columns mb + 4*(s%4)..+3, so lane j receives
-    // row mb + j at k0..k0+3.
+    // row mb + j at k0..k0+3; a second read gives k0+4..k0+7.
     const int g = lane >> 4, s = lane & 15;
-    const int mb = rb + 16 * (g & 1), k0 = kk + 8 * (g >> 1);
-    const uint16_t *p = lds + (k0 + (s >> 2)) * LD + mb + 4 * (s & 3);
+    const int k = kk + 8 * (g >> 1) + (s >> 2);
+    const int col = rb + 16 * (g & 1) + 4 * (s & 3);
+    const int c = (col >> 3) ^ (4 * (k & 3));          // (k + 4) & 3 == k & 3
+    const uint16_t *p = lds + k * 256 + 8 * c + (col & 7);
     typedef short v4i16 __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
     v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
-    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 4 * LD));
+    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 4 * 256));
     u32x2_t a = __builtin_bit_cast(u32x2_t, lo), b = __builtin_bit_cast(u32x2_t, hi);
     return __builtin_bit_cast(bf16x8_t, u32x4_t{a[0], a[1], b[0], b[1]});
   }
 };
-
 
 // The plain GEMM: 8 waves as 2 x 4, each 128 rows x 64 columns.
 using Cfg = MfmaCfg<256, 256, 64, 2, 4>;
@@ -109,65 +121,70 @@ using CfgWide = MfmaCfg<256, 256, 64, 4, 2>;
 
 template <bool A_K, bool B_K, typename C = Cfg>
 struct Smem {
-  using SA = Stager<C::BM, C::BK, C::NT, A_K>;
-  using SB = Stager<C::BN, C::BK, C::NT, B_K>;
-  uint16_t a[2][SA::kBytes / 2];
-  uint16_t b[2][SB::kBytes / 2];
+  uint16_t a[2][256 * 64];
+  uint16_t b[2][256 * 64];
 };
 
+AJ_DEV void wait_lds_dma() { __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // acc[i][j] (lane's share of the wave's block) = sum over k in [kbeg, kend)
-// of A(m, k) B(n, k) for the tile at (m0, n0).
+// of A(m, k) B(n, k) for the 256x256 tile at (m0, n0).  The next k-step's
+// loads stream into the other LDS buffer while this one is consumed; the
+// fragments of the next 16-wide k slice are read while the current one's
+// MFMAs issue.
 template <bool A_K, bool B_K, typename C = Cfg>
 AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda,
                      const bf16_t *B, int64_t ldb, int M, int N, int m0, int n0, int kbeg,
                      int kend, Smem<A_K, B_K, C> &sm) {
-  using Cfg = C;
-  constexpr int BK = Cfg::BK;
-  using SA = typename Smem<A_K, B_K, C>::SA;
-  using SB = typename Smem<A_K, B_K, C>::SB;
+  static_assert(C::BM == 256 && C::BN == 256 && C::BK == 64 && C::NT == 512, "tile");
+  using TA = Tile<C::NT, A_K>;
+  using TB = Tile<C::NT, B_K>;
+  constexpr int BK = C::BK;
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int wave = threadIdx.x >> 6;
-  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+  const int wm = wave / C::WN, wn = wave % C::WN;
 #pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i)
+  for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-    for (int j = 0; j < Cfg::TN; ++j)
+    for (int j = 0; j < C::TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  SA sa;
-  SB sb;
   if (nk > 0) {
-    sa.load(A, lda, m0, M, kbeg, kend);
-    sb.load(B, ldb, n0, N, kbeg, kend);
-    sa.store(sm.a[0]);
-    sb.store(sm.b[0]);
+    TA::load(sm.a[0], A, lda, m0, M, kbeg, kend);
+    TB::load(sm.b[0], B, ldb, n0, N, kbeg, kend);
   }
+  wait_lds_dma();
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nk) {
-      sa.load(A, lda, m0, M, kbeg + (kt + 1) * BK, kend);
-      sb.load(B, ldb, n0, N, kbeg + (kt + 1) * BK, kend);
+      TA::load(sm.a[buf ^ 1], A, lda, m0, M, kbeg + (kt + 1) * BK, kend);
+      TB::load(sm.b[buf ^ 1], B, ldb, n0, N, kbeg + (kt + 1) * BK, kend);
     }
+    bf16x8_t af[2][C::TM], bfr[2][C::TN];
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8_t af[Cfg::TM], bfr[Cfg::TN];
+    for (int i = 0; i < C::TM; ++i) af[0][i] = TA::frag(sm.a[buf], wm * C::WTM + i * 32, 0);
 #pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i) af[i] = sa.frag(sm.a[buf], wm * Cfg::WTM + i * 32, kk);
+    for (int j = 0; j < C::TN; ++j) bfr[0][j] = TB::frag(sm.b[buf], wn * C::WTN + j * 32, 0);
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) bfr[j] = sb.frag(sm.b[buf], wn * Cfg::WTN + j * 32, kk);
+    for (int s = 0; s < BK / 16; ++s) {
+      const int cur = s & 1;
+      if (s + 1 < BK / 16) {
 #pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i)
+        for (int i = 0; i < C::TM; ++i)
+          af[cur ^ 1][i] = TA::frag(sm.a[buf], wm * C::WTM + i * 32, 16 * (s + 1));
 #pragma unroll
-        for (int j = 0; j < Cfg::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < C::TN; ++j)
+          bfr[cur ^ 1][j] = TB::frag(sm.b[buf], wn * C::WTN + j * 32, 16 * (s + 1));
+      }
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j],
+                                                              0, 0, 0);
     }
-    // the other buffer was last read before the previous barrier; the loads
-    // for it had the whole step to arrive
-    if (kt + 1 < nk) {
-      sa.store(sm.a[buf ^ 1]);
-      sb.store(sm.b[buf ^ 1]);
-    }
+    wait_lds_dma();
     __syncthreads();
   }
 }
