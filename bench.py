@@ -33,7 +33,44 @@ def parse():
     ap.add_argument("--no-unmerged", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES three times and exit: the "
+                         "reference for scaling the HBM byte counters")
     return ap.parse_args()
+
+
+# HBM bytes per launch of the dominant kernel, from two rocprofv3 --pmc passes
+# (FETCH_SIZE, WRITE_SIZE) over the same bench command, each scaled by the
+# counter's reading for a plain copy of known size.  Keyed by (kernel class,
+# workload); `sources` are hashed so that a changed kernel reports null.
+TRAFFIC = {
+    ("gemm_nn", "block1.5b-64x8"): {"bytes_per_launch": 6013.6e6, "sources": "d603a30e0ed29a18"},
+}
+
+
+def source_hash(files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2606_04484_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+GEMM_SOURCES = ("gemm_core.h", "gemm.hip")
+
+
+def copy_calibration(nbytes):
+    """A plain elementwise copy (one read and one write of nbytes each) for
+    calibrating FETCH_SIZE / WRITE_SIZE against known traffic."""
+    import torch
+    n = nbytes // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": 4 * n, "dispatches": 3}), flush=True)
 
 
 def attention_flops(cu, m):
@@ -106,9 +143,12 @@ def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                          "(the multi-GPU layout is a design note, not a code path)"}))
+        print(json.dumps({"error": "the actor update runs on one GPU only; --gpus must be 1 "
+                          "(sharding over GPUs is designed, not implemented)"}))
         sys.exit(2)
     import torch
     from paper_2606_04484_amd import actor, capi
@@ -177,6 +217,11 @@ def main():
             "frac": round(fl_dom / (d["ms"] * 1e-3) / 1e12 / peak, 4), "traffic": None,
             "launches": d["launches"], "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}
 
+    tr = TRAFFIC.get((dom, cfg.name))
+    if tr and dom.startswith("gemm") and tr["sources"] == source_hash(GEMM_SOURCES):
+        roof["traffic"] = tr["bytes_per_launch"]
+        roof["traffic_unit"] = "bytes"
+
     out = {
         "metric": "merged actor-update tokens/sec/GPU",
         "value": round(Lm.n_tok / t_m, 1),
@@ -203,7 +248,7 @@ def main():
         out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
         out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)
     if not args.no_cpu_baseline:
-        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 128)
+        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 1024)
         out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)
     print(json.dumps(out), flush=True)
 

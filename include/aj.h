@@ -43,7 +43,7 @@ typedef enum {
   AJ_OK = 0,
   AJ_ERR_NULL = 1,          /* a required pointer is NULL */
   AJ_ERR_SHAPE = 2,         /* a size or offset is out of range / not monotone */
-  AJ_ERR_UNSUPPORTED = 3,   /* a valid request this build does not implement */
+  AJ_ERR_UNSUPPORTED = 3,   /* a valid request the library does not implement */
   AJ_ERR_WORKSPACE = 4,     /* workspace smaller than the *_bytes query asked for */
   AJ_ERR_HIP = 5            /* a HIP launch or runtime call failed */
 } aj_status;
