@@ -22,17 +22,17 @@ struct EpArgs {
   void *C; int64_t ldc;
   int c_f32, accum;
   const void *R;
+  int vec;   // 4-column vector stores are aligned (C, R, partial rows)
 };
 
 using gemm_core::Cfg;
 using gemm_core::f32x16_t;
-using gemm_core::Smem;
 
 template <bool A_K, bool B_K>
 __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) Smem<A_K, B_K> sm;
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K> sm;
   const int tiles_m = (M + Cfg::BM - 1) / Cfg::BM, tiles_n = (N + Cfg::BN - 1) / Cfg::BN;
   const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
   const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
@@ -43,30 +43,77 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
   f32x16_t acc[Cfg::TM][Cfg::TN];
   gemm_core::mainloop<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
 
-  // epilogue: lane holds column (lane & 31); register r holds row 8*(r/4) + 4*(lane/32) + r%4
+  // Epilogue through LDS, 32 rows of each wave row at a time: the lane's
+  // accumulators (column lane%32, rows 8*(r/4) + 4*(lane/32) + r%4 of each
+  // 32x32 tile) are staged as rows, then written out 4 columns per lane.
+  float *stage = reinterpret_cast<float *>(&sm);
+  constexpr int LDW = Cfg::BN + 8;
+  float *P = partial ? partial + (int64_t)blockIdx.z * M * N : nullptr;
+  const int64_t ldo = partial ? N : ep.ldc;
 #pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i)
+  for (int i = 0; i < Cfg::TM; ++i) {
 #pragma unroll
     for (int j = 0; j < Cfg::TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + gemm_core::acc_row(wm, i, r, lane);
-        const int n = n0 + gemm_core::acc_col(wn, j, lane);
-        if (m >= M || n >= N) continue;
-        const float v = acc[i][j][r];
-        if (partial) {
-          partial[((int64_t)blockIdx.z * M + m) * N + n] = v;
-        } else if (ep.accum) {
-          float *c = (float *)ep.C + (int64_t)m * ep.ldc + n;
-          *c += v;
+        const int lr = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        stage[lr * LDW + wn * Cfg::WTN + j * 32 + (lane & 31)] = acc[i][j][r];
+      }
+    __syncthreads();
+#pragma unroll 4
+    for (int q = 0; q < 64 * 64 / Cfg::NT; ++q) {
+      const int c = threadIdx.x + Cfg::NT * q;
+      const int row = c >> 6, c4 = (c & 63) * 4;
+      const int m = m0 + (row >> 5) * 128 + 32 * i + (row & 31), n = n0 + c4;
+      if (m >= M || n >= N) continue;
+      const float4 v = *reinterpret_cast<const float4 *>(stage + row * LDW + c4);
+      const int64_t o = (int64_t)m * ldo + n;
+      if (ep.vec && n + 4 <= N) {
+        if (P) {
+          *reinterpret_cast<float4 *>(P + o) = v;
         } else if (ep.c_f32) {
-          float *c = (float *)ep.C + (int64_t)m * ep.ldc + n;
-          *c = v + (ep.R ? ((const float *)ep.R)[(int64_t)m * ep.ldc + n] : 0.f);
+          float4 *cp = reinterpret_cast<float4 *>((float *)ep.C + o);
+          float4 w = v;
+          if (ep.accum) {
+            const float4 u = *cp;
+            w.x += u.x; w.y += u.y; w.z += u.z; w.w += u.w;
+          } else if (ep.R) {
+            const float4 u = *reinterpret_cast<const float4 *>((const float *)ep.R + o);
+            w.x += u.x; w.y += u.y; w.z += u.z; w.w += u.w;
+          }
+          *cp = w;
         } else {
-          bf16_t *c = (bf16_t *)ep.C + (int64_t)m * ep.ldc + n;
-          *c = f2bf(v + (ep.R ? bf2f(((const bf16_t *)ep.R)[(int64_t)m * ep.ldc + n]) : 0.f));
+          float w0 = v.x, w1 = v.y, w2 = v.z, w3 = v.w;
+          if (ep.R) {
+            const uint2 u = *reinterpret_cast<const uint2 *>((const bf16_t *)ep.R + o);
+            w0 += __uint_as_float(u.x << 16); w1 += __uint_as_float(u.x & 0xffff0000u);
+            w2 += __uint_as_float(u.y << 16); w3 += __uint_as_float(u.y & 0xffff0000u);
+          }
+          uint2 out;
+          out.x = (uint32_t)f2bf(w0) | ((uint32_t)f2bf(w1) << 16);
+          out.y = (uint32_t)f2bf(w2) | ((uint32_t)f2bf(w3) << 16);
+          *reinterpret_cast<uint2 *>((bf16_t *)ep.C + o) = out;
+        }
+      } else {
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (n + e >= N) break;
+          const float x = vv[e];
+          if (P) {
+            P[o + e] = x;
+          } else if (ep.accum) {
+            ((float *)ep.C)[o + e] += x;
+          } else if (ep.c_f32) {
+            ((float *)ep.C)[o + e] = x + (ep.R ? ((const float *)ep.R)[o + e] : 0.f);
+          } else {
+            ((bf16_t *)ep.C)[o + e] = f2bf(x + (ep.R ? bf2f(((const bf16_t *)ep.R)[o + e]) : 0.f));
+          }
         }
       }
+    }
+    __syncthreads();
+  }
 }
 
 // ---------------------------------------------------------------- float32 / fallback
@@ -144,8 +191,14 @@ template <typename T>
 int gemm(const Gemm &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return AJ_OK;
   if (g.split_k > 1 && !g.partial) return fail(AJ_ERR_WORKSPACE, "gemm: split-K without workspace");
-  EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R};
+  EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R, 0};
   if (ep.accum) ep.c_f32 = 1;
+  {
+    const uintptr_t al = ep.c_f32 ? 15 : 7;
+    const bool split = g.split_k > 1;
+    ep.vec = split ? (g.N % 4 == 0 && ((uintptr_t)g.partial & 15) == 0)
+                   : (g.ldc % 4 == 0 && ((uintptr_t)g.C & al) == 0 && ((uintptr_t)g.R & al) == 0);
+  }
   const int S = g.split_k > 1 ? g.split_k : 1;
   int kps = (g.K + S - 1) / S;
   kps = (kps + 63) / 64 * 64;

@@ -55,6 +55,10 @@ struct MfmaCfg {
 // output rows / columns that are never stored); k past K reads zeros.
 __device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0, 0, 0, 0};
 
+AJ_DEV uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
 template <int NT, bool KMAJOR>
 struct Tile {
   static constexpr int R = 256, BK = 64;
@@ -87,31 +91,47 @@ struct Tile {
   }
 
   // MFMA 32x32x16 operand of rows [rb, rb+32), k [kk, kk+16): lane l gets row
-  // rb + l%32 and k = kk + 8*(l/32) + 0..7.
+  // rb + l%32 and k = kk + 8*(l/32) + 0..7.  The reads are issued as inline
+  // assembly: the compiler cannot tell them apart from the LDS writes of the
+  // in-flight direct-to-LDS copies and would otherwise wait for those copies
+  // before every read; the caller waits for the reads itself (frag_wait).
   AJ_DEV static bf16x8_t frag(const uint16_t *lds, int rb, int kk) {
     const int lane = threadIdx.x & 63;
+    bf16x8_t v;
     if (KMAJOR) {
       const int m = rb + (lane & 31);
       const int c = (kk >> 3) + (lane >> 5);
-      return *(const bf16x8_t *)(lds + m * 64 + 8 * (c ^ ((m >> 1) & 7)));
+      const uint32_t a = lds_addr(lds + m * 64 + 8 * (c ^ ((m >> 1) & 7)));
+      asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+      return v;
     }
-    // ds_read_tr16_b64: in each 16-lane group, lane j receives element j%4 of
-    // the 4-element run addressed by lane 4e + j/4 (e = 0..3).  Source lane s
-    // points at k row k0 + s/4, columns mb + 4*(s%4)..+3, so lane j receives
-    // row mb + j at k0..k0+3; a second read gives k0+4..k0+7.
+    // ds_read_b64_tr_b16: in each 16-lane group, lane j receives element j%4
+    // of the 4-element run addressed by lane 4e + j/4 (e = 0..3).  Source lane
+    // s points at k row k0 + s/4, columns mb + 4*(s%4)..+3, so lane j
+    // receives row mb + j at k0..k0+3; a second read gives k0+4..k0+7.
     const int g = lane >> 4, s = lane & 15;
     const int k = kk + 8 * (g >> 1) + (s >> 2);
     const int col = rb + 16 * (g & 1) + 4 * (s & 3);
     const int c = (col >> 3) ^ (4 * (k & 3));          // (k + 4) & 3 == k & 3
-    const uint16_t *p = lds + k * 256 + 8 * c + (col & 7);
-    typedef short v4i16 __attribute__((ext_vector_type(4)));
-    typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-    v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
-    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 4 * 256));
-    u32x2_t a = __builtin_bit_cast(u32x2_t, lo), b = __builtin_bit_cast(u32x2_t, hi);
-    return __builtin_bit_cast(bf16x8_t, u32x4_t{a[0], a[1], b[0], b[1]});
+    const uint32_t a = lds_addr(lds + k * 256 + 8 * c + (col & 7));
+    u32x2_t lo, hi;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:2048" : "=v"(hi) : "v"(a) : "memory");
+    return __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
   }
 };
+
+// Waits for every LDS read in flight; the fragments pass through empty
+// statements after the wait so that no MFMA consuming them is scheduled
+// above it.
+template <int TM, int TN>
+AJ_DEV void frag_wait(bf16x8_t (&a)[TM], bf16x8_t (&b)[TN]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(a[i]));
+#pragma unroll
+  for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(b[j]));
+}
 
 // The plain GEMM: 8 waves as 2 x 4, each 128 rows x 64 columns.
 using Cfg = MfmaCfg<256, 256, 64, 2, 4>;
@@ -169,6 +189,7 @@ AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
       const int cur = s & 1;
+      frag_wait(af[cur], bfr[cur]);
       if (s + 1 < BK / 16) {
 #pragma unroll
         for (int i = 0; i < C::TM; ++i)
