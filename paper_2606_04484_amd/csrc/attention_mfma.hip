@@ -26,8 +26,6 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kKT = 64;       // keys per staged tile (forward, dQ)
-constexpr int kQT = 64;       // queries per staged tile (dK/dV)
 
 AJ_DEV f32x16_t mfma(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -41,13 +39,6 @@ AJ_DEV uint32_t pack2(float lo, float hi) {
 AJ_DEV bf16x8_t pack8(const f32x16_t &v, int r0) {
   u32x4_t u{pack2(v[r0], v[r0 + 1]), pack2(v[r0 + 2], v[r0 + 3]), pack2(v[r0 + 4], v[r0 + 5]),
             pack2(v[r0 + 6], v[r0 + 7])};
-  return __builtin_bit_cast(bf16x8_t, u);
-}
-
-// Two 4-element runs from a transposed LDS row: [p, p+4) and [p+8, p+12).
-AJ_DEV bf16x8_t ld_split(const uint16_t *p) {
-  u32x2_t a = *(const u32x2_t *)p, b = *(const u32x2_t *)(p + 8);
-  u32x4_t u{a[0], a[1], b[0], b[1]};
   return __builtin_bit_cast(bf16x8_t, u);
 }
 
@@ -79,46 +70,154 @@ AJ_DEV float wave_min_f(float v) {
   return v;
 }
 
-// rows [r0, r0+R) x HD of a strided bf16 matrix -> LDS [R][LDR], zero past `rows`
-template <int R, int HD, int LDR>
-AJ_DEV void stage_rows(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows) {
-  constexpr int kVec = R * HD / 8;
-  for (int v = threadIdx.x; v < kVec; v += 256) {
-    const int r = v / (HD / 8), c = (v % (HD / 8)) * 8;
-    u32x4_t x{0, 0, 0, 0};
-    if (r0 + r < rows) x = *(const u32x4_t *)(src + (int64_t)(r0 + r) * ld + c);
-    *(u32x4_t *)(lds + r * LDR + c) = x;
+// ------------------------------------------------------------------ LDS tiles
+// A tile of 64 token rows x HD bfloat16, row-major in LDS (HD*2 bytes per
+// row), filled by asynchronous direct-to-LDS copies (a wave instruction moves
+// 64 x 16 bytes; lane l's bytes land at dst + 16*l).  Both fragment shapes
+// read it:
+//   row fragments (ds_read_b128): 32 consecutive tokens x 8 features, for the
+//     products whose rows are tokens (S = Q K^T and its transposes);
+//   column fragments (ds_read_b64_tr_b16): 32 consecutive features x 8
+//     tokens, for the products whose rows are features (O^T = V^T P^T,
+//     dQ^T = K^T dS^T, dV^T = dO^T P, dK^T = Q^T dS).
+// 16-byte chunk c of token row r sits at chunk position c ^ swz(r).  With 64
+// LDS banks (256 bytes a line), swz makes the 16 rows of a row read and the
+// 4 rows x 2 chunks of a transposed read hit distinct bank groups:
+//   HD = 128 (one row a line):  swz(r) = 2*(r & 7) | ((r >> 3) & 1)
+//   HD = 64 (two rows a line):  swz(r) = 2*((r >> 1) & 3) | ((r >> 3) & 1)
+// (bijective on 16 consecutive rows; within an aligned group of 4 rows the
+// values differ in a bit other than bit 0, so chunks c and c^1 never meet).
+constexpr int kTR = 64;       // token rows per staged tile
+
+AJ_DEV uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+template <int HD>
+struct TokTile {
+  static constexpr int CPR = HD / 8;                 // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;               // rows per 1 KB wave instruction
+  static constexpr int kInstr = kTR * HD * 2 / 1024 / 4;   // per wave (4 waves)
+  static constexpr int kHalfs = kTR * HD;
+
+  AJ_DEV static int swz(int r) {
+    return HD == 128 ? ((r & 7) << 1) | ((r >> 3) & 1) : (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+  }
+  // token rows [r0, r0 + 64) of `src` (row stride ld elements); rows at or
+  // past `rows` copy row rows - 1 (their products are masked out)
+  AJ_DEV static void load(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < kInstr; ++q) {
+      const int blk = wave * kInstr + q;
+      const int r = blk * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ swz(r);
+      const int rr = min(r0 + r, rows - 1);
+      __builtin_amdgcn_global_load_lds(src + (int64_t)rr * ld + 8 * c,
+                                       (__attribute__((address_space(3))) void *)(lds + blk * 512),
+                                       16, 0, 0);
+    }
+  }
+  // MFMA operand: rows = tokens [t0, t0 + 32), k = features [f0, f0 + 16)
+  AJ_DEV static bf16x8_t row_frag(const uint16_t *lds, int t0, int f0) {
+    const int lane = threadIdx.x & 63;
+    const int r = t0 + (lane & 31), c = (f0 >> 3) + (lane >> 5);
+    const uint32_t a = lds_addr(lds + r * HD + 8 * (c ^ swz(r)));
+    bf16x8_t v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+  }
+  // MFMA operand: rows = features [f0, f0 + 32), k = 8 tokens in the order
+  // the accumulator-to-operand packing (pack8) produces: lane half h holds
+  // tokens t0 + 4h + 0..3 and t0 + 8 + 4h + 0..3.  ds_read_b64_tr_b16: in a
+  // 16-lane group, lane j receives element j%4 of the 4-element run addressed
+  // by lane 4e + j/4; source lane s addresses token row t + s/4, features
+  // fb + 4*(s%4)..+3, so lane j receives feature fb + j at 4 tokens.
+  AJ_DEV static bf16x8_t col_frag(const uint16_t *lds, int f0, int t0) {
+    const int lane = threadIdx.x & 63, g = lane >> 4, s = lane & 15;
+    const int f = f0 + 16 * (g & 1) + 4 * (s & 3);
+    const int r = t0 + 4 * (g >> 1) + (s >> 2);
+    const uint32_t a0 = lds_addr(lds + r * HD + 8 * ((f >> 3) ^ swz(r)) + (f & 7));
+    const uint32_t a1 = lds_addr(lds + (r + 8) * HD + 8 * ((f >> 3) ^ swz(r + 8)) + (f & 7));
+    u32x2_t lo, hi;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a0) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a1) : "memory");
+    return __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
+  }
+};
+
+// Waits for every LDS read in flight; the operands pass through empty
+// statements after the wait so that no MFMA consuming them moves above it.
+template <int N>
+AJ_DEV void lds_wait(bf16x8_t (&v)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+AJ_DEV void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+// 4 consecutive floats from LDS (inline assembly, like the fragment reads:
+// the tile copies of the next item may still be in flight)
+AJ_DEV f32x4_t lds_read_f4(const float *p) {
+  f32x4_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(p)) : "memory");
+  return v;
+}
+AJ_DEV void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile) += tile rows x B,
+// B = per-lane operands bv[kk] (k = features 16kk..16kk+15)
+template <int HD>
+AJ_DEV void rows_times(f32x16_t (&acc)[2], const uint16_t *tile, const bf16x8_t (&bv)[HD / 16]) {
+  constexpr int KS = HD / 16;
+  bf16x8_t f[2][2];
+  f[0][0] = TokTile<HD>::row_frag(tile, 0, 0);
+  f[0][1] = TokTile<HD>::row_frag(tile, 32, 0);
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    const int cur = kk & 1;
+    lds_wait(f[cur]);
+    if (kk + 1 < KS) {
+      f[cur ^ 1][0] = TokTile<HD>::row_frag(tile, 0, 16 * (kk + 1));
+      f[cur ^ 1][1] = TokTile<HD>::row_frag(tile, 32, 16 * (kk + 1));
+    }
+    acc[0] = mfma(f[cur][0], bv[kk], acc[0]);
+    acc[1] = mfma(f[cur][1], bv[kk], acc[1]);
   }
 }
 
-// rows [r0, r0+R) x HD -> LDS transposed [HD][LDT] (LDT >= R), zero past `rows`
-template <int R, int HD, int LDT>
-AJ_DEV void stage_rows_t(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows) {
-  constexpr int kSlots = (R / 4) * (HD / 8);
-  for (int s = threadIdx.x; s < kSlots; s += 256) {
-    const int cb = s % (HD / 8), rb = s / (HD / 8);
-    u32x4_t x[4];
+// acc[i] (features 32i..32i+31) += tile^T x P, P given per 16-token chunk j as
+// packed accumulator halves pj[j] (tokens 32(j/2) + 16(j%2) + pack8 order)
+template <int HD>
+AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const uint16_t *tile, const bf16x8_t (&pj)[4]) {
+  constexpr int DT = HD / 32;
+  bf16x8_t f[2][DT];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int r = r0 + rb * 4 + k;
-      x[k] = r < rows ? *(const u32x4_t *)(src + (int64_t)r * ld + cb * 8) : u32x4_t{0, 0, 0, 0};
+  for (int i = 0; i < DT; ++i) f[0][i] = TokTile<HD>::col_frag(tile, 32 * i, 0);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int cur = j & 1;
+    lds_wait(f[cur]);
+    if (j + 1 < 4) {
+#pragma unroll
+      for (int i = 0; i < DT; ++i)
+        f[cur ^ 1][i] = TokTile<HD>::col_frag(tile, 32 * i, 32 * ((j + 1) >> 1) + 16 * ((j + 1) & 1));
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int w = e >> 1, sh = (e & 1) * 16;
-      const uint32_t a0 = (x[0][w] >> sh) & 0xffffu, a1 = (x[1][w] >> sh) & 0xffffu;
-      const uint32_t a2 = (x[2][w] >> sh) & 0xffffu, a3 = (x[3][w] >> sh) & 0xffffu;
-      *(u32x2_t *)(lds + (cb * 8 + e) * LDT + rb * 4) = u32x2_t{a0 | (a1 << 16), a2 | (a3 << 16)};
-    }
+    for (int i = 0; i < DT; ++i) acc[i] = mfma(f[cur][i], pj[j], acc[i]);
   }
 }
 
 // ------------------------------------------------------------------ forward
+// One workgroup: 128 queries of one head (4 waves of 32), key tiles of 64
+// double-buffered; a lane owns one query.
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n_qt) {
-  constexpr int LDK = HD + 8, LDV = kKT + 8, KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * LDV];
+  using TT = TokTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
   __shared__ int rng[2];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   const int h = t % a.Hq, qt = n_qt - 1 - t / a.Hq;
@@ -152,24 +251,25 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);   // latest query row of the wave
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
+  const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
   const bf16_t *kbase = qkv + (a.Hq + g) * HD, *vbase = qkv + (a.Hq + a.Hkv + g) * HD;
-  for (int k0 = kv_lo; k0 <= kv_hi; k0 += kKT) {
-    stage_rows<kKT, HD, LDK>(Ks, kbase, ld, k0, kv_hi + 1);
-    stage_rows_t<kKT, HD, LDV>(Vt, vbase, ld, k0, kv_hi + 1);
-    __syncthreads();
-    if (k0 <= w_hi && k0 + kKT - 1 >= w_lo) {
+  TT::load(Ks[0], kbase, ld, kv_lo, kv_hi + 1);
+  TT::load(Vs[0], vbase, ld, kv_lo, kv_hi + 1);
+  dma_wait();
+  __syncthreads();
+  for (int it = 0; it < n_kt; ++it) {
+    const int buf = it & 1, k0 = kv_lo + it * kTR;
+    if (it + 1 < n_kt) {
+      TT::load(Ks[buf ^ 1], kbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(Vs[buf ^ 1], vbase, ld, k0 + kTR, kv_hi + 1);
+    }
+    if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2];
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[tt][r] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          bf16x8_t kf = *(const bf16x8_t *)(Ks + (32 * tt + lq) * LDK + 16 * kk + 8 * hl);
-          s[tt] = mfma(kf, qf[kk], s[tt]);
-        }
+      rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
       float mx = -INFINITY;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
@@ -199,17 +299,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
       for (int i = 0; i < DT; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16x8_t pf = pack8(s[j >> 1], 8 * (j & 1));
-        const int kvo = 32 * (j >> 1) + 16 * (j & 1) + 4 * hl;
-#pragma unroll
-        for (int i = 0; i < DT; ++i) {
-          const bf16x8_t vf = ld_split(Vt + (32 * i + lq) * LDV + kvo);
-          o[i] = mfma(vf, pf, o[i]);
-        }
-      }
+      const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
+      cols_times<HD>(o, Vs[buf], pj);                    // O^T += V^T P^T
     }
+    lds_wait();
+    dma_wait();
     __syncthreads();
   }
   if (!qv) return;
@@ -227,12 +321,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
 }
 
 // ------------------------------------------------------------------ dQ
+// Same workgroup shape as the forward; a lane owns one query.
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int n_qt) {
-  constexpr int LDK = HD + 8, LDT = kKT + 8, KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[kKT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[HD * LDT];
+  using TT = TokTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
   __shared__ int rng[2];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   const int h = t % a.Hq, qt = n_qt - 1 - t / a.Hq;
@@ -272,26 +367,26 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
+  const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
   const bf16_t *kbase = qkv + (a.Hq + g) * HD, *vbase = qkv + (a.Hq + a.Hkv + g) * HD;
-  for (int k0 = kv_lo; k0 <= kv_hi; k0 += kKT) {
-    stage_rows<kKT, HD, LDK>(Ks, kbase, ld, k0, kv_hi + 1);
-    stage_rows<kKT, HD, LDK>(Vs, vbase, ld, k0, kv_hi + 1);
-    stage_rows_t<kKT, HD, LDT>(Kt, kbase, ld, k0, kv_hi + 1);
-    __syncthreads();
-    if (k0 <= w_hi && k0 + kKT - 1 >= w_lo) {
+  TT::load(Ks[0], kbase, ld, kv_lo, kv_hi + 1);
+  TT::load(Vs[0], vbase, ld, kv_lo, kv_hi + 1);
+  dma_wait();
+  __syncthreads();
+  for (int it = 0; it < n_kt; ++it) {
+    const int buf = it & 1, k0 = kv_lo + it * kTR;
+    if (it + 1 < n_kt) {
+      TT::load(Ks[buf ^ 1], kbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(Vs[buf ^ 1], vbase, ld, k0 + kTR, kv_hi + 1);
+    }
+    if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2], dp[2];
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          const int off = (32 * tt + lq) * LDK + 16 * kk + 8 * hl;
-          s[tt] = mfma(*(const bf16x8_t *)(Ks + off), qf[kk], s[tt]);
-          dp[tt] = mfma(*(const bf16x8_t *)(Vs + off), df[kk], dp[tt]);
-        }
+      rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
+      rows_times<HD>(dp, Vs[buf], df);                   // dP^T = V dO^T
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
@@ -301,15 +396,11 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
           const float p = ok ? exp2f(s[tt][r] * c - lse2) : 0.f;
           s[tt][r] = p * (dp[tt][r] - dlt);
         }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16x8_t sf = pack8(s[j >> 1], 8 * (j & 1));
-        const int kvo = 32 * (j >> 1) + 16 * (j & 1) + 4 * hl;
-#pragma unroll
-        for (int i = 0; i < DT; ++i)
-          acc[i] = mfma(ld_split(Kt + (32 * i + lq) * LDT + kvo), sf, acc[i]);
-      }
+      const bf16x8_t sj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
+      cols_times<HD>(acc, Ks[buf], sj);                  // dQ^T += K^T dS^T
     }
+    lds_wait();
+    dma_wait();
     __syncthreads();
   }
   if (!qv) return;
@@ -325,14 +416,17 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
 }
 
 // ------------------------------------------------------------------ dK, dV
+// One workgroup: 128 keys of one key/value head (4 waves of 32), a lane owns
+// one key; it walks every query head of the group and the segment's query
+// tiles of 64 after the keys, double-buffered (Q, dO and the queries' LSE and
+// delta).
 template <int HD>
 __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n_kt) {
-  constexpr int LDQ = HD + 8, LDT = kQT + 8, KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[kQT * LDQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Ds[kQT * LDQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[HD * LDT];
-  __shared__ __attribute__((aligned(16))) uint16_t Dt[HD * LDT];
-  __shared__ float Ls[kQT], Dl[kQT];
+  using TT = TokTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[2][TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) uint16_t Ds[2][TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) float Ls[2][kTR], Dl[2][kTR];
   __shared__ int rng[1];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   const int g = t % a.Hkv, kt = t / a.Hkv;   // early keys of a segment see the most queries
@@ -368,59 +462,62 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
   __syncthreads();
   const int q_hi = rng[0];    // queries [k0, q_hi)
   const int group = a.Hq / a.Hkv;
-  for (int hh = 0; hh < group; ++hh) {
-    const int h = g * group + hh;
-    for (int qb = k0; qb < q_hi; qb += kQT) {
-      stage_rows<kQT, HD, LDQ>(Qs, qkv + h * HD, ld, qb, q_hi);
-      stage_rows<kQT, HD, LDQ>(Ds, dout + h * HD, ldo, qb, q_hi);
-      stage_rows_t<kQT, HD, LDT>(Qt, qkv + h * HD, ld, qb, q_hi);
-      stage_rows_t<kQT, HD, LDT>(Dt, dout + h * HD, ldo, qb, q_hi);
-      if (threadIdx.x < kQT) {
-        const int qr = qb + threadIdx.x;
-        Ls[threadIdx.x] = qr < q_hi ? a.lse[(int64_t)h * a.n_tok + qr] * kLog2e : 0.f;
-        Dl[threadIdx.x] = qr < q_hi ? a.delta[(int64_t)h * a.n_tok + qr] : 0.f;
-      }
-      __syncthreads();
-      if (qb + kQT - 1 >= w_lo && qb <= w_hi) {
-        // S = Q K^T, dP = dO V^T: [64 queries x 32 keys] as two row tiles
-        f32x16_t s[2], dp[2];
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-          for (int tt = 0; tt < 2; ++tt) {
-            const int off = (32 * tt + lq) * LDQ + 16 * kk + 8 * hl;
-            s[tt] = mfma(*(const bf16x8_t *)(Qs + off), kf[kk], s[tt]);
-            dp[tt] = mfma(*(const bf16x8_t *)(Ds + off), vf[kk], dp[tt]);
-          }
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int ql = 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-            const int qr = qb + ql;
-            const bool ok = kvv && qr >= kv && qr < ke;
-            const float p = ok ? exp2f(s[tt][r] * c - Ls[ql]) : 0.f;
-            s[tt][r] = p;
-            dp[tt][r] = p * (dp[tt][r] - Dl[ql]);
-          }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const bf16x8_t pf = pack8(s[j >> 1], 8 * (j & 1));
-          const bf16x8_t sf = pack8(dp[j >> 1], 8 * (j & 1));
-          const int qo = 32 * (j >> 1) + 16 * (j & 1) + 4 * hl;
-#pragma unroll
-          for (int i = 0; i < DT; ++i) {
-            dv[i] = mfma(ld_split(Dt + (32 * i + lq) * LDT + qo), pf, dv[i]);
-            dk[i] = mfma(ld_split(Qt + (32 * i + lq) * LDT + qo), sf, dk[i]);
-          }
-        }
-      }
-      __syncthreads();
+  const int n_qb = q_hi > k0 ? (q_hi - k0 + kTR - 1) / kTR : 0;
+  const int n_it = group * n_qb;
+  // item it: query head g*group + it / n_qb, query tile k0 + 64 * (it % n_qb)
+  auto load_item = [&](int it, int buf) {
+    const int h = g * group + it / n_qb, qb = k0 + kTR * (it % n_qb);
+    TT::load(Qs[buf], qkv + h * HD, ld, qb, q_hi);
+    TT::load(Ds[buf], dout + h * HD, ldo, qb, q_hi);
+    if (w < 2) {                // one float per lane: LSE (wave 0), delta (wave 1)
+      const float *src = (w == 0 ? a.lse : a.delta) + (int64_t)h * a.n_tok + min(qb + lane, q_hi - 1);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(w == 0 ? Ls[buf] : Dl[buf]),
+                                       4, 0, 0);
     }
+  };
+  if (n_it > 0) load_item(0, 0);
+  dma_wait();
+  __syncthreads();
+  for (int it = 0; it < n_it; ++it) {
+    const int buf = it & 1, qb = k0 + kTR * (it % n_qb);
+    if (it + 1 < n_it) load_item(it + 1, buf ^ 1);
+    if (qb + kTR - 1 >= w_lo && qb <= w_hi) {
+      // S = Q K^T, dP = dO V^T: [64 queries x 32 keys] as two row tiles
+      f32x16_t s[2], dp[2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
+      // the lane's 32 query rows: 32tt + 8(r/4) + 4hl + r%4
+      f32x4_t lv[2][4], dl[2][4];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          lv[tt][r4] = lds_read_f4(Ls[buf] + 32 * tt + 8 * r4 + 4 * hl);
+          dl[tt][r4] = lds_read_f4(Dl[buf] + 32 * tt + 8 * r4 + 4 * hl);
+        }
+      rows_times<HD>(s, Qs[buf], kf);
+      rows_times<HD>(dp, Ds[buf], vf);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int ql = 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
+          const int qr = qb + ql;
+          const bool ok = kvv && qr >= kv && qr < ke;
+          const float p = ok ? exp2f(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e) : 0.f;
+          s[tt][r] = p;
+          dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
+        }
+      const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
+      const bf16x8_t sj[4] = {pack8(dp[0], 0), pack8(dp[0], 8), pack8(dp[1], 0), pack8(dp[1], 8)};
+      cols_times<HD>(dv, Ds[buf], pj);                   // dV^T += dO^T P
+      cols_times<HD>(dk, Qs[buf], sj);                   // dK^T += Q^T dS
+    }
+    lds_wait();
+    dma_wait();
+    __syncthreads();
   }
   if (!kvv) return;
   bf16_t *base = (bf16_t *)a.dqkv + (int64_t)kv * ld;
