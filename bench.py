@@ -209,7 +209,9 @@ def main():
               key=lambda k: classes[k]["ms"])
     d = classes[dom]
     kernel_names = {"gemm_nt": "gemm_mfma_kernel<true, true>", "gemm_nn": "gemm_mfma_kernel<true, false>",
-                    "gemm_tn": "gemm_mfma_kernel<false, false>", "attn_fwd": "attn_fwd_mfma_kernel",
+                    "gemm_tn": "gemm_mfma_kernel<false, false>",
+                    "gemm4_nt": "gemm_mfma4_kernel<true, true>", "gemm4_nn": "gemm_mfma4_kernel<true, false>",
+                    "gemm4_tn": "gemm_mfma4_kernel<false, false>", "attn_fwd": "attn_fwd_mfma_kernel",
                     "lm_fwd": "lm_fwd_fused_kernel", "lm_dz": "lm_dz_fused_kernel"}
     fl_dom = {"attn_fwd": att_fwd}.get(dom, rec[dom][2])
     roof = {"kernel": kernel_names.get(dom, dom), "bound": "mfma", "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2),

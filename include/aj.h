@@ -252,7 +252,9 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
  * keeps besides the error text) and meant for a single-threaded driver.
  *   AJ_KC_MERGE      one aj_merge_timelines / aj_flatten_timelines call
  *   AJ_KC_GEMM_*     the MFMA GEMM, by operand layout (NT: both K-major;
- *                    NN: B N-major; TN: A M-major and B N-major)
+ *                    NN: B N-major; TN: A M-major and B N-major), 8-wave
+ *                    kernel (reductions shorter than 4096 per split)
+ *   AJ_KC_GEMM4_*    the same layouts, 4-wave kernel (longer reductions)
  *   AJ_KC_ATTN_FWD / AJ_KC_ATTN_BWD   the attention kernels of one call
  *   AJ_KC_LM_FWD     the fused logits + log-sum-exp kernel of the LM head
  *   AJ_KC_LM_DZ      the fused logits-recompute + d logits kernel (one per chunk)
@@ -261,7 +263,7 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
  * forward product, and for the other classes). */
 enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
        AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_LM_FWD = 6, AJ_KC_LM_DZ = 7,
-       AJ_KC_COUNT = 8 };
+       AJ_KC_GEMM4_NT = 8, AJ_KC_GEMM4_NN = 9, AJ_KC_GEMM4_TN = 10, AJ_KC_COUNT = 11 };
 /* on != 0 starts recording (clearing any earlier record); 0 stops. */
 int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */

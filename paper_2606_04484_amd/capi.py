@@ -108,7 +108,8 @@ EXPORTS = {
     "aj_timing_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
 }
 
-KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd", "lm_fwd", "lm_dz")
+KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd", "lm_fwd", "lm_dz",
+            "gemm4_nt", "gemm4_nn", "gemm4_tn")
 
 
 def _declare(L):

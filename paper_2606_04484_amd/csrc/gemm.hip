@@ -25,14 +25,14 @@ struct EpArgs {
   int vec;   // 4-column vector stores are aligned (C, R, partial rows)
 };
 
-using gemm_core::Cfg;
 using gemm_core::f32x16_t;
 
-template <bool A_K, bool B_K>
-__global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
-    int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
-    int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K> sm;
+// Shared body of the two GEMM kernels: main loop of configuration C, then
+// the epilogue through LDS.
+template <bool A_K, bool B_K, typename Cfg>
+AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda,
+                      const bf16_t *B, int64_t ldb, const EpArgs &ep, float *partial,
+                      gemm_core::Smem<A_K, B_K, Cfg> &sm) {
   const int tiles_m = (M + Cfg::BM - 1) / Cfg::BM, tiles_n = (N + Cfg::BN - 1) / Cfg::BN;
   const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
   const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
@@ -41,7 +41,11 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  if constexpr (Cfg::NT == 512)
+    gemm_core::mainloop<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  else
+    gemm_core::mainloop4<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  __syncthreads();
 
   // Epilogue through LDS, 32 rows of each wave row at a time: the lane's
   // accumulators (column lane%32, rows 8*(r/4) + 4*(lane/32) + r%4 of each
@@ -116,6 +120,26 @@ __global__ __launch_bounds__(Cfg::NT, 1) void gemm_mfma_kernel(
   }
 }
 
+// 8 waves of 128x64: the default.
+template <bool A_K, bool B_K>
+__global__ __launch_bounds__(gemm_core::Cfg::NT, 1) void gemm_mfma_kernel(
+    int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
+    int64_t ldb, EpArgs ep, float *partial) {
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K, gemm_core::Cfg> sm;
+  gemm_tile<A_K, B_K, gemm_core::Cfg>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
+}
+
+// 4 waves of 128x128 with the fixed issue order: reductions of kLongK and more.
+template <bool A_K, bool B_K>
+__global__ __launch_bounds__(gemm_core::Cfg4::NT, 1) void gemm_mfma4_kernel(
+    int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
+    int64_t ldb, EpArgs ep, float *partial) {
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K, gemm_core::Cfg4> sm;
+  gemm_tile<A_K, B_K, gemm_core::Cfg4>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
+}
+
+constexpr int kLongK = 4096;
+
 // ---------------------------------------------------------------- float32 / fallback
 template <typename T>
 __global__ __launch_bounds__(256) void gemm_simple_kernel(int M, int N, int K, int k_per_split,
@@ -175,12 +199,16 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(int M, int N, int K, i
 }
 
 template <bool A_K, bool B_K>
-void launch_mfma(const Gemm &g, const EpArgs &ep, int kps, hipStream_t s) {
-  const int tiles = ((g.M + Cfg::BM - 1) / Cfg::BM) * ((g.N + Cfg::BN - 1) / Cfg::BN);
+void launch_mfma(const Gemm &g, const EpArgs &ep, int kps, bool long_k, hipStream_t s) {
+  const int tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   dim3 grid(tiles, 1, g.split_k);
-  gemm_mfma_kernel<A_K, B_K><<<grid, Cfg::NT, 0, s>>>(
-      g.M, g.N, g.K, kps, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, ep,
-      g.split_k > 1 ? g.partial : nullptr);
+  float *part = g.split_k > 1 ? g.partial : nullptr;
+  if (long_k)
+    gemm_mfma4_kernel<A_K, B_K><<<grid, gemm_core::Cfg4::NT, 0, s>>>(
+        g.M, g.N, g.K, kps, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, ep, part);
+  else
+    gemm_mfma_kernel<A_K, B_K><<<grid, gemm_core::Cfg::NT, 0, s>>>(
+        g.M, g.N, g.K, kps, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, ep, part);
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
@@ -214,12 +242,14 @@ int gemm(const Gemm &g, hipStream_t s) {
            aligned16(g.A) && aligned16(g.B);
   }
   if (mfma) {
-    const int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
+    const bool long_k = kps >= kLongK;
+    int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
+    if (long_k) kc += AJ_KC_GEMM4_NT - AJ_KC_GEMM_NT;
     const int tk = timing_begin(s, kc, g.recompute ? 0.0 : 2.0 * g.M * g.N * (double)g.K);
-    if (g.a_kmajor && g.b_kmajor) launch_mfma<true, true>(g, ep, kps, s);
-    else if (g.a_kmajor) launch_mfma<true, false>(g, ep, kps, s);
-    else if (g.b_kmajor) launch_mfma<false, true>(g, ep, kps, s);
-    else launch_mfma<false, false>(g, ep, kps, s);
+    if (g.a_kmajor && g.b_kmajor) launch_mfma<true, true>(g, ep, kps, long_k, s);
+    else if (g.a_kmajor) launch_mfma<true, false>(g, ep, kps, long_k, s);
+    else if (g.b_kmajor) launch_mfma<false, true>(g, ep, kps, long_k, s);
+    else launch_mfma<false, false>(g, ep, kps, long_k, s);
     timing_end(s, tk);
   } else {
     dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, S);

@@ -210,6 +210,193 @@ AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda
   }
 }
 
+// ---------------------------------------------------------------------------
+// Four waves, one per SIMD, as 2 x 2, each 128x128 (4x4 MFMA tiles, 256
+// float32 accumulators per lane, held in AGPRs).  Against 8 waves of 128x64
+// this halves the LDS fragment traffic per MFMA; with a single wave per SIMD
+// nothing else hides latency, so the k loop is issued in a fixed order: in
+// every 16-wide slice the next slice's 8 fragment reads follow the first 8
+// MFMAs, and in the first slice of a k-step each of the 16 MFMAs is followed
+// by one of the next k-step's 16 direct-to-LDS copies (scheduling barriers
+// keep the compiler from regrouping them).  Used for long reductions, where
+// its heavier per-tile prologue and epilogue are amortised.
+using Cfg4 = MfmaCfg<256, 256, 64, 2, 2>;
+
+// Loop-invariant part of a wave's direct-to-LDS copies of one operand: the
+// byte offset of each lane's 16 bytes from the tile's first element, for a
+// k-step that lies wholly inside [kbeg, kend).  Only the uniform tile base
+// moves from k-step to k-step.
+template <bool KMAJOR>
+struct Copier {
+  static constexpr int kInstr = Tile<256, KMAJOR>::kInstr;
+  uint32_t off[kInstr];
+  int64_t step;                       // elements from one k-step's tile to the next
+
+  AJ_DEV void init(int64_t ld, int r0, int rows) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < kInstr; ++q) {
+      const int blk = wave * kInstr + q;
+      if (KMAJOR) {
+        const int r = blk * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        const int rr = min(r0 + r, rows - 1) - r0;
+        off[q] = (uint32_t)(((int64_t)rr * ld + 8 * c) * 2);
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        const int c = (lane & 31) ^ (4 * (kr & 3));
+        const int rr = min(r0 + 8 * c, rows - 8) - r0;
+        off[q] = (uint32_t)(((int64_t)kr * ld + rr) * 2);
+      }
+    }
+    step = KMAJOR ? 64 : 64 * ld;
+  }
+  // tile: first element of the k-step's operand tile (row r0, k k0)
+  AJ_DEV void issue(uint16_t *lds, const bf16_t *tile) const {
+    const int wave = threadIdx.x >> 6;
+    const char *base = reinterpret_cast<const char *>(tile);
+#pragma unroll
+    for (int q = 0; q < kInstr; ++q)
+      __builtin_amdgcn_global_load_lds(
+          base + off[q], (__attribute__((address_space(3))) void *)(lds + (wave * kInstr + q) * 512),
+          16, 0, 0);
+  }
+};
+
+template <bool A_K, bool B_K>
+struct Sched4 {
+  using TA = Tile<256, A_K>;
+  using TB = Tile<256, B_K>;
+  // next-slice fragment read number q (0..7): A fragments first, then B
+  AJ_DEV static void read_one(int q, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4], const uint16_t *as,
+                              const uint16_t *bs, int wm, int wn, int kk) {
+    if (q < 4) fa[q] = TA::frag(as, wm * 128 + q * 32, kk);
+    else fb[q - 4] = TB::frag(bs, wn * 128 + (q - 4) * 32, kk);
+  }
+};
+
+// One 16-wide k slice: 16 MFMAs on (fa, fb) in a fixed issue order with the
+// next slice's 8 fragment reads after the first 8 MFMAs and, in the first
+// slice of a k-step, one of the next k-step's 16 copies after each MFMA.
+template <bool A_K, bool B_K, bool kCopy, bool kRead>
+AJ_DEV void slice4(f32x16_t (&acc)[4][4], const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4],
+                   bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as, const uint16_t *bs,
+                   int wm, int wn, int kk_next, const Copier<A_K> &ca, const Copier<B_K> &cb,
+                   uint16_t *la, uint16_t *lb, const bf16_t *ta, const bf16_t *tb) {
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    acc[t >> 2][t & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[t >> 2], fb[t & 3],
+                                                                  acc[t >> 2][t & 3], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kRead && t < 8) Sched4<A_K, B_K>::read_one(t, na, nb, as, bs, wm, wn, kk_next);
+    if (kCopy) {
+      if (t < Copier<A_K>::kInstr) {
+        __builtin_amdgcn_global_load_lds(
+            reinterpret_cast<const char *>(ta) + ca.off[t],
+            (__attribute__((address_space(3))) void *)(la + (wave * Copier<A_K>::kInstr + t) * 512),
+            16, 0, 0);
+      } else {
+        const int u = t - Copier<A_K>::kInstr;
+        __builtin_amdgcn_global_load_lds(
+            reinterpret_cast<const char *>(tb) + cb.off[u],
+            (__attribute__((address_space(3))) void *)(lb + (wave * Copier<B_K>::kInstr + u) * 512),
+            16, 0, 0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <bool A_K, bool B_K>
+AJ_DEV void mainloop4(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, const bf16_t *B,
+                      int64_t ldb, int M, int N, int m0, int n0, int kbeg, int kend,
+                      Smem<A_K, B_K, Cfg4> &sm) {
+  using TA = Tile<256, A_K>;
+  using TB = Tile<256, B_K>;
+  static_assert(Copier<A_K>::kInstr + Copier<B_K>::kInstr == 16, "copies per k-step");
+  constexpr int BK = 64;
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  const int nfull = kend > kbeg ? (kend - kbeg) / BK : 0;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  if (nk == 0) return;
+  Copier<A_K> ca;
+  Copier<B_K> cb;
+  ca.init(lda, m0, M);
+  cb.init(ldb, n0, N);
+  const bf16_t *ta = A + (A_K ? (int64_t)m0 * lda + kbeg : (int64_t)kbeg * lda + m0);
+  const bf16_t *tb = B + (B_K ? (int64_t)n0 * ldb + kbeg : (int64_t)kbeg * ldb + n0);
+  auto load_step = [&](int kt, int buf) {
+    if (kt < nfull) {
+      ca.issue(sm.a[buf], ta + kt * ca.step);
+      cb.issue(sm.b[buf], tb + kt * cb.step);
+    } else if (kt < nk) {
+      TA::load(sm.a[buf], A, lda, m0, M, kbeg + kt * BK, kend);
+      TB::load(sm.b[buf], B, ldb, n0, N, kbeg + kt * BK, kend);
+    }
+  };
+  bf16x8_t f0a[4], f0b[4], f1a[4], f1b[4];
+  auto read_slice = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[4], const uint16_t *as,
+                        const uint16_t *bs, int kk) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) Sched4<A_K, B_K>::read_one(q, fa, fb, as, bs, wm, wn, kk);
+  };
+  load_step(0, 0);
+  wait_lds_dma();
+  __syncthreads();
+  read_slice(f0a, f0b, sm.a[0], sm.b[0], 0);
+  int kt = 0;
+  // steady state: the next k-step is a full one, copied in the first slice
+  for (; kt + 1 < nfull; ++kt) {
+    const int buf = kt & 1;
+    const uint16_t *as = sm.a[buf], *bs = sm.b[buf];
+    const bf16_t *na = ta + (kt + 1) * ca.step, *nb = tb + (kt + 1) * cb.step;
+    frag_wait(f0a, f0b);
+    slice4<A_K, B_K, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
+                                 sm.a[buf ^ 1], sm.b[buf ^ 1], na, nb);
+    frag_wait(f1a, f1b);
+    slice4<A_K, B_K, false, true>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 32, ca, cb,
+                                  nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f0a, f0b);
+    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 48, ca, cb,
+                                  nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f1a, f1b);
+    slice4<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
+                                   nullptr, nullptr, nullptr, nullptr);
+    wait_lds_dma();
+    __syncthreads();
+    read_slice(f0a, f0b, sm.a[buf ^ 1], sm.b[buf ^ 1], 0);
+  }
+  // the last one or two k-steps (the last may be ragged)
+  for (; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    const uint16_t *as = sm.a[buf], *bs = sm.b[buf];
+    load_step(kt + 1, buf ^ 1);
+    frag_wait(f0a, f0b);
+    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
+                                  nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f1a, f1b);
+    slice4<A_K, B_K, false, true>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 32, ca, cb,
+                                  nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f0a, f0b);
+    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 48, ca, cb,
+                                  nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f1a, f1b);
+    slice4<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
+                                   nullptr, nullptr, nullptr, nullptr);
+    wait_lds_dma();
+    __syncthreads();
+    if (kt + 1 < nk) read_slice(f0a, f0b, sm.a[buf ^ 1], sm.b[buf ^ 1], 0);
+  }
+}
+
 // Row / column of accumulator element r of tile (i, j) for this lane: the
 // lane holds column lane%32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32.
 template <typename C = Cfg>
