@@ -200,11 +200,8 @@ int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w, cons
  *   logprob[i] = log softmax(hn[p-1] W_vocab^T)[tok[p]]
  *   r = exp(logprob[i] - old_logprob[p])
  *   loss += -min(r A, clip(r, 1-eps, 1+eps) A) * inv_n_mask,   A = adv[p]
- * bfloat16: the forward stores the float32 logits of the scored rows in
- * `saved` (n_tgt x vocab x 4 bytes, sized by aj_loss_saved_bytes) and the
- * backward reads them back instead of recomputing the vocab projection;
- * float32: the logits are recomputed one vocab_chunk-wide slab at a time.
- * The backward materialises one vocab_chunk-wide slab of d logits at a time.
+ * The vocab projection is streamed: logits never reach memory in the forward;
+ * the backward materialises one vocab_chunk-wide slab of d logits at a time.
  * d loss / d logprob = -A r inv_n_mask where the unclipped branch is active
  * ((A > 0 and r <= 1+eps) or (A < 0 and r >= 1-eps)), else 0.
  * Only the rows feeding a target are touched: the loss does not depend on
@@ -235,7 +232,7 @@ size_t aj_loss_workspace_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
  * logprob, lse: [n_tgt] float32 (written).  stats: float32[4] accumulated:
  * [0] loss (already scaled by inv_n_mask), [1] clipped-branch count,
  * [2] sum of r, [3] targets seen.  `saved` (aj_loss_saved_bytes) keeps the
- * normalised rows (and, bfloat16, the logits) for the backward. */
+ * normalised rows for the backward. */
 int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
                            const void *final_norm, const void *w_vocab, void *saved,
                            float *logprob, float *lse, float *stats, int32_t *err,

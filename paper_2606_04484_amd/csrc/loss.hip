@@ -4,12 +4,10 @@
 // Only the rows that feed a target are normalised and projected (the loss
 // reads no other logits).
 // bfloat16: the forward is one MFMA GEMM over the whole vocab whose epilogue
-// stores the float32 logits (kept in the `saved` arena for the backward),
 // reduces each 256-column logit tile to a per-row (max, sum of exp) partial
-// and picks up the target's logit; a small kernel then combines the partials
-// into the log-sum-exp.  The backward reads the stored logits back (a pass
-// over HBM instead of a second vocab-wide GEMM) and writes, per
-// vocab_chunk-wide slab,
+// and picks up the target's logit, so logits never reach memory; a small
+// kernel then combines the partials into the log-sum-exp.  The backward
+// recomputes each vocab_chunk-wide slab of logits and its epilogue writes
 //   dz = g * (onehot(target) - softmax)        g = d loss / d logprob
 // in bfloat16, then dhn += dz W_chunk and dW_chunk += dz^T hn are GEMMs.
 // float32 (the small workload): the same arithmetic with each chunk of logits
@@ -56,7 +54,6 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
 struct LossSaved {
   void *hn;
   float *rstd;
-  float *z;               // bfloat16 path: the float32 logits [n_tgt][vocab]
   size_t bytes;
 };
 
@@ -66,7 +63,6 @@ LossSaved carve_saved(const aj_loss_cfg &c, int n_tgt, void *base) {
   LossSaved s;
   s.hn = cv.take<char>((int64_t)n_tgt * c.d_model * es);
   s.rstd = cv.take<float>(n_tgt);
-  s.z = cv.take<float>(c.dtype == AJ_BF16 ? (int64_t)n_tgt * c.vocab : 1);
   s.bytes = cv.bytes();
   return s;
 }
@@ -244,12 +240,12 @@ AJ_DEV float half_sum(float v) {
   return v;
 }
 
-// logits tile z = hn W^T (rows: targets, columns: 256 vocab ids), stored to
-// z_out and reduced in registers: per row, the tile's max and sum of exp
-// (log2 units) and, in the tile that holds it, the target's logit.
+// logits tile z = hn W^T (rows: targets, columns: 256 vocab ids) reduced in
+// registers: per row, the tile's max and sum of exp (log2 units) and, in the
+// tile that holds it, the target's logit.  Logits never leave the chip.
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     int n, int V, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
-    const int32_t *tok, float2 *tile_ms, float *zt, float *z_out) {
+    const int32_t *tok, float2 *tile_ms, float *zt) {
   __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
   __shared__ int ttok[Cfg::BM];
   __shared__ float2 red[Cfg::WN][Cfg::BM];
@@ -270,16 +266,12 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     for (int r = 0; r < 16; ++r) {
       const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
       float v[Cfg::TN], mx = -INFINITY;
-      float *zrow = z_out + (int64_t)(m0 + rl) * V;
 #pragma unroll
       for (int j = 0; j < Cfg::TN; ++j) {
         const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
         v[j] = col < V ? acc[i][j][r] * kLog2e : -INFINITY;
         mx = fmaxf(mx, v[j]);
-        if (m0 + rl < n) {
-          if (col < V) zrow[col] = acc[i][j][r];
-          if (col == ttok[rl]) zt[m0 + rl] = acc[i][j][r];
-        }
+        if (col == ttok[rl] && m0 + rl < n) zt[m0 + rl] = acc[i][j][r];
       }
       mx = half_max(mx);
       float sm_ = 0.f;
@@ -325,35 +317,41 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(int n, int n_tiles, con
 }
 
 // dz = g (onehot(target) - softmax) for vocab columns [c0, c0 + cw), from the
-// stored logits, to bfloat16; 8 columns per thread.
-__global__ __launch_bounds__(256) void lm_dz_kernel(int n, int V, int cw, int c0, const float *z,
-                                                    const int32_t *tpos, const int32_t *tok,
-                                                    const float *lse, const float *g,
-                                                    bf16_t *dz) {
-  const int per_row = (cw + 7) / 8;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)n * per_row) return;
-  const int m = (int)(idx / per_row), j0 = (int)(idx % per_row) * 8;
-  const float *zr = z + (int64_t)m * V + c0 + j0;
-  bf16_t *out = dz + (int64_t)m * cw + j0;
-  const float l = lse[m] * kLog2e, gm = g[m];
-  const int t = tok[tpos[m]] - c0 - j0;
-  if (j0 + 8 <= cw && ((uintptr_t)zr & 15) == 0 && ((uintptr_t)out & 15) == 0) {
-    const float4 a = *reinterpret_cast<const float4 *>(zr);
-    const float4 b = *reinterpret_cast<const float4 *>(zr + 4);
-    const float e[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 8; k += 2) {
-      const float d0 = gm * ((t == k ? 1.f : 0.f) - exp2f(e[k] * kLog2e - l));
-      const float d1 = gm * ((t == k + 1 ? 1.f : 0.f) - exp2f(e[k + 1] * kLog2e - l));
-      o[k / 2] = (uint32_t)f2bf(d0) | ((uint32_t)f2bf(d1) << 16);
-    }
-    *reinterpret_cast<uint4 *>(out) = make_uint4(o[0], o[1], o[2], o[3]);
-  } else {
-    for (int k = 0; k < 8 && j0 + k < cw; ++k)
-      out[k] = f2bf(gm * ((t == k ? 1.f : 0.f) - exp2f(zr[k] * kLog2e - l)));
+// recomputed logits, straight to bfloat16.
+__global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
+    int n, int cw, int c0, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
+    const int32_t *tok, const float *lse, const float *g, bf16_t *dz) {
+  __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
+  __shared__ int ttok[Cfg::BM];
+  __shared__ float tl[Cfg::BM], tg[Cfg::BM];
+  const int tiles_m = (n + Cfg::BM - 1) / Cfg::BM, tiles_n = (cw + Cfg::BN - 1) / Cfg::BN;
+  const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
+  const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
+  if (threadIdx.x < Cfg::BM) {
+    const int m = m0 + threadIdx.x;
+    ttok[threadIdx.x] = m < n ? tok[tpos[m]] - c0 : -1;
+    tl[threadIdx.x] = m < n ? lse[m] * kLog2e : 0.f;
+    tg[threadIdx.x] = m < n ? g[m] : 0.f;
   }
+  f32x16_t acc[Cfg::TM][Cfg::TN];
+  gemm_core::mainloop<true, true, Cfg>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+#pragma unroll
+  for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
+      const int m = m0 + rl;
+      if (m >= n) continue;
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j) {
+        const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
+        if (col >= cw) continue;
+        const float p = exp2f(acc[i][j][r] * kLog2e - tl[rl]);
+        dz[(int64_t)m * cw + col] = f2bf(tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p));
+      }
+    }
 }
 
 int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
@@ -400,7 +398,7 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     const int tk = aj::timing_begin(st, AJ_KC_LM_FWD, 2.0 * n * (double)c.vocab * d);
     lm_fwd_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, c.vocab, d, (const bf16_t *)sv.hn,
                                                    (const bf16_t *)w_vocab, w.tpos, in.tok,
-                                                   w.tile_ms, w.zt, sv.z);
+                                                   w.tile_ms, w.zt);
     aj::timing_end(st, tk);
     lm_combine_kernel<<<(n + 3) / 4, 256, 0, st>>>(n, tiles_n, w.tile_ms, w.zt, lse, logprob);
     token_check_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, in.tok, c.vocab, err);
@@ -439,11 +437,11 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
     int r;
     if (sizeof(T) == 2) {
-      const int64_t work = (int64_t)n * ((cw + 7) / 8);
-      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);
-      lm_dz_kernel<<<(unsigned)((work + 255) / 256), 256, 0, st>>>(n, c.vocab, cw, c0, sv.z,
-                                                                   w.tpos, in.tok, lse, w.g,
-                                                                   (bf16_t *)w.dz);
+      const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
+      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
+      lm_dz_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, cw, c0, d, (const bf16_t *)sv.hn,
+                                                    (const bf16_t *)w_vocab, w.tpos, in.tok, lse,
+                                                    w.g, (bf16_t *)w.dz);
       aj::timing_end(st, tk);
     } else {
       if ((r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true))) return r;
