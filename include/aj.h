@@ -204,6 +204,12 @@ int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w, cons
  * the backward materialises one vocab_chunk-wide slab of d logits at a time.
  * d loss / d logprob = -A r inv_n_mask where the unclipped branch is active
  * ((A > 0 and r <= 1+eps) or (A < 0 and r >= 1-eps)), else 0.
+ * Optional KL penalty against a reference policy (the low-variance KL the
+ * GRPO recipe of Section 6 names, coefficient kl_coef): with
+ * delta = ref_logprob[i] - logprob[i],
+ *   kl = exp(delta) - delta - 1, clamped to [-10, 10],
+ *   loss += kl_coef * kl * inv_n_mask,  d loss / d logprob += kl_coef * (1 - exp(delta)) * inv_n_mask
+ * (the clamped side contributes no gradient).
  * Only the rows feeding a target are touched: the loss does not depend on
  * the logits of any other row.
  */
@@ -224,14 +230,17 @@ typedef struct {
   const float *old_logprob;     /* indexed by p */
   const float *adv;             /* indexed by p */
   float inv_n_mask;             /* 1 / (loss-masked tokens of the WHOLE batch) */
+  const float *ref_logprob;     /* [n_tgt] reference-policy log-prob of each target, or NULL */
+  float kl_coef;                /* KL penalty weight; no KL term when 0 or ref_logprob NULL */
 } aj_loss_in;
 
 size_t aj_loss_saved_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
 size_t aj_loss_workspace_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
 /* h [n_tok, d], final_norm [d], w_vocab [vocab, d] in cfg->dtype.
- * logprob, lse: [n_tgt] float32 (written).  stats: float32[4] accumulated:
- * [0] loss (already scaled by inv_n_mask), [1] clipped-branch count,
- * [2] sum of r, [3] targets seen.  `saved` (aj_loss_saved_bytes) keeps the
+ * logprob, lse: [n_tgt] float32 (written).  stats: float32[5] accumulated:
+ * [0] loss (policy-gradient plus KL terms, already scaled by inv_n_mask),
+ * [1] clipped-branch count, [2] sum of r, [3] targets seen, [4] sum of kl
+ * (unscaled; 0 without the KL term).  `saved` (aj_loss_saved_bytes) keeps the
  * normalised rows for the backward. */
 int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
                            const void *final_norm, const void *w_vocab, void *saved,

@@ -23,6 +23,14 @@ Its gradient with respect to logprob is -A r / N_mask where the unclipped
 branch is the active one -- (A > 0 and r <= 1+eps) or (A < 0 and r >= 1-eps),
 ties counting as unclipped -- and 0 elsewhere.
 
+Optional KL penalty against a frozen reference policy (Section 6's GRPO
+recipe names a KL loss with coefficient 2e-3 and the "low_var_kl"
+estimator; the paper gives no formula, so this is a reading: the k3
+estimator of KL(pi || pi_ref) at the sampled token, clamped to [-10, 10]):
+  delta = ref_logprob - logprob,   kl = exp(delta) - delta - 1
+  L += kl_coef * sum_mask kl / N_mask,   d kl / d logprob = 1 - exp(delta)
+(zero where the clamp binds).
+
 The backward pass is written out by hand from these formulas.
 """
 import numpy as np
@@ -123,6 +131,15 @@ def pg_terms(logprob, old, adv, eps):
     active = ((adv > 0) & (r <= 1.0 + eps)) | ((adv < 0) & (r >= 1.0 - eps))
     dterm = np.where(active, -adv * r, 0.0)
     return term, dterm, r
+
+
+def kl_terms(logprob, ref_logprob):
+    """Per-token low-variance KL estimate and its derivative with respect to logprob."""
+    delta = ref_logprob - logprob
+    e = np.exp(delta)
+    kl = e - delta - 1.0
+    inside = (kl >= -10.0) & (kl <= 10.0)
+    return np.clip(kl, -10.0, 10.0), np.where(inside, 1.0 - e, 0.0)
 
 
 def target_positions(cu_seqlens, n_tok):
@@ -239,12 +256,14 @@ def lm_head_backward(dlp, hn, rf, y, W, tok, tgt, lse, m, row_chunk=2048):
     return dy, dgf, dWv
 
 
-def actor_update(packed, W, m, n_mask=None):
+def actor_update(packed, W, m, n_mask=None, ref_logprob=None, kl_coef=0.0):
     """Forward + backward of the whole actor update over one packed batch.
 
     packed: oracle.merge.Packed (tok, pos, mask, old_logprob, adv, cu_seqlens).
     W: weights (any float dtype; used as float64).  n_mask: the loss
     normaliser, default the batch's own count of masked targets.
+    ref_logprob: optional [n_tok] reference-policy log-probs (read at the
+    masked targets) for the KL penalty with weight kl_coef.
     Returns dict: logprob [n_tok] (NaN at segment starts), loss, n_mask,
     grads {name: array} including 'emb', plus 'dx' (grad wrt the embeddings
     gathered per token) and per-target 'lse'.
@@ -264,6 +283,11 @@ def actor_update(packed, W, m, n_mask=None):
     sel = packed.mask[tgt] == 1
     term, dterm, r = pg_terms(lp_t[sel], packed.old_logprob[tgt][sel], packed.adv[tgt][sel],
                               m.clip_eps)
+    kl = np.zeros(len(term))
+    if ref_logprob is not None and kl_coef != 0.0:
+        kl, dkl = kl_terms(lp_t[sel], np.asarray(ref_logprob, np.float64)[tgt][sel])
+        term = term + kl_coef * kl
+        dterm = dterm + kl_coef * dkl
     loss = float(np.sum(term) / n_mask) if n_mask else 0.0
     dlp = np.zeros(len(tgt))
     if n_mask:
@@ -276,7 +300,8 @@ def actor_update(packed, W, m, n_mask=None):
     np.add.at(dE, tok, dx)
     g["emb"] = dE
     return {"logprob": logprob, "loss": loss, "n_mask": n_mask, "grads": g, "dx": dx,
-            "dy": dy, "y": y, "tgt": tgt, "lse": lse_t, "ratio": r, "term": term}
+            "dy": dy, "y": y, "tgt": tgt, "lse": lse_t, "ratio": r, "term": term,
+            "kl": kl}
 
 
 def current_logprob(packed, W, m):

@@ -121,7 +121,8 @@ class ActorUpdate:
         self.lcfg = C.loss_cfg(m)
         self.G = {k: torch.zeros(v.shape, dtype=torch.float32, device=self.dev)
                   for k, v in weights.items()}
-        self.stats = torch.zeros(4, dtype=torch.float32, device=self.dev)
+        # [0] loss, [1] clipped count, [2] sum of r, [3] targets, [4] sum of KL
+        self.stats = torch.zeros(5, dtype=torch.float32, device=self.dev)
         self.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
         self._cap = (0, 0)
 
@@ -153,8 +154,12 @@ class ActorUpdate:
         self.logprob = torch.empty(max(L.n_mask, 1), dtype=torch.float32, device=self.dev)
         self.lse = torch.empty(max(L.n_mask, 1), dtype=torch.float32, device=self.dev)
 
-    def step(self, L):
-        """Forward + backward over every pack of L; gradients accumulate into self.G."""
+    def step(self, L, ref_logprob=None, kl_coef=0.0):
+        """Forward + backward over every pack of L; gradients accumulate into self.G.
+
+        ref_logprob: optional [n_mask] float32 log-probs of L's targets under a
+        reference policy (e.g. forward_logprob of a frozen copy), for the KL
+        penalty with weight kl_coef."""
         if not hasattr(self, "logprob") or self.logprob.numel() < max(L.n_mask, 1):
             self.prepare(L)
         W, G = self.W, self.G
@@ -172,14 +177,16 @@ class ActorUpdate:
             C.aj_embed_fwd(tok, W["emb"], x, self.err)
             C.aj_varlen_block_fwd(self.bcfg, bw, cu, pos, p["max_len"], x, y, self.saved,
                                   base=t0)
+            ref = ref_logprob[r0:r1] if ref_logprob is not None else None
             C.aj_logprob_pg_loss_fwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
                                      self.logprob[r0:r1], self.lse[r0:r1], self.stats, self.lws,
-                                     self.err, row_base=t0)
+                                     self.err, row_base=t0, ref_logprob=ref, kl_coef=kl_coef)
             C.aj_logprob_pg_loss_bwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
                                      self.logprob[r0:r1], self.lse[r0:r1], dh,
-                                     G["final_norm"], G["w_vocab"], self.lws, row_base=t0)
+                                     G["final_norm"], G["w_vocab"], self.lws, row_base=t0,
+                                     ref_logprob=ref, kl_coef=kl_coef)
             C.aj_varlen_block_bwd(self.bcfg, bw, cu, pos, p["max_len"], x, self.saved, dh, dh, bg,
                                   self.bws, base=t0)
             C.aj_embed_bwd(tok, dh, G["emb"])

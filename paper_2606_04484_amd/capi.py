@@ -78,7 +78,8 @@ class LossCfg(C.Structure):
 
 class LossIn(C.Structure):
     _fields_ = [("n_tok", i32), ("n_tgt", i32), ("row_base", i32), ("targets", vp), ("tok", vp),
-                ("old_logprob", vp), ("adv", vp), ("inv_n_mask", f32)]
+                ("old_logprob", vp), ("adv", vp), ("inv_n_mask", f32), ("ref_logprob", vp),
+                ("kl_coef", f32)]
 
 
 EXPORTS = {
@@ -266,15 +267,16 @@ def aj_loss_workspace_bytes(cfg, n_tgt):
     return int(lib().aj_loss_workspace_bytes(C.byref(cfg), n_tgt))
 
 
-def _loss_in(n_tok, row_base, targets, tok, old_logprob, adv, inv_n_mask):
+def _loss_in(n_tok, row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob, kl_coef):
     return LossIn(n_tok, targets.numel(), row_base, ptr(targets), ptr(tok), ptr(old_logprob),
-                  ptr(adv), float(inv_n_mask))
+                  ptr(adv), float(inv_n_mask), ptr(ref_logprob), float(kl_coef))
 
 
 def aj_logprob_pg_loss_fwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
                            w_vocab, saved, logprob, lse, stats, ws, err=None, stream=None,
-                           row_base=0):
-    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask)
+                           row_base=0, ref_logprob=None, kl_coef=0.0):
+    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob,
+                  kl_coef)
     _check(lib().aj_logprob_pg_loss_fwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
                                         ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
                                         ptr(stats), ptr(err), ptr(ws),
@@ -284,8 +286,9 @@ def aj_logprob_pg_loss_fwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, f
 
 def aj_logprob_pg_loss_bwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
                            w_vocab, saved, logprob, lse, dh, d_final_norm, d_w_vocab, ws,
-                           stream=None, row_base=0):
-    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask)
+                           stream=None, row_base=0, ref_logprob=None, kl_coef=0.0):
+    li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob,
+                  kl_coef)
     _check(lib().aj_logprob_pg_loss_bwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
                                         ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
                                         ptr(dh), ptr(d_final_norm), ptr(d_w_vocab), ptr(ws),

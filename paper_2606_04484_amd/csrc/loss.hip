@@ -42,7 +42,7 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   w.g = cv.take<float>(n_tgt);
   w.tpos = cv.take<int32_t>(n_tgt);
   w.trow = cv.take<int32_t>(n_tgt);
-  w.part = cv.take<float>(kFinBlocks * 4);
+  w.part = cv.take<float>(kFinBlocks * 8);
   w.dhn = cv.take<float>((int64_t)n_tgt * c.d_model);
   w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n_tgt, c.d_model));
   const size_t sk = aj::gemm_split_floats((int)cw, c.d_model, n_tgt);
@@ -149,13 +149,30 @@ AJ_DEV float pg_grad(float lp, float old, float A, float eps, float *term, int *
   return active ? -A * r : 0.f;
 }
 
+// Low-variance KL estimate of the policy against the reference at one
+// target (delta = ref - lp): exp(delta) - delta - 1, clamped to [-10, 10];
+// *dkl = d kl / d lp (0 where clamped).
+AJ_DEV float kl_low_var(float lp, float ref, float *dkl) {
+  const float delta = ref - lp;
+  const float e = __expf(delta);
+  const float kl = e - delta - 1.f;
+  if (kl > 10.f || kl < -10.f) {
+    *dkl = 0.f;
+    return kl > 10.f ? 10.f : -10.f;
+  }
+  *dkl = 1.f - e;
+  return kl;
+}
+
+constexpr int kStats = 5;
+
 // run_m == nullptr: logprob (and lse) are already written.
 __global__ __launch_bounds__(256) void loss_finalize_kernel(
     int n, const int32_t *tpos, const float *old_lp, const float *adv, float eps, float inv_n,
-    const float *run_m, const float *run_s, const float *zt, float *logprob, float *lse,
-    float *part) {
-  __shared__ float red[4][256];
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    const float *ref_lp, float kl_coef, const float *run_m, const float *run_s, const float *zt,
+    float *logprob, float *lse, float *part) {
+  __shared__ float red[kStats][256];
+  float acc[kStats] = {0.f, 0.f, 0.f, 0.f, 0.f};
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
     float lp;
     if (run_m) {
@@ -170,40 +187,53 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(
     float term, r;
     int clipped;
     pg_grad(lp, old_lp[p], adv[p], eps, &term, &clipped, &r);
+    float kl = 0.f;
+    if (ref_lp) {
+      float dkl;
+      kl = kl_low_var(lp, ref_lp[i], &dkl);
+      term += kl_coef * kl;
+    }
     acc[0] += term * inv_n;
     acc[1] += (float)clipped;
     acc[2] += r;
     acc[3] += 1.f;
+    acc[4] += kl;
   }
 #pragma unroll
-  for (int k = 0; k < 4; ++k) red[k][threadIdx.x] = acc[k];
+  for (int k = 0; k < kStats; ++k) red[k][threadIdx.x] = acc[k];
   __syncthreads();
   for (int s = 128; s > 0; s >>= 1) {
     if ((int)threadIdx.x < s)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + s];
+      for (int k = 0; k < kStats; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + s];
     __syncthreads();
   }
-  if (threadIdx.x < 4) part[blockIdx.x * 4 + threadIdx.x] = red[threadIdx.x][0];
+  if (threadIdx.x < kStats) part[blockIdx.x * kStats + threadIdx.x] = red[threadIdx.x][0];
 }
 
 __global__ void stats_reduce_kernel(const float *part, int nb, float *stats) {
   const int k = threadIdx.x;
-  if (k >= 4) return;
+  if (k >= kStats) return;
   float s = 0.f;
-  for (int b = 0; b < nb; ++b) s += part[b * 4 + k];
+  for (int b = 0; b < nb; ++b) s += part[b * kStats + k];
   stats[k] += s;
 }
 
 __global__ void loss_grad_kernel(int n, const int32_t *tpos, const float *logprob,
                                  const float *old_lp, const float *adv, float eps, float inv_n,
-                                 float *g) {
+                                 const float *ref_lp, float kl_coef, float *g) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int p = tpos[i];
   float term, r;
   int clipped;
-  g[i] = pg_grad(logprob[i], old_lp[p], adv[p], eps, &term, &clipped, &r) * inv_n;
+  float d = pg_grad(logprob[i], old_lp[p], adv[p], eps, &term, &clipped, &r);
+  if (ref_lp) {
+    float dkl;
+    kl_low_var(logprob[i], ref_lp[i], &dkl);
+    d += kl_coef * dkl;
+  }
+  g[i] = d * inv_n;
 }
 
 // dz[i][j] = g_i * ((c0 + j == target_i) - exp(z_ij - lse_i))
@@ -414,9 +444,11 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   }
   int nb = (n + 255) / 256;
   if (nb > kFinBlocks) nb = kFinBlocks;
+  const float *ref = in.kl_coef != 0.f ? in.ref_logprob : nullptr;
   loss_finalize_kernel<<<nb, 256, 0, st>>>(n, w.tpos, in.old_logprob, in.adv, c.clip_eps,
-                                           in.inv_n_mask, fused ? nullptr : w.run_m, w.run_s,
-                                           w.zt, logprob, lse, w.part);
+                                           in.inv_n_mask, ref, in.kl_coef,
+                                           fused ? nullptr : w.run_m, w.run_s, w.zt, logprob,
+                                           lse, w.part);
   stats_reduce_kernel<<<1, 64, 0, st>>>(w.part, nb, stats);
   return aj::check_launch("aj_logprob_pg_loss_fwd");
 }
@@ -430,8 +462,10 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   if (n == 0) return aj::check_launch("aj_logprob_pg_loss_bwd");
   sanitize_targets_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, in.targets, in.row_base, in.n_tok,
                                                            w.tpos, w.trow, nullptr);
+  const float *ref = in.kl_coef != 0.f ? in.ref_logprob : nullptr;
   loss_grad_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, logprob, in.old_logprob, in.adv,
-                                                    c.clip_eps, in.inv_n_mask, w.g);
+                                                    c.clip_eps, in.inv_n_mask, ref, in.kl_coef,
+                                                    w.g);
   aj::fill_f32(w.dhn, (int64_t)n * d, 0.f, st);
   for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;

@@ -19,13 +19,18 @@ GRADS = ("emb", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down", 
          "w_vocab")
 
 
-def run_gpu(case, merged=True, pack_tokens=131072):
+def run_gpu(case, merged=True, pack_tokens=131072, ref_pos=None, kl_coef=0.0):
+    """ref_pos: optional reference log-probs per merged position (host array)."""
     from paper_2606_04484_amd import actor
     dev = actor.upload_timelines(case.tl, case.old)
     L = actor.merge(dev, merged=merged, pack_tokens=pack_tokens)
     A = actor.ActorUpdate(case.m, case.device_weights())
     A.zero_grads()
-    A.step(L)
+    ref = None
+    if ref_pos is not None:
+        tg = L.targets[:L.n_mask].cpu().numpy()
+        ref = torch.from_numpy(np.asarray(ref_pos, np.float32)[tg]).cuda()
+    A.step(L, ref_logprob=ref, kl_coef=kl_coef)
     torch.cuda.synchronize()
     lp = A.logprob[:L.n_mask].cpu().numpy().astype(np.float64)
     tg = L.targets[:L.n_mask].cpu().numpy()
@@ -35,8 +40,8 @@ def run_gpu(case, merged=True, pack_tokens=131072):
     return dict(lp=lp, targets=tg, grads=grads, loss=float(stats[0]), stats=stats, err=err, L=L)
 
 
-def check(case, got, merged, tol_lp, tol_loss, tol_g, min_cos):
-    ref = case.oracle(merged)
+def check(case, got, merged, tol_lp, tol_loss, tol_g, min_cos, ref=None):
+    ref = case.oracle(merged) if ref is None else ref
     assert got["err"] == 0
     np.testing.assert_array_equal(got["targets"],
                                   ref["tgt"][(case.merged if merged else case.unmerged).mask[ref["tgt"]] == 1])
@@ -127,3 +132,38 @@ def test_deterministic_except_embedding():
     for k in GRADS:
         if k != "emb":
             assert np.array_equal(a["grads"][k], b["grads"][k]), k
+
+
+def _ref_policy(case, merged=True, seed=2000):
+    """Reference log-probs per position: the oracle's forward under a second,
+    nearby set of weights (the frozen reference policy)."""
+    from oracle import model as M
+    from workloads import make_weights_numpy, bf16_round
+    W2 = make_weights_numpy(case.m, seed=seed, gain_std=0.1)
+    Wr = {k: case.W[k] + 0.3 * (W2[k] - case.W[k]) for k in case.W}
+    if case.m.dtype == "bf16":
+        Wr = {k: bf16_round(v) for k, v in Wr.items()}
+    return M.current_logprob(case.merged if merged else case.unmerged, Wr, case.m)
+
+
+@pytest.mark.parametrize("merged", [True, False])
+def test_tiny_f32_kl(merged):
+    from oracle import model as M
+    case = Case(get_config(0), margin=0.01)
+    ref_pos = _ref_policy(case, merged)
+    exp = M.actor_update(case.merged if merged else case.unmerged, case.W, case.m,
+                         ref_logprob=ref_pos, kl_coef=0.5)
+    assert np.max(exp["kl"]) < 10 and np.sum(exp["kl"]) > 0
+    got = run_gpu(case, merged, ref_pos=ref_pos, kl_coef=0.5)
+    check(case, got, merged, 1e-4, 1e-4, 1e-4, 0.99999, ref=exp)
+    assert abs(got["stats"][4] - np.sum(exp["kl"])) <= 1e-4 * np.sum(exp["kl"])
+
+
+def test_bf16_kl():
+    from oracle import model as M
+    m = bf16_case_model(**BF16_CASES["hd128_gqa3"])
+    case = Case(workload(m), noise_std=0.3, margin=0.05)
+    ref_pos = _ref_policy(case)
+    exp = M.actor_update(case.merged, case.W, case.m, ref_logprob=ref_pos, kl_coef=0.5)
+    got = run_gpu(case, True, ref_pos=ref_pos, kl_coef=0.5)
+    check(case, got, True, 2e-2, 1e-2, 1e-2, 0.999, ref=exp)

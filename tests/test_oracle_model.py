@@ -338,3 +338,67 @@ def test_block_forward_rows_matches_full():
     y, _ = M.block_forward(x, W, p.cu_seqlens, p.pos, m)
     rows = np.array([0, 4, 12])
     np.testing.assert_allclose(M.block_forward_rows(x, p.pos, rows, W, m), y[rows], atol=1e-13)
+
+
+# ------------------------------------------------------------------ KL penalty
+
+def test_kl_estimate_is_unbiased_for_the_divergence():
+    """Averaged over tokens drawn from the policy, exp(d) - d - 1 with
+    d = log pi_ref - log pi is exactly KL(pi || pi_ref) (scipy's rel_entr);
+    a flipped sign or a missing term breaks the identity."""
+    from scipy.special import rel_entr, log_softmax
+    rng = np.random.default_rng(3)
+    for _ in range(5):
+        z = rng.normal(0, 1.5, 50)
+        lp = log_softmax(z)
+        ref = log_softmax(z + rng.normal(0, 0.5, 50))
+        kl, _ = M.kl_terms(lp, ref)
+        assert np.all(kl < 10)
+        np.testing.assert_allclose(np.sum(np.exp(lp) * kl), np.sum(rel_entr(np.exp(lp), np.exp(ref))),
+                                   rtol=1e-12, atol=1e-14)
+
+
+def test_kl_closed_forms():
+    d = np.array([0.0, 1e-4, -1e-4, 40.0])
+    lp = np.full(4, -2.0)
+    kl, dkl = M.kl_terms(lp, lp + d)
+    assert kl[0] == 0.0 and dkl[0] == 0.0
+    np.testing.assert_allclose(kl[1:3], d[1:3] ** 2 / 2, rtol=1e-3)   # second order at 0
+    np.testing.assert_allclose(dkl[1:3], -d[1:3], rtol=1e-3)
+    assert kl[3] == 10.0 and dkl[3] == 0.0                              # the clamp binds
+
+
+@pytest.mark.parametrize("name", ["w_o", "final_norm", "w_vocab"])
+def test_kl_gradients_match_finite_differences(name):
+    m = SMALL
+    rng = np.random.default_rng(21)
+    W = M.f64_weights(make_weights_numpy(m, seed=12, gain_std=0.3))
+    p = _packed([6, 5, 4], m.vocab, rng, mask_p=0.7)
+    ref = rng.normal(-3.0, 0.7, p.n_tok)
+    out = M.actor_update(p, W, m, n_mask=7, ref_logprob=ref, kl_coef=0.37)
+    assert np.all(np.abs(np.abs(out["ratio"] - 1) - m.clip_eps) > 1e-3)
+    assert np.any(out["kl"] > 0)
+    g = out["grads"][name]
+    flat = list(np.ndindex(g.shape))
+
+    def loss(h, idx):
+        W2 = {k: v.copy() for k, v in W.items()}
+        W2[name][idx] += h
+        return M.actor_update(p, W2, m, n_mask=7, ref_logprob=ref, kl_coef=0.37)["loss"]
+
+    for idx in [flat[i] for i in rng.choice(len(flat), size=min(25, len(flat)), replace=False)]:
+        h = 1e-6 * max(1.0, abs(W[name][idx]))
+        fd = (loss(h, idx) - loss(-h, idx)) / (2 * h)
+        assert abs(fd - g[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (name, idx, fd, g[idx])
+
+
+def test_kl_coef_zero_is_the_plain_loss():
+    m = SMALL
+    rng = np.random.default_rng(5)
+    W = M.f64_weights(make_weights_numpy(m, seed=12, gain_std=0.3))
+    p = _packed([7, 5], m.vocab, rng)
+    a = M.actor_update(p, W, m)
+    b = M.actor_update(p, W, m, ref_logprob=rng.normal(-3, 1, p.n_tok), kl_coef=0.0)
+    assert a["loss"] == b["loss"]
+    for k in a["grads"]:
+        assert np.array_equal(a["grads"][k], b["grads"][k])
