@@ -33,6 +33,8 @@ def parse():
     ap.add_argument("--no-unmerged", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the KL / GRPO selection / AdamW measurements")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES three times and exit: the "
                          "reference for scaling the HBM byte counters")
@@ -110,6 +112,83 @@ def timed(A, merger, merged, steps, warmup, torch, capi, record=False):
         rec = capi.aj_timing_read()
         capi.aj_timing_enable(False)
     return L, dt, rec
+
+
+def extras(A, merger, m, tl, dev, torch, capi, actor, steps):
+    """The steps around the update, measured on the same workload:
+    the update with the KL penalty (a reference forward of a frozen copy of
+    the policy, then the step with the penalty), GRPO advantages + the
+    non-dummy episode selection, and one AdamW step over every parameter."""
+    from workloads import make_rewards
+    out = {}
+    # KL: reference log-probs (forward only) + the step with the penalty
+    Wref = {k: v.clone() for k, v in A.W.items()}
+    R = actor.ActorUpdate(m, Wref)
+    merger.launch(True)
+    L = merger.layout(m.pack_tokens)
+    R.prepare(L)
+    A.prepare(L)
+    for i in range(steps + 1):
+        if i == 1:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        A.zero_grads()
+        merger.launch(True)
+        L = merger.layout(m.pack_tokens)
+        ref = R.forward_logprob(L)
+        A.step(L, ref_logprob=ref, kl_coef=2e-3)
+    torch.cuda.synchronize()
+    out["kl_step"] = {"ms_per_step": round((time.perf_counter() - t0) / steps * 1e3, 3),
+                      "kl_coef": 2e-3, "includes": "reference forward + step with the KL term"}
+    del R, Wref
+    # GRPO advantages + selection (groups of 8 episodes)
+    off, rew = make_rewards(tl.n_traj, 8, seed=1)
+    goff, grew = torch.from_numpy(off).cuda(), torch.from_numpy(rew).cuda()
+    adv = torch.empty(tl.n_traj, dtype=torch.float32, device="cuda")
+    keep = torch.empty(tl.n_traj, dtype=torch.uint8, device="cuda")
+    so = {"traj_tl_off": torch.empty(tl.n_traj + 1, dtype=torch.int32, device="cuda"),
+          "tl_tok_off": torch.empty(tl.n_tl + 1, dtype=torch.int64, device="cuda"),
+          "tok": torch.empty(tl.n_tok, dtype=torch.int32, device="cuda"),
+          "flags": torch.empty(tl.n_tok, dtype=torch.uint8, device="cuda"),
+          "old_logprob": torch.empty(tl.n_tok, dtype=torch.float32, device="cuda"),
+          "adv": torch.empty(tl.n_tok, dtype=torch.float32, device="cuda"),
+          "counts": torch.zeros(3, dtype=torch.int64, device="cuda")}
+    ws = torch.empty(capi.aj_select_workspace_bytes(tl.n_traj, tl.n_tl), dtype=torch.uint8,
+                     device="cuda")
+    for i in range(3):
+        if i == 2:
+            capi.aj_timing_enable(True)
+        capi.aj_grpo_advantages(goff, grew, 1e-6, adv, keep)
+        capi.aj_select_episodes(dev, keep, adv, so, ws)
+    rec = capi.aj_timing_read()
+    capi.aj_timing_enable(False)
+    kept = so["counts"].cpu().numpy()
+    ms = rec["select"][0]
+    # bytes: every input token's flags + the kept ones' id, flags, log-prob read and
+    # id, flags, log-prob, advantage written; offsets are negligible
+    nb = tl.n_tok * 1 + int(kept[2]) * (4 + 1 + 4 + 4 + 1 + 4 + 4)
+    out["grpo_select"] = {"ms": round(ms, 4), "launches": rec["select"][1],
+                          "episodes_kept": int(kept[0]), "tokens_kept": int(kept[2]),
+                          "tokens_in": int(tl.n_tok), "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
+                          "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    # AdamW over every parameter: float32 master copy, moments, bfloat16 copy out
+    n = sum(v.numel() for v in A.W.values())
+    P = torch.cat([v.float().flatten() for v in A.W.values()])
+    G = torch.cat([v.flatten() for v in A.G.values()])
+    M1, M2 = torch.zeros_like(P), torch.zeros_like(P)
+    Pc = torch.empty(n, dtype=A.W["emb"].dtype, device="cuda")
+    for i in range(4):
+        if i == 1:
+            capi.aj_timing_enable(True)
+        capi.aj_adamw_step(P, G, M1, M2, 1e-6, 0.9, 0.999, 1e-8, 0.01, i + 1, param_copy=Pc)
+    rec = capi.aj_timing_read()
+    capi.aj_timing_enable(False)
+    ms = rec["adamw"][0] / rec["adamw"][1]
+    nb = n * (4 * 4 + 3 * 4 + Pc.element_size())
+    out["adamw"] = {"params": n, "ms": round(ms, 4), "bytes_per_param": nb // n,
+                    "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    return out
 
 
 def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
@@ -249,6 +328,8 @@ def main():
     if res_u:
         out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
         out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)
+    if not args.no_extras:
+        out["extras"] = extras(A, merger, m, tl, dev, torch, capi, actor, max(1, args.steps // 2))
     if not args.no_cpu_baseline:
         st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 1024)
         out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)

@@ -254,6 +254,57 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
                            float *d_final_norm, float *d_w_vocab, void *ws, size_t ws_bytes,
                            void *stream);
 
+/* ------------------------------------------------------------------ 4. around the update
+ * GRPO advantages (Section 3: GRPO-style updates; groups of rollouts per
+ * task, e.g. group size 8 in Section 5.3).  The episodes of group g are
+ * [group_off[g], group_off[g+1]) (group_off: [n_groups+1], tiling the
+ * episodes in order).  With the group's mean mu and sample standard deviation
+ * sd (Bessel's correction):
+ *   ep_adv[e] = (reward[e] - mu) / (sd + eps)
+ * Section 4.3's strategy C3 trains only on groups whose rewards are not all
+ * equal: ep_keep[e] = 1 iff e's group holds two different rewards; otherwise
+ * (one distinct reward, or a group of one) ep_adv[e] = 0 and ep_keep[e] = 0.
+ * float32 arithmetic; the keep decision compares rewards exactly.  Offsets
+ * that are not monotone from 0 raise AJ_DEVERR_OFFSETS (that group is left
+ * unwritten). */
+int aj_grpo_advantages(int32_t n_groups, const int32_t *group_off, const float *reward,
+                       float eps, float *ep_adv, uint8_t *ep_keep, int32_t *err, void *stream);
+
+/* A compacted copy of timelines: capacities are the input's sizes
+ * (traj_tl_off n_traj+1, tl_tok_off n_tl+1, per-token arrays n_tok). */
+typedef struct {
+  int32_t *traj_tl_off;
+  int64_t *tl_tok_off;
+  int32_t *tok;
+  uint8_t *flags;
+  float *old_logprob;
+  float *adv;
+  int64_t *counts;              /* [3] episodes, timelines, tokens kept */
+} aj_timelines_out;
+
+size_t aj_select_workspace_bytes(int32_t n_traj, int32_t n_tl);
+/* Keeps the episodes e with keep[e] != 0, in order, with their timelines and
+ * tokens; every kept llm token's advantage becomes ep_adv[e] (the episode's
+ * outcome advantage on all of its responses), 0 on the other tokens.
+ * in->adv is not read.  Offsets must tile as for aj_merge_timelines
+ * (checked on the device: AJ_DEVERR_OFFSETS and counts 0 otherwise). */
+int aj_select_episodes(const aj_timelines *in, const uint8_t *keep, const float *ep_adv,
+                       aj_timelines_out *out, int32_t *err, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* AdamW with decoupled weight decay (Loshchilov and Hutter) on n float32
+ * master parameters; step (4) of Section 4.2 runs optimizer steps after the
+ * loss (the optimizer is not named).  With t = step >= 1:
+ *   g = grad * grad_scale
+ *   m = beta1 m + (1 - beta1) g;   v = beta2 v + (1 - beta2) g^2
+ *   param -= lr * weight_decay * param + lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * param_copy (optional, n elements of copy_dtype, an aj_dtype) receives the
+ * updated parameters in the storage dtype the forward reads.  Elementwise;
+ * any n >= 0; pointers need no alignment. */
+int aj_adamw_step(int64_t n, float *param, const float *grad, float *m, float *v, float lr,
+                  float beta1, float beta2, float eps, float weight_decay, int32_t step,
+                  float grad_scale, void *param_copy, int copy_dtype, void *stream);
+
 /* ------------------------------------------------------------------ timing
  * Benchmark instrumentation.  While enabled, every launch of the kernel
  * classes below is bracketed by two hipEvents recorded on the launch's own
@@ -267,12 +318,15 @@ int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
  *   AJ_KC_ATTN_FWD / AJ_KC_ATTN_BWD   the attention kernels of one call
  *   AJ_KC_LM_FWD     the fused logits + log-sum-exp kernel of the LM head
  *   AJ_KC_LM_DZ      the fused logits-recompute + d logits kernel (one per chunk)
+ *   AJ_KC_ADAMW      one aj_adamw_step call
+ *   AJ_KC_SELECT     one aj_grpo_advantages or aj_select_episodes call
  * `flops` accumulates algorithmic flops where the library knows them
  * (2*M*N*K per GEMM and LM_FWD launch; 0 for LM_DZ, which recomputes a
  * forward product, and for the other classes). */
 enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
        AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_LM_FWD = 6, AJ_KC_LM_DZ = 7,
-       AJ_KC_GEMM4_NT = 8, AJ_KC_GEMM4_NN = 9, AJ_KC_GEMM4_TN = 10, AJ_KC_COUNT = 11 };
+       AJ_KC_GEMM4_NT = 8, AJ_KC_GEMM4_NN = 9, AJ_KC_GEMM4_TN = 10, AJ_KC_ADAMW = 11,
+       AJ_KC_SELECT = 12, AJ_KC_COUNT = 13 };
 /* on != 0 starts recording (clearing any earlier record); 0 stops. */
 int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */

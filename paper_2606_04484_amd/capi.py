@@ -53,6 +53,11 @@ class Packed(C.Structure):
                 ("adv", vp), ("targets", vp)]
 
 
+class TimelinesOut(C.Structure):
+    _fields_ = [("traj_tl_off", vp), ("tl_tok_off", vp), ("tok", vp), ("flags", vp),
+                ("old_logprob", vp), ("adv", vp), ("counts", vp)]
+
+
 class BlockCfg(C.Structure):
     _fields_ = [("d_model", i32), ("n_q_heads", i32), ("n_kv_heads", i32), ("head_dim", i32),
                 ("d_ff", i32), ("rms_eps", f32), ("rope_theta", f32), ("dtype", i32)]
@@ -105,12 +110,18 @@ EXPORTS = {
                                          vp, vp, vp, vp, vp, sz, vp]),
     "aj_logprob_pg_loss_bwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
                                          vp, vp, vp, vp, vp, vp, sz, vp]),
+    "aj_grpo_advantages": (C.c_int, [i32, vp, vp, f32, vp, vp, vp, vp]),
+    "aj_select_workspace_bytes": (sz, [i32, i32]),
+    "aj_select_episodes": (C.c_int, [C.POINTER(Timelines), vp, vp, C.POINTER(TimelinesOut), vp,
+                                     vp, sz, vp]),
+    "aj_adamw_step": (C.c_int, [i64, vp, vp, vp, vp, f32, f32, f32, f32, f32, i32, f32, vp,
+                                C.c_int, vp]),
     "aj_timing_enable": (C.c_int, [C.c_int]),
     "aj_timing_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
 }
 
 KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd", "lm_fwd", "lm_dz",
-            "gemm4_nt", "gemm4_nn", "gemm4_tn")
+            "gemm4_nt", "gemm4_nn", "gemm4_tn", "adamw", "select")
 
 
 def _declare(L):
@@ -153,7 +164,7 @@ def aj_merge_workspace_bytes(n_traj, n_tl, n_tok):
 def _timelines(t):
     return Timelines(int(t["traj_tl_off"].numel() - 1), int(t["tl_tok_off"].numel() - 1),
                      int(t["tok"].numel()), ptr(t["traj_tl_off"]), ptr(t["tl_tok_off"]),
-                     ptr(t["tok"]), ptr(t["flags"]), ptr(t["old_logprob"]), ptr(t["adv"]))
+                     ptr(t["tok"]), ptr(t["flags"]), ptr(t["old_logprob"]), ptr(t.get("adv")))
 
 
 def _packed(o):
@@ -294,6 +305,46 @@ def aj_logprob_pg_loss_bwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, f
                                         ptr(dh), ptr(d_final_norm), ptr(d_w_vocab), ptr(ws),
                                         ws.numel() * ws.element_size(), stream_handle(stream)),
            "aj_logprob_pg_loss_bwd")
+
+
+# ------------------------------------------------------------------ around the update
+
+def aj_grpo_advantages(group_off, reward, eps, ep_adv, ep_keep, err=None, stream=None):
+    _check(lib().aj_grpo_advantages(int(group_off.numel() - 1), ptr(group_off), ptr(reward),
+                                    float(eps), ptr(ep_adv), ptr(ep_keep), ptr(err),
+                                    stream_handle(stream)), "aj_grpo_advantages")
+
+
+def aj_select_workspace_bytes(n_traj, n_tl):
+    return int(lib().aj_select_workspace_bytes(n_traj, n_tl))
+
+
+def aj_select_episodes(tl, keep, ep_adv, out, ws, err=None, stream=None):
+    """tl: dict as for aj_merge_timelines (adv not read); out: dict of capacity-sized tensors
+    traj_tl_off, tl_tok_off, tok, flags, old_logprob, adv, counts (int64 [3])."""
+    o = TimelinesOut(*[ptr(out[k]) for k in ("traj_tl_off", "tl_tok_off", "tok", "flags",
+                                             "old_logprob", "adv", "counts")])
+    _check(lib().aj_select_episodes(C.byref(_timelines(tl)), ptr(keep), ptr(ep_adv), C.byref(o),
+                                    ptr(err), ptr(ws), ws.numel() * ws.element_size(),
+                                    stream_handle(stream)), "aj_select_episodes")
+
+
+def aj_adamw_step(param, grad, m, v, lr, beta1, beta2, eps, weight_decay, step, grad_scale=1.0,
+                  param_copy=None, stream=None):
+    """param, grad, m, v: float32 tensors of equal size; param_copy: optional float32 or
+    bfloat16 tensor receiving the updated parameters."""
+    for t in (param, grad, m, v):
+        if t.dtype != torch.float32 or t.numel() != param.numel():
+            raise AjError("aj_adamw_step: param, grad, m, v must be float32 of one size")
+    dt = 0
+    if param_copy is not None:
+        if param_copy.dtype not in (torch.float32, torch.bfloat16) or param_copy.numel() != param.numel():
+            raise AjError("aj_adamw_step: param_copy must be float32 or bfloat16 of the same size")
+        dt = 1 if param_copy.dtype == torch.bfloat16 else 0
+    _check(lib().aj_adamw_step(param.numel(), ptr(param), ptr(grad), ptr(m), ptr(v), float(lr),
+                               float(beta1), float(beta2), float(eps), float(weight_decay),
+                               int(step), float(grad_scale), ptr(param_copy), dt,
+                               stream_handle(stream)), "aj_adamw_step")
 
 
 # ------------------------------------------------------------------ timing

@@ -19,7 +19,16 @@ from oracle import model as M
 from workloads import get_config, make_timelines, make_weights_numpy
 from workloads.configs import ModelConfig
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _float64_torch():
+    """torch references in float64 for this module only (the session default
+    is restored afterwards, so other modules' tensors keep float32)."""
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
 
 SMALL = ModelConfig(d_model=16, n_q_heads=4, n_kv_heads=2, head_dim=8, d_ff=24, vocab=37,
                     dtype="f32", init_std=0.3)

@@ -225,3 +225,22 @@ def make_weights_torch(m, seed=1000, device="cuda", gain_std=0.0):
             w.mul_(m.init_std)
         out[name] = w.to(dt)
     return out
+
+
+def make_rewards(n_traj, group_size=8, seed=0, p_one=0.5, p_flat=0.25):
+    """Outcome rewards for consecutive groups of `group_size` episodes (the last
+    group may be shorter): group_off int32[n_groups+1], reward float32[n_traj].
+
+    A group is flat (every episode 0, or every episode 1) with probability
+    p_flat; otherwise each episode draws Bernoulli(p_one), which can also
+    come out flat.  Draw order: per group, the flat flag, then the rewards.
+    """
+    rng = np.random.default_rng(seed)
+    off = list(range(0, n_traj, group_size)) + [n_traj]
+    reward = np.zeros(n_traj, np.float32)
+    for a, b in zip(off[:-1], off[1:]):
+        if rng.random() < p_flat:
+            reward[a:b] = float(rng.integers(0, 2))
+        else:
+            reward[a:b] = (rng.random(b - a) < p_one).astype(np.float32)
+    return np.array(off, np.int32), reward
