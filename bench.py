@@ -46,7 +46,7 @@ def parse():
 # counter's reading for a plain copy of known size.  Keyed by (kernel class,
 # workload); `sources` are hashed so that a changed kernel reports null.
 TRAFFIC = {
-    ("gemm_nn", "block1.5b-64x8"): {"bytes_per_launch": 6013.6e6, "sources": "d603a30e0ed29a18"},
+    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 7548.4e6, "sources": "170cadc60ac095c9"},
 }
 
 
@@ -193,7 +193,8 @@ def extras(A, merger, m, tl, dev, torch, capi, actor, steps):
 
 def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
     """The oracle, as is, on a bounded sample of the same workload: the first
-    episode, merged by the oracle, its first segment cut to `sample_tokens`."""
+    episode, merged by the oracle, its first `sample_tokens` merged tokens
+    (whole segments, the last one cut)."""
     from threadpoolctl import threadpool_info
     from oracle import merge as om
     from oracle import model as M
@@ -204,8 +205,9 @@ def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
     t0 = time.perf_counter()
     packed, _ = om.merge_batch(eps)
     t_merge = time.perf_counter() - t0
-    L = min(sample_tokens, int(packed.cu_seqlens[1]))
-    cut = om.Packed([0, L], packed.tok[:L], packed.mask[:L], packed.old_logprob[:L],
+    L = min(sample_tokens, packed.n_tok)
+    cu = [int(c) for c in packed.cu_seqlens if c < L] + [L]
+    cut = om.Packed(cu, packed.tok[:L], packed.mask[:L], packed.old_logprob[:L],
                     packed.adv[:L], packed.pos[:L])
     W = {k: v.float().cpu().numpy() for k, v in W_dev.items()}
     t0 = time.perf_counter()
@@ -214,9 +216,10 @@ def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": L / (t_model + t_merge * L / max(n0, 1)), "unit": "tokens/s",
             "cores": int(threads), "kind": "oracle",
-            "sample": f"episode 0 of the same batch merged by the oracle ({n0} tokens, "
-                      f"{t_merge:.2f} s), then the float64 actor update on its first {L} "
-                      f"tokens ({t_model:.1f} s); merge time pro-rated to {L} tokens",
+            "sample": f"episode 0 of the same batch merged by the oracle ({n0} unmerged -> "
+                      f"{packed.n_tok} merged tokens, {t_merge:.2f} s), then the float64 actor "
+                      f"update on its first {L} merged tokens ({len(cu) - 1} segments, "
+                      f"{t_model:.1f} s); merge time pro-rated to {L} tokens",
             "host_cpus": os.cpu_count()}
 
 
@@ -331,7 +334,7 @@ def main():
     if not args.no_extras:
         out["extras"] = extras(A, merger, m, tl, dev, torch, capi, actor, max(1, args.steps // 2))
     if not args.no_cpu_baseline:
-        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 1024)
+        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 4096)
         out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)
     print(json.dumps(out), flush=True)
 

@@ -25,6 +25,10 @@ AJ_DEV TileIdx tile_of(int wg, int nwg, int tiles_m, int tiles_n) {
   const int per = nwg / kXcds, rem = nwg % kXcds;
   const int xcd = wg % kXcds, idx = wg / kXcds;
   const int t = xcd * per + (xcd < rem ? xcd : rem) + idx;
+  // a skinny product runs whole tile rows (or columns) side by side, so that
+  // each operand tile is fetched once for all the tiles that share it
+  if (tiles_n <= 16) return {t / tiles_n, t % tiles_n};
+  if (tiles_m <= 16) return {t % tiles_m, t / tiles_m};
   const int span = kGroupM * tiles_n;
   const int first_m = (t / span) * kGroupM;
   const int gm = min(tiles_m - first_m, kGroupM);
