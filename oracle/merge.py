@@ -1,16 +1,33 @@
-"""Timeline merging, token-level Match (Section 4.4.2, Algorithm 1).
+"""Timeline merging (Section 4.4.2, Algorithm 1) with either Match strategy
+of its Relaxed Matching paragraph -- test infrastructure only.
 
 Data model (Section 4.4.2, the block tuple equation): a timeline is an ordered
-list of message blocks; each block has token ids, an author in
-{user, env, llm}, a per-token log-prob and a loss mask that is 1 exactly on
+list of message blocks; each block has its message text, token ids, an author
+in {user, env, llm}, a per-token log-prob and a loss mask that is 1 exactly on
 llm-authored tokens.  The per-token advantage rides along with the log-prob
 (the reading that per-turn advantages travel with the tokens they score).
 
 Readings taken where the paper is silent:
   * |T| counts blocks and Match compares aligned blocks (the pairwise
     mergeability definition above Algorithm 1);
-  * Match is token-id equality of the block's tokens; authors are not compared;
-  * merging stays inside one episode.
+  * token-level Match is token-id equality of the two blocks; text-level Match
+    is equality of the two blocks' message texts.  A block's text is held as
+    a key with equal text <=> equal key (an interned id; the oracle compares
+    the keys as the texts themselves).  Authors are not compared;
+  * merging stays inside one episode;
+  * a block's author is the author bits of its first token.
+
+Under text-level Match a transfer replaces the survivor's block by the
+absorbed block's tokens, so the block -- and the timeline -- can change
+length (Figure: text- vs token-level matching, where a stripped thinking
+section makes the two renderings of one message differ in token ids).
+
+Train-inference (TI) consistency report (a reading of the trade-off the
+Relaxed Matching paragraph names): an llm block of a merged segment is
+consistent when the tokens before it in the segment equal the tokens before it
+in the timeline that generated it, i.e. its log-probs are scored in the
+context they were sampled in.  Token-level Match never breaks this; text-level
+Match breaks it exactly where a re-rendering changed token ids.
 """
 import numpy as np
 
@@ -19,36 +36,56 @@ BLOCK_START = 4
 
 
 class Block:
-    __slots__ = ("tokens", "author", "logprob", "adv")
+    """One message block.  `src` = (timeline, block) within the episode of the
+    block whose tokens this is: itself, or the absorbed block a transfer
+    copied (the provenance the TI report needs)."""
+    __slots__ = ("tokens", "author", "logprob", "adv", "text", "src")
 
-    def __init__(self, tokens, author, logprob, adv):
+    def __init__(self, tokens, author, logprob, adv, text=None, src=None):
         self.tokens = np.asarray(tokens, dtype=np.int64)
         self.author = int(author)
         self.logprob = np.asarray(logprob, dtype=np.float64)
         self.adv = np.asarray(adv, dtype=np.float64)
+        self.text = text
+        self.src = src
 
     def copy(self):
-        return Block(self.tokens.copy(), self.author, self.logprob.copy(), self.adv.copy())
+        return Block(self.tokens.copy(), self.author, self.logprob.copy(), self.adv.copy(),
+                     self.text, self.src)
 
 
-def split_blocks(tok, flags, logprob, adv):
-    """Cut one timeline's flat token arrays into blocks at the block-start bits."""
+def split_blocks(tok, flags, logprob, adv, text=None, tl_index=None):
+    """Cut one timeline's flat token arrays into blocks at the block-start bits.
+    `text`: the blocks' text keys in order (or None)."""
     starts = np.flatnonzero(np.asarray(flags) & BLOCK_START).tolist()
     if not starts or starts[0] != 0:
         raise ValueError("a timeline must start a block at its first token")
+    if text is not None and len(text) != len(starts):
+        raise ValueError("one text key per block")
     ends = starts[1:] + [len(tok)]
-    return [Block(tok[s:e], int(flags[s]) & 3, logprob[s:e], adv[s:e])
-            for s, e in zip(starts, ends)]
+    return [Block(tok[s:e], int(flags[s]) & 3, logprob[s:e], adv[s:e],
+                  None if text is None else text[k], None if tl_index is None else (tl_index, k))
+            for k, (s, e) in enumerate(zip(starts, ends))]
 
 
-def episodes_from_flat(traj_tl_off, tl_tok_off, tok, flags, logprob, adv):
-    """Flat compressed-row timelines -> [episode][timeline][block]."""
+def episodes_from_flat(traj_tl_off, tl_tok_off, tok, flags, logprob, adv, blk_text=None):
+    """Flat compressed-row timelines -> [episode][timeline][block].
+
+    blk_text: optional text key of every block, blocks in token order."""
+    starts = np.flatnonzero(np.asarray(flags) & BLOCK_START)
+    if blk_text is not None and len(blk_text) != len(starts):
+        raise ValueError("blk_text needs one key per block start")
     eps = []
     for e in range(len(traj_tl_off) - 1):
         tls = []
-        for i in range(int(traj_tl_off[e]), int(traj_tl_off[e + 1])):
+        e0 = int(traj_tl_off[e])
+        for i in range(e0, int(traj_tl_off[e + 1])):
             s, t = int(tl_tok_off[i]), int(tl_tok_off[i + 1])
-            tls.append(split_blocks(tok[s:t], flags[s:t], logprob[s:t], adv[s:t]))
+            text = None
+            if blk_text is not None:
+                b0, b1 = np.searchsorted(starts, [s, t])
+                text = [int(k) for k in blk_text[b0:b1]]
+            tls.append(split_blocks(tok[s:t], flags[s:t], logprob[s:t], adv[s:t], text, i - e0))
         eps.append(tls)
     return eps
 
@@ -56,6 +93,13 @@ def episodes_from_flat(traj_tl_off, tl_tok_off, tok, flags, logprob, adv):
 def match_token(a: Block, b: Block) -> bool:
     """Token-level Match: identical token-id arrays."""
     return a.tokens.shape == b.tokens.shape and bool(np.array_equal(a.tokens, b.tokens))
+
+
+def match_text(a: Block, b: Block) -> bool:
+    """Text-level Match: identical message texts (the blocks' text keys)."""
+    if a.text is None or b.text is None:
+        raise ValueError("text-level Match needs the blocks' texts")
+    return a.text == b.text
 
 
 def merge_episode(timelines, match=match_token):
@@ -71,6 +115,10 @@ def merge_episode(timelines, match=match_token):
     the timeline that absorbed it or -1.
     """
     T = [[b.copy() for b in tl] for tl in timelines]
+    for i, tl in enumerate(T):
+        for k, b in enumerate(tl):
+            if b.src is None:
+                b.src = (i, k)
     n = len(T)
     absorbed = set()
     absorber = [-1] * n
@@ -87,6 +135,7 @@ def merge_episode(timelines, match=match_token):
                         T[i][k].tokens = T[j][k].tokens.copy()
                         T[i][k].logprob = T[j][k].logprob.copy()
                         T[i][k].adv = T[j][k].adv.copy()
+                        T[i][k].src = T[j][k].src
                 absorbed.add(j)
                 absorber[j] = i
     survivors = [T[i] for i in range(n) if i not in absorbed]
@@ -147,6 +196,26 @@ def merge_batch(episodes, match=match_token):
         segs.extend(surv)
         absorbers.append(absb)
     return flatten(segs), absorbers
+
+
+def ti_report(episodes, match=match_token):
+    """TI consistency of the merged batch: (llm blocks, llm tokens) whose
+    context in their merged segment differs from the context they were
+    generated in (the tokens before them in their own original timeline)."""
+    n_blk = n_tok = 0
+    for tls in episodes:
+        surv, _ = merge_episode(tls, match)
+        for tl in surv:
+            for k, b in enumerate(tl):
+                if b.author != LLM:
+                    continue
+                i, kk = b.src
+                trained = [t for blk in tl[:k] for t in blk.tokens.tolist()]
+                sampled = [t for blk in tls[i][:kk] for t in blk.tokens.tolist()]
+                if trained != sampled:
+                    n_blk += 1
+                    n_tok += len(b.tokens)
+    return n_blk, n_tok
 
 
 def unmerged_batch(episodes):

@@ -31,6 +31,11 @@ class Timelines:
     flags: np.ndarray
     adv: np.ndarray
     lp_noise: np.ndarray
+    blk_text: np.ndarray = None      # uint64 text key per block (token order), when drawn
+
+    @property
+    def n_blk(self) -> int:
+        return int(np.count_nonzero(self.flags & FLAG_BLOCK_START))
 
     @property
     def n_traj(self) -> int:
@@ -56,8 +61,14 @@ class Timelines:
             base = tok_off[-1] - s
             tok_off.extend((self.tl_tok_off[a + 1:b + 1] + base).tolist())
         take = np.concatenate([np.arange(s, t) for s, t in parts]) if parts else np.zeros(0, np.int64)
+        text = None
+        if self.blk_text is not None:
+            starts = np.flatnonzero(self.flags & FLAG_BLOCK_START)
+            keep = [np.arange(*np.searchsorted(starts, [s, t])) for s, t in parts]
+            text = self.blk_text[np.concatenate(keep)] if keep else np.zeros(0, np.uint64)
         return Timelines(np.asarray(tl_off, np.int32), np.asarray(tok_off, np.int64),
-                         self.tok[take], self.flags[take], self.adv[take], self.lp_noise[take])
+                         self.tok[take], self.flags[take], self.adv[take], self.lp_noise[take],
+                         text)
 
 
 class _Ids:
@@ -79,7 +90,7 @@ def _u(rng, lohi):
     return int(rng.integers(lohi[0], lohi[1] + 1))
 
 
-def make_timelines(cfg, seed=None, n_traj=None) -> Timelines:
+def make_timelines(cfg, seed=None, n_traj=None, think_p=None) -> Timelines:
     """Draw a batch of unmerged timelines for workload `cfg`.
 
     Draw order (numpy default_rng(seed)), per episode: number of calls n; the
@@ -88,11 +99,29 @@ def make_timelines(cfg, seed=None, n_traj=None) -> Timelines:
     (single-role workloads skip the permutation): the rewrite coin (t >= 2) and
     fresh context tokens when it lands; the response length, tokens, advantage
     and log-prob noise; and, unless t == n, the observation length and tokens.
+
+    think_p: None draws no texts.  A number also gives every message block a
+    text key (a fresh key per message; a message keeps its key wherever it is
+    re-rendered) and, from a second stream default_rng([seed, 1]), gives each
+    response with probability think_p a thinking section of U{1..na//2}
+    leading tokens that later calls' contexts leave out (a chat template that
+    strips earlier thinking): the same text, other token ids.  The first
+    stream's draws do not depend on think_p (rewrites and the length cap count
+    unstripped lengths), so every timeline's blocks are those of think_p=None
+    except for the stripped re-renderings.
     """
     seed = cfg.seed if seed is None else seed
     n_traj = cfg.n_traj if n_traj is None else n_traj
     rng = np.random.default_rng(seed)
     ids = _Ids(rng, cfg.model.vocab, cfg.zipf_s)
+    texts = think_p is not None
+    rng2 = np.random.default_rng([seed, 1]) if texts else None
+    keys = []
+    next_key = [1]
+
+    def new_key():
+        next_key[0] += 1
+        return next_key[0] - 1
 
     traj_tl_off = [0]
     tl_lens = []
@@ -107,11 +136,12 @@ def make_timelines(cfg, seed=None, n_traj=None) -> Timelines:
     for _ in range(n_traj):
         n = _u(rng, cfg.turns)
         t_star = int(rng.integers(2, n + 1)) if cfg.one_rewrite else -1
-        ctx = []          # per role: list of (tokens, author)
+        # per role: list of (tokens, author, text key, length before any stripping)
+        ctx = []
         alive = []
         for _r in range(cfg.roles):
             plen = _u(rng, cfg.prompt)
-            ctx.append([(ids(plen), AUTHOR_USER)])
+            ctx.append([(ids(plen), AUTHOR_USER, new_key(), plen)])
             alive.append(True)
         n_here = 0
         for t in range(1, n + 1):
@@ -124,31 +154,37 @@ def make_timelines(cfg, seed=None, n_traj=None) -> Timelines:
                     coin = rng.random()
                     rewrite = (t == t_star) if cfg.one_rewrite else (coin < cfg.rewrite_p)
                     if rewrite:
-                        clen = sum(len(b[0]) for b in c)
-                        c = [(ids(clen), AUTHOR_USER)]
+                        clen = sum(b[3] for b in c)
+                        c = [(ids(clen), AUTHOR_USER, new_key(), clen)]
                 na = _u(rng, cfg.resp)
                 a = ids(na)
                 adv = np.float32(rng.standard_normal())
                 noise = rng.normal(0.0, 0.05, na).astype(np.float32)
-                clen = sum(len(b[0]) for b in c)
+                clen = sum(b[3] for b in c)
                 if clen + na > cfg.max_tokens:
                     alive[r] = False
                     continue
-                for btok, auth in c:
+                a_key = new_key()
+                for btok, auth, key, _ in c:
                     toks.append(btok)
                     flags.append(block_flags(len(btok), auth))
                     advs.append(np.zeros(len(btok), np.float32))
                     noises.append(np.zeros(len(btok), np.float32))
+                    keys.append(key)
                 toks.append(a)
                 flags.append(block_flags(na, AUTHOR_LLM))
                 advs.append(np.full(na, adv, np.float32))
                 noises.append(noise)
-                tl_lens.append(clen + na)
+                keys.append(a_key)
+                tl_lens.append(sum(len(b[0]) for b in c) + na)
                 n_here += 1
                 if t < n:
                     no = _u(rng, cfg.obs)
                     o = ids(no)
-                    c = c + [(a, AUTHOR_USER), (o, AUTHOR_ENV)]
+                    shown = a
+                    if texts and na >= 2 and rng2.random() < think_p:
+                        shown = a[int(rng2.integers(1, na // 2 + 1)):]
+                    c = c + [(shown, AUTHOR_USER, a_key, na), (o, AUTHOR_ENV, new_key(), no)]
                 ctx[r] = c
         traj_tl_off.append(traj_tl_off[-1] + n_here)
 
@@ -157,7 +193,8 @@ def make_timelines(cfg, seed=None, n_traj=None) -> Timelines:
     cat = lambda xs, dt: np.concatenate(xs).astype(dt) if xs else np.zeros(0, dt)
     return Timelines(np.asarray(traj_tl_off, np.int32), tl_tok_off,
                      cat(toks, np.int32), cat(flags, np.uint8),
-                     cat(advs, np.float32), cat(noises, np.float32))
+                     cat(advs, np.float32), cat(noises, np.float32),
+                     np.asarray(keys, np.uint64) if texts else None)
 
 
 def bf16_round(a: np.ndarray) -> np.ndarray:
