@@ -114,11 +114,13 @@ def timed(A, merger, merged, steps, warmup, torch, capi, record=False):
     return L, dt, rec
 
 
-def extras(A, merger, m, tl, dev, torch, capi, actor, steps):
+def extras(A, merger, cfg, tl, dev, torch, capi, actor, steps):
     """The steps around the update, measured on the same workload:
     the update with the KL penalty (a reference forward of a frozen copy of
     the policy, then the step with the penalty), GRPO advantages + the
-    non-dummy episode selection, and one AdamW step over every parameter."""
+    non-dummy episode selection, one AdamW step over every parameter, and
+    text-level Match on a stripped-thinking draw of the workload."""
+    m = cfg.model
     from workloads import make_rewards
     out = {}
     # KL: reference log-probs (forward only) + the step with the penalty
@@ -188,7 +190,42 @@ def extras(A, merger, m, tl, dev, torch, capi, actor, steps):
     out["adamw"] = {"params": n, "ms": round(ms, 4), "bytes_per_param": nb // n,
                     "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
                     "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del P, G, M1, M2, Pc
+    out["text_merge"] = text_merge(A, cfg, torch, capi, actor, steps)
     return out
+
+
+def text_merge(A, cfg, torch, capi, actor, steps):
+    """Text- vs token-level Match on the same workload drawn with every
+    response's thinking section stripped from later calls' contexts: merge
+    time and sizes, the TI report, and the update step on either layout."""
+    from workloads import make_timelines
+    m = A.m
+    tl = make_timelines(cfg, think_p=1.0)
+    llm = (tl.flags & 3) == 2
+    old = np.where(llm, -np.log(m.vocab) + tl.lp_noise, 0.0).astype(np.float32)
+    dev = actor.upload_timelines(tl, old)
+    res = {"think_p": 1.0, "unmerged_tokens": int(tl.n_tok), "blocks": int(tl.n_blk)}
+    for name, text in (("text", True), ("token", False)):
+        mg = actor.Merger(dev, text=text)
+        for i in range(4):
+            if i == 1:
+                capi.aj_timing_enable(True)
+            mg.launch(True)
+        rec = capi.aj_timing_read()
+        capi.aj_timing_enable(False)
+        L = mg.layout(m.pack_tokens)
+        A.prepare(L)
+        L, t, _ = timed(A, mg, True, steps, 1, torch, capi)
+        r = {"merged_tokens": L.n_tok, "segments": L.n_seg, "loss_tokens": L.n_mask,
+             "merge_ms": round(rec["merge"][0] / rec["merge"][1], 4),
+             "step_ms": round(t * 1e3, 3), "tokens_per_s": round(L.n_tok / t, 1)}
+        if text:
+            ti = mg.ti.cpu().tolist()
+            r["ti_drift_blocks"], r["ti_drift_tokens"] = int(ti[0]), int(ti[1])
+        res[name] = r
+    res["step_speedup_text_vs_token"] = round(res["token"]["step_ms"] / res["text"]["step_ms"], 3)
+    return res
 
 
 def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
@@ -332,7 +369,7 @@ def main():
         out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
         out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)
     if not args.no_extras:
-        out["extras"] = extras(A, merger, m, tl, dev, torch, capi, actor, max(1, args.steps // 2))
+        out["extras"] = extras(A, merger, cfg, tl, dev, torch, capi, actor, max(1, args.steps // 2))
     if not args.no_cpu_baseline:
         st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 4096)
         out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)

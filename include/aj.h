@@ -3,7 +3,7 @@
  *
  * The actor (policy) update over multi-turn agent trajectories, in three
  * stages:
- *   1. timeline merging          (Section 4.4.2, Algorithm 1, token-level Match)
+ *   1. timeline merging          (Section 4.4.2, Algorithm 1, token- or text-level Match)
  *   2. one packed variable-length causal decoder block, forward and backward
  *   3. the fused LM head: vocab projection, log-softmax, token log-prob and the
  *      clipped policy-gradient loss (Section 3: GRPO-style updates), forward
@@ -61,7 +61,9 @@ enum {
   AJ_DEVERR_TOKEN_RANGE = 1,   /* a token id outside [0, vocab) */
   AJ_DEVERR_BAD_FLAGS = 2,     /* author 3, or a timeline not starting a block */
   AJ_DEVERR_EMPTY = 4,         /* an empty timeline */
-  AJ_DEVERR_OFFSETS = 8        /* offsets not monotone, out of range, or not tiling [0, n) */
+  AJ_DEVERR_OFFSETS = 8,       /* offsets not monotone, out of range, or not tiling [0, n) */
+  AJ_DEVERR_BLOCKS = 16        /* text-level merge: the block-start bits do not give n_blk
+                                  blocks, or a timeline does not start a block */
 };
 
 const char *aj_status_str(int status);
@@ -125,6 +127,43 @@ int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
  * (absorber all -1).  The unmerged baseline the paper compares against. */
 int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
                          void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------ 1b. merge, text-level Match
+ * Section 4.4.2, Relaxed Matching Strategies: Match compares the MESSAGE TEXT
+ * of aligned blocks instead of their token ids (the paper's default
+ * strategy).  It tolerates tokenizer drift: a chat template that re-renders an
+ * earlier message differently (for instance without its thinking section)
+ * keeps the text and changes the ids, so token-level Match would keep the two
+ * timelines apart.  The library never sees text: the caller passes one 64-bit
+ * key per block, with equal text <=> equal key (an interned message id is
+ * exact; a 64-bit hash of the text is exact up to collisions).
+ *
+ * A transfer copies the absorbed block's tokens, log-probs and advantages
+ * over the survivor's block (Algorithm 1), so a block -- and its segment --
+ * can change length; the output is laid out again from the chosen blocks
+ * (every input block lands in at most one place, so the output is still never
+ * longer than the input).  A block's author is the author bits of its first
+ * token; mask is 1 on every token of an llm block of the output.
+ *
+ * Train-inference (TI) consistency report, `ti` [2] (optional, int64): the
+ * llm blocks of the output -- and their tokens -- whose tokens before them in
+ * their output segment differ from the tokens before them in the timeline
+ * that generated them: log-probs the update scores in a context other than
+ * the one they were sampled in.  Token-level Match never produces any.
+ */
+typedef struct {
+  int32_t n_blk;                /* blocks of all timelines = number of AJ_FLAG_BLOCK_START bits */
+  const uint64_t *key;          /* [n_blk] text key of each block, blocks in token order */
+} aj_block_texts;
+
+/* Workspace for aj_merge_timelines_text. */
+size_t aj_merge_text_workspace_bytes(int32_t n_traj, int32_t n_tl, int64_t n_tok, int32_t n_blk);
+/* Algorithm 1 with text-level Match; outputs as aj_merge_timelines.  Beyond
+ * its device errors, block-start bits that do not give n_blk blocks, or a
+ * timeline that does not start a block, raise AJ_DEVERR_BLOCKS and every
+ * count comes back 0.  `ti` may be NULL.  Bit-identical on every call. */
+int aj_merge_timelines_text(const aj_timelines *in, const aj_block_texts *text, aj_packed *out,
+                            int64_t *ti, int32_t *err, void *ws, size_t ws_bytes, void *stream);
 
 /* Host: greedy in-order packing of segments into packs of at most max_tokens
  * tokens (a longer segment gets a pack of its own).  cu_seqlens is a HOST copy
@@ -310,7 +349,7 @@ int aj_adamw_step(int64_t n, float *param, const float *grad, float *m, float *v
  * classes below is bracketed by two hipEvents recorded on the launch's own
  * stream.  The record is process-wide (the one piece of state the library
  * keeps besides the error text) and meant for a single-threaded driver.
- *   AJ_KC_MERGE      one aj_merge_timelines / aj_flatten_timelines call
+ *   AJ_KC_MERGE      one aj_merge_timelines / aj_merge_timelines_text / aj_flatten_timelines call
  *   AJ_KC_GEMM_*     the MFMA GEMM, by operand layout (NT: both K-major;
  *                    NN: B N-major; TN: A M-major and B N-major), 8-wave
  *                    kernel (reductions shorter than 4096 per split)

@@ -210,9 +210,10 @@ def ti_report(episodes, match=match_token):
                 if b.author != LLM:
                     continue
                 i, kk = b.src
-                trained = [t for blk in tl[:k] for t in blk.tokens.tolist()]
-                sampled = [t for blk in tls[i][:kk] for t in blk.tokens.tolist()]
-                if trained != sampled:
+                trained = np.concatenate([blk.tokens for blk in tl[:k]] + [np.zeros(0, np.int64)])
+                sampled = np.concatenate([blk.tokens for blk in tls[i][:kk]] +
+                                         [np.zeros(0, np.int64)])
+                if not np.array_equal(trained, sampled):
                     n_blk += 1
                     n_tok += len(b.tokens)
     return n_blk, n_tok

@@ -19,10 +19,11 @@ BLOCK_NAMES = ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
 
 
 def upload_timelines(tl, old_logprob, device="cuda"):
-    """Host Timelines (+ rollout log-probs, float32 [n_tok]) -> device tensors."""
+    """Host Timelines (+ rollout log-probs, float32 [n_tok]) -> device tensors; the block
+    text keys too when the timelines carry them (bit patterns in an int64 tensor)."""
     def t(a, dt):
         return torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dt)
-    return {
+    d = {
         "traj_tl_off": t(tl.traj_tl_off, torch.int32),
         "tl_tok_off": t(tl.tl_tok_off, torch.int64),
         "tok": t(tl.tok, torch.int32),
@@ -30,6 +31,9 @@ def upload_timelines(tl, old_logprob, device="cuda"):
         "old_logprob": t(old_logprob.astype(np.float32), torch.float32),
         "adv": t(tl.adv, torch.float32),
     }
+    if getattr(tl, "blk_text", None) is not None:
+        d["blk_text"] = t(np.asarray(tl.blk_text, np.uint64).view(np.int64), torch.int64)
+    return d
 
 
 @dataclass
@@ -52,9 +56,10 @@ class Layout:
 
 
 class Merger:
-    """Owns the output and workspace buffers of aj_merge_timelines for one input size."""
+    """Owns the output and workspace buffers of aj_merge_timelines (text=False) or
+    aj_merge_timelines_text (text=True: Match on tl_dev["blk_text"]) for one input size."""
 
-    def __init__(self, tl_dev):
+    def __init__(self, tl_dev, text=False):
         dev = tl_dev["tok"].device
         n_traj = tl_dev["traj_tl_off"].numel() - 1
         n_tl = tl_dev["tl_tok_off"].numel() - 1
@@ -76,10 +81,22 @@ class Merger:
             "targets": torch.empty(cap, **i32),
         }
         self.err = torch.zeros(1, **i32)
-        self.ws = torch.empty(C.aj_merge_workspace_bytes(n_traj, n_tl, n_tok), dtype=torch.uint8,
-                              device=dev)
+        self.text = text
+        if text:
+            n_blk = tl_dev["blk_text"].numel()
+            nbytes = C.aj_merge_text_workspace_bytes(n_traj, n_tl, n_tok, n_blk)
+            self.ti = torch.zeros(2, dtype=torch.int64, device=dev)
+        else:
+            nbytes = C.aj_merge_workspace_bytes(n_traj, n_tl, n_tok)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
 
     def launch(self, merged=True):
+        if self.text:
+            if not merged:
+                raise ValueError("text-level Match is a merge; flatten with text=False")
+            C.aj_merge_timelines_text(self.tl, self.tl["blk_text"], self.out, self.err, self.ws,
+                                      self.ti)
+            return
         fn = C.aj_merge_timelines if merged else C.aj_flatten_timelines
         fn(self.tl, self.out, self.err, self.ws)
 
@@ -103,8 +120,8 @@ class Merger:
         return C.aj_read_device_error(self.err)
 
 
-def merge(tl_dev, merged=True, pack_tokens=131072):
-    m = Merger(tl_dev)
+def merge(tl_dev, merged=True, pack_tokens=131072, text=False):
+    m = Merger(tl_dev, text=text)
     m.launch(merged)
     return m.layout(pack_tokens)
 

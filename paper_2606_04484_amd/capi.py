@@ -53,6 +53,10 @@ class Packed(C.Structure):
                 ("adv", vp), ("targets", vp)]
 
 
+class BlockTexts(C.Structure):
+    _fields_ = [("n_blk", i32), ("key", vp)]
+
+
 class TimelinesOut(C.Structure):
     _fields_ = [("traj_tl_off", vp), ("tl_tok_off", vp), ("tok", vp), ("flags", vp),
                 ("old_logprob", vp), ("adv", vp), ("counts", vp)]
@@ -94,6 +98,9 @@ EXPORTS = {
     "aj_merge_workspace_bytes": (sz, [i32, i32, i64]),
     "aj_merge_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
     "aj_flatten_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
+    "aj_merge_text_workspace_bytes": (sz, [i32, i32, i64, i32]),
+    "aj_merge_timelines_text": (C.c_int, [C.POINTER(Timelines), C.POINTER(BlockTexts),
+                                          C.POINTER(Packed), vp, vp, vp, sz, vp]),
     "aj_plan_packs": (C.c_int, [vp, i32, i32, vp, C.POINTER(i32)]),
     "aj_embed_fwd": (C.c_int, [vp, i32, vp, i32, i32, C.c_int, vp, vp, vp]),
     "aj_embed_bwd": (C.c_int, [vp, i32, vp, i32, i32, vp, vp]),
@@ -185,6 +192,24 @@ def aj_flatten_timelines(tl, out, err, ws, stream=None):
     _check(lib().aj_flatten_timelines(C.byref(_timelines(tl)), C.byref(_packed(out)), ptr(err),
                                       ptr(ws), ws.numel() * ws.element_size(),
                                       stream_handle(stream)), "aj_flatten_timelines")
+
+
+def aj_merge_text_workspace_bytes(n_traj, n_tl, n_tok, n_blk):
+    return int(lib().aj_merge_text_workspace_bytes(n_traj, n_tl, n_tok, n_blk))
+
+
+def aj_merge_timelines_text(tl, blk_text, out, err, ws, ti=None, stream=None):
+    """As aj_merge_timelines with text-level Match; blk_text: device uint64 (or int64) text key
+    per block, blocks in token order; ti: optional device int64 [2] for the TI report."""
+    if blk_text.dtype not in (torch.int64, torch.uint64):
+        raise AjError(f"aj_merge_timelines_text: blk_text must be 64-bit, got {blk_text.dtype}")
+    if ti is not None and (ti.dtype != torch.int64 or ti.numel() < 2):
+        raise AjError("aj_merge_timelines_text: ti must be int64 [2]")
+    texts = BlockTexts(int(blk_text.numel()), ptr(blk_text))
+    _check(lib().aj_merge_timelines_text(C.byref(_timelines(tl)), C.byref(texts),
+                                         C.byref(_packed(out)), ptr(ti), ptr(err), ptr(ws),
+                                         ws.numel() * ws.element_size(), stream_handle(stream)),
+           "aj_merge_timelines_text")
 
 
 def aj_plan_packs(cu_seqlens_host, max_tokens):

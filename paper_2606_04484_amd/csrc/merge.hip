@@ -1,4 +1,5 @@
-// Timeline merging on the GPU (Section 4.4.2, Algorithm 1, token-level Match).
+// Timeline merging on the GPU (Section 4.4.2, Algorithm 1), token-level Match
+// and, further down, text-level Match (the Relaxed Matching Strategies).
 //
 // Algorithm 1 is a sequential double loop, but its result has a closed form
 // that parallelises:
@@ -30,7 +31,7 @@ constexpr int kBlock = 256;
 constexpr int kChunk = 1024;          // outputs per workgroup in the target compaction
 // Offsets that do not tile the input stop the merge (every count 0); bad flag
 // bytes are reported and the token is treated as written (author 3: not llm).
-constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY;
+constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY | AJ_DEVERR_BLOCKS;
 
 struct MergeArgs {
   int32_t n_traj, n_tl;
@@ -54,6 +55,18 @@ struct MergeArgs {
   int32_t *chunk_cnt;   // [n_chunks]
   int32_t *chunk_off;   // [n_chunks]
   int32_t *user_err;
+  // text-level Match only
+  int32_t n_blk;
+  const uint64_t *blk_text;   // [n_blk] text key per block
+  int64_t *ti;                // [2] TI report, or null
+  int32_t *blk_start;         // [n_blk+1] first token of each block, then n_tok
+  int32_t *tl_blk;            // [n_tl+1]  first block of each timeline, then n_blk
+  int32_t *blk_tl;            // [n_blk]   timeline of each block
+  int32_t *blk_claim;         // [n_blk]   largest absorbed timeline with an llm block here
+  int32_t *src_blk;           // [n_blk]   block whose tokens a survivor block carries (-1: none)
+  int32_t *blk_off;           // [n_blk+1] output offset of each survivor block
+  int32_t *dst_off;           // [n_blk]   output offset a source block lands at (-1: nowhere)
+  int32_t *dst_pos;           // [n_blk]   its position inside the segment
 };
 
 AJ_DEV bool fatal(const MergeArgs &a) { return (a.status[0] & kFatal) != 0; }
@@ -106,6 +119,7 @@ AJ_DEV int block_scan_incl(int v, int *total) {
 
 __global__ void init_status_kernel(MergeArgs a) {
   if (threadIdx.x < 4) a.status[threadIdx.x] = 0;
+  if (a.ti && threadIdx.x < 2) a.ti[threadIdx.x] = 0;
 }
 
 __global__ void validate_kernel(MergeArgs a) {
@@ -290,7 +304,9 @@ __global__ __launch_bounds__(kBlock) void tgt_count_kernel(MergeArgs a) {
   if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
 }
 
-__global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunks) {
+// Exclusive offsets of the per-chunk counts; the total goes to counts[2] (the
+// target compaction) or, for the block-start compaction, must equal n_blk.
+__global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunks, int blocks) {
   __shared__ int carry;
   if (threadIdx.x == 0) carry = 0;
   __syncthreads();
@@ -304,7 +320,10 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
     if (threadIdx.x == 0) carry += tot;
     __syncthreads();
   }
-  if (threadIdx.x == 0) a.counts[2] = carry;
+  if (threadIdx.x == 0) {
+    if (!blocks) a.counts[2] = carry;
+    else if (!fatal(a) && carry != a.n_blk) raise(a, AJ_DEVERR_BLOCKS);
+  }
 }
 
 __global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
@@ -335,27 +354,289 @@ __global__ void cu_targets_kernel(MergeArgs a) {
   a.cu_targets[s] = lo;
 }
 
+// ---------------------------------------------------------------- text-level Match
+// Match compares each aligned block's text key.  Keys never change while
+// Algorithm 1 runs (a transfer copies a block with the same text), so the
+// closed form above holds with "T_j <= T_i" read as: T_i has at least as many
+// blocks and the first |T_j| keys agree.  Transfers may change block lengths:
+// a survivor block carries the tokens of one source block (its own, or the
+// block of the largest absorbed timeline with an llm block there), and the
+// output is laid out from the chosen blocks' lengths.
+AJ_DEV bool llm_block(const MergeArgs &a, int b) {
+  return (a.flags[a.blk_start[b]] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
+}
+
+// Largest index b in [lo, hi] with off[b] <= v (off ascending, off[lo] <= v).
+AJ_DEV int upper_index(const int32_t *off, int64_t v, int lo, int hi) {
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Block starts per chunk of kChunk tokens.
+__global__ __launch_bounds__(kBlock) void blk_count_kernel(MergeArgs a) {
+  const int64_t u0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
+  int c = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    c += (u0 + r < a.n_tok) && (a.flags[u0 + r] & AJ_FLAG_BLOCK_START);
+  int tot;
+  block_scan_incl<kBlock>(c, &tot);
+  if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
+}
+
+// blk_start[b] = first token of block b (the scan checked there are n_blk).
+__global__ __launch_bounds__(kBlock) void blk_write_kernel(MergeArgs a) {
+  if (fatal(a)) return;
+  const int64_t u0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
+  int f[4], c = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = (u0 + r < a.n_tok) && (a.flags[u0 + r] & AJ_FLAG_BLOCK_START);
+    c += f[r];
+  }
+  int tot;
+  int incl = block_scan_incl<kBlock>(c, &tot);
+  int w = a.chunk_off[blockIdx.x] + incl - c;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    if (f[r]) a.blk_start[w++] = (int32_t)(u0 + r);
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.blk_start[a.n_blk] = (int32_t)a.n_tok;
+}
+
+// tl_blk[i] = the block that starts at timeline i's first token.
+__global__ void tl_blk_kernel(MergeArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i > a.n_tl || fatal(a)) return;
+  if (i == a.n_tl) { a.tl_blk[i] = a.n_blk; return; }
+  const int64_t u = a.tl_tok_off[i];
+  int lo = 0, hi = a.n_blk;          // first block starting at or after u
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if (a.blk_start[mid] < u) lo = mid + 1; else hi = mid;
+  }
+  if (lo == a.n_blk || a.blk_start[lo] != u) raise(a, AJ_DEVERR_BLOCKS);
+  a.tl_blk[i] = lo;
+}
+
+__global__ void blk_tl_kernel(MergeArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.n_blk || fatal(a)) return;
+  a.blk_tl[b] = upper_index(a.tl_blk, b, 0, a.n_tl - 1);
+  a.blk_claim[b] = -1;
+  a.dst_off[b] = -1;
+}
+
+// One wavefront per timeline j: candidates from the episode's last timeline
+// down, key comparison with early exit.
+__global__ __launch_bounds__(64) void find_absorber_text_kernel(MergeArgs a) {
+  const int j = blockIdx.x;
+  if (fatal(a)) {
+    if (threadIdx.x == 0) a.absorber[j] = -1;
+    return;
+  }
+  int lo = 0, hi = a.n_traj - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (a.traj_tl_off[mid] <= j) lo = mid; else hi = mid - 1;
+  }
+  while (lo + 1 < a.n_traj && a.traj_tl_off[lo + 1] <= j) ++lo;
+  const int last = a.traj_tl_off[lo + 1] - 1;
+  const int bj = a.tl_blk[j], nj = a.tl_blk[j + 1] - bj;
+  int result = -1;
+  for (int i = last; i > j; --i) {
+    const int bi = a.tl_blk[i];
+    if (a.tl_blk[i + 1] - bi < nj) continue;
+    bool equal = true;
+    for (int k0 = 0; k0 < nj; k0 += 64) {
+      const int k = k0 + (int)threadIdx.x;
+      const bool bad = k < nj && a.blk_text[bj + k] != a.blk_text[bi + k];
+      if (__ballot(bad)) { equal = false; break; }
+    }
+    if (equal) { result = i; break; }
+  }
+  if (threadIdx.x == 0) a.absorber[j] = result;
+}
+
+// llm blocks of absorbed timelines vote for the survivor block they align with.
+__global__ void claim_text_kernel(MergeArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.n_blk || fatal(a)) return;
+  const int t = a.blk_tl[b];
+  const int s = a.absorber[t];
+  if (s < 0 || !llm_block(a, b)) return;
+  atomicMax(&a.blk_claim[a.tl_blk[s] + (b - a.tl_blk[t])], t);
+}
+
+// Source block and output length of every block (0 for absorbed timelines).
+__global__ void select_text_kernel(MergeArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.n_blk || fatal(a)) return;
+  const int t = a.blk_tl[b];
+  int src = -1;
+  if (a.absorber[t] < 0) {
+    src = b;
+    const int c = a.blk_claim[b];
+    if (!llm_block(a, b) && c >= 0) src = a.tl_blk[c] + (b - a.tl_blk[t]);
+  }
+  a.src_blk[b] = src;
+  a.blk_off[b] = src >= 0 ? a.blk_start[src + 1] - a.blk_start[src] : 0;
+}
+
+// Single workgroup of 1024 threads: output offsets of the blocks (exclusive
+// scan of their lengths, in place), then the survivor scan as in resolve.
+__global__ __launch_bounds__(1024) void resolve_text_kernel(MergeArgs a) {
+  __shared__ int carry_seg, carry_tok, carry_max;
+  if (threadIdx.x == 0) { carry_seg = 0; carry_tok = 0; carry_max = 0; }
+  __syncthreads();
+  const bool bad = fatal(a);
+  if (!bad) {
+    for (int base = 0; base < a.n_blk; base += 1024) {
+      const int b = base + threadIdx.x;
+      const int len = b < a.n_blk ? a.blk_off[b] : 0;
+      int tot;
+      const int incl = block_scan_incl<1024>(len, &tot);
+      if (b < a.n_blk) a.blk_off[b] = carry_tok + incl - len;
+      __syncthreads();
+      if (threadIdx.x == 0) carry_tok += tot;
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) a.blk_off[a.n_blk] = carry_tok;
+  }
+  // the block offsets written above are read back by other threads
+  __syncthreads();
+  for (int base = 0; base < a.n_tl; base += 1024) {
+    const int i = base + threadIdx.x;
+    const int surv = !bad && i < a.n_tl && a.absorber[i] < 0;
+    int tot_s;
+    const int is = block_scan_incl<1024>(surv, &tot_s);
+    if (i < a.n_tl) {
+      if (surv) {
+        const int seg = carry_seg + is - 1;
+        const int o0 = a.blk_off[a.tl_blk[i]];
+        a.tl_seg[i] = seg;
+        a.seg_src[seg] = i;
+        a.cu_seqlens[seg] = o0;
+        atomicMax(&carry_max, a.blk_off[a.tl_blk[i + 1]] - o0);
+      } else {
+        a.tl_seg[i] = -1;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) carry_seg += tot_s;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int n_out = bad ? 0 : carry_tok;
+    a.cu_seqlens[carry_seg] = n_out;
+    a.counts[0] = carry_seg;
+    a.counts[1] = n_out;
+    a.counts[2] = 0;
+    a.counts[3] = carry_max;
+  }
+}
+
+// Where each chosen source block lands.
+__global__ void place_text_kernel(MergeArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.n_blk || fatal(a)) return;
+  const int src = a.src_blk[b];
+  if (src < 0) return;
+  const int o = a.blk_off[b];
+  a.dst_off[src] = o;
+  a.dst_pos[src] = o - a.blk_off[a.tl_blk[a.blk_tl[b]]];
+}
+
+// One thread per input token: copy it to where its block lands, if anywhere.
+__global__ __launch_bounds__(kBlock) void emit_text_kernel(MergeArgs a) {
+  if (fatal(a)) return;
+  const int64_t u0 = (int64_t)blockIdx.x * blockDim.x;
+  __shared__ int r[2];
+  if (threadIdx.x == 0) {
+    int64_t u1 = u0 + blockDim.x - 1;
+    if (u1 >= a.n_tok) u1 = a.n_tok - 1;
+    r[0] = upper_index(a.blk_start, u0, 0, a.n_blk - 1);
+    r[1] = upper_index(a.blk_start, u1, r[0], a.n_blk - 1);
+  }
+  __syncthreads();
+  const int64_t u = u0 + threadIdx.x;
+  if (u >= a.n_tok) return;
+  if ((a.flags[u] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK) raise(a, AJ_DEVERR_BAD_FLAGS);
+  const int b = upper_index(a.blk_start, u, r[0], r[1]);
+  const int o0 = a.dst_off[b];
+  if (o0 < 0) return;
+  const int p = (int)(u - a.blk_start[b]);
+  const bool llm = llm_block(a, b);
+  a.otok[o0 + p] = a.tok[u];
+  a.opos[o0 + p] = a.dst_pos[b] + p;
+  a.omask[o0 + p] = llm;
+  a.olp[o0 + p] = llm ? a.old_logprob[u] : 0.f;
+  a.oadv[o0 + p] = llm ? a.adv[u] : 0.f;
+}
+
+// One wavefront per block: an llm block of the output whose tokens before it
+// in its segment differ from those before it in its own timeline.
+__global__ __launch_bounds__(64) void ti_kernel(MergeArgs a) {
+  const int b = blockIdx.x;
+  if (fatal(a)) return;
+  const int src = a.src_blk[b];
+  if (src < 0 || !llm_block(a, src)) return;
+  const int o1 = a.blk_off[b];
+  const int o0 = a.blk_off[a.tl_blk[a.blk_tl[b]]];
+  const int64_t u1 = a.blk_start[src];
+  const int64_t u0 = a.tl_tok_off[a.blk_tl[src]];
+  bool drift = (int64_t)(o1 - o0) != u1 - u0;
+  for (int64_t q0 = 0; !drift && q0 < o1 - o0; q0 += 64 * 4) {
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t q = q0 + r * 64 + threadIdx.x;
+      if (q < o1 - o0) bad |= a.otok[o0 + q] != a.tok[u0 + q];
+    }
+    drift = __ballot(bad) != 0;
+  }
+  if (drift && threadIdx.x == 0) {
+    atomicAdd((unsigned long long *)&a.ti[0], 1ull);
+    atomicAdd((unsigned long long *)&a.ti[1],
+              (unsigned long long)(a.blk_start[src + 1] - a.blk_start[src]));
+  }
+}
+
 struct MergeWs {
   int32_t *status, *tl_seg, *claim, *chunk_cnt, *chunk_off;
+  int32_t *blk_start, *tl_blk, *blk_tl, *blk_claim, *src_blk, *blk_off, *dst_off, *dst_pos;
   size_t bytes;
 };
 
-MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok) {
+// n_blk < 0: token-level Match or no merge (no per-block arrays).
+MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok, int32_t n_blk = -1) {
   aj::Carver c(ws);
-  MergeWs w;
+  MergeWs w{};
   int64_t n_chunks = (n_tok + kChunk - 1) / kChunk;
+  auto at_least1 = [](int64_t n) { return n > 0 ? n : 1; };
   w.status = c.take<int32_t>(4);
-  w.tl_seg = c.take<int32_t>(n_tl > 0 ? n_tl : 1);
-  w.claim = c.take<int32_t>(n_tok > 0 ? n_tok : 1);
-  w.chunk_cnt = c.take<int32_t>(n_chunks > 0 ? n_chunks : 1);
-  w.chunk_off = c.take<int32_t>(n_chunks > 0 ? n_chunks : 1);
+  w.tl_seg = c.take<int32_t>(at_least1(n_tl));
+  w.chunk_cnt = c.take<int32_t>(at_least1(n_chunks));
+  w.chunk_off = c.take<int32_t>(at_least1(n_chunks));
+  if (n_blk < 0) {
+    w.claim = c.take<int32_t>(at_least1(n_tok));
+  } else {
+    w.blk_start = c.take<int32_t>(n_blk + 1);
+    w.tl_blk = c.take<int32_t>((int64_t)n_tl + 1);
+    w.blk_tl = c.take<int32_t>(at_least1(n_blk));
+    w.blk_claim = c.take<int32_t>(at_least1(n_blk));
+    w.src_blk = c.take<int32_t>(at_least1(n_blk));
+    w.blk_off = c.take<int32_t>(n_blk + 1);
+    w.dst_off = c.take<int32_t>(at_least1(n_blk));
+    w.dst_pos = c.take<int32_t>(at_least1(n_blk));
+  }
   w.bytes = c.bytes();
   return w;
 }
 
-int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t ws_bytes,
-        void *stream, bool merge) {
-  const char *name = merge ? "aj_merge_timelines" : "aj_flatten_timelines";
+int check_io(const aj_timelines *in, aj_packed *out, const char *name) {
   AJ_REQUIRE(in && out, AJ_ERR_NULL, "%s: null argument struct", name);
   AJ_REQUIRE(in->n_traj >= 0 && in->n_tl >= 0 && in->n_tok >= 0 && in->n_tok < (int64_t)1 << 31,
              AJ_ERR_SHAPE, "%s: n_traj=%d n_tl=%d n_tok=%lld out of range", name, in->n_traj,
@@ -370,12 +651,11 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
   AJ_REQUIRE(in->n_tok == 0 || (out->tok && out->pos && out->mask && out->old_logprob &&
                                 out->adv && out->targets),
              AJ_ERR_NULL, "%s: null token outputs", name);
-  MergeWs w = carve(ws, in->n_tl, in->n_tok);
-  AJ_REQUIRE(ws, AJ_ERR_NULL, "%s: null workspace", name);
-  AJ_REQUIRE(ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes", name,
-             ws_bytes, w.bytes);
+  return AJ_OK;
+}
 
-  MergeArgs a;
+MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const MergeWs &w) {
+  MergeArgs a{};
   a.n_traj = in->n_traj; a.n_tl = in->n_tl; a.n_tok = in->n_tok;
   a.traj_tl_off = in->traj_tl_off; a.tl_tok_off = in->tl_tok_off;
   a.tok = in->tok; a.flags = in->flags; a.old_logprob = in->old_logprob; a.adv = in->adv;
@@ -385,6 +665,29 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
   a.oadv = out->adv; a.targets = out->targets;
   a.status = w.status; a.tl_seg = w.tl_seg; a.claim = w.claim;
   a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
+  a.blk_start = w.blk_start; a.tl_blk = w.tl_blk; a.blk_tl = w.blk_tl; a.blk_claim = w.blk_claim;
+  a.src_blk = w.src_blk; a.blk_off = w.blk_off; a.dst_off = w.dst_off; a.dst_pos = w.dst_pos;
+  return a;
+}
+
+// The target list and per-segment target offsets, once tok/pos/mask are out.
+void launch_targets(const MergeArgs &a, hipStream_t s) {
+  const int64_t n_chunks = (a.n_tok + kChunk - 1) / kChunk;
+  if (a.n_tok > 0) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
+  if (a.n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  cu_targets_kernel<<<(a.n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+}
+
+int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t ws_bytes,
+        void *stream, bool merge) {
+  const char *name = merge ? "aj_merge_timelines" : "aj_flatten_timelines";
+  if (int rc = check_io(in, out, name)) return rc;
+  MergeWs w = carve(ws, in->n_tl, in->n_tok);
+  AJ_REQUIRE(ws, AJ_ERR_NULL, "%s: null workspace", name);
+  AJ_REQUIRE(ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes", name,
+             ws_bytes, w.bytes);
+  MergeArgs a = make_args(in, out, err, w);
 
   hipStream_t s = (hipStream_t)stream;
   const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
@@ -398,7 +701,6 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
       fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
   }
   resolve_kernel<<<1, 1024, 0, s>>>(a);
-  const int64_t n_chunks = (in->n_tok + kChunk - 1) / kChunk;
   if (in->n_tok > 0) {
     const int64_t gtok = (in->n_tok + kBlock - 1) / kBlock;
     if (merge) {
@@ -406,11 +708,56 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
       claim_kernel<<<gtok, kBlock, 0, s>>>(a);
     }
     emit_kernel<<<gtok, kBlock, 0, s>>>(a, merge ? 1 : 0);
-    tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   }
-  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks);
-  if (in->n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
-  cu_targets_kernel<<<(in->n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  launch_targets(a, s);
+  aj::timing_end(s, tk);
+  return aj::check_launch(name);
+}
+
+int run_text(const aj_timelines *in, const aj_block_texts *text, aj_packed *out, int64_t *ti,
+             int32_t *err, void *ws, size_t ws_bytes, void *stream) {
+  const char *name = "aj_merge_timelines_text";
+  if (int rc = check_io(in, out, name)) return rc;
+  AJ_REQUIRE(text, AJ_ERR_NULL, "%s: null text keys", name);
+  AJ_REQUIRE(text->n_blk >= 0 && text->n_blk <= in->n_tok, AJ_ERR_SHAPE,
+             "%s: n_blk=%d outside [0, n_tok=%lld] (blocks are never empty)", name, text->n_blk,
+             (long long)in->n_tok);
+  AJ_REQUIRE(text->n_blk == 0 || text->key, AJ_ERR_NULL, "%s: null key array", name);
+  MergeWs w = carve(ws, in->n_tl, in->n_tok, text->n_blk);
+  AJ_REQUIRE(ws, AJ_ERR_NULL, "%s: null workspace", name);
+  AJ_REQUIRE(ws_bytes >= w.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes", name,
+             ws_bytes, w.bytes);
+  MergeArgs a = make_args(in, out, err, w);
+  a.n_blk = text->n_blk;
+  a.blk_text = text->key;
+  a.ti = ti;
+
+  const int n_blk = text->n_blk;
+  const int64_t n_chunks = (in->n_tok + kChunk - 1) / kChunk;
+  const int gblk = (n_blk + kBlock - 1) / kBlock;
+  hipStream_t s = (hipStream_t)stream;
+  const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
+  init_status_kernel<<<1, 64, 0, s>>>(a);
+  const int n_val = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
+  validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  // blocks: first tokens, first block per timeline, timeline per block
+  if (in->n_tok > 0) blk_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 1);
+  if (in->n_tok > 0) blk_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  tl_blk_kernel<<<(in->n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  if (n_blk > 0) blk_tl_kernel<<<gblk, kBlock, 0, s>>>(a);
+  // Algorithm 1 in closed form on the keys, then the chosen blocks
+  if (in->n_tl > 0) find_absorber_text_kernel<<<in->n_tl, 64, 0, s>>>(a);
+  if (n_blk > 0) {
+    claim_text_kernel<<<gblk, kBlock, 0, s>>>(a);
+    select_text_kernel<<<gblk, kBlock, 0, s>>>(a);
+  }
+  resolve_text_kernel<<<1, 1024, 0, s>>>(a);
+  if (n_blk > 0) place_text_kernel<<<gblk, kBlock, 0, s>>>(a);
+  if (in->n_tok > 0)
+    emit_text_kernel<<<(in->n_tok + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  launch_targets(a, s);
+  if (ti && n_blk > 0) ti_kernel<<<n_blk, 64, 0, s>>>(a);
   aj::timing_end(s, tk);
   return aj::check_launch(name);
 }
@@ -420,6 +767,18 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
 extern "C" size_t aj_merge_workspace_bytes(int32_t n_traj, int32_t n_tl, int64_t n_tok) {
   (void)n_traj;
   return carve(nullptr, n_tl, n_tok).bytes;
+}
+
+extern "C" size_t aj_merge_text_workspace_bytes(int32_t n_traj, int32_t n_tl, int64_t n_tok,
+                                                int32_t n_blk) {
+  (void)n_traj;
+  return carve(nullptr, n_tl, n_tok, n_blk < 0 ? 0 : n_blk).bytes;
+}
+
+extern "C" int aj_merge_timelines_text(const aj_timelines *in, const aj_block_texts *text,
+                                       aj_packed *out, int64_t *ti, int32_t *err, void *ws,
+                                       size_t ws_bytes, void *stream) {
+  return run_text(in, text, out, ti, err, ws, ws_bytes, stream);
 }
 
 extern "C" int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws,

@@ -29,7 +29,8 @@ def workload(model, n_traj=8, seed=0, **kw):
 
 
 def episodes(tl, old):
-    return om.episodes_from_flat(tl.traj_tl_off, tl.tl_tok_off, tl.tok, tl.flags, old, tl.adv)
+    return om.episodes_from_flat(tl.traj_tl_off, tl.tl_tok_off, tl.tok, tl.flags, old, tl.adv,
+                                 tl.blk_text)
 
 
 def nudge_old(cur, noise, llm, eps, margin):
@@ -45,10 +46,13 @@ def nudge_old(cur, noise, llm, eps, margin):
 class Case:
     """One seeded actor-update case with the oracle's merged/unmerged results."""
 
-    def __init__(self, cfg, noise_std=0.05, margin=0.0, gain_std=0.1, wseed=1000):
+    def __init__(self, cfg, noise_std=0.05, margin=0.0, gain_std=0.1, wseed=1000, think_p=None,
+                 text=False):
+        """think_p: draw text keys and strip thinking (see make_timelines);
+        text: the merged layout uses text-level Match."""
         m = cfg.model
-        self.cfg, self.m = cfg, m
-        self.tl = tl = make_timelines(cfg)
+        self.cfg, self.m, self.text = cfg, m, text
+        self.tl = tl = make_timelines(cfg, think_p=think_p)
         self.W = make_weights_numpy(m, seed=wseed, gain_std=gain_std)
         if m.dtype == "bf16":
             from workloads import bf16_round
@@ -56,12 +60,22 @@ class Case:
         zero = np.zeros(tl.n_tok, np.float32)
         un = om.unmerged_batch(episodes(tl, zero))
         cur = M.current_logprob(un, self.W, m)
+        if text:
+            # under text-level Match a response can be scored in another
+            # context than it was sampled in: keep the clip margin around the
+            # log-probs of the text-merged layout, traced back to input tokens
+            tr, _ = om.merge_batch(episodes(tl, np.arange(tl.n_tok, dtype=np.float64)),
+                                   om.match_text)
+            cur_m = M.current_logprob(tr, self.W, m)
+            sel = tr.mask == 1
+            cur = np.full(tl.n_tok, np.nan)
+            cur[tr.old_logprob[sel].astype(np.int64)] = cur_m[sel]
         llm = (tl.flags & 3) == 2
         rng = np.random.default_rng(cfg.seed + 77)
         noise = tl.lp_noise if noise_std == 0.05 else rng.normal(0, noise_std, tl.n_tok)
         self.old = nudge_old(np.nan_to_num(cur), noise, llm, m.clip_eps, margin)
         eps_ = episodes(tl, self.old)
-        self.merged, self.absorbers = om.merge_batch(eps_)
+        self.merged, self.absorbers = om.merge_batch(eps_, om.match_text if text else om.match_token)
         self.unmerged = om.unmerged_batch(eps_)
         self._ref = {}
 

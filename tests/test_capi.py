@@ -82,6 +82,30 @@ def test_host_validation_needs_no_gpu():
     assert L.aj_logprob_pg_loss_fwd(C.byref(lc), C.byref(li), *([None] * 9), 0, None) == 2
 
 
+def test_text_merge_host_validation():
+    """aj_merge_timelines_text: argument errors return before any HIP call."""
+    capi = _lib()
+    L = capi.lib()
+    d = C.c_void_p(256)                       # never dereferenced on the host
+    tl = capi.Timelines(1, 2, 10, d, d, d, d, d, d)
+    out = capi.Packed(*[d] * 11)
+    assert L.aj_merge_timelines_text(C.byref(tl), None, C.byref(out), None, None, d, 1 << 20,
+                                     None) == 1
+    txt = capi.BlockTexts(11, d)              # more blocks than tokens
+    assert L.aj_merge_timelines_text(C.byref(tl), C.byref(txt), C.byref(out), None, None, d,
+                                     1 << 20, None) == 2
+    assert b"n_blk" in L.aj_last_error()
+    txt = capi.BlockTexts(4, None)
+    assert L.aj_merge_timelines_text(C.byref(tl), C.byref(txt), C.byref(out), None, None, d,
+                                     1 << 20, None) == 1
+    txt = capi.BlockTexts(4, d)
+    need = capi.aj_merge_text_workspace_bytes(1, 2, 10, 4)
+    assert L.aj_merge_timelines_text(C.byref(tl), C.byref(txt), C.byref(out), None, None, d,
+                                     need - 1, None) == 4
+    assert capi.aj_merge_text_workspace_bytes(4, 32, 5000, 200) > \
+        capi.aj_merge_text_workspace_bytes(4, 32, 5000, 100)
+
+
 def test_workspace_queries_grow_with_size():
     capi = _lib()
     L = capi.lib()

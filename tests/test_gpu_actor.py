@@ -10,7 +10,9 @@ import numpy as np
 import pytest
 import torch
 
-from tests.gpu_cases import Case, bf16_case_model, workload, rel_l2, cosine, loss_rel_err
+from oracle import merge as om
+from tests.gpu_cases import (Case, bf16_case_model, workload, rel_l2, cosine, loss_rel_err,
+                             episodes)
 from workloads import get_config
 
 pytestmark = pytest.mark.gpu
@@ -23,7 +25,7 @@ def run_gpu(case, merged=True, pack_tokens=131072, ref_pos=None, kl_coef=0.0):
     """ref_pos: optional reference log-probs per merged position (host array)."""
     from paper_2606_04484_amd import actor
     dev = actor.upload_timelines(case.tl, case.old)
-    L = actor.merge(dev, merged=merged, pack_tokens=pack_tokens)
+    L = actor.merge(dev, merged=merged, pack_tokens=pack_tokens, text=merged and case.text)
     A = actor.ActorUpdate(case.m, case.device_weights())
     A.zero_grads()
     ref = None
@@ -62,6 +64,21 @@ def test_tiny_f32(merged):
     case = Case(get_config(0), margin=0.01)
     print(f"tiny f32 merged={merged}", flush=True)
     check(case, run_gpu(case, merged), merged, 1e-4, 1e-4, 1e-4, 0.99999)
+
+
+def test_tiny_f32_text_match():
+    """The update over a text-level merge: every response's thinking section
+    stripped from later contexts, so blocks change length and positions are
+    laid out again; the oracle runs the same text-level merge."""
+    case = Case(get_config(0), margin=0.01, think_p=1.0, text=True)
+    assert case.merged.n_seg < len(om.merge_batch(episodes(case.tl, case.old))[0].cu_seqlens) - 1
+    check(case, run_gpu(case, True), True, 1e-4, 1e-4, 1e-4, 0.99999)
+
+
+def test_bf16_text_match():
+    m = bf16_case_model(**BF16_CASES["hd128_gqa3"])
+    case = Case(workload(m), noise_std=0.3, margin=0.05, think_p=0.5, text=True)
+    check(case, run_gpu(case, True), True, 2e-2, 1e-2, 1e-2, 0.999)
 
 
 BF16_CASES = {
