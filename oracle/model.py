@@ -1,4 +1,5 @@
-"""One decoder block + LM head + clipped policy-gradient loss, float64, forward and backward.
+"""Decoder block(s) + LM head + clipped policy-gradient loss, float64, forward
+and backward -- test infrastructure only.
 
 What is computed (the policy is a one-block Qwen2-style decoder; the paper
 trains Qwen2/Qwen2.5/Qwen3 models and defines no architecture, so these are
@@ -12,6 +13,9 @@ readings):
   x1  = x + o W_o^T
   b   = RMSNorm(x1) * g2
   y   = x1 + (silu(b W_gate^T) * (b W_up^T)) W_down^T
+        (with n_layers > 1 the block repeats, each layer with its own weights,
+        the output of one the input of the next: step (4) of Section 4.2
+        updates the whole model; the repetition is the standard decoder stack)
   hn  = RMSNorm(y) * gf
   logprob[p] = log softmax(hn[p-1] W_vocab^T)[tok[p]]  for p after its segment's start
 The loss is GRPO's clipped surrogate (Section 3 cites GRPO-style updates; the
@@ -34,6 +38,8 @@ estimator of KL(pi || pi_ref) at the sampled token, clamped to [-10, 10]):
 The backward pass is written out by hand from these formulas.
 """
 import numpy as np
+
+from workloads import BLOCK_WEIGHTS, layer_key
 
 
 # ---------------------------------------------------------------- pieces
@@ -222,6 +228,29 @@ def block_backward(dy, c, W, cu_seqlens, m):
     return dx, g
 
 
+def layer_weights(W, layer):
+    return {name: W[layer_key(name, layer)] for name in BLOCK_WEIGHTS}
+
+
+def stack_forward(x, W, cu_seqlens, pos, m):
+    """The m.n_layers blocks in order; returns the last output and every layer's cache."""
+    caches = []
+    for layer in range(m.n_layers):
+        x, c = block_forward(x, layer_weights(W, layer), cu_seqlens, pos, m)
+        caches.append(c)
+    return x, caches
+
+
+def stack_backward(dy, caches, W, cu_seqlens, m):
+    """The blocks in reverse; gradients keyed like the weights."""
+    g = {}
+    for layer in reversed(range(m.n_layers)):
+        dy, gl = block_backward(dy, caches[layer], layer_weights(W, layer), cu_seqlens, m)
+        for name, v in gl.items():
+            g[layer_key(name, layer)] = v
+    return dy, g
+
+
 def lm_head_forward(y, W, tok, tgt, m, row_chunk=2048):
     """Final norm, then log-prob of tok[p] from row p-1, for the target positions `tgt`.
 
@@ -276,7 +305,7 @@ def actor_update(packed, W, m, n_mask=None, ref_logprob=None, kl_coef=0.0):
     if n_mask is None:
         n_mask = len(masked)
     x = W["emb"][tok]
-    y, c = block_forward(x, W, packed.cu_seqlens, packed.pos, m)
+    y, c = stack_forward(x, W, packed.cu_seqlens, packed.pos, m)
     hn, rf, lp_t, lse_t = lm_head_forward(y, W, tok, tgt, m)
     logprob = np.full(n, np.nan)
     logprob[tgt] = lp_t
@@ -293,7 +322,7 @@ def actor_update(packed, W, m, n_mask=None, ref_logprob=None, kl_coef=0.0):
     if n_mask:
         dlp[sel] = dterm / n_mask
     dy, dgf, dWv = lm_head_backward(dlp, hn, rf, y, W, tok, tgt, lse_t, m)
-    dx, g = block_backward(dy, c, W, packed.cu_seqlens, m)
+    dx, g = stack_backward(dy, c, W, packed.cu_seqlens, m)
     g["final_norm"] = dgf
     g["w_vocab"] = dWv
     dE = np.zeros_like(W["emb"])
@@ -308,7 +337,7 @@ def current_logprob(packed, W, m):
     """Log-probs of every target under W (forward only); NaN at segment starts."""
     W = f64_weights(W)
     x = W["emb"][packed.tok]
-    y, _ = block_forward(x, W, packed.cu_seqlens, packed.pos, m)
+    y, _ = stack_forward(x, W, packed.cu_seqlens, packed.pos, m)
     tgt = target_positions(packed.cu_seqlens, packed.n_tok)
     _, _, lp, _ = lm_head_forward(y, W, packed.tok, tgt, m)
     out = np.full(packed.n_tok, np.nan)
@@ -323,6 +352,8 @@ def block_forward_rows(x_seg, pos_seg, rows, W, m):
     values of every earlier position of the segment, everything else only at
     `rows`.  Used to check outputs of very long segments one row at a time.
     """
+    if m.n_layers != 1:
+        raise ValueError("block_forward_rows follows one block")
     W = f64_weights(W)
     rows = np.asarray(rows, np.int64)
     Hq, Hkv, hd, F = m.n_q_heads, m.n_kv_heads, m.head_dim, m.d_ff

@@ -232,40 +232,46 @@ def test_gradients_match_finite_differences(name):
         assert abs(fd - g[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (name, idx, fd, g[idx])
 
 
-def test_gradients_match_torch_autograd():
+@pytest.mark.parametrize("n_layers", [1, 3])
+def test_gradients_match_torch_autograd(n_layers):
     """A torch float64 forward built from library ops, differentiated by autograd."""
-    m = SMALL
+    m = dataclasses.replace(SMALL, n_layers=n_layers)
     rng = np.random.default_rng(13)
     Wn = M.f64_weights(make_weights_numpy(m, seed=14, gain_std=0.3))
     p = _packed([7, 9], m.vocab, rng, mask_p=0.7)
     out = M.actor_update(p, Wn, m)
     W = {k: torch.tensor(v, requires_grad=True) for k, v in Wn.items()}
     Hq, Hkv, hd, Fd = m.n_q_heads, m.n_kv_heads, m.head_dim, m.d_ff
-    x = W["emb"][torch.tensor(p.tok)]
-    a = F.rms_norm(x, (m.d_model,), W["attn_norm"], eps=m.rms_eps)
-    qkv = a @ W["w_qkv"].T
     n = p.n_tok
-    q = qkv[:, :Hq * hd].reshape(n, Hq, hd)
-    k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(n, Hkv, hd)
-    v = qkv[:, (Hq + Hkv) * hd:].reshape(n, Hkv, hd)
     ang = torch.tensor(p.pos, dtype=torch.float64)[:, None] * (m.rope_theta ** (-torch.arange(0, hd, 2) / hd))
     def rot(t):
         z = torch.view_as_complex(torch.stack([t[..., :hd // 2], t[..., hd // 2:]], -1).contiguous())
         zr = torch.view_as_real(z * torch.polar(torch.ones_like(ang), ang)[:, None, :])
         return torch.cat([zr[..., 0], zr[..., 1]], -1)
-    q, k = rot(q), rot(k)
-    outs = []
-    for s in range(p.n_seg):
-        lo, hi = p.cu_seqlens[s], p.cu_seqlens[s + 1]
-        tq = q[lo:hi].permute(1, 0, 2)
-        tk = k[lo:hi].permute(1, 0, 2).repeat_interleave(Hq // Hkv, 0)
-        tv = v[lo:hi].permute(1, 0, 2).repeat_interleave(Hq // Hkv, 0)
-        outs.append(F.scaled_dot_product_attention(tq, tk, tv, is_causal=True).permute(1, 0, 2))
-    o = torch.cat(outs).reshape(n, Hq * hd)
-    x1 = x + o @ W["w_o"].T
-    b = F.rms_norm(x1, (m.d_model,), W["mlp_norm"], eps=m.rms_eps)
-    gu = b @ W["w_gate_up"].T
-    y = x1 + (F.silu(gu[:, :Fd]) * gu[:, Fd:]) @ W["w_down"].T
+
+    def block(x, sfx):
+        a = F.rms_norm(x, (m.d_model,), W["attn_norm" + sfx], eps=m.rms_eps)
+        qkv = a @ W["w_qkv" + sfx].T
+        q = qkv[:, :Hq * hd].reshape(n, Hq, hd)
+        k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(n, Hkv, hd)
+        v = qkv[:, (Hq + Hkv) * hd:].reshape(n, Hkv, hd)
+        q, k = rot(q), rot(k)
+        outs = []
+        for s in range(p.n_seg):
+            lo, hi = p.cu_seqlens[s], p.cu_seqlens[s + 1]
+            tq = q[lo:hi].permute(1, 0, 2)
+            tk = k[lo:hi].permute(1, 0, 2).repeat_interleave(Hq // Hkv, 0)
+            tv = v[lo:hi].permute(1, 0, 2).repeat_interleave(Hq // Hkv, 0)
+            outs.append(F.scaled_dot_product_attention(tq, tk, tv, is_causal=True).permute(1, 0, 2))
+        o = torch.cat(outs).reshape(n, Hq * hd)
+        x1 = x + o @ W["w_o" + sfx].T
+        b = F.rms_norm(x1, (m.d_model,), W["mlp_norm" + sfx], eps=m.rms_eps)
+        gu = b @ W["w_gate_up" + sfx].T
+        return x1 + (F.silu(gu[:, :Fd]) * gu[:, Fd:]) @ W["w_down" + sfx].T
+
+    y = W["emb"][torch.tensor(p.tok)]
+    for layer in range(n_layers):
+        y = block(y, "" if layer == 0 else f".{layer}")
     hn = F.rms_norm(y, (m.d_model,), W["final_norm"], eps=m.rms_eps)
     tgt = torch.tensor(out["tgt"])
     lp = torch.log_softmax(hn[tgt - 1] @ W["w_vocab"].T, -1).gather(1, torch.tensor(p.tok)[tgt][:, None])[:, 0]
@@ -279,6 +285,44 @@ def test_gradients_match_torch_autograd():
     for kname, t in W.items():
         np.testing.assert_allclose(out["grads"][kname], t.grad.numpy(), atol=1e-12, rtol=1e-9,
                                    err_msg=kname)
+
+
+@pytest.mark.parametrize("name", ["w_qkv.1", "w_down.1", "attn_norm.1", "w_o", "mlp_norm"])
+def test_two_layer_gradients_match_finite_differences(name):
+    m = dataclasses.replace(SMALL, n_layers=2)
+    rng = np.random.default_rng(21)
+    W = M.f64_weights(make_weights_numpy(m, seed=22, gain_std=0.3))
+    p = _packed([6, 5], m.vocab, rng, mask_p=0.7)
+    out = M.actor_update(p, W, m, n_mask=7)
+    assert np.all(np.abs(np.abs(out["ratio"] - 1) - m.clip_eps) > 1e-3)
+    g = out["grads"][name]
+    flat = list(np.ndindex(g.shape))
+    for idx in [flat[i] for i in rng.choice(len(flat), size=min(25, len(flat)), replace=False)]:
+        h = 1e-6 * max(1.0, abs(W[name][idx]))
+        fd = (_loss_with(p, W, m, name, idx, h) - _loss_with(p, W, m, name, idx, -h)) / (2 * h)
+        assert abs(fd - g[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (name, idx, fd, g[idx])
+
+
+def test_identity_layers_leave_the_model_unchanged():
+    """Layers whose output and down projections are zero pass x through: a
+    3-layer stack with two such layers is the 1-layer model exactly."""
+    m1 = SMALL
+    m3 = dataclasses.replace(SMALL, n_layers=3)
+    rng = np.random.default_rng(23)
+    W3 = M.f64_weights(make_weights_numpy(m3, seed=24, gain_std=0.3))
+    for layer in (1, 2):
+        W3[f"w_o.{layer}"][:] = 0.0
+        W3[f"w_down.{layer}"][:] = 0.0
+    W1 = {k: v for k, v in W3.items() if "." not in k}
+    p = _packed([8, 3, 6], m1.vocab, rng, mask_p=0.7)
+    a, b = M.actor_update(p, W1, m1), M.actor_update(p, W3, m3)
+    np.testing.assert_array_equal(a["logprob"], b["logprob"])
+    assert a["loss"] == b["loss"]
+    for k in W1:
+        np.testing.assert_array_equal(a["grads"][k], b["grads"][k], err_msg=k)
+    # nothing flows into the zeroed branches' inputs
+    for layer in (1, 2):
+        assert not np.any(b["grads"][f"w_qkv.{layer}"]) and not np.any(b["grads"][f"w_gate_up.{layer}"])
 
 
 # ------------------------------------------------------------------ merged == unmerged

@@ -30,6 +30,7 @@ class ModelConfig:
     clip_eps: float = 0.2
     vocab_chunk: int = 32768
     pack_tokens: int = 131072
+    n_layers: int = 1            # decoder blocks between the embedding and the final norm
 
     @property
     def qkv_dim(self) -> int:

@@ -207,16 +207,29 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
 
 WEIGHT_NAMES = ("emb", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down",
                 "final_norm", "w_vocab")
+BLOCK_WEIGHTS = ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+
+
+def layer_key(name, layer):
+    """Key of a block weight in the weight dict: layer 0 under its plain name,
+    layer l >= 1 under "name.l"."""
+    return name if layer == 0 else f"{name}.{layer}"
 
 
 def weight_shapes(m):
+    """Shapes by key: the one-block names first (drawn first), then the block
+    weights of layers 1 .. n_layers-1."""
     d = m.d_model
-    return {
+    shapes = {
         "emb": (m.vocab, d), "attn_norm": (d,), "w_qkv": (m.qkv_dim, d),
         "w_o": (d, m.n_q_heads * m.head_dim), "mlp_norm": (d,),
         "w_gate_up": (2 * m.d_ff, d), "w_down": (d, m.d_ff), "final_norm": (d,),
         "w_vocab": (m.vocab, d),
     }
+    for layer in range(1, m.n_layers):
+        for name in BLOCK_WEIGHTS:
+            shapes[layer_key(name, layer)] = shapes[name]
+    return shapes
 
 
 def make_weights_numpy(m, seed=1000, gain_std=0.0, scale=None):
@@ -230,12 +243,13 @@ def make_weights_numpy(m, seed=1000, gain_std=0.0, scale=None):
     rng = np.random.default_rng(seed)
     out = {}
     for name, shape in weight_shapes(m).items():
-        if name.endswith("norm"):
+        base = name.split(".")[0]
+        if base.endswith("norm"):
             w = np.ones(shape, np.float32)
             if gain_std:
                 w += rng.normal(0.0, gain_std, shape).astype(np.float32)
         else:
-            std = m.init_std if scale is None else scale.get(name, m.init_std)
+            std = m.init_std if scale is None else scale.get(base, m.init_std)
             w = (rng.standard_normal(shape, dtype=np.float32) * np.float32(std))
         out[name] = bf16_round(w) if m.dtype == "bf16" else w.astype(np.float32)
     return out
@@ -253,7 +267,7 @@ def make_weights_torch(m, seed=1000, device="cuda", gain_std=0.0):
     dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
     out = {}
     for name, shape in weight_shapes(m).items():
-        if name.endswith("norm"):
+        if name.split(".")[0].endswith("norm"):
             w = torch.ones(shape, device=device, dtype=torch.float32)
             if gain_std:
                 w += torch.randn(shape, generator=g, device=device) * gain_std
