@@ -192,7 +192,40 @@ def extras(A, merger, cfg, tl, dev, torch, capi, actor, steps):
                     "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     del P, G, M1, M2, Pc
     out["text_merge"] = text_merge(A, cfg, torch, capi, actor, steps)
+    out["full_model"] = full_model(merger, cfg, torch, capi, actor)
     return out
+
+
+FULL_LAYERS = 28        # decoder blocks of a 1.5B-class model at this block shape
+
+
+def full_model(merger, cfg, torch, capi, actor):
+    """The whole actor update of a FULL_LAYERS-block policy on the same merged
+    batch: activation checkpointing (layer inputs kept, every block but the
+    last recomputed in the backward).  Flops count the model once (the
+    recompute is not credited)."""
+    import dataclasses
+    from workloads import make_weights_torch
+    m = dataclasses.replace(cfg.model, n_layers=FULL_LAYERS)
+    W = make_weights_torch(m, seed=1000, device="cuda")
+    A = actor.ActorUpdate(m, W)
+    merger.launch(True)
+    L = merger.layout(m.pack_tokens)
+    A.prepare(L)
+    L, t, _ = timed(A, merger, True, 1, 1, torch, capi)
+    blk, lm, att, _ = step_flops(L, m)
+    total = FULL_LAYERS * (blk + att) + lm
+    peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_F32_TFLOPS
+    ckpt = capi.aj_stack_ckpt_bytes(A.bcfg, FULL_LAYERS, max(p["t1"] - p["t0"] for p in L.packs))
+    res = {"n_layers": FULL_LAYERS, "params": sum(v.numel() for v in W.values()),
+           "merged_tokens": L.n_tok, "ms_per_step": round(t * 1e3, 1),
+           "tokens_per_s": round(L.n_tok / t, 1),
+           "algorithmic_tflop_per_step": round(total / 1e12, 2),
+           "mfma_util": round(total / t / 1e12 / peak, 4),
+           "checkpoint_GB_per_pack": round(ckpt / 1e9, 2)}
+    del A, W
+    torch.cuda.empty_cache()
+    return res
 
 
 def text_merge(A, cfg, torch, capi, actor, steps):

@@ -234,6 +234,31 @@ int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w, cons
                         const void *x, const void *saved, const float *dy, float *dx,
                         const aj_block_grads *g, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------ 2b. layer stack
+ * A policy of n_layers such blocks, each with its own weights, the output of
+ * one the input of the next (step (4) of Section 4.2 updates the whole model;
+ * the stack is the standard decoder).  Activation checkpointing: the forward
+ * keeps each layer's INPUT -- x for layer 0, then n_layers-1 slabs of
+ * [n_tok, d] in `ckpt` -- and leaves the last layer's saved activations in
+ * `saved`.  The backward runs the last layer's backward, then for each earlier
+ * layer recomputes its forward into the same `saved` arena (rewriting its
+ * output slab with the same values) right before its backward.  Memory: one
+ * arena plus (n_layers-1)*n_tok*d elements instead of n_layers arenas; cost:
+ * one more forward of every layer but the last.  With n_layers == 1 these
+ * are aj_varlen_block_fwd / _bwd and ckpt may be NULL.
+ * w, g: HOST arrays of n_layers structs holding device pointers.
+ * x must stay unchanged from the forward to the backward and alias nothing;
+ * dx may alias dy; `saved` and `ckpt` must not be touched in between.
+ */
+size_t aj_stack_ckpt_bytes(const aj_block_cfg *cfg, int32_t n_layers, int32_t n_tok);
+int aj_stack_fwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                 const aj_varlen *vl, const void *x, void *y, void *ckpt, void *saved,
+                 void *stream);
+/* ws: aj_block_workspace_bytes(cfg, n_tok, n_seg). */
+int aj_stack_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                 const aj_varlen *vl, const void *x, void *ckpt, void *saved, const float *dy,
+                 float *dx, const aj_block_grads *g, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------ 3. loss
  * hn = RMSNorm(h) * g_final; for every target position p (targets[i]):
  *   logprob[i] = log softmax(hn[p-1] W_vocab^T)[tok[p]]

@@ -18,6 +18,12 @@ from . import capi as C
 BLOCK_NAMES = ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
 
 
+def layer_key(name, layer):
+    """Weight-dict key of a block weight: layer 0 under its plain name, layer l >= 1
+    under "name.l"."""
+    return name if layer == 0 else f"{name}.{layer}"
+
+
 def upload_timelines(tl, old_logprob, device="cuda"):
     """Host Timelines (+ rollout log-probs, float32 [n_tok]) -> device tensors; the block
     text keys too when the timelines carry them (bit patterns in an int64 tensor)."""
@@ -127,11 +133,13 @@ def merge(tl_dev, merged=True, pack_tokens=131072, text=False):
 
 
 class ActorUpdate:
-    """Weights, gradient accumulators and step buffers of one policy block + LM head."""
+    """Weights, gradient accumulators and step buffers of the policy: embedding,
+    m.n_layers decoder blocks (checkpointed: aj_stack_fwd / aj_stack_bwd), LM head."""
 
     def __init__(self, m, weights, device="cuda"):
         self.m = m
         self.W = weights
+        self.n_layers = getattr(m, "n_layers", 1)
         self.dev = torch.device(device)
         self.dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
         self.bcfg = C.block_cfg(m)
@@ -142,6 +150,10 @@ class ActorUpdate:
         self.stats = torch.zeros(5, dtype=torch.float32, device=self.dev)
         self.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
         self._cap = (0, 0)
+        self.layers = [{k: weights[layer_key(k, l)] for k in BLOCK_NAMES}
+                       for l in range(self.n_layers)]
+        self.layer_grads = [{k: self.G[layer_key(k, l)] for k in BLOCK_NAMES}
+                            for l in range(self.n_layers)]
 
     def zero_grads(self):
         for g in self.G.values():
@@ -158,6 +170,7 @@ class ActorUpdate:
         self.y = torch.empty(n_tok, d, dtype=self.dt, device=dev)
         self.dh = torch.empty(n_tok, d, dtype=torch.float32, device=dev)
         self.saved = u8(C.aj_block_saved_bytes(self.bcfg, n_tok))
+        self.ckpt = u8(C.aj_stack_ckpt_bytes(self.bcfg, self.n_layers, n_tok))
         self.bws = u8(C.aj_block_workspace_bytes(self.bcfg, n_tok, n_tok))
         self.lsaved = u8(C.aj_loss_saved_bytes(self.lcfg, n_tgt))
         self.lws = u8(C.aj_loss_workspace_bytes(self.lcfg, n_tgt))
@@ -181,8 +194,6 @@ class ActorUpdate:
             self.prepare(L)
         W, G = self.W, self.G
         inv = 1.0 / L.n_mask if L.n_mask else 0.0
-        bw = {k: W[k] for k in BLOCK_NAMES}
-        bg = {k: G[k] for k in BLOCK_NAMES}
         for p in L.packs:
             t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
             n = t1 - t0
@@ -192,8 +203,8 @@ class ActorUpdate:
             pos = L.pos[t0:t1]
             tg = L.targets[r0:r1]
             C.aj_embed_fwd(tok, W["emb"], x, self.err)
-            C.aj_varlen_block_fwd(self.bcfg, bw, cu, pos, p["max_len"], x, y, self.saved,
-                                  base=t0)
+            C.aj_stack_fwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, y, self.ckpt,
+                           self.saved, base=t0)
             ref = ref_logprob[r0:r1] if ref_logprob is not None else None
             C.aj_logprob_pg_loss_fwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
@@ -204,8 +215,8 @@ class ActorUpdate:
                                      self.logprob[r0:r1], self.lse[r0:r1], dh,
                                      G["final_norm"], G["w_vocab"], self.lws, row_base=t0,
                                      ref_logprob=ref, kl_coef=kl_coef)
-            C.aj_varlen_block_bwd(self.bcfg, bw, cu, pos, p["max_len"], x, self.saved, dh, dh, bg,
-                                  self.bws, base=t0)
+            C.aj_stack_bwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, self.ckpt,
+                           self.saved, dh, dh, self.layer_grads, self.bws, base=t0)
             C.aj_embed_bwd(tok, dh, G["emb"])
         return self.stats
 
@@ -213,13 +224,12 @@ class ActorUpdate:
         """Log-probs of every target under the current weights (forward only)."""
         self.prepare(L)
         inv = 1.0 / L.n_mask if L.n_mask else 0.0
-        bw = {k: self.W[k] for k in BLOCK_NAMES}
         for p in L.packs:
             t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
             n = t1 - t0
             C.aj_embed_fwd(L.tok[t0:t1], self.W["emb"], self.x[:n], self.err)
-            C.aj_varlen_block_fwd(self.bcfg, bw, L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1],
-                                  p["max_len"], self.x[:n], self.y[:n], self.saved, base=t0)
+            C.aj_stack_fwd(self.bcfg, self.layers, L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1],
+                           p["max_len"], self.x[:n], self.y[:n], self.ckpt, self.saved, base=t0)
             C.aj_logprob_pg_loss_fwd(self.lcfg, L.targets[r0:r1], L.tok, L.old_logprob, L.adv,
                                      inv, self.y[:n], self.W["final_norm"], self.W["w_vocab"],
                                      self.lsaved, self.logprob[r0:r1], self.lse[r0:r1],

@@ -111,6 +111,12 @@ EXPORTS = {
     "aj_varlen_block_bwd": (C.c_int, [C.POINTER(BlockCfg), C.POINTER(BlockWeights),
                                       C.POINTER(Varlen), vp, vp, vp, vp,
                                       C.POINTER(BlockGrads), vp, sz, vp]),
+    "aj_stack_ckpt_bytes": (sz, [C.POINTER(BlockCfg), i32, i32]),
+    "aj_stack_fwd": (C.c_int, [C.POINTER(BlockCfg), i32, C.POINTER(BlockWeights),
+                               C.POINTER(Varlen), vp, vp, vp, vp, vp]),
+    "aj_stack_bwd": (C.c_int, [C.POINTER(BlockCfg), i32, C.POINTER(BlockWeights),
+                               C.POINTER(Varlen), vp, vp, vp, vp, vp, C.POINTER(BlockGrads), vp,
+                               sz, vp]),
     "aj_loss_saved_bytes": (sz, [C.POINTER(LossCfg), i32]),
     "aj_loss_workspace_bytes": (sz, [C.POINTER(LossCfg), i32]),
     "aj_logprob_pg_loss_fwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
@@ -286,6 +292,37 @@ def aj_varlen_block_bwd(cfg, w, cu_seqlens, pos, max_seqlen, x, saved, dy, dx, g
                                      ptr(saved), ptr(dy), ptr(dx), C.byref(g), ptr(ws),
                                      ws.numel() * ws.element_size(), stream_handle(stream)),
            "aj_varlen_block_bwd")
+
+
+def aj_stack_ckpt_bytes(cfg, n_layers, n_tok):
+    return int(lib().aj_stack_ckpt_bytes(C.byref(cfg), n_layers, n_tok))
+
+
+def _layers(ws, kind, names=("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")):
+    arr = (kind * len(ws))()
+    for i, w in enumerate(ws):
+        arr[i] = kind(*[ptr(w[k]) for k in names])
+    return arr
+
+
+def aj_stack_fwd(cfg, layers, cu_seqlens, pos, max_seqlen, x, y, ckpt, saved, stream=None, base=0):
+    """layers: list of per-layer weight dicts (the keys of aj_block_weights)."""
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    _check(lib().aj_stack_fwd(C.byref(cfg), len(layers), _layers(layers, BlockWeights),
+                              C.byref(vl), ptr(x), ptr(y), ptr(ckpt), ptr(saved),
+                              stream_handle(stream)), "aj_stack_fwd")
+
+
+def aj_stack_bwd(cfg, layers, cu_seqlens, pos, max_seqlen, x, ckpt, saved, dy, dx, grads, ws,
+                 stream=None, base=0):
+    """grads: list of per-layer float32 gradient dicts, accumulated into."""
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    _check(lib().aj_stack_bwd(C.byref(cfg), len(layers), _layers(layers, BlockWeights),
+                              C.byref(vl), ptr(x), ptr(ckpt), ptr(saved), ptr(dy), ptr(dx),
+                              _layers(grads, BlockGrads), ptr(ws), ws.numel() * ws.element_size(),
+                              stream_handle(stream)), "aj_stack_bwd")
 
 
 # ------------------------------------------------------------------ loss

@@ -1,4 +1,5 @@
-// aj_varlen_block_fwd / aj_varlen_block_bwd and the embedding entry points.
+// aj_varlen_block_fwd / aj_varlen_block_bwd, the checkpointed layer stack
+// (aj_stack_fwd / aj_stack_bwd) and the embedding entry points.
 //
 // Forward:  a = RMSNorm(x) g1 -> qkv = a W_qkv^T -> RoPE(q, k) -> o = attention
 //           -> x1 = x + o W_o^T -> b = RMSNorm(x1) g2 -> gu = b W_gu^T
@@ -196,6 +197,44 @@ int check_weights(const aj_block_weights *w, const char *name) {
   return AJ_OK;
 }
 
+int check_grads(const aj_block_grads *g, const char *name) {
+  AJ_REQUIRE(g && g->attn_norm && g->w_qkv && g->w_o && g->mlp_norm && g->w_gate_up && g->w_down,
+             AJ_ERR_NULL, "%s: null gradient", name);
+  return AJ_OK;
+}
+
+// Layer l reads x (l == 0) or checkpoint slab l-1, and writes slab l (or y for
+// the last layer): the checkpoints are the inputs of layers 1 .. n-1.
+template <typename T>
+int stack_fwd(const aj_block_cfg &c, int nl, const aj_block_weights *w, const aj_varlen &v,
+              const T *x, T *y, T *ckpt, const Saved &sv, hipStream_t st) {
+  const int64_t slab = (int64_t)v.n_tok * c.d_model;
+  for (int l = 0; l < nl; ++l) {
+    const T *in = l == 0 ? x : ckpt + (l - 1) * slab;
+    T *out = l == nl - 1 ? y : ckpt + l * slab;
+    if (int r = block_fwd<T>(c, w[l], v, in, out, sv, st)) return r;
+  }
+  return AJ_OK;
+}
+
+// Last layer first, from the arena the forward left; every earlier layer is
+// recomputed into the same arena right before its backward (its output slab
+// is rewritten with the same values: the forward is deterministic).
+template <typename T>
+int stack_bwd(const aj_block_cfg &c, int nl, const aj_block_weights *w, const aj_varlen &v,
+              const T *x, T *ckpt, const Saved &sv, const float *dy, float *dx,
+              const aj_block_grads *g, const BwdWs &ws, hipStream_t st) {
+  const int64_t slab = (int64_t)v.n_tok * c.d_model;
+  for (int l = nl - 1; l >= 0; --l) {
+    const T *in = l == 0 ? x : ckpt + (l - 1) * slab;
+    if (l < nl - 1)
+      if (int r = block_fwd<T>(c, w[l], v, in, ckpt + l * slab, sv, st)) return r;
+    if (int r = block_bwd<T>(c, w[l], v, in, sv, l == nl - 1 ? dy : dx, dx, g[l], ws, st))
+      return r;
+  }
+  return AJ_OK;
+}
+
 }  // namespace
 
 extern "C" size_t aj_block_saved_bytes(const aj_block_cfg *cfg, int32_t n_tok) {
@@ -234,8 +273,7 @@ extern "C" int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weigh
   int r;
   if ((r = check_cfg(cfg, name)) || (r = check_varlen(vl, name)) || (r = check_weights(w, name)))
     return r;
-  AJ_REQUIRE(g && g->attn_norm && g->w_qkv && g->w_o && g->mlp_norm && g->w_gate_up && g->w_down,
-             AJ_ERR_NULL, "%s: null gradient", name);
+  if ((r = check_grads(g, name))) return r;
   if (vl->n_tok == 0) return AJ_OK;
   AJ_REQUIRE(x && saved && dy && dx && ws, AJ_ERR_NULL, "%s: null x/saved/dy/dx/ws", name);
   BwdWs bw = carve_bwd(*cfg, vl->n_tok, ws);
@@ -246,6 +284,60 @@ extern "C" int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weigh
   if (cfg->dtype == AJ_BF16)
     return block_bwd<bf16_t>(*cfg, *w, *vl, (const bf16_t *)x, sv, dy, dx, *g, bw, st);
   return block_bwd<float>(*cfg, *w, *vl, (const float *)x, sv, dy, dx, *g, bw, st);
+}
+
+extern "C" size_t aj_stack_ckpt_bytes(const aj_block_cfg *cfg, int32_t n_layers, int32_t n_tok) {
+  if (!cfg || n_layers < 1 || n_tok < 0) return 0;
+  const size_t es = cfg->dtype == AJ_BF16 ? 2 : 4;
+  return (size_t)(n_layers - 1) * (size_t)n_tok * (size_t)cfg->d_model * es;
+}
+
+extern "C" int aj_stack_fwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                            const aj_varlen *vl, const void *x, void *y, void *ckpt, void *saved,
+                            void *stream) {
+  const char *name = "aj_stack_fwd";
+  int r;
+  if ((r = check_cfg(cfg, name)) || (r = check_varlen(vl, name))) return r;
+  AJ_REQUIRE(n_layers >= 1 && n_layers <= 1024, AJ_ERR_SHAPE, "%s: n_layers %d", name, n_layers);
+  AJ_REQUIRE(w, AJ_ERR_NULL, "%s: null weight array", name);
+  for (int l = 0; l < n_layers; ++l)
+    if ((r = check_weights(&w[l], name))) return r;
+  if (vl->n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(x && y && saved && (ckpt || n_layers == 1), AJ_ERR_NULL,
+             "%s: null x/y/ckpt/saved", name);
+  Saved sv = carve_saved(*cfg, vl->n_tok, saved);
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return stack_fwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)y,
+                             (bf16_t *)ckpt, sv, st);
+  return stack_fwd<float>(*cfg, n_layers, w, *vl, (const float *)x, (float *)y, (float *)ckpt, sv,
+                          st);
+}
+
+extern "C" int aj_stack_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                            const aj_varlen *vl, const void *x, void *ckpt, void *saved,
+                            const float *dy, float *dx, const aj_block_grads *g, void *ws,
+                            size_t ws_bytes, void *stream) {
+  const char *name = "aj_stack_bwd";
+  int r;
+  if ((r = check_cfg(cfg, name)) || (r = check_varlen(vl, name))) return r;
+  AJ_REQUIRE(n_layers >= 1 && n_layers <= 1024, AJ_ERR_SHAPE, "%s: n_layers %d", name, n_layers);
+  AJ_REQUIRE(w && g, AJ_ERR_NULL, "%s: null weight or gradient array", name);
+  for (int l = 0; l < n_layers; ++l)
+    if ((r = check_weights(&w[l], name)) || (r = check_grads(&g[l], name))) return r;
+  if (vl->n_tok == 0) return AJ_OK;
+  AJ_REQUIRE(x && saved && dy && dx && ws && (ckpt || n_layers == 1), AJ_ERR_NULL,
+             "%s: null x/ckpt/saved/dy/dx/ws", name);
+  BwdWs bw = carve_bwd(*cfg, vl->n_tok, ws);
+  AJ_REQUIRE(ws_bytes >= bw.bytes, AJ_ERR_WORKSPACE, "%s: workspace %zu < %zu", name, ws_bytes,
+             bw.bytes);
+  Saved sv = carve_saved(*cfg, vl->n_tok, saved);
+  hipStream_t st = (hipStream_t)stream;
+  if (cfg->dtype == AJ_BF16)
+    return stack_bwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)ckpt, sv, dy, dx,
+                             g, bw, st);
+  return stack_bwd<float>(*cfg, n_layers, w, *vl, (const float *)x, (float *)ckpt, sv, dy, dx, g,
+                          bw, st);
 }
 
 extern "C" int aj_embed_fwd(const int32_t *tok, int32_t n_tok, const void *emb, int32_t d,

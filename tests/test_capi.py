@@ -106,6 +106,26 @@ def test_text_merge_host_validation():
         capi.aj_merge_text_workspace_bytes(4, 32, 5000, 100)
 
 
+def test_stack_host_validation():
+    capi = _lib()
+    L = capi.lib()
+    cfg = capi.BlockCfg(128, 4, 4, 32, 512, 1e-6, 1e6, 1)
+    vl = capi.Varlen(0, 0, 0, 0, None, None)
+    ws = (capi.BlockWeights * 2)(*[capi.BlockWeights(*[C.c_void_p(16)] * 6)] * 2)
+    assert L.aj_stack_fwd(C.byref(cfg), 0, ws, C.byref(vl), None, None, None, None, None) == 2
+    assert L.aj_stack_fwd(C.byref(cfg), 2, None, C.byref(vl), None, None, None, None, None) == 1
+    ws[1].w_o = None
+    assert L.aj_stack_fwd(C.byref(cfg), 2, ws, C.byref(vl), None, None, None, None, None) == 1
+    ws[1].w_o = C.c_void_p(16)
+    gs = (capi.BlockGrads * 2)(*[capi.BlockGrads(*[C.c_void_p(16)] * 6)] * 2)
+    vl = capi.Varlen(10, 1, 10, 0, C.c_void_p(16), C.c_void_p(16))
+    # two layers need the checkpoint buffer
+    assert L.aj_stack_bwd(C.byref(cfg), 2, ws, C.byref(vl), C.c_void_p(16), None, C.c_void_p(16),
+                          C.c_void_p(16), C.c_void_p(16), gs, C.c_void_p(16), 1 << 30, None) == 1
+    assert capi.aj_stack_ckpt_bytes(cfg, 1, 1000) == 0
+    assert capi.aj_stack_ckpt_bytes(cfg, 4, 1000) == 3 * 1000 * 128 * 2
+
+
 def test_workspace_queries_grow_with_size():
     capi = _lib()
     L = capi.lib()
