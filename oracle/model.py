@@ -35,11 +35,19 @@ estimator of KL(pi || pi_ref) at the sampled token, clamped to [-10, 10]):
   L += kl_coef * sum_mask kl / N_mask,   d kl / d logprob = 1 - exp(delta)
 (zero where the clamp binds).
 
+LoRA (Section 4.2, step (4): the update trains "either the full model weights
+or the LoRA matrix weights", citing Hu et al.): every block projection
+W in {W_qkv, W_o, W_gate_up, W_down} of every layer is used as
+  W_eff = W + scale * B A,   A [rank, in], B [out, rank],
+with only A and B trained (norm gains, embedding and LM head frozen).  The
+oracle runs the model with W_eff and takes A's and B's gradients from
+W_eff's by the chain rule: dA = scale B^T dW_eff, dB = scale dW_eff A^T.
+
 The backward pass is written out by hand from these formulas.
 """
 import numpy as np
 
-from workloads import BLOCK_WEIGHTS, layer_key
+from workloads import BLOCK_WEIGHTS, LORA_PROJ, layer_key, lora_key
 
 
 # ---------------------------------------------------------------- pieces
@@ -331,6 +339,32 @@ def actor_update(packed, W, m, n_mask=None, ref_logprob=None, kl_coef=0.0):
     return {"logprob": logprob, "loss": loss, "n_mask": n_mask, "grads": g, "dx": dx,
             "dy": dy, "y": y, "tgt": tgt, "lse": lse_t, "ratio": r, "term": term,
             "kl": kl}
+
+
+def lora_effective(W, lora, scale, m):
+    """The weights with every adapted projection replaced by W + scale B A."""
+    W = f64_weights(W)
+    for layer in range(m.n_layers):
+        for proj in LORA_PROJ:
+            A = np.asarray(lora[lora_key("a", proj, layer)], np.float64)
+            B = np.asarray(lora[lora_key("b", proj, layer)], np.float64)
+            W[layer_key(proj, layer)] = W[layer_key(proj, layer)] + scale * (B @ A)
+    return W
+
+
+def lora_actor_update(packed, W, lora, scale, m, n_mask=None):
+    """actor_update with LoRA adapters; grads holds the adapters' gradients only."""
+    out = actor_update(packed, lora_effective(W, lora, scale, m), m, n_mask=n_mask)
+    g = {}
+    for layer in range(m.n_layers):
+        for proj in LORA_PROJ:
+            dW = out["grads"][layer_key(proj, layer)]
+            A = np.asarray(lora[lora_key("a", proj, layer)], np.float64)
+            B = np.asarray(lora[lora_key("b", proj, layer)], np.float64)
+            g[lora_key("a", proj, layer)] = scale * (B.T @ dW)
+            g[lora_key("b", proj, layer)] = scale * (dW @ A.T)
+    out["grads"] = g
+    return out
 
 
 def current_logprob(packed, W, m):

@@ -16,7 +16,7 @@ import torch.nn.functional as F
 
 from oracle import merge as om
 from oracle import model as M
-from workloads import get_config, make_timelines, make_weights_numpy
+from workloads import get_config, make_timelines, make_weights_numpy, make_lora_numpy
 from workloads.configs import ModelConfig
 
 
@@ -232,26 +232,28 @@ def test_gradients_match_finite_differences(name):
         assert abs(fd - g[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (name, idx, fd, g[idx])
 
 
-@pytest.mark.parametrize("n_layers", [1, 3])
-def test_gradients_match_torch_autograd(n_layers):
-    """A torch float64 forward built from library ops, differentiated by autograd."""
-    m = dataclasses.replace(SMALL, n_layers=n_layers)
-    rng = np.random.default_rng(13)
-    Wn = M.f64_weights(make_weights_numpy(m, seed=14, gain_std=0.3))
-    p = _packed([7, 9], m.vocab, rng, mask_p=0.7)
-    out = M.actor_update(p, Wn, m)
-    W = {k: torch.tensor(v, requires_grad=True) for k, v in Wn.items()}
+def _torch_loss(W, p, m, tgt, L=None, scale=0.0):
+    """A torch float64 forward built from library ops: log-probs at tgt and the
+    clipped loss.  W (and the LoRA matrices L, if any) are torch tensors; a
+    projection with adapters is v W^T + scale (v A^T) B^T, written out."""
     Hq, Hkv, hd, Fd = m.n_q_heads, m.n_kv_heads, m.head_dim, m.d_ff
     n = p.n_tok
     ang = torch.tensor(p.pos, dtype=torch.float64)[:, None] * (m.rope_theta ** (-torch.arange(0, hd, 2) / hd))
+
     def rot(t):
         z = torch.view_as_complex(torch.stack([t[..., :hd // 2], t[..., hd // 2:]], -1).contiguous())
         zr = torch.view_as_real(z * torch.polar(torch.ones_like(ang), ang)[:, None, :])
         return torch.cat([zr[..., 0], zr[..., 1]], -1)
 
+    def proj(v, name, sfx):
+        out = v @ W[name + sfx].T
+        if L is not None:
+            out = out + scale * (v @ L["lora_a." + name + sfx].T) @ L["lora_b." + name + sfx].T
+        return out
+
     def block(x, sfx):
         a = F.rms_norm(x, (m.d_model,), W["attn_norm" + sfx], eps=m.rms_eps)
-        qkv = a @ W["w_qkv" + sfx].T
+        qkv = proj(a, "w_qkv", sfx)
         q = qkv[:, :Hq * hd].reshape(n, Hq, hd)
         k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(n, Hkv, hd)
         v = qkv[:, (Hq + Hkv) * hd:].reshape(n, Hkv, hd)
@@ -264,27 +266,110 @@ def test_gradients_match_torch_autograd(n_layers):
             tv = v[lo:hi].permute(1, 0, 2).repeat_interleave(Hq // Hkv, 0)
             outs.append(F.scaled_dot_product_attention(tq, tk, tv, is_causal=True).permute(1, 0, 2))
         o = torch.cat(outs).reshape(n, Hq * hd)
-        x1 = x + o @ W["w_o" + sfx].T
+        x1 = x + proj(o, "w_o", sfx)
         b = F.rms_norm(x1, (m.d_model,), W["mlp_norm" + sfx], eps=m.rms_eps)
-        gu = b @ W["w_gate_up" + sfx].T
-        return x1 + (F.silu(gu[:, :Fd]) * gu[:, Fd:]) @ W["w_down" + sfx].T
+        gu = proj(b, "w_gate_up", sfx)
+        return x1 + proj(F.silu(gu[:, :Fd]) * gu[:, Fd:], "w_down", sfx)
 
     y = W["emb"][torch.tensor(p.tok)]
-    for layer in range(n_layers):
+    for layer in range(m.n_layers):
         y = block(y, "" if layer == 0 else f".{layer}")
     hn = F.rms_norm(y, (m.d_model,), W["final_norm"], eps=m.rms_eps)
-    tgt = torch.tensor(out["tgt"])
-    lp = torch.log_softmax(hn[tgt - 1] @ W["w_vocab"].T, -1).gather(1, torch.tensor(p.tok)[tgt][:, None])[:, 0]
-    sel = torch.tensor(p.mask[out["tgt"]] == 1)
-    r = torch.exp(lp[sel] - torch.tensor(p.old_logprob[out["tgt"]])[sel])
-    A = torch.tensor(p.adv[out["tgt"]])[sel]
+    tg = torch.tensor(tgt)
+    lp = torch.log_softmax(hn[tg - 1] @ W["w_vocab"].T, -1).gather(1, torch.tensor(p.tok)[tg][:, None])[:, 0]
+    sel = torch.tensor(p.mask[tgt] == 1)
+    r = torch.exp(lp[sel] - torch.tensor(p.old_logprob[tgt])[sel])
+    A = torch.tensor(p.adv[tgt])[sel]
     loss = -torch.minimum(r * A, torch.clamp(r, 1 - m.clip_eps, 1 + m.clip_eps) * A).sum() / sel.sum()
+    return lp, loss
+
+
+@pytest.mark.parametrize("n_layers", [1, 3])
+def test_gradients_match_torch_autograd(n_layers):
+    """A torch float64 forward built from library ops, differentiated by autograd."""
+    m = dataclasses.replace(SMALL, n_layers=n_layers)
+    rng = np.random.default_rng(13)
+    Wn = M.f64_weights(make_weights_numpy(m, seed=14, gain_std=0.3))
+    p = _packed([7, 9], m.vocab, rng, mask_p=0.7)
+    out = M.actor_update(p, Wn, m)
+    W = {k: torch.tensor(v, requires_grad=True) for k, v in Wn.items()}
+    lp, loss = _torch_loss(W, p, m, out["tgt"])
     loss.backward()
     np.testing.assert_allclose(lp.detach().numpy(), out["logprob"][out["tgt"]], atol=1e-12)
     assert abs(loss.item() - out["loss"]) < 1e-12
     for kname, t in W.items():
         np.testing.assert_allclose(out["grads"][kname], t.grad.numpy(), atol=1e-12, rtol=1e-9,
                                    err_msg=kname)
+
+
+# ------------------------------------------------------------------ LoRA
+
+@pytest.mark.parametrize("n_layers", [1, 2])
+def test_lora_gradients_match_torch_autograd(n_layers):
+    """Adapters written out as v W^T + scale (v A^T) B^T in torch and
+    differentiated by autograd: the oracle's merged-weight form and chain
+    rule give the same log-probs, loss and A/B gradients."""
+    m = dataclasses.replace(SMALL, n_layers=n_layers)
+    rng = np.random.default_rng(31)
+    Wn = M.f64_weights(make_weights_numpy(m, seed=32, gain_std=0.3))
+    Ln = {k: v.astype(np.float64) for k, v in make_lora_numpy(m, 8, seed=33, b_std=0.2).items()}
+    scale = 2.0
+    p = _packed([7, 9], m.vocab, rng, mask_p=0.7)
+    out = M.lora_actor_update(p, Wn, Ln, scale, m)
+    W = {k: torch.tensor(v) for k, v in Wn.items()}
+    L = {k: torch.tensor(v, requires_grad=True) for k, v in Ln.items()}
+    lp, loss = _torch_loss(W, p, m, out["tgt"], L, scale)
+    loss.backward()
+    np.testing.assert_allclose(lp.detach().numpy(), out["logprob"][out["tgt"]], atol=1e-12)
+    assert abs(loss.item() - out["loss"]) < 1e-12
+    assert set(out["grads"]) == set(L)
+    for kname, t in L.items():
+        np.testing.assert_allclose(out["grads"][kname], t.grad.numpy(), atol=1e-12, rtol=1e-9,
+                                   err_msg=kname)
+
+
+def test_lora_zero_b_is_the_base_model():
+    """B = 0 (the usual start): the base model's log-probs and loss exactly, no
+    gradient into A (it only reaches the loss through B)."""
+    m = dataclasses.replace(SMALL, n_layers=2)
+    rng = np.random.default_rng(34)
+    W = M.f64_weights(make_weights_numpy(m, seed=35, gain_std=0.3))
+    Ln = make_lora_numpy(m, 8, seed=36)
+    p = _packed([5, 8], m.vocab, rng, mask_p=0.7)
+    a = M.actor_update(p, W, m)
+    b = M.lora_actor_update(p, W, Ln, 4.0, m)
+    np.testing.assert_array_equal(a["logprob"], b["logprob"])
+    assert a["loss"] == b["loss"]
+    for k, g in b["grads"].items():
+        if k.startswith("lora_a"):
+            assert not np.any(g), k
+        else:
+            assert np.any(g), k
+
+
+@pytest.mark.parametrize("name", ["lora_a.w_qkv", "lora_b.w_down.1", "lora_a.w_gate_up.1",
+                                  "lora_b.w_o"])
+def test_lora_gradients_match_finite_differences(name):
+    m = dataclasses.replace(SMALL, n_layers=2)
+    rng = np.random.default_rng(37)
+    W = M.f64_weights(make_weights_numpy(m, seed=38, gain_std=0.3))
+    Ln = {k: v.astype(np.float64) for k, v in make_lora_numpy(m, 8, seed=39, b_std=0.2).items()}
+    p = _packed([6, 5], m.vocab, rng, mask_p=0.7)
+    scale = 0.5
+    out = M.lora_actor_update(p, W, Ln, scale, m, n_mask=7)
+    assert np.all(np.abs(np.abs(out["ratio"] - 1) - m.clip_eps) > 1e-3)
+    g = out["grads"][name]
+
+    def loss_at(idx, h):
+        L2 = {k: v.copy() for k, v in Ln.items()}
+        L2[name][idx] += h
+        return M.lora_actor_update(p, W, L2, scale, m, n_mask=7)["loss"]
+
+    flat = list(np.ndindex(g.shape))
+    for idx in [flat[i] for i in rng.choice(len(flat), size=min(20, len(flat)), replace=False)]:
+        h = 1e-6 * max(1.0, abs(Ln[name][idx]))
+        fd = (loss_at(idx, h) - loss_at(idx, -h)) / (2 * h)
+        assert abs(fd - g[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (name, idx, fd, g[idx])
 
 
 @pytest.mark.parametrize("name", ["w_qkv.1", "w_down.1", "attn_norm.1", "w_o", "mlp_norm"])

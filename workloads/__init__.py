@@ -9,9 +9,11 @@ method's arithmetic, so both the CPU oracle and the GPU path may consume it.
 from .configs import CONFIGS, WorkloadConfig, ModelConfig, get_config
 from .gen import (Timelines, make_timelines, make_weights_numpy, make_weights_torch,
                   AUTHOR_USER, AUTHOR_ENV, AUTHOR_LLM, AUTHOR_MASK, FLAG_BLOCK_START,
-                  bf16_round, make_rewards, layer_key, BLOCK_WEIGHTS)
+                  bf16_round, make_rewards, layer_key, BLOCK_WEIGHTS, LORA_PROJ, lora_key,
+                  lora_shapes, make_lora_numpy)
 
 __all__ = ["CONFIGS", "WorkloadConfig", "ModelConfig", "get_config", "Timelines",
            "make_timelines", "make_weights_numpy", "make_weights_torch",
            "AUTHOR_USER", "AUTHOR_ENV", "AUTHOR_LLM", "AUTHOR_MASK", "FLAG_BLOCK_START",
-           "bf16_round", "make_rewards", "layer_key", "BLOCK_WEIGHTS"]
+           "bf16_round", "make_rewards", "layer_key", "BLOCK_WEIGHTS", "LORA_PROJ", "lora_key",
+           "lora_shapes", "make_lora_numpy"]

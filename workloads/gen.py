@@ -13,7 +13,9 @@ Layout of a batch of unmerged timelines (compressed rows, collection order):
 Each timeline is one intercepted LLM call: its prompt (the context so far, as
 user/env blocks) followed by its own response as the single llm block.
 """
+import dataclasses
 from dataclasses import dataclass
+
 import numpy as np
 
 AUTHOR_USER = 0
@@ -252,6 +254,43 @@ def make_weights_numpy(m, seed=1000, gain_std=0.0, scale=None):
             std = m.init_std if scale is None else scale.get(base, m.init_std)
             w = (rng.standard_normal(shape, dtype=np.float32) * np.float32(std))
         out[name] = bf16_round(w) if m.dtype == "bf16" else w.astype(np.float32)
+    return out
+
+
+LORA_PROJ = ("w_qkv", "w_o", "w_gate_up", "w_down")
+
+
+def lora_key(kind, proj, layer):
+    """Key of a LoRA matrix: kind "a" ([rank, in]) or "b" ([out, rank]) of the
+    block projection `proj` in `layer`, e.g. "lora_a.w_qkv", "lora_b.w_o.2"."""
+    return layer_key(f"lora_{kind}.{proj}", layer)
+
+
+def lora_shapes(m, rank):
+    shapes = weight_shapes(dataclasses.replace(m, n_layers=1))
+    out = {}
+    for layer in range(m.n_layers):
+        for proj in LORA_PROJ:
+            n_out, n_in = shapes[proj]
+            out[lora_key("a", proj, layer)] = (rank, n_in)
+            out[lora_key("b", proj, layer)] = (n_out, rank)
+    return out
+
+
+def make_lora_numpy(m, rank, seed=2000, a_std=None, b_std=0.0):
+    """float32 LoRA matrices (bf16-representable when m.dtype == 'bf16'):
+    A ~ N(0, a_std^2) (default 1/sqrt(in)), B ~ N(0, b_std^2) -- b_std = 0 is
+    the usual zero start; tests draw B too so that the adapters act."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for name, shape in lora_shapes(m, rank).items():
+        if name.startswith("lora_a"):
+            std = a_std if a_std is not None else 1.0 / np.sqrt(shape[1])
+        else:
+            std = b_std
+        w = (rng.standard_normal(shape, dtype=np.float32) * np.float32(std)) if std else \
+            np.zeros(shape, np.float32)
+        out[name] = bf16_round(w) if m.dtype == "bf16" else w
     return out
 
 
