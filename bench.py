@@ -223,7 +223,19 @@ def full_model(merger, cfg, torch, capi, actor):
            "algorithmic_tflop_per_step": round(total / 1e12, 2),
            "mfma_util": round(total / t / 1e12 / peak, 4),
            "checkpoint_GB_per_pack": round(ckpt / 1e9, 2)}
-    del A, W
+    del A
+    # the same model trained through LoRA adapters (rank 32, alpha 64) on all
+    # four projections of every block: base weights, embedding and LM head frozen
+    from workloads import make_lora_numpy
+    rank = 32
+    lora = {k: torch.from_numpy(v).to(device="cuda", dtype=W["emb"].dtype)
+            for k, v in make_lora_numpy(m, rank, seed=2000, b_std=1e-3).items()}
+    A = actor.ActorUpdate(m, W, lora=lora, lora_rank=rank, lora_scale=64.0 / rank)
+    A.prepare(L)
+    L, t, _ = timed(A, merger, True, 1, 1, torch, capi)
+    res["lora"] = {"rank": rank, "alpha": 64, "trainable_params": sum(v.numel() for v in lora.values()),
+                   "ms_per_step": round(t * 1e3, 1), "tokens_per_s": round(L.n_tok / t, 1)}
+    del A, W, lora
     torch.cuda.empty_cache()
     return res
 

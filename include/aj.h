@@ -259,6 +259,43 @@ int aj_stack_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weigh
                  const aj_varlen *vl, const void *x, void *ckpt, void *saved, const float *dy,
                  float *dx, const aj_block_grads *g, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------ 2c. LoRA
+ * Section 4.2, step (4): the update may train LoRA matrices (Hu et al.)
+ * instead of the full weights.  Each of the four projections of every block,
+ * with frozen weight W [out, in], becomes
+ *   P(v) = v W^T + scale * (v A^T) B^T,     A [rank, in], B [out, rank]
+ * (qkv: in d, out (Hq+2Hkv)*hd, before RoPE; o: in Hq*hd, out d; gate_up: in
+ * d, out 2*d_ff; down: in d_ff, out d).  Only A and B train: the block's
+ * weights and norm gains get no gradient (and the caller leaves the embedding
+ * and the LM head frozen too: aj_logprob_pg_loss_bwd takes NULL for their
+ * gradients).  A, B are row-major in cfg->dtype; the products v A^T and
+ * d_out B are scaled and rounded once to cfg->dtype.  rank: a multiple of 8,
+ * 8..256, the same (with the same scale) in every layer.
+ * The forward and backward are those of the layer stack (2b), checkpointed
+ * the same way; `saved` holds aj_lora_saved_bytes (the block's activations
+ * plus the four v A^T products), the backward workspace is
+ * aj_lora_workspace_bytes.  lora, g: HOST arrays of n_layers structs.
+ */
+typedef struct {
+  int32_t rank;
+  float scale;                  /* alpha / rank */
+  const void *a_qkv, *b_qkv, *a_o, *b_o, *a_gate_up, *b_gate_up, *a_down, *b_down;
+} aj_lora;
+
+typedef struct {                /* float32, accumulated */
+  float *a_qkv, *b_qkv, *a_o, *b_o, *a_gate_up, *b_gate_up, *a_down, *b_down;
+} aj_lora_grads;
+
+size_t aj_lora_saved_bytes(const aj_block_cfg *cfg, int32_t rank, int32_t n_tok);
+size_t aj_lora_workspace_bytes(const aj_block_cfg *cfg, int32_t rank, int32_t n_tok);
+int aj_stack_lora_fwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                      const aj_lora *lora, const aj_varlen *vl, const void *x, void *y,
+                      void *ckpt, void *saved, void *stream);
+int aj_stack_lora_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_weights *w,
+                      const aj_lora *lora, const aj_varlen *vl, const void *x, void *ckpt,
+                      void *saved, const float *dy, float *dx, const aj_lora_grads *g, void *ws,
+                      size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------ 3. loss
  * hn = RMSNorm(h) * g_final; for every target position p (targets[i]):
  *   logprob[i] = log softmax(hn[p-1] W_vocab^T)[tok[p]]
@@ -311,7 +348,8 @@ int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
                            float *logprob, float *lse, float *stats, int32_t *err,
                            void *ws, size_t ws_bytes, void *stream);
 /* dh: float32 [n_tok, d], WRITTEN (rows that feed no target become 0).
- * d_final_norm [d], d_w_vocab [vocab, d]: float32, accumulated. */
+ * d_final_norm [d], d_w_vocab [vocab, d]: float32, accumulated; NULL = that
+ * weight is frozen and its gradient is not computed. */
 int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,
                            const void *final_norm, const void *w_vocab, const void *saved,
                            const float *logprob, const float *lse, float *dh,

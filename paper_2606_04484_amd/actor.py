@@ -24,6 +24,15 @@ def layer_key(name, layer):
     return name if layer == 0 else f"{name}.{layer}"
 
 
+LORA_PROJ = {"qkv": "w_qkv", "o": "w_o", "gate_up": "w_gate_up", "down": "w_down"}
+
+
+def lora_key(kind, proj, layer):
+    """Key of a LoRA matrix ("a" [rank, in] or "b" [out, rank]) of projection `proj`
+    (a block weight name) in `layer`: "lora_a.w_qkv", "lora_b.w_o.2", ..."""
+    return layer_key(f"lora_{kind}.{proj}", layer)
+
+
 def upload_timelines(tl, old_logprob, device="cuda"):
     """Host Timelines (+ rollout log-probs, float32 [n_tok]) -> device tensors; the block
     text keys too when the timelines carry them (bit patterns in an int64 tensor)."""
@@ -136,7 +145,10 @@ class ActorUpdate:
     """Weights, gradient accumulators and step buffers of the policy: embedding,
     m.n_layers decoder blocks (checkpointed: aj_stack_fwd / aj_stack_bwd), LM head."""
 
-    def __init__(self, m, weights, device="cuda"):
+    def __init__(self, m, weights, device="cuda", lora=None, lora_rank=0, lora_scale=1.0):
+        """lora: optional dict of LoRA matrices keyed by lora_key (storage dtype of the
+        weights); then only they train (self.G holds their gradients) and every
+        weight, gain, the embedding and the LM head stay frozen."""
         self.m = m
         self.W = weights
         self.n_layers = getattr(m, "n_layers", 1)
@@ -144,16 +156,26 @@ class ActorUpdate:
         self.dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
         self.bcfg = C.block_cfg(m)
         self.lcfg = C.loss_cfg(m)
+        self.lora, self.rank, self.scale = lora, lora_rank, lora_scale
+        trained = lora if lora is not None else weights
         self.G = {k: torch.zeros(v.shape, dtype=torch.float32, device=self.dev)
-                  for k, v in weights.items()}
+                  for k, v in trained.items()}
         # [0] loss, [1] clipped count, [2] sum of r, [3] targets, [4] sum of KL
         self.stats = torch.zeros(5, dtype=torch.float32, device=self.dev)
         self.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
         self._cap = (0, 0)
         self.layers = [{k: weights[layer_key(k, l)] for k in BLOCK_NAMES}
                        for l in range(self.n_layers)]
-        self.layer_grads = [{k: self.G[layer_key(k, l)] for k in BLOCK_NAMES}
-                            for l in range(self.n_layers)]
+        if lora is None:
+            self.layer_grads = [{k: self.G[layer_key(k, l)] for k in BLOCK_NAMES}
+                                for l in range(self.n_layers)]
+        else:
+            def fields(src):
+                return [{f"{kind}_{short}": src[lora_key(kind, proj, l)]
+                         for short, proj in LORA_PROJ.items() for kind in ("a", "b")}
+                        for l in range(self.n_layers)]
+            self.adapters = fields(lora)
+            self.layer_grads = fields(self.G)
 
     def zero_grads(self):
         for g in self.G.values():
@@ -169,9 +191,13 @@ class ActorUpdate:
         self.x = torch.empty(n_tok, d, dtype=self.dt, device=dev)
         self.y = torch.empty(n_tok, d, dtype=self.dt, device=dev)
         self.dh = torch.empty(n_tok, d, dtype=torch.float32, device=dev)
-        self.saved = u8(C.aj_block_saved_bytes(self.bcfg, n_tok))
+        if self.lora is None:
+            self.saved = u8(C.aj_block_saved_bytes(self.bcfg, n_tok))
+            self.bws = u8(C.aj_block_workspace_bytes(self.bcfg, n_tok, n_tok))
+        else:
+            self.saved = u8(C.aj_lora_saved_bytes(self.bcfg, self.rank, n_tok))
+            self.bws = u8(C.aj_lora_workspace_bytes(self.bcfg, self.rank, n_tok))
         self.ckpt = u8(C.aj_stack_ckpt_bytes(self.bcfg, self.n_layers, n_tok))
-        self.bws = u8(C.aj_block_workspace_bytes(self.bcfg, n_tok, n_tok))
         self.lsaved = u8(C.aj_loss_saved_bytes(self.lcfg, n_tgt))
         self.lws = u8(C.aj_loss_workspace_bytes(self.lcfg, n_tgt))
         self._cap = (n_tok, n_tgt)
@@ -203,8 +229,7 @@ class ActorUpdate:
             pos = L.pos[t0:t1]
             tg = L.targets[r0:r1]
             C.aj_embed_fwd(tok, W["emb"], x, self.err)
-            C.aj_stack_fwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, y, self.ckpt,
-                           self.saved, base=t0)
+            self._stack_fwd(cu, pos, p["max_len"], x, y, t0)
             ref = ref_logprob[r0:r1] if ref_logprob is not None else None
             C.aj_logprob_pg_loss_fwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
@@ -213,12 +238,25 @@ class ActorUpdate:
             C.aj_logprob_pg_loss_bwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
                                      self.logprob[r0:r1], self.lse[r0:r1], dh,
-                                     G["final_norm"], G["w_vocab"], self.lws, row_base=t0,
-                                     ref_logprob=ref, kl_coef=kl_coef)
-            C.aj_stack_bwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, self.ckpt,
-                           self.saved, dh, dh, self.layer_grads, self.bws, base=t0)
-            C.aj_embed_bwd(tok, dh, G["emb"])
+                                     G.get("final_norm"), G.get("w_vocab"), self.lws,
+                                     row_base=t0, ref_logprob=ref, kl_coef=kl_coef)
+            if self.lora is None:
+                C.aj_stack_bwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, self.ckpt,
+                               self.saved, dh, dh, self.layer_grads, self.bws, base=t0)
+                C.aj_embed_bwd(tok, dh, G["emb"])
+            else:
+                C.aj_stack_lora_bwd(self.bcfg, self.layers, self.adapters, self.rank, self.scale,
+                                    cu, pos, p["max_len"], x, self.ckpt, self.saved, dh, dh,
+                                    self.layer_grads, self.bws, base=t0)
         return self.stats
+
+    def _stack_fwd(self, cu, pos, max_len, x, y, t0):
+        if self.lora is None:
+            C.aj_stack_fwd(self.bcfg, self.layers, cu, pos, max_len, x, y, self.ckpt, self.saved,
+                           base=t0)
+        else:
+            C.aj_stack_lora_fwd(self.bcfg, self.layers, self.adapters, self.rank, self.scale, cu,
+                                pos, max_len, x, y, self.ckpt, self.saved, base=t0)
 
     def forward_logprob(self, L):
         """Log-probs of every target under the current weights (forward only)."""
@@ -228,8 +266,8 @@ class ActorUpdate:
             t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
             n = t1 - t0
             C.aj_embed_fwd(L.tok[t0:t1], self.W["emb"], self.x[:n], self.err)
-            C.aj_stack_fwd(self.bcfg, self.layers, L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1],
-                           p["max_len"], self.x[:n], self.y[:n], self.ckpt, self.saved, base=t0)
+            self._stack_fwd(L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1], p["max_len"], self.x[:n],
+                            self.y[:n], t0)
             C.aj_logprob_pg_loss_fwd(self.lcfg, L.targets[r0:r1], L.tok, L.old_logprob, L.adv,
                                      inv, self.y[:n], self.W["final_norm"], self.W["w_vocab"],
                                      self.lsaved, self.logprob[r0:r1], self.lse[r0:r1],

@@ -75,6 +75,17 @@ class BlockGrads(C.Structure):
     _fields_ = [(n, vp) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
 
 
+LORA_FIELDS = ("a_qkv", "b_qkv", "a_o", "b_o", "a_gate_up", "b_gate_up", "a_down", "b_down")
+
+
+class Lora(C.Structure):
+    _fields_ = [("rank", i32), ("scale", f32)] + [(n, vp) for n in LORA_FIELDS]
+
+
+class LoraGrads(C.Structure):
+    _fields_ = [(n, vp) for n in LORA_FIELDS]
+
+
 class Varlen(C.Structure):
     _fields_ = [("n_tok", i32), ("n_seg", i32), ("max_seqlen", i32), ("base", i32),
                 ("cu_seqlens", vp), ("pos", vp)]
@@ -117,6 +128,13 @@ EXPORTS = {
     "aj_stack_bwd": (C.c_int, [C.POINTER(BlockCfg), i32, C.POINTER(BlockWeights),
                                C.POINTER(Varlen), vp, vp, vp, vp, vp, C.POINTER(BlockGrads), vp,
                                sz, vp]),
+    "aj_lora_saved_bytes": (sz, [C.POINTER(BlockCfg), i32, i32]),
+    "aj_lora_workspace_bytes": (sz, [C.POINTER(BlockCfg), i32, i32]),
+    "aj_stack_lora_fwd": (C.c_int, [C.POINTER(BlockCfg), i32, C.POINTER(BlockWeights),
+                                    C.POINTER(Lora), C.POINTER(Varlen), vp, vp, vp, vp, vp]),
+    "aj_stack_lora_bwd": (C.c_int, [C.POINTER(BlockCfg), i32, C.POINTER(BlockWeights),
+                                    C.POINTER(Lora), C.POINTER(Varlen), vp, vp, vp, vp, vp,
+                                    C.POINTER(LoraGrads), vp, sz, vp]),
     "aj_loss_saved_bytes": (sz, [C.POINTER(LossCfg), i32]),
     "aj_loss_workspace_bytes": (sz, [C.POINTER(LossCfg), i32]),
     "aj_logprob_pg_loss_fwd": (C.c_int, [C.POINTER(LossCfg), C.POINTER(LossIn), vp, vp, vp, vp,
@@ -323,6 +341,45 @@ def aj_stack_bwd(cfg, layers, cu_seqlens, pos, max_seqlen, x, ckpt, saved, dy, d
                               C.byref(vl), ptr(x), ptr(ckpt), ptr(saved), ptr(dy), ptr(dx),
                               _layers(grads, BlockGrads), ptr(ws), ws.numel() * ws.element_size(),
                               stream_handle(stream)), "aj_stack_bwd")
+
+
+def aj_lora_saved_bytes(cfg, rank, n_tok):
+    return int(lib().aj_lora_saved_bytes(C.byref(cfg), rank, n_tok))
+
+
+def aj_lora_workspace_bytes(cfg, rank, n_tok):
+    return int(lib().aj_lora_workspace_bytes(C.byref(cfg), rank, n_tok))
+
+
+def _lora_array(adapters, rank, scale):
+    """adapters: list (one per layer) of dicts keyed by LORA_FIELDS."""
+    arr = (Lora * len(adapters))()
+    for i, a in enumerate(adapters):
+        arr[i] = Lora(rank, scale, *[ptr(a[k]) for k in LORA_FIELDS])
+    return arr
+
+
+def aj_stack_lora_fwd(cfg, layers, adapters, rank, scale, cu_seqlens, pos, max_seqlen, x, y, ckpt,
+                      saved, stream=None, base=0):
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    _check(lib().aj_stack_lora_fwd(C.byref(cfg), len(layers), _layers(layers, BlockWeights),
+                                   _lora_array(adapters, rank, scale), C.byref(vl), ptr(x),
+                                   ptr(y), ptr(ckpt), ptr(saved), stream_handle(stream)),
+           "aj_stack_lora_fwd")
+
+
+def aj_stack_lora_bwd(cfg, layers, adapters, rank, scale, cu_seqlens, pos, max_seqlen, x, ckpt,
+                      saved, dy, dx, grads, ws, stream=None, base=0):
+    """grads: list of per-layer float32 dicts keyed by LORA_FIELDS, accumulated into."""
+    n_tok, n_seg = x.shape[0], cu_seqlens.numel() - 1
+    vl = _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos)
+    _check(lib().aj_stack_lora_bwd(C.byref(cfg), len(layers), _layers(layers, BlockWeights),
+                                   _lora_array(adapters, rank, scale), C.byref(vl), ptr(x),
+                                   ptr(ckpt), ptr(saved), ptr(dy), ptr(dx),
+                                   _layers(grads, LoraGrads, LORA_FIELDS), ptr(ws),
+                                   ws.numel() * ws.element_size(), stream_handle(stream)),
+           "aj_stack_lora_bwd")
 
 
 # ------------------------------------------------------------------ loss

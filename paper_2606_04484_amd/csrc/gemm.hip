@@ -27,12 +27,20 @@ struct EpArgs {
 
 using gemm_core::f32x16_t;
 
-// Shared body of the two GEMM kernels: main loop of configuration C, then
-// the epilogue through LDS.
-template <bool A_K, bool B_K, typename Cfg>
+// A second reduction segment with the operand layouts of the first:
+// C = A B + A2 B2 over k in [0, K) and [0, K2).
+struct Seg2 {
+  const bf16_t *A; int64_t lda;
+  const bf16_t *B; int64_t ldb;
+  int K;
+};
+
+// Shared body of the two GEMM kernels: main loop of configuration C (and the
+// second segment's, SEG2), then the epilogue through LDS.
+template <bool A_K, bool B_K, typename Cfg, bool SEG2 = false>
 AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda,
                       const bf16_t *B, int64_t ldb, const EpArgs &ep, float *partial,
-                      gemm_core::Smem<A_K, B_K, Cfg> &sm) {
+                      gemm_core::Smem<A_K, B_K, Cfg> &sm, const Seg2 &s2 = Seg2{}) {
   const int tiles_m = (M + Cfg::BM - 1) / Cfg::BM, tiles_n = (N + Cfg::BN - 1) / Cfg::BN;
   const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
   const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
@@ -41,10 +49,15 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  if constexpr (Cfg::NT == 512)
+  if constexpr (Cfg::NT == 512) {
     gemm_core::mainloop<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
-  else
+    if constexpr (SEG2)
+      gemm_core::mainloop<A_K, B_K, Cfg>(acc, s2.A, s2.lda, s2.B, s2.ldb, M, N, m0, n0, 0, s2.K,
+                                         sm, false);
+  } else {
+    static_assert(!SEG2, "the second segment runs on the 8-wave kernel");
     gemm_core::mainloop4<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  }
   __syncthreads();
 
   // Epilogue through LDS, 32 rows of each wave row at a time: the lane's
@@ -138,6 +151,16 @@ __global__ __launch_bounds__(gemm_core::Cfg4::NT, 1) void gemm_mfma4_kernel(
   gemm_tile<A_K, B_K, gemm_core::Cfg4>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
 }
 
+// The 8-wave kernel with a second reduction segment (no split-K; used with
+// either reduction length).
+template <bool A_K, bool B_K>
+__global__ __launch_bounds__(gemm_core::Cfg::NT, 1) void gemm_mfma_seg2_kernel(
+    int M, int N, int K, const bf16_t *A, int64_t lda, const bf16_t *B, int64_t ldb, Seg2 s2,
+    EpArgs ep) {
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K, gemm_core::Cfg> sm;
+  gemm_tile<A_K, B_K, gemm_core::Cfg, true>(M, N, K, K, A, lda, B, ldb, ep, nullptr, sm, s2);
+}
+
 constexpr int kLongK = 4096;
 
 // ---------------------------------------------------------------- float32 / fallback
@@ -145,37 +168,45 @@ template <typename T>
 __global__ __launch_bounds__(256) void gemm_simple_kernel(int M, int N, int K, int k_per_split,
                                                           const T *A, int64_t lda, int a_k,
                                                           const T *B, int64_t ldb, int b_k,
-                                                          EpArgs ep, float *partial) {
+                                                          EpArgs ep, float *partial,
+                                                          const T *A2, int64_t lda2,
+                                                          const T *B2, int64_t ldb2, int K2) {
   constexpr int BM = 64, BN = 64, BK = 16;
   __shared__ float As[BK][BM + 1];
   __shared__ float Bs[BK][BN + 1];
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  const int kbeg = blockIdx.z * k_per_split, kend = min(K, kbeg + k_per_split);
   float acc[4][4] = {};
-  for (int k0 = kbeg; k0 < kend; k0 += BK) {
-    for (int e = threadIdx.x; e < BM * BK; e += 256) {
-      int mm = e % BM, kk = e / BM;
-      int m = m0 + mm, k = k0 + kk;
-      float va = 0.f, vb = 0.f;
-      if (m < M && k < kend) va = ldf(A + (a_k ? (int64_t)m * lda + k : (int64_t)k * lda + m));
-      int n = n0 + mm;
-      if (n < N && k < kend) vb = ldf(B + (b_k ? (int64_t)n * ldb + k : (int64_t)k * ldb + n));
-      As[kk][mm] = va;
-      Bs[kk][mm] = vb;
+  // segment 0: [kbeg, kend) of (A, B); segment 1 (no split): [0, K2) of (A2, B2)
+  for (int seg = 0; seg < (K2 > 0 ? 2 : 1); ++seg) {
+    const T *X = seg ? A2 : A, *Y = seg ? B2 : B;
+    const int64_t ldx = seg ? lda2 : lda, ldy = seg ? ldb2 : ldb;
+    const int kbeg = seg ? 0 : blockIdx.z * k_per_split;
+    const int kend = seg ? K2 : min(K, kbeg + k_per_split);
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+      for (int e = threadIdx.x; e < BM * BK; e += 256) {
+        int mm = e % BM, kk = e / BM;
+        int m = m0 + mm, k = k0 + kk;
+        float va = 0.f, vb = 0.f;
+        if (m < M && k < kend) va = ldf(X + (a_k ? (int64_t)m * ldx + k : (int64_t)k * ldx + m));
+        int n = n0 + mm;
+        if (n < N && k < kend) vb = ldf(Y + (b_k ? (int64_t)n * ldy + k : (int64_t)k * ldy + n));
+        As[kk][mm] = va;
+        Bs[kk][mm] = vb;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < BK; ++kk) {
+        float a[4], b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { a[i] = As[kk][ty + 16 * i]; b[i] = Bs[kk][tx + 16 * i]; }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+      }
+      __syncthreads();
     }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < BK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { a[i] = As[kk][ty + 16 * i]; b[i] = Bs[kk][tx + 16 * i]; }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
-    }
-    __syncthreads();
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -203,6 +234,12 @@ void launch_mfma(const Gemm &g, const EpArgs &ep, int kps, bool long_k, hipStrea
   const int tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   dim3 grid(tiles, 1, g.split_k);
   float *part = g.split_k > 1 ? g.partial : nullptr;
+  if (g.K2 > 0) {
+    const Seg2 s2{(const bf16_t *)g.A2, g.lda2, (const bf16_t *)g.B2, g.ldb2, g.K2};
+    gemm_mfma_seg2_kernel<A_K, B_K><<<tiles, gemm_core::Cfg::NT, 0, s>>>(
+        g.M, g.N, g.K, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, s2, ep);
+    return;
+  }
   if (long_k)
     gemm_mfma4_kernel<A_K, B_K><<<grid, gemm_core::Cfg4::NT, 0, s>>>(
         g.M, g.N, g.K, kps, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, ep, part);
@@ -219,6 +256,8 @@ template <typename T>
 int gemm(const Gemm &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return AJ_OK;
   if (g.split_k > 1 && !g.partial) return fail(AJ_ERR_WORKSPACE, "gemm: split-K without workspace");
+  if (g.K2 > 0 && (g.split_k > 1 || !g.A2 || !g.B2))
+    return fail(AJ_ERR_UNSUPPORTED, "gemm: a second segment needs its operands and no split-K");
   EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R, 0};
   if (ep.accum) ep.c_f32 = 1;
   {
@@ -240,12 +279,18 @@ int gemm(const Gemm &g, hipStream_t s) {
     const int a_contig = g.a_kmajor ? g.K : g.M, b_contig = g.b_kmajor ? g.K : g.N;
     mfma = a_contig % 8 == 0 && b_contig % 8 == 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
            aligned16(g.A) && aligned16(g.B);
+    if (g.K2 > 0) {
+      const int a2 = g.a_kmajor ? g.K2 : g.M, b2 = g.b_kmajor ? g.K2 : g.N;
+      mfma = mfma && a2 % 8 == 0 && b2 % 8 == 0 && g.lda2 % 8 == 0 && g.ldb2 % 8 == 0 &&
+             aligned16(g.A2) && aligned16(g.B2);
+    }
   }
   if (mfma) {
-    const bool long_k = kps >= kLongK;
+    const bool long_k = kps >= kLongK && g.K2 == 0;   // the second segment runs 8-wave
     int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
     if (long_k) kc += AJ_KC_GEMM4_NT - AJ_KC_GEMM_NT;
-    const int tk = timing_begin(s, kc, g.recompute ? 0.0 : 2.0 * g.M * g.N * (double)g.K);
+    const int tk =
+        timing_begin(s, kc, g.recompute ? 0.0 : 2.0 * g.M * g.N * ((double)g.K + g.K2));
     if (g.a_kmajor && g.b_kmajor) launch_mfma<true, true>(g, ep, kps, long_k, s);
     else if (g.a_kmajor) launch_mfma<true, false>(g, ep, kps, long_k, s);
     else if (g.b_kmajor) launch_mfma<false, true>(g, ep, kps, long_k, s);
@@ -255,7 +300,8 @@ int gemm(const Gemm &g, hipStream_t s) {
     dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, S);
     gemm_simple_kernel<T><<<grid, 256, 0, s>>>(g.M, g.N, g.K, kps, (const T *)g.A, g.lda,
                                                g.a_kmajor, (const T *)g.B, g.ldb, g.b_kmajor, ep,
-                                               S > 1 ? g.partial : nullptr);
+                                               S > 1 ? g.partial : nullptr, (const T *)g.A2,
+                                               g.lda2, (const T *)g.B2, g.ldb2, g.K2);
   }
   int st = check_launch("gemm");
   if (st != AJ_OK) return st;

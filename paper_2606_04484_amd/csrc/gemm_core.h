@@ -152,14 +152,15 @@ struct Smem {
 AJ_DEV void wait_lds_dma() { __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // acc[i][j] (lane's share of the wave's block) = sum over k in [kbeg, kend)
-// of A(m, k) B(n, k) for the 256x256 tile at (m0, n0).  The next k-step's
+// of A(m, k) B(n, k) for the 256x256 tile at (m0, n0) (added to acc instead
+// when zero is false: a second reduction segment).  The next k-step's
 // loads stream into the other LDS buffer while this one is consumed; the
 // fragments of the next 16-wide k slice are read while the current one's
 // MFMAs issue.
 template <bool A_K, bool B_K, typename C = Cfg>
 AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda,
                      const bf16_t *B, int64_t ldb, int M, int N, int m0, int n0, int kbeg,
-                     int kend, Smem<A_K, B_K, C> &sm) {
+                     int kend, Smem<A_K, B_K, C> &sm, bool zero = true) {
   static_assert(C::BM == 256 && C::BN == 256 && C::BK == 64 && C::NT == 512, "tile");
   using TA = Tile<C::NT, A_K>;
   using TB = Tile<C::NT, B_K>;
@@ -167,12 +168,13 @@ AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
+  if (zero)
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i)
+    for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j)
+      for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   if (nk > 0) {
     TA::load(sm.a[0], A, lda, m0, M, kbeg, kend);
     TB::load(sm.b[0], B, ldb, n0, N, kbeg, kend);

@@ -488,6 +488,7 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     g.B = (const T *)w_vocab + (int64_t)c0 * d; g.ldb = d; g.b_kmajor = false;
     g.C = w.dhn; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
     if ((r = aj::gemm<T>(g, st))) return r;
+    if (!dwv) continue;   // frozen LM head
     g = aj::Gemm();   // dW_chunk += dz^T hn
     g.M = cw; g.N = d; g.K = n; g.A = w.dz; g.lda = cw; g.a_kmajor = false;
     g.B = sv.hn; g.ldb = d; g.b_kmajor = false;
@@ -542,7 +543,7 @@ extern "C" int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *
   int r;
   if ((r = check_cfg(cfg, in, name))) return r;
   if (in->n_tok == 0) return AJ_OK;
-  AJ_REQUIRE(dh && d_final_norm && d_w_vocab, AJ_ERR_NULL, "%s: null gradient", name);
+  AJ_REQUIRE(dh, AJ_ERR_NULL, "%s: null dh", name);
   AJ_REQUIRE(in->n_tgt == 0 || (h && final_norm && w_vocab && saved && logprob && lse && ws),
              AJ_ERR_NULL, "%s: null pointer", name);
   LossWs w = carve_ws(*cfg, in->n_tgt, ws);

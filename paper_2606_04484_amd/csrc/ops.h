@@ -15,7 +15,7 @@ template <typename T>
 void rmsnorm_fwd(const T *x, const T *g, int n, int d, float eps, const int32_t *rows, int shift,
                  T *out, float *rstd, hipStream_t s);
 // Backward of the above; dg += sum over rows (deterministic, via dg_part of
-// rmsnorm_bwd_part_floats floats).  dx / dx_t (either may be null) receive
+// rmsnorm_bwd_part_floats floats; dg null: the gain is frozen, not reduced).  dx / dx_t (either may be null) receive
 // add + d x; with scatter they are indexed by r instead of i.
 size_t rmsnorm_bwd_part_floats(int n, int d);
 template <typename T>
@@ -36,6 +36,10 @@ void swiglu_bwd(const TI *ds, const T *gu, int n, int F, T *dgu, hipStream_t s);
 
 template <typename T>
 void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s);
+// out[i] = scale * in[i] rounded once to T; lo (optional) receives the
+// rounding residual, also in T, so that out + lo carries ~twice T's precision.
+template <typename T>
+void scale_cast(const float *in, int64_t n, float scale, T *out, T *lo, hipStream_t s);
 void fill_f32(float *p, int64_t n, float v, hipStream_t s);
 void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumulate, hipStream_t s);
 
@@ -55,6 +59,11 @@ struct Gemm {
   int split_k = 1;             // > 1: partial sums in `partial`, reduced in fixed order
   float *partial = nullptr;    // split_k * M * N floats (OUT_ACCUM_F32 or c_f32 only)
   bool recompute = false;      // recomputes a forward product: no algorithmic flops
+  // optional second reduction segment, same operand layouts, no split-K:
+  // C (op) A B + A2 B2 with k in [0, K) and [0, K2)
+  const void *A2 = nullptr; int64_t lda2 = 0;
+  const void *B2 = nullptr; int64_t ldb2 = 0;
+  int K2 = 0;
 };
 template <typename T>
 int gemm(const Gemm &g, hipStream_t s);

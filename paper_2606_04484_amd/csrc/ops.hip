@@ -268,6 +268,15 @@ __global__ void cast_kernel(const float *in, int64_t n, T *out) {
   }
 }
 
+template <typename T>
+__global__ void scale_cast_kernel(const float *in, int64_t n, float scale, T *out, T *lo) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float v = scale * in[i];
+  stf(out + i, v);
+  if (lo) stf(lo + i, v - ldf(out + i));
+}
+
 __global__ void fill_kernel(float *p, int64_t n, float v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -331,7 +340,7 @@ void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int
   if (nb > (unsigned)kBwdBlocks) nb = kBwdBlocks;
   AJ_NV_DISPATCH(d, (rmsnorm_bwd_kernel<T, NV><<<nb, 256, 0, s>>>(
                         dy, x, rstd, g, n, d, rows, shift, scatter, add, dx, dx_t, dg_part)));
-  col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb, d, dg);
+  if (dg) col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb, d, dg);
 }
 
 template <typename T>
@@ -360,6 +369,11 @@ void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s) {
   if (n > 0) cast_kernel<T><<<blocks_for((n + 7) / 8, 256), 256, 0, s>>>(in, n, out);
 }
 
+template <typename T>
+void scale_cast(const float *in, int64_t n, float scale, T *out, T *lo, hipStream_t s) {
+  if (n > 0) scale_cast_kernel<T><<<blocks_for(n, 256), 256, 0, s>>>(in, n, scale, out, lo);
+}
+
 void fill_f32(float *p, int64_t n, float v, hipStream_t s) {
   if (n > 0) fill_kernel<<<blocks_for(n, 256), 256, 0, s>>>(p, n, v);
 }
@@ -379,7 +393,8 @@ void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumul
   template void rope<T>(T *, int, const int32_t *, int, int, int, float, bool, hipStream_t);    \
   template void swiglu_fwd<T>(const T *, int, int, T *, hipStream_t);                           \
   template void swiglu_bwd<float, T>(const float *, const T *, int, int, T *, hipStream_t);     \
-  template void cast_from_f32<T>(const float *, int64_t, T *, hipStream_t);
+  template void cast_from_f32<T>(const float *, int64_t, T *, hipStream_t);                     \
+  template void scale_cast<T>(const float *, int64_t, float, T *, T *, hipStream_t);
 AJ_INST(float)
 AJ_INST(bf16_t)
 template void swiglu_bwd<bf16_t, bf16_t>(const bf16_t *, const bf16_t *, int, int, bf16_t *, hipStream_t);

@@ -47,11 +47,13 @@ class Case:
     """One seeded actor-update case with the oracle's merged/unmerged results."""
 
     def __init__(self, cfg, noise_std=0.05, margin=0.0, gain_std=0.1, wseed=1000, think_p=None,
-                 text=False):
+                 text=False, lora=None, lora_scale=1.0):
         """think_p: draw text keys and strip thinking (see make_timelines);
-        text: the merged layout uses text-level Match."""
+        text: the merged layout uses text-level Match; lora: LoRA matrices (then
+        only they train, scaled by lora_scale)."""
         m = cfg.model
         self.cfg, self.m, self.text = cfg, m, text
+        self.lora, self.lora_scale = lora, lora_scale
         self.tl = tl = make_timelines(cfg, think_p=think_p)
         self.W = make_weights_numpy(m, seed=wseed, gain_std=gain_std)
         if m.dtype == "bf16":
@@ -59,14 +61,15 @@ class Case:
             self.W = {k: bf16_round(v) for k, v in self.W.items()}
         zero = np.zeros(tl.n_tok, np.float32)
         un = om.unmerged_batch(episodes(tl, zero))
-        cur = M.current_logprob(un, self.W, m)
+        W_used = self.W if lora is None else M.lora_effective(self.W, lora, lora_scale, m)
+        cur = M.current_logprob(un, W_used, m)
         if text:
             # under text-level Match a response can be scored in another
             # context than it was sampled in: keep the clip margin around the
             # log-probs of the text-merged layout, traced back to input tokens
             tr, _ = om.merge_batch(episodes(tl, np.arange(tl.n_tok, dtype=np.float64)),
                                    om.match_text)
-            cur_m = M.current_logprob(tr, self.W, m)
+            cur_m = M.current_logprob(tr, W_used, m)
             sel = tr.mask == 1
             cur = np.full(tl.n_tok, np.nan)
             cur[tr.old_logprob[sel].astype(np.int64)] = cur_m[sel]
@@ -81,13 +84,18 @@ class Case:
 
     def oracle(self, merged=True):
         if merged not in self._ref:
-            self._ref[merged] = M.actor_update(self.merged if merged else self.unmerged, self.W,
-                                               self.m)
+            p = self.merged if merged else self.unmerged
+            if self.lora is None:
+                self._ref[merged] = M.actor_update(p, self.W, self.m)
+            else:
+                self._ref[merged] = M.lora_actor_update(p, self.W, self.lora, self.lora_scale,
+                                                        self.m)
         return self._ref[merged]
 
-    def device_weights(self, device="cuda"):
+    def device_weights(self, device="cuda", which=None):
         dt = torch.bfloat16 if self.m.dtype == "bf16" else torch.float32
-        return {k: torch.from_numpy(v).to(device=device, dtype=dt) for k, v in self.W.items()}
+        src = self.W if which is None else which
+        return {k: torch.from_numpy(v).to(device=device, dtype=dt) for k, v in src.items()}
 
 
 def rel_l2(a, b):
