@@ -31,9 +31,11 @@ AJ_DEV f32x16_t mfma(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-AJ_DEV uint32_t pack2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
-}
+AJ_DEV uint32_t pack2(float lo, float hi) { return f2bf2(lo, hi); }
+
+// 2^x on the hardware unit (v_exp_f32): the arguments here are <= 0 or -inf,
+// where it needs none of exp2f's range handling.
+AJ_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 8 accumulator values r0..r0+7 -> one bf16x8 operand
 AJ_DEV bf16x8_t pack8(const f32x16_t &v, int r0) {
@@ -249,6 +251,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
   const float c = a.scale * kLog2e;
   const int w_lo = (int)wave_min_f((float)qs);          // earliest key any row of the wave reads
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);   // latest query row of the wave
+  const int w_qs = (int)-wave_min_f(-(float)qs);        // latest segment start of the wave
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
@@ -271,24 +274,34 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
         for (int r = 0; r < 16; ++r) s[tt][r] = 0.f;
       rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
       float mx = -INFINITY;
+      if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+        for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-          const bool ok = kv >= qs && kv <= q;
-          s[tt][r] = ok ? s[tt][r] * c : -INFINITY;
-          mx = fmaxf(mx, s[tt][r]);
-        }
+          for (int r = 0; r < 16; ++r) {
+            s[tt][r] *= c;
+            mx = fmaxf(mx, s[tt][r]);
+          }
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
+            const bool ok = kv >= qs && kv <= q;
+            s[tt][r] = ok ? s[tt][r] * c : -INFINITY;
+            mx = fmaxf(mx, s[tt][r]);
+          }
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mn = fmaxf(m, mx);
-      const float alpha = mn == -INFINITY ? 1.f : exp2f(m - mn);
+      const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m - mn);
       float ls = 0.f;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = mn == -INFINITY ? 0.f : exp2f(s[tt][r] - mn);
+          const float p = mn == -INFINITY ? 0.f : fast_exp2(s[tt][r] - mn);
           s[tt][r] = p;
           ls += p;
         }
@@ -365,6 +378,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const float c = a.scale * kLog2e;
   const int w_lo = (int)wave_min_f((float)qs);
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);
+  const int w_qs = (int)-wave_min_f(-(float)qs);
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
@@ -387,15 +401,23 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
         for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
       rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
       rows_times<HD>(dp, Vs[buf], df);                   // dP^T = V dO^T
+      if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+        for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-          const bool ok = kv >= qs && kv <= q;
-          const float p = ok ? exp2f(s[tt][r] * c - lse2) : 0.f;
-          s[tt][r] = p * (dp[tt][r] - dlt);
-        }
+          for (int r = 0; r < 16; ++r)
+            s[tt][r] = fast_exp2(s[tt][r] * c - lse2) * (dp[tt][r] - dlt);
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
+            const bool ok = kv >= qs && kv <= q;
+            const float p = ok ? fast_exp2(s[tt][r] * c - lse2) : 0.f;
+            s[tt][r] = p * (dp[tt][r] - dlt);
+          }
+      }
       const bf16x8_t sj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
       cols_times<HD>(acc, Ks[buf], sj);                  // dQ^T += K^T dS^T
     }
@@ -459,6 +481,7 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
   const float c = a.scale * kLog2e;
   const int w_lo = min(k0 + 32 * w, a.n_tok);               // first query any key of the wave sees
   const int w_hi = (int)-wave_min_f(kvv ? -(float)(ke - 1) : 1.f);   // last one
+  const int w_ke = (int)wave_min_f(kvv ? (float)ke : 0.f);   // earliest segment end (0: a key is past the end)
   __syncthreads();
   const int q_hi = rng[0];    // queries [k0, q_hi)
   const int group = a.Hq / a.Hkv;
@@ -499,17 +522,28 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
         }
       rows_times<HD>(s, Qs[buf], kf);
       rows_times<HD>(dp, Ds[buf], vf);
+      if (qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke) {   // every query sees every key
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+        for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ql = 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-          const int qr = qb + ql;
-          const bool ok = kvv && qr >= kv && qr < ke;
-          const float p = ok ? exp2f(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e) : 0.f;
-          s[tt][r] = p;
-          dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
-        }
+          for (int r = 0; r < 16; ++r) {
+            const float p = fast_exp2(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e);
+            s[tt][r] = p;
+            dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
+          }
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int ql = 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
+            const int qr = qb + ql;
+            const bool ok = kvv && qr >= kv && qr < ke;
+            const float p = ok ? fast_exp2(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e) : 0.f;
+            s[tt][r] = p;
+            dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
+          }
+      }
       const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
       const bf16x8_t sj[4] = {pack8(dp[0], 0), pack8(dp[0], 8), pack8(dp[1], 0), pack8(dp[1], 8)};
       cols_times<HD>(dv, Ds[buf], pj);                   // dV^T += dO^T P

@@ -11,13 +11,17 @@ typedef uint16_t bf16_t;   // bfloat16 storage (upper half of a float32)
 
 AJ_DEV float bf2f(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
 
-// float32 -> bfloat16, round to nearest even; NaN stays NaN.
-AJ_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+typedef __bf16 bf16x2_hw_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_hw_t __attribute__((ext_vector_type(2)));
+
+// Two float32 -> two bfloat16 in one word (lo in bits 0..15), round to
+// nearest even, NaN stays NaN: one v_cvt_pk_bf16_f32 on gfx950.
+AJ_DEV uint32_t f2bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_hw_t{lo, hi}, bf16x2_hw_t));
 }
+
+// float32 -> bfloat16, round to nearest even; NaN stays NaN.
+AJ_DEV bf16_t f2bf(float f) { return (bf16_t)(f2bf2(f, 0.f) & 0xffffu); }
 
 template <typename T> AJ_DEV float ldf(const T *p);
 template <> AJ_DEV float ldf<float>(const float *p) { return *p; }

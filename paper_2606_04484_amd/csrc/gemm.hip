@@ -107,8 +107,8 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
             w2 += __uint_as_float(u.y << 16); w3 += __uint_as_float(u.y & 0xffff0000u);
           }
           uint2 out;
-          out.x = (uint32_t)f2bf(w0) | ((uint32_t)f2bf(w1) << 16);
-          out.y = (uint32_t)f2bf(w2) | ((uint32_t)f2bf(w3) << 16);
+          out.x = f2bf2(w0, w1);
+          out.y = f2bf2(w2, w3);
           *reinterpret_cast<uint2 *>((bf16_t *)ep.C + o) = out;
         }
       } else {

@@ -257,6 +257,9 @@ using Cfg = gemm_core::CfgWide;
 template <bool A_K, bool B_K> using Smem = gemm_core::Smem<A_K, B_K, Cfg>;
 using gemm_core::f32x16_t;
 constexpr float kLog2e = 1.4426950408889634f;
+// 2^x on the hardware unit (v_exp_f32) for arguments <= 0 or -inf (a
+// logit minus a running maximum or the log-sum-exp): no range handling needed.
+AJ_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float kLn2 = 0.6931471805599453f;
 
 AJ_DEV float half_max(float v) {   // max over the 32 lanes of this half-wave
@@ -306,7 +309,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
       mx = half_max(mx);
       float sm_ = 0.f;
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) sm_ += v[j] == -INFINITY ? 0.f : exp2f(v[j] - mx);
+      for (int j = 0; j < Cfg::TN; ++j) sm_ += v[j] == -INFINITY ? 0.f : fast_exp2(v[j] - mx);
       sm_ = half_sum(sm_);
       if ((lane & 31) == 0) red[wn][rl] = make_float2(mx, sm_);
     }
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
 #pragma unroll
     for (int w = 0; w < Cfg::WN; ++w)   // a wave past the vocab end holds (-inf, 0)
       S += red[w][threadIdx.x].x == -INFINITY ? 0.f
-                                               : red[w][threadIdx.x].y * exp2f(red[w][threadIdx.x].x - M);
+                                               : red[w][threadIdx.x].y * fast_exp2(red[w][threadIdx.x].x - M);
     tile_ms[(int64_t)(m0 + threadIdx.x) * tiles_n + ti.tn] = make_float2(M, S);
   }
 }
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(int n, int n_tiles, con
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
   float S = 0.f;
-  for (int t = lane; t < n_tiles; t += 64) S += p[t].x == -INFINITY ? 0.f : p[t].y * exp2f(p[t].x - M);
+  for (int t = lane; t < n_tiles; t += 64) S += p[t].x == -INFINITY ? 0.f : p[t].y * fast_exp2(p[t].x - M);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
   if (lane == 0) {
@@ -378,7 +381,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
       for (int j = 0; j < Cfg::TN; ++j) {
         const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
         if (col >= cw) continue;
-        const float p = exp2f(acc[i][j][r] * kLog2e - tl[rl]);
+        const float p = fast_exp2(acc[i][j][r] * kLog2e - tl[rl]);
         dz[(int64_t)m * cw + col] = f2bf(tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p));
       }
     }

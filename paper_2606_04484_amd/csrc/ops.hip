@@ -66,7 +66,7 @@ AJ_DEV void store8(float *p, const float (&v)[8]) {
 AJ_DEV void store8(bf16_t *p, const float (&v)[8]) {
   u32x4v u;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) u[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+  for (int k = 0; k < 4; ++k) u[k] = f2bf2(v[2 * k], v[2 * k + 1]);
   *(u32x4v *)p = u;
 }
 
