@@ -283,13 +283,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
             mx = fmaxf(mx, s[tt][r]);
           }
       } else {
+        const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-            const bool ok = kv >= qs && kv <= q;
-            s[tt][r] = ok ? s[tt][r] * c : -INFINITY;
+            const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+            s[tt][r] = (off >= lo && off <= hi) ? s[tt][r] * c : -INFINITY;
             mx = fmaxf(mx, s[tt][r]);
           }
       }
@@ -378,7 +378,6 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const float c = a.scale * kLog2e;
   const int w_lo = (int)wave_min_f((float)qs);
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);
-  const int w_qs = (int)-wave_min_f(-(float)qs);
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
@@ -401,23 +400,17 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
         for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
       rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
       rows_times<HD>(dp, Vs[buf], df);                   // dP^T = V dO^T
-      if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
+      // key k0 + 4hl + off (off a constant per element) is visible iff
+      // lo <= off <= hi
+      const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+      for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            s[tt][r] = fast_exp2(s[tt][r] * c - lse2) * (dp[tt][r] - dlt);
-      } else {
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int kv = k0 + 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-            const bool ok = kv >= qs && kv <= q;
-            const float p = ok ? fast_exp2(s[tt][r] * c - lse2) : 0.f;
-            s[tt][r] = p * (dp[tt][r] - dlt);
-          }
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+          const float p = (off >= lo && off <= hi) ? fast_exp2(s[tt][r] * c - lse2) : 0.f;
+          s[tt][r] = p * (dp[tt][r] - dlt);
+        }
       const bf16x8_t sj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
       cols_times<HD>(acc, Ks[buf], sj);                  // dQ^T += K^T dS^T
     }
@@ -532,13 +525,14 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
             dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
           }
       } else {
+        // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
+        const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int ql = 32 * tt + 8 * (r >> 2) + 4 * hl + (r & 3);
-            const int qr = qb + ql;
-            const bool ok = kvv && qr >= kv && qr < ke;
+            const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+            const bool ok = off >= lo && off < hi;
             const float p = ok ? fast_exp2(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e) : 0.f;
             s[tt][r] = p;
             dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
