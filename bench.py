@@ -410,6 +410,16 @@ def main():
         "roofline": roof,
         "loss": float(stats[0]),
     }
+    # the merge against HBM: algorithmic bytes = every unmerged token's id and
+    # flags, the llm tokens' log-prob and advantage read once; every merged
+    # token's id, position, mask, log-prob and advantage and every target written
+    if "merge" in rec and rec["merge"][1]:
+        mms = rec["merge"][0] / rec["merge"][1]
+        n_llm = int(np.count_nonzero((tl.flags & 3) == 2))
+        mb = 5 * tl.n_tok + 8 * n_llm + 17 * Lm.n_tok + 4 * Lm.n_mask
+        out["merge"] = {"ms": round(mms, 4), "algorithmic_MB": round(mb / 1e6, 2),
+                        "GB/s": round(mb / (mms * 1e-3) / 1e9, 1),
+                        "hbm_frac": round(mb / (mms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     if res_u:
         out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
         out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)

@@ -186,13 +186,27 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(
   for (int c = threadIdx.x; c < d; c += blockDim.x) dg_part[(int64_t)blockIdx.x * d + c] = red[c];
 }
 
-// out[c] += sum_b part[b][c], b ascending (deterministic).
-__global__ void col_reduce_kernel(const float *part, int nb, int d, float *out) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= d) return;
-  float s = 0.f;
-  for (int b = 0; b < nb; ++b) s += part[(int64_t)b * d + c];
-  out[c] += s;
+// out[c] += sum_b part[b][c] in a fixed order (deterministic): a block takes
+// 64 columns; thread (phase p, column) sums rows b = p + 4k with four
+// independent accumulators (k mod 4), combined in order, then the four
+// phases are added in order.  Coalesced 256-byte rows, 16 loads in flight.
+__global__ __launch_bounds__(256) void col_reduce_kernel(const float *part, int nb, int d,
+                                                         float *out) {
+  __shared__ float ph[4][64];
+  const int lane = threadIdx.x & 63, p = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  if (c < d) {
+    int b = p;
+    for (; b + 12 < nb; b += 16) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] += part[(int64_t)(b + 4 * u) * d + c];
+    }
+    for (int u = 0; b < nb; b += 4, ++u) a[u & 3] += part[(int64_t)b * d + c];
+  }
+  ph[p][lane] = (a[0] + a[1]) + (a[2] + a[3]);
+  __syncthreads();
+  if (p == 0 && c < d) out[c] += ((ph[0][lane] + ph[1][lane]) + ph[2][lane]) + ph[3][lane];
 }
 
 // ---------------------------------------------------------------- RoPE
@@ -340,7 +354,7 @@ void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int
   if (nb > (unsigned)kBwdBlocks) nb = kBwdBlocks;
   AJ_NV_DISPATCH(d, (rmsnorm_bwd_kernel<T, NV><<<nb, 256, 0, s>>>(
                         dy, x, rstd, g, n, d, rows, shift, scatter, add, dx, dx_t, dg_part)));
-  if (dg) col_reduce_kernel<<<blocks_for(d, 256), 256, 0, s>>>(dg_part, (int)nb, d, dg);
+  if (dg) col_reduce_kernel<<<(d + 63) / 64, 256, 0, s>>>(dg_part, (int)nb, d, dg);
 }
 
 template <typename T>
