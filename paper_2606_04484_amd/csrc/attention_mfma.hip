@@ -513,6 +513,16 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
           lv[tt][r4] = lds_read_f4(Ls[buf] + 32 * tt + 8 * r4 + 4 * hl);
           dl[tt][r4] = lds_read_f4(Dl[buf] + 32 * tt + 8 * r4 + 4 * hl);
         }
+      // the reads above are inline assembly: wait for them, and pass the
+      // values through empty statements so no use moves above the wait
+      lds_wait();
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          asm volatile("" : "+v"(lv[tt][r4]));
+          asm volatile("" : "+v"(dl[tt][r4]));
+        }
       rows_times<HD>(s, Qs[buf], kf);
       rows_times<HD>(dp, Ds[buf], vf);
       if (qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke) {   // every query sees every key
