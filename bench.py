@@ -46,7 +46,7 @@ def parse():
 # counter's reading for a plain copy of known size.  Keyed by (kernel class,
 # workload); `sources` are hashed so that a changed kernel reports null.
 TRAFFIC = {
-    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 7508.6e6, "sources": "05f7f1ef2648f15e"},
+    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 7514.2e6, "sources": "7bdae5d7d5c4c37c"},
 }
 
 
