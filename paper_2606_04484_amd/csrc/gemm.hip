@@ -37,10 +37,11 @@ struct Seg2 {
 
 // Shared body of the two GEMM kernels: main loop of configuration C (and the
 // second segment's, SEG2), then the epilogue through LDS.
-template <bool A_K, bool B_K, typename Cfg, bool SEG2 = false>
+template <bool A_K, bool B_K, typename Cfg, bool SEG2 = false, bool STAGED = false,
+          typename SM = gemm_core::Smem<A_K, B_K, Cfg>>
 AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda,
-                      const bf16_t *B, int64_t ldb, const EpArgs &ep, float *partial,
-                      gemm_core::Smem<A_K, B_K, Cfg> &sm, const Seg2 &s2 = Seg2{}) {
+                      const bf16_t *B, int64_t ldb, const EpArgs &ep, float *partial, SM &sm,
+                      const Seg2 &s2 = Seg2{}) {
   const int tiles_m = (M + Cfg::BM - 1) / Cfg::BM, tiles_n = (N + Cfg::BN - 1) / Cfg::BN;
   const gemm_core::TileIdx ti = gemm_core::tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n);
   const int m0 = ti.tm * Cfg::BM, n0 = ti.tn * Cfg::BN;
@@ -49,14 +50,15 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  if constexpr (Cfg::NT == 512) {
+  if constexpr (STAGED) {
+    static_assert(!SEG2 && Cfg::NT == 256, "the staged loop is the 4-wave one, one segment");
+    gemm_core::mainloop4s<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  } else {
+    static_assert(Cfg::NT == 512, "8-wave tile");
     gemm_core::mainloop<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
     if constexpr (SEG2)
       gemm_core::mainloop<A_K, B_K, Cfg>(acc, s2.A, s2.lda, s2.B, s2.ldb, M, N, m0, n0, 0, s2.K,
                                          sm, false);
-  } else {
-    static_assert(!SEG2, "the second segment runs on the 8-wave kernel");
-    gemm_core::mainloop4<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
   }
   __syncthreads();
 
@@ -142,13 +144,15 @@ __global__ __launch_bounds__(gemm_core::Cfg::NT, 1) void gemm_mfma_kernel(
   gemm_tile<A_K, B_K, gemm_core::Cfg>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
 }
 
-// 4 waves of 128x128 with the fixed issue order: reductions of kLongK and more.
+// 4 waves of 128x128 with 32-wide k-steps in four LDS stages (copies three
+// k-steps ahead): reductions of kLongK and more.
 template <bool A_K, bool B_K>
-__global__ __launch_bounds__(gemm_core::Cfg4::NT, 1) void gemm_mfma4_kernel(
+__global__ __launch_bounds__(gemm_core::Cfg4::NT, 1) void gemm_mfma4s_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K, gemm_core::Cfg4> sm;
-  gemm_tile<A_K, B_K, gemm_core::Cfg4>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K> sm;
+  gemm_tile<A_K, B_K, gemm_core::Cfg4, false, true>(M, N, K, k_per_split, A, lda, B, ldb, ep,
+                                                    partial, sm);
 }
 
 // The 8-wave kernel with a second reduction segment (no split-K; used with
@@ -241,7 +245,7 @@ void launch_mfma(const Gemm &g, const EpArgs &ep, int kps, bool long_k, hipStrea
     return;
   }
   if (long_k)
-    gemm_mfma4_kernel<A_K, B_K><<<grid, gemm_core::Cfg4::NT, 0, s>>>(
+    gemm_mfma4s_kernel<A_K, B_K><<<grid, gemm_core::Cfg4::NT, 0, s>>>(
         g.M, g.N, g.K, kps, (const bf16_t *)g.A, g.lda, (const bf16_t *)g.B, g.ldb, ep, part);
   else
     gemm_mfma_kernel<A_K, B_K><<<grid, gemm_core::Cfg::NT, 0, s>>>(

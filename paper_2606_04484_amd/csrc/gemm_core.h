@@ -220,23 +220,93 @@ AJ_DEV void mainloop(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda
 // Four waves, one per SIMD, as 2 x 2, each 128x128 (4x4 MFMA tiles, 256
 // float32 accumulators per lane, held in AGPRs).  Against 8 waves of 128x64
 // this halves the LDS fragment traffic per MFMA; with a single wave per SIMD
-// nothing else hides latency, so the k loop is issued in a fixed order: in
-// every 16-wide slice the next slice's 8 fragment reads follow the first 8
-// MFMAs, and in the first slice of a k-step each of the 16 MFMAs is followed
-// by one of the next k-step's 16 direct-to-LDS copies (scheduling barriers
-// keep the compiler from regrouping them).  Used for long reductions, where
-// its heavier per-tile prologue and epilogue are amortised.
+// nothing else hides latency, so the k loop (mainloop4s below) is issued in a
+// fixed order.  Used for long reductions, where its heavier per-tile prologue
+// and epilogue are amortised.
 using Cfg4 = MfmaCfg<256, 256, 64, 2, 2>;
 
-// Loop-invariant part of a wave's direct-to-LDS copies of one operand: the
-// byte offset of each lane's 16 bytes from the tile's first element, for a
-// k-step that lies wholly inside [kbeg, kend).  Only the uniform tile base
-// moves from k-step to k-step.
+// Row / column of accumulator element r of tile (i, j) for this lane: the
+// lane holds column lane%32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32.
+template <typename C = Cfg>
+AJ_DEV int acc_row(int wm, int i, int r, int lane) {
+  return wm * C::WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+template <typename C = Cfg>
+AJ_DEV int acc_col(int wn, int j, int lane) { return wn * C::WTN + j * 32 + (lane & 31); }
+
+// ---------------------------------------------------------------------------
+// The 4-wave tile with 32-wide k-steps in four LDS stages (4 x 2 x 16 KB, the
+// same 128 KB): the copies of a k-step are issued three k-steps before its
+// products, and the end of a k-step waits only for the copies of the next
+// one (the vector-memory counter lets the two younger steps' copies stay in
+// flight), so a copy has three k-steps of matrix work to land instead of one.
+// Layouts as above with 32 k: a K-major row is 64 bytes (4 chunks), chunk c
+// of row r at r*64 + 16*(c ^ ((r >> 2) & 3)) -- the 16 rows of one read pass
+// hit each of the 64 banks once; an M/N-major operand keeps [k][256] rows.
 template <bool KMAJOR>
-struct Copier {
-  static constexpr int kInstr = Tile<256, KMAJOR>::kInstr;
+struct Tile32 {
+  static constexpr int BK = 32;
+  static constexpr int kHalfs = 256 * BK;
+  static constexpr int kInstr = 256 * BK * 2 / 1024 / 4;   // copies per wave (4 waves)
+
+  AJ_DEV static int swz(int r) { return (r >> 2) & 3; }
+
+  // bounded copy of the k-step at k0 (rows past the end repeat the last row,
+  // k past K reads zeros)
+  AJ_DEV static void load(uint16_t *lds, const bf16_t *X, int64_t ld, int r0, int rows, int k0,
+                          int K) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < kInstr; ++q) {
+      const int blk = wave * kInstr + q;
+      const void *src;
+      if (KMAJOR) {
+        const int r = blk * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ swz(r);
+        const int k = k0 + 8 * c;
+        const int rr = min(r0 + r, rows - 1);
+        src = k < K ? (const void *)(X + (int64_t)rr * ld + k) : (const void *)kZero16;
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        const int c = (lane & 31) ^ (4 * (kr & 3));
+        const int k = k0 + kr;
+        const int rr = min(r0 + 8 * c, rows - 8);
+        src = k < K ? (const void *)(X + (int64_t)k * ld + rr) : (const void *)kZero16;
+      }
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(lds + blk * 512),
+                                       16, 0, 0);
+    }
+  }
+
+  // MFMA operand of rows [rb, rb+32), k [kk, kk+16), as Tile::frag
+  AJ_DEV static bf16x8_t frag(const uint16_t *lds, int rb, int kk) {
+    const int lane = threadIdx.x & 63;
+    bf16x8_t v;
+    if (KMAJOR) {
+      const int m = rb + (lane & 31);
+      const int c = (kk >> 3) + (lane >> 5);
+      const uint32_t a = lds_addr(lds + m * 32 + 8 * (c ^ swz(m)));
+      asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+      return v;
+    }
+    const int g = lane >> 4, s = lane & 15;
+    const int k = kk + 8 * (g >> 1) + (s >> 2);
+    const int col = rb + 16 * (g & 1) + 4 * (s & 3);
+    const int c = (col >> 3) ^ (4 * (k & 3));
+    const uint32_t a = lds_addr(lds + k * 256 + 8 * c + (col & 7));
+    u32x2_t lo, hi;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:2048" : "=v"(hi) : "v"(a) : "memory");
+    return __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
+  }
+};
+
+// Loop-invariant per-lane offsets of the copies of a whole 32-wide k-step.
+template <bool KMAJOR>
+struct Copier32 {
+  static constexpr int kInstr = Tile32<KMAJOR>::kInstr;
   uint32_t off[kInstr];
-  int64_t step;                       // elements from one k-step's tile to the next
+  int64_t step;
 
   AJ_DEV void init(int64_t ld, int r0, int rows) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -244,8 +314,8 @@ struct Copier {
     for (int q = 0; q < kInstr; ++q) {
       const int blk = wave * kInstr + q;
       if (KMAJOR) {
-        const int r = blk * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        const int r = blk * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ Tile32<true>::swz(r);
         const int rr = min(r0 + r, rows - 1) - r0;
         off[q] = (uint32_t)(((int64_t)rr * ld + 8 * c) * 2);
       } else {
@@ -255,73 +325,83 @@ struct Copier {
         off[q] = (uint32_t)(((int64_t)kr * ld + rr) * 2);
       }
     }
-    step = KMAJOR ? 64 : 64 * ld;
+    step = KMAJOR ? 32 : 32 * ld;
   }
-  // tile: first element of the k-step's operand tile (row r0, k k0)
-  AJ_DEV void issue(uint16_t *lds, const bf16_t *tile) const {
+  AJ_DEV void issue_one(int q, uint16_t *lds, const bf16_t *tile) const {
     const int wave = threadIdx.x >> 6;
-    const char *base = reinterpret_cast<const char *>(tile);
-#pragma unroll
-    for (int q = 0; q < kInstr; ++q)
-      __builtin_amdgcn_global_load_lds(
-          base + off[q], (__attribute__((address_space(3))) void *)(lds + (wave * kInstr + q) * 512),
-          16, 0, 0);
+    __builtin_amdgcn_global_load_lds(
+        reinterpret_cast<const char *>(tile) + off[q],
+        (__attribute__((address_space(3))) void *)(lds + (wave * kInstr + q) * 512), 16, 0, 0);
   }
 };
 
 template <bool A_K, bool B_K>
-struct Sched4 {
-  using TA = Tile<256, A_K>;
-  using TB = Tile<256, B_K>;
-  // next-slice fragment read number q (0..7): A fragments first, then B
-  AJ_DEV static void read_one(int q, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4], const uint16_t *as,
-                              const uint16_t *bs, int wm, int wn, int kk) {
-    if (q < 4) fa[q] = TA::frag(as, wm * 128 + q * 32, kk);
-    else fb[q - 4] = TB::frag(bs, wn * 128 + (q - 4) * 32, kk);
-  }
+struct Smem4s {
+  uint16_t a[4][256 * 32];
+  uint16_t b[4][256 * 32];
 };
 
-// One 16-wide k slice: 16 MFMAs on (fa, fb) in a fixed issue order with the
-// next slice's 8 fragment reads after the first 8 MFMAs and, in the first
-// slice of a k-step, one of the next k-step's 16 copies after each MFMA.
-template <bool A_K, bool B_K, bool kCopy, bool kRead>
-AJ_DEV void slice4(f32x16_t (&acc)[4][4], const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4],
-                   bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as, const uint16_t *bs,
-                   int wm, int wn, int kk_next, const Copier<A_K> &ca, const Copier<B_K> &cb,
-                   uint16_t *la, uint16_t *lb, const bf16_t *ta, const bf16_t *tb) {
-  const int wave = threadIdx.x >> 6;
+// A workgroup barrier without the memory fence of __syncthreads: that fence
+// waits for every outstanding vector-memory operation, the direct-to-LDS
+// copies still meant to fly included.  Visibility of the copies and reads that
+// must be complete is ensured by explicit vmcnt / lgkmcnt waits before it; the
+// empty asm statements keep the compiler from moving memory operations across.
+AJ_DEV void bar_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Waits until at most n k-steps' copies (8 per wave each) are still in flight.
+AJ_DEV void wait_copies(int n) {
+  if (n >= 2) __asm__ volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else if (n == 1) __asm__ volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// One 16-wide k slice of the staged loop: 16 MFMAs in a fixed order, a whole
+// k-step's 8 copies after the first 8, the next slice's 8 fragment reads
+// after the last 8.  With kBar the k-step's closing wait and barrier sit
+// after the first 8 MFMAs (this wave's reads of the current stage are all
+// complete by then), so that the reads of the next k-step's first slice, from
+// as / bs, overlap the last 8.
+template <bool A_K, bool B_K, bool kCopy, bool kRead, bool kBar = false>
+AJ_DEV void slice4s(f32x16_t (&acc)[4][4], const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4],
+                    bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as, const uint16_t *bs,
+                    int wm, int wn, int kk_next, const Copier32<A_K> &ca,
+                    const Copier32<B_K> &cb, uint16_t *la, uint16_t *lb, const bf16_t *ta,
+                    const bf16_t *tb) {
 #pragma unroll
   for (int t = 0; t < 16; ++t) {
     acc[t >> 2][t & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[t >> 2], fb[t & 3],
                                                                   acc[t >> 2][t & 3], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
-    if (kRead && t < 8) Sched4<A_K, B_K>::read_one(t, na, nb, as, bs, wm, wn, kk_next);
-    if (kCopy) {
-      if (t < Copier<A_K>::kInstr) {
-        __builtin_amdgcn_global_load_lds(
-            reinterpret_cast<const char *>(ta) + ca.off[t],
-            (__attribute__((address_space(3))) void *)(la + (wave * Copier<A_K>::kInstr + t) * 512),
-            16, 0, 0);
-      } else {
-        const int u = t - Copier<A_K>::kInstr;
-        __builtin_amdgcn_global_load_lds(
-            reinterpret_cast<const char *>(tb) + cb.off[u],
-            (__attribute__((address_space(3))) void *)(lb + (wave * Copier<B_K>::kInstr + u) * 512),
-            16, 0, 0);
-      }
+    if (kCopy && t < 8) {
+      if (t < Copier32<A_K>::kInstr) ca.issue_one(t, la, ta);
+      else cb.issue_one(t - Copier32<A_K>::kInstr, lb, tb);
+    }
+    if (kBar && t == 7) {
+      // the next k-step's copies have landed (those of the two after it may fly)
+      wait_copies(2);
+      bar_nofence();
+    }
+    if (kRead && t >= 8) {
+      const int q = t - 8;
+      if (q < 4) na[q] = Tile32<A_K>::frag(as, wm * 128 + q * 32, kk_next);
+      else nb[q - 4] = Tile32<B_K>::frag(bs, wn * 128 + (q - 4) * 32, kk_next);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 template <bool A_K, bool B_K>
-AJ_DEV void mainloop4(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, const bf16_t *B,
-                      int64_t ldb, int M, int N, int m0, int n0, int kbeg, int kend,
-                      Smem<A_K, B_K, Cfg4> &sm) {
-  using TA = Tile<256, A_K>;
-  using TB = Tile<256, B_K>;
-  static_assert(Copier<A_K>::kInstr + Copier<B_K>::kInstr == 16, "copies per k-step");
-  constexpr int BK = 64;
+AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, const bf16_t *B,
+                       int64_t ldb, int M, int N, int m0, int n0, int kbeg, int kend,
+                       Smem4s<A_K, B_K> &sm) {
+  using TA = Tile32<A_K>;
+  using TB = Tile32<B_K>;
+  static_assert(Copier32<A_K>::kInstr + Copier32<B_K>::kInstr == 8, "copies per k-step");
+  constexpr int BK = 32;
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int nfull = kend > kbeg ? (kend - kbeg) / BK : 0;
   const int wave = threadIdx.x >> 6;
@@ -333,84 +413,68 @@ AJ_DEV void mainloop4(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, const
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   if (nk == 0) return;
-  Copier<A_K> ca;
-  Copier<B_K> cb;
+  Copier32<A_K> ca;
+  Copier32<B_K> cb;
   ca.init(lda, m0, M);
   cb.init(ldb, n0, N);
   const bf16_t *ta = A + (A_K ? (int64_t)m0 * lda + kbeg : (int64_t)kbeg * lda + m0);
   const bf16_t *tb = B + (B_K ? (int64_t)n0 * ldb + kbeg : (int64_t)kbeg * ldb + n0);
-  auto load_step = [&](int kt, int buf) {
+  // all 8 copies of k-step kt (< nk) into its stage
+  auto copy_step = [&](int kt) {
+    const int st = kt & 3;
     if (kt < nfull) {
-      ca.issue(sm.a[buf], ta + kt * ca.step);
-      cb.issue(sm.b[buf], tb + kt * cb.step);
-    } else if (kt < nk) {
-      TA::load(sm.a[buf], A, lda, m0, M, kbeg + kt * BK, kend);
-      TB::load(sm.b[buf], B, ldb, n0, N, kbeg + kt * BK, kend);
+#pragma unroll
+      for (int q = 0; q < Copier32<A_K>::kInstr; ++q) ca.issue_one(q, sm.a[st], ta + kt * ca.step);
+#pragma unroll
+      for (int q = 0; q < Copier32<B_K>::kInstr; ++q) cb.issue_one(q, sm.b[st], tb + kt * cb.step);
+    } else {
+      TA::load(sm.a[st], A, lda, m0, M, kbeg + kt * BK, kend);
+      TB::load(sm.b[st], B, ldb, n0, N, kbeg + kt * BK, kend);
     }
   };
   bf16x8_t f0a[4], f0b[4], f1a[4], f1b[4];
-  auto read_slice = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[4], const uint16_t *as,
-                        const uint16_t *bs, int kk) {
+  const int pro = nk < 3 ? nk : 3;
+  for (int kt = 0; kt < pro; ++kt) copy_step(kt);
+  wait_copies(pro - 1);
+  bar_nofence();
+  auto read_first = [&](int kt) {
+    const int st = kt & 3;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) Sched4<A_K, B_K>::read_one(q, fa, fb, as, bs, wm, wn, kk);
+    for (int q = 0; q < 4; ++q) {
+      f0a[q] = TA::frag(sm.a[st], wm * 128 + q * 32, 0);
+      f0b[q] = TB::frag(sm.b[st], wn * 128 + q * 32, 0);
+    }
   };
-  load_step(0, 0);
-  wait_lds_dma();
-  __syncthreads();
-  read_slice(f0a, f0b, sm.a[0], sm.b[0], 0);
+  read_first(0);
   int kt = 0;
-  // steady state: the next k-step is a full one, copied in the first slice
-  for (; kt + 1 < nfull; ++kt) {
-    const int buf = kt & 1;
-    const uint16_t *as = sm.a[buf], *bs = sm.b[buf];
-    const bf16_t *na = ta + (kt + 1) * ca.step, *nb = tb + (kt + 1) * cb.step;
+  // steady state: the k-step three ahead is a full one, copied in the first slice
+  for (; kt + 3 < nfull; ++kt) {
+    const int st = kt & 3, nx = (kt + 3) & 3;
+    const uint16_t *as = sm.a[st], *bs = sm.b[st];
     frag_wait(f0a, f0b);
-    slice4<A_K, B_K, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
-                                 sm.a[buf ^ 1], sm.b[buf ^ 1], na, nb);
+    slice4s<A_K, B_K, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, sm.a[nx],
+                                  sm.b[nx], ta + (kt + 3) * ca.step, tb + (kt + 3) * cb.step);
     frag_wait(f1a, f1b);
-    slice4<A_K, B_K, false, true>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 32, ca, cb,
-                                  nullptr, nullptr, nullptr, nullptr);
-    frag_wait(f0a, f0b);
-    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 48, ca, cb,
-                                  nullptr, nullptr, nullptr, nullptr);
-    frag_wait(f1a, f1b);
-    slice4<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
-                                   nullptr, nullptr, nullptr, nullptr);
-    wait_lds_dma();
-    __syncthreads();
-    read_slice(f0a, f0b, sm.a[buf ^ 1], sm.b[buf ^ 1], 0);
+    const int s1 = (kt + 1) & 3;
+    slice4s<A_K, B_K, false, true, true>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1], wm, wn, 0,
+                                         ca, cb, nullptr, nullptr, nullptr, nullptr);
   }
-  // the last one or two k-steps (the last may be ragged)
+  // the last three k-steps (the last may be ragged, its copies bounded)
   for (; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const uint16_t *as = sm.a[buf], *bs = sm.b[buf];
-    load_step(kt + 1, buf ^ 1);
+    const int st = kt & 3;
+    const uint16_t *as = sm.a[st], *bs = sm.b[st];
+    if (kt + 3 < nk) copy_step(kt + 3);
     frag_wait(f0a, f0b);
-    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
-                                  nullptr, nullptr, nullptr, nullptr);
+    slice4s<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, nullptr,
+                                   nullptr, nullptr, nullptr);
     frag_wait(f1a, f1b);
-    slice4<A_K, B_K, false, true>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 32, ca, cb,
-                                  nullptr, nullptr, nullptr, nullptr);
-    frag_wait(f0a, f0b);
-    slice4<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 48, ca, cb,
-                                  nullptr, nullptr, nullptr, nullptr);
-    frag_wait(f1a, f1b);
-    slice4<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
-                                   nullptr, nullptr, nullptr, nullptr);
-    wait_lds_dma();
-    __syncthreads();
-    if (kt + 1 < nk) read_slice(f0a, f0b, sm.a[buf ^ 1], sm.b[buf ^ 1], 0);
+    slice4s<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb, nullptr,
+                                    nullptr, nullptr, nullptr);
+    wait_copies((kt + 2 < nk) + (kt + 3 < nk));
+    bar_nofence();
+    if (kt + 1 < nk) read_first(kt + 1);
   }
 }
-
-// Row / column of accumulator element r of tile (i, j) for this lane: the
-// lane holds column lane%32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32.
-template <typename C = Cfg>
-AJ_DEV int acc_row(int wm, int i, int r, int lane) {
-  return wm * C::WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-}
-template <typename C = Cfg>
-AJ_DEV int acc_col(int wn, int j, int lane) { return wn * C::WTN + j * 32 + (lane & 31); }
 
 }  // namespace gemm_core
 }  // namespace aj
