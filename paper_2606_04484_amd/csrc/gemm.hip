@@ -35,6 +35,70 @@ struct Seg2 {
   int K;
 };
 
+// Output modes of the epilogue's fast path (interior tiles, aligned rows).
+enum { kEpPartial, kEpAccum, kEpF32, kEpF32R, kEpBf16, kEpBf16R };
+
+// One pass of the fast epilogue: the 64 staged rows (32 of each wave row)
+// x 256 columns, 4 columns per thread and instruction; every LDS read of the
+// pass is issued before the first store.
+template <int MODE, typename Cfg>
+AJ_DEV void store_pass(const float *stage, int i, int m0, int n0, int64_t ldo, float *P,
+                       const EpArgs &ep) {
+  static_assert(Cfg::WTM == 128 && Cfg::BN == 256, "two wave rows of 128, 256 columns");
+  constexpr int LDW = Cfg::BN + 8;
+  constexpr int Q = 64 * 64 / Cfg::NT;
+  float4 v[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int c = threadIdx.x + Cfg::NT * q;
+    v[q] = *reinterpret_cast<const float4 *>(stage + (c >> 6) * LDW + (c & 63) * 4);
+  }
+  auto offset = [&](int q) {
+    const int c = threadIdx.x + Cfg::NT * q;
+    const int row = c >> 6;
+    return (int64_t)(m0 + (row >> 5) * 128 + 32 * i + (row & 31)) * ldo + n0 + (c & 63) * 4;
+  };
+  if constexpr (MODE == kEpAccum || MODE == kEpF32R) {
+    const float *src = MODE == kEpAccum ? (const float *)ep.C : (const float *)ep.R;
+    float4 u[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) u[q] = *reinterpret_cast<const float4 *>(src + offset(q));
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const float4 w = make_float4(v[q].x + u[q].x, v[q].y + u[q].y, v[q].z + u[q].z,
+                                   v[q].w + u[q].w);
+      *reinterpret_cast<float4 *>((float *)ep.C + offset(q)) = w;
+    }
+  } else if constexpr (MODE == kEpBf16R) {
+    uint2 u[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) u[q] = *reinterpret_cast<const uint2 *>((const bf16_t *)ep.R + offset(q));
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      uint2 out;
+      out.x = f2bf2(v[q].x + __uint_as_float(u[q].x << 16),
+                    v[q].y + __uint_as_float(u[q].x & 0xffff0000u));
+      out.y = f2bf2(v[q].z + __uint_as_float(u[q].y << 16),
+                    v[q].w + __uint_as_float(u[q].y & 0xffff0000u));
+      *reinterpret_cast<uint2 *>((bf16_t *)ep.C + offset(q)) = out;
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      if constexpr (MODE == kEpPartial) {
+        *reinterpret_cast<float4 *>(P + offset(q)) = v[q];
+      } else if constexpr (MODE == kEpF32) {
+        *reinterpret_cast<float4 *>((float *)ep.C + offset(q)) = v[q];
+      } else {
+        uint2 out;
+        out.x = f2bf2(v[q].x, v[q].y);
+        out.y = f2bf2(v[q].z, v[q].w);
+        *reinterpret_cast<uint2 *>((bf16_t *)ep.C + offset(q)) = out;
+      }
+    }
+  }
+}
+
 // Shared body of the two GEMM kernels: main loop of configuration C (and the
 // second segment's, SEG2), then the epilogue through LDS.
 template <bool A_K, bool B_K, typename Cfg, bool SEG2 = false, bool STAGED = false,
@@ -50,9 +114,12 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  if constexpr (STAGED) {
-    static_assert(!SEG2 && Cfg::NT == 256, "the staged loop is the 4-wave one, one segment");
+  if constexpr (STAGED && Cfg::NT == 256) {
+    static_assert(!SEG2, "the staged loops take one segment");
     gemm_core::mainloop4s<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+  } else if constexpr (STAGED) {
+    static_assert(!SEG2, "the staged loops take one segment");
+    gemm_core::mainloop8s<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
   } else {
     static_assert(Cfg::NT == 512, "8-wave tile");
     gemm_core::mainloop<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
@@ -65,10 +132,18 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   // Epilogue through LDS, 32 rows of each wave row at a time: the lane's
   // accumulators (column lane%32, rows 8*(r/4) + 4*(lane/32) + r%4 of each
   // 32x32 tile) are staged as rows, then written out 4 columns per lane.
+  // Interior tiles with aligned rows take a pass specialised to the output
+  // mode (no per-element branches, the pass's LDS reads issued together);
+  // edge tiles go element by element.
   float *stage = reinterpret_cast<float *>(&sm);
   constexpr int LDW = Cfg::BN + 8;
   float *P = partial ? partial + (int64_t)blockIdx.z * M * N : nullptr;
   const int64_t ldo = partial ? N : ep.ldc;
+  const bool fast = ep.vec && m0 + Cfg::BM <= M && n0 + Cfg::BN <= N;
+  const int mode = P ? kEpPartial
+                   : ep.accum ? kEpAccum
+                   : ep.c_f32 ? (ep.R ? kEpF32R : kEpF32)
+                              : (ep.R ? kEpBf16R : kEpBf16);
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i) {
 #pragma unroll
@@ -79,6 +154,18 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
         stage[lr * LDW + wn * Cfg::WTN + j * 32 + (lane & 31)] = acc[i][j][r];
       }
     __syncthreads();
+    if (fast) {
+      switch (mode) {
+        case kEpPartial: store_pass<kEpPartial, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        case kEpAccum: store_pass<kEpAccum, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        case kEpF32: store_pass<kEpF32, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        case kEpF32R: store_pass<kEpF32R, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        case kEpBf16: store_pass<kEpBf16, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        default: store_pass<kEpBf16R, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+      }
+      __syncthreads();
+      continue;
+    }
 #pragma unroll 4
     for (int q = 0; q < 64 * 64 / Cfg::NT; ++q) {
       const int c = threadIdx.x + Cfg::NT * q;
@@ -140,8 +227,9 @@ template <bool A_K, bool B_K>
 __global__ __launch_bounds__(gemm_core::Cfg::NT, 1) void gemm_mfma_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) gemm_core::Smem<A_K, B_K, gemm_core::Cfg> sm;
-  gemm_tile<A_K, B_K, gemm_core::Cfg>(M, N, K, k_per_split, A, lda, B, ldb, ep, partial, sm);
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K> sm;
+  gemm_tile<A_K, B_K, gemm_core::Cfg, false, true>(M, N, K, k_per_split, A, lda, B, ldb, ep,
+                                                   partial, sm);
 }
 
 // 4 waves of 128x128 with 32-wide k-steps in four LDS stages (copies three

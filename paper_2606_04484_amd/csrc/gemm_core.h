@@ -243,11 +243,11 @@ AJ_DEV int acc_col(int wn, int j, int lane) { return wn * C::WTN + j * 32 + (lan
 // Layouts as above with 32 k: a K-major row is 64 bytes (4 chunks), chunk c
 // of row r at r*64 + 16*(c ^ ((r >> 2) & 3)) -- the 16 rows of one read pass
 // hit each of the 64 banks once; an M/N-major operand keeps [k][256] rows.
-template <bool KMAJOR>
+template <bool KMAJOR, int NW = 4>
 struct Tile32 {
   static constexpr int BK = 32;
   static constexpr int kHalfs = 256 * BK;
-  static constexpr int kInstr = 256 * BK * 2 / 1024 / 4;   // copies per wave (4 waves)
+  static constexpr int kInstr = 256 * BK * 2 / 1024 / NW;   // copies per wave (NW waves)
 
   AJ_DEV static int swz(int r) { return (r >> 2) & 3; }
 
@@ -302,9 +302,9 @@ struct Tile32 {
 };
 
 // Loop-invariant per-lane offsets of the copies of a whole 32-wide k-step.
-template <bool KMAJOR>
+template <bool KMAJOR, int NW = 4>
 struct Copier32 {
-  static constexpr int kInstr = Tile32<KMAJOR>::kInstr;
+  static constexpr int kInstr = Tile32<KMAJOR, NW>::kInstr;
   uint32_t off[kInstr];
   int64_t step;
 
@@ -359,22 +359,89 @@ AJ_DEV void wait_copies(int n) {
   else __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// One 16-wide k slice of the staged loop: 16 MFMAs in a fixed order, a whole
-// k-step's 8 copies after the first 8, the next slice's 8 fragment reads
-// after the last 8.  With kBar the k-step's closing wait and barrier sit
-// after the first 8 MFMAs (this wave's reads of the current stage are all
-// complete by then), so that the reads of the next k-step's first slice, from
-// as / bs, overlap the last 8.
+// Fragment reads of one 16-wide slice, issued one after each of the last 8
+// MFMAs of the slice before, in the order B0 A0 B1 B2 B3 A1 A2 A3, so that
+// each MFMA of the slice waits only for the reads it consumes (the MFMAs run
+// A-major: t uses A[t/4], B[t%4]).  LDS reads complete in order, so the wait
+// before MFMA t is "at most n reads in flight" with n the LDS instructions
+// issued after the last one it needs (an M/N-major fragment is two reads).
+template <bool A_K, bool B_K>
+struct ReadPlan {
+  static constexpr int nA = A_K ? 1 : 2, nB = B_K ? 1 : 2;
+  static constexpr int kTotal = 4 * nA + 4 * nB;
+  AJ_DEV static constexpr bool is_b(int q) { return q == 0 || (q >= 2 && q <= 4); }
+  AJ_DEV static constexpr int index(int q) { return q <= 1 ? 0 : q <= 4 ? q - 1 : q - 4; }
+  // LDS instructions issued by reads 0..q-1
+  AJ_DEV static constexpr int issued(int q) {
+    int n = 0;
+    for (int i = 0; i < q; ++i) n += is_b(i) ? nB : nA;
+    return n;
+  }
+  // LDS instructions allowed in flight before MFMA t (-1: no wait): the
+  // slice's own reads after the last one MFMA t needs, plus the next slice's
+  // reads already issued (one after each MFMA from the 8th on) when kRead
+  AJ_DEV static constexpr int wait_before(int t, bool kRead) {
+    const int last = t == 0 ? 1 : t <= 3 ? t + 1 : t == 4 ? 5 : t == 8 ? 6 : t == 12 ? 7 : -1;
+    if (last < 0) return -1;
+    const int next = kRead && t > 8 ? issued(t - 8) : 0;
+    return kTotal - issued(last + 1) + next;
+  }
+};
+
+AJ_DEV void lgkm_wait(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt lgkmcnt(1)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt lgkmcnt(2)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt lgkmcnt(3)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt lgkmcnt(5)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt lgkmcnt(6)" ::: "memory"); break;
+    case 7: asm volatile("s_waitcnt lgkmcnt(7)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt lgkmcnt(8)" ::: "memory"); break;
+    case 9: asm volatile("s_waitcnt lgkmcnt(9)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt lgkmcnt(10)" ::: "memory"); break;
+    case 11: asm volatile("s_waitcnt lgkmcnt(11)" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt lgkmcnt(12)" ::: "memory"); break;
+    case 13: asm volatile("s_waitcnt lgkmcnt(13)" ::: "memory"); break;
+    case 14: asm volatile("s_waitcnt lgkmcnt(14)" ::: "memory"); break;
+    default: break;
+  }
+}
+
+// read number q (0..7) of a slice's fragments, in ReadPlan order
+template <bool A_K, bool B_K>
+AJ_DEV void read_frag4s(int q, bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as,
+                        const uint16_t *bs, int wm, int wn, int kk) {
+  using P = ReadPlan<A_K, B_K>;
+  const int i = P::index(q);
+  if (P::is_b(q)) nb[i] = Tile32<B_K>::frag(bs, wn * 128 + i * 32, kk);
+  else na[i] = Tile32<A_K>::frag(as, wm * 128 + i * 32, kk);
+}
+
+// One 16-wide k slice of the staged loop: 16 MFMAs in a fixed order, each
+// after the partial wait for its fragments, a whole k-step's 8 copies after
+// the first 8, the next slice's 8 fragment reads after the last 8.  With kBar
+// the k-step's closing wait and barrier sit after the first 8 MFMAs (this
+// wave's reads of the current stage are all complete by then), so that the
+// reads of the next k-step's first slice, from as / bs, overlap the last 8.
 template <bool A_K, bool B_K, bool kCopy, bool kRead, bool kBar = false>
-AJ_DEV void slice4s(f32x16_t (&acc)[4][4], const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4],
+AJ_DEV void slice4s(f32x16_t (&acc)[4][4], bf16x8_t (&fa)[4], bf16x8_t (&fb)[4],
                     bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as, const uint16_t *bs,
                     int wm, int wn, int kk_next, const Copier32<A_K> &ca,
                     const Copier32<B_K> &cb, uint16_t *la, uint16_t *lb, const bf16_t *ta,
                     const bf16_t *tb) {
+  using P = ReadPlan<A_K, B_K>;
 #pragma unroll
   for (int t = 0; t < 16; ++t) {
-    acc[t >> 2][t & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[t >> 2], fb[t & 3],
-                                                                  acc[t >> 2][t & 3], 0, 0, 0);
+    const int a = t >> 2, b = t & 3;
+    if (P::wait_before(t, kRead) >= 0) {
+      lgkm_wait(P::wait_before(t, kRead));
+      // the MFMA's operands pass through the wait so that it stays below it
+      asm volatile("" : "+v"(fa[a]));
+      asm volatile("" : "+v"(fb[b]));
+    }
+    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
     if (kCopy && t < 8) {
       if (t < Copier32<A_K>::kInstr) ca.issue_one(t, la, ta);
@@ -385,11 +452,7 @@ AJ_DEV void slice4s(f32x16_t (&acc)[4][4], const bf16x8_t (&fa)[4], const bf16x8
       wait_copies(2);
       bar_nofence();
     }
-    if (kRead && t >= 8) {
-      const int q = t - 8;
-      if (q < 4) na[q] = Tile32<A_K>::frag(as, wm * 128 + q * 32, kk_next);
-      else nb[q - 4] = Tile32<B_K>::frag(bs, wn * 128 + (q - 4) * 32, kk_next);
-    }
+    if (kRead && t >= 8) read_frag4s<A_K, B_K>(t - 8, na, nb, as, bs, wm, wn, kk_next);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -440,10 +503,7 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
   auto read_first = [&](int kt) {
     const int st = kt & 3;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      f0a[q] = TA::frag(sm.a[st], wm * 128 + q * 32, 0);
-      f0b[q] = TB::frag(sm.b[st], wn * 128 + q * 32, 0);
-    }
+    for (int q = 0; q < 8; ++q) read_frag4s<A_K, B_K>(q, f0a, f0b, sm.a[st], sm.b[st], wm, wn, 0);
   };
   read_first(0);
   int kt = 0;
@@ -451,10 +511,8 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
   for (; kt + 3 < nfull; ++kt) {
     const int st = kt & 3, nx = (kt + 3) & 3;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
-    frag_wait(f0a, f0b);
     slice4s<A_K, B_K, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, sm.a[nx],
                                   sm.b[nx], ta + (kt + 3) * ca.step, tb + (kt + 3) * cb.step);
-    frag_wait(f1a, f1b);
     const int s1 = (kt + 1) & 3;
     slice4s<A_K, B_K, false, true, true>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1], wm, wn, 0,
                                          ca, cb, nullptr, nullptr, nullptr, nullptr);
@@ -464,13 +522,142 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
     const int st = kt & 3;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
     if (kt + 3 < nk) copy_step(kt + 3);
-    frag_wait(f0a, f0b);
     slice4s<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, nullptr,
                                    nullptr, nullptr, nullptr);
-    frag_wait(f1a, f1b);
     slice4s<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb, nullptr,
                                     nullptr, nullptr, nullptr);
     wait_copies((kt + 2 < nk) + (kt + 3 < nk));
+    bar_nofence();
+    if (kt + 1 < nk) read_first(kt + 1);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The 8-wave tiles (Cfg, CfgWide) on the same staged k loop: 32-wide k-steps
+// through four LDS stages, copies three k-steps ahead, one fence-free barrier
+// per k-step.  A wave holds TM x TN = 8 MFMA tiles, so a slice is 8 MFMAs: the
+// k-step's 4 copies per wave follow the first 4 MFMAs of its first slice, the
+// closing wait and barrier the 4th MFMA of its second, and the next slice's
+// TM + TN fragment reads are spread over the last 4 (two waves per SIMD cover
+// each other's waits, so the slices wait for their fragments as a whole).
+AJ_DEV void wait_copies8(int n) {   // 4 copies per wave per k-step
+  if (n >= 2) __asm__ volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if (n == 1) __asm__ volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+template <bool A_K, bool B_K, typename C>
+AJ_DEV void read_frag8s(int q, bf16x8_t (&na)[C::TM], bf16x8_t (&nb)[C::TN], const uint16_t *as,
+                        const uint16_t *bs, int wm, int wn, int kk) {
+  if (q < C::TM) na[q] = Tile32<A_K, 8>::frag(as, wm * C::WTM + q * 32, kk);
+  else nb[q - C::TM] = Tile32<B_K, 8>::frag(bs, wn * C::WTN + (q - C::TM) * 32, kk);
+}
+
+template <bool A_K, bool B_K, typename C, bool kCopy, bool kRead, bool kBar = false>
+AJ_DEV void slice8s(f32x16_t (&acc)[C::TM][C::TN], const bf16x8_t (&fa)[C::TM],
+                    const bf16x8_t (&fb)[C::TN], bf16x8_t (&na)[C::TM], bf16x8_t (&nb)[C::TN],
+                    const uint16_t *as, const uint16_t *bs, int wm, int wn, int kk_next,
+                    const Copier32<A_K, 8> &ca, const Copier32<B_K, 8> &cb, uint16_t *la,
+                    uint16_t *lb, const bf16_t *ta, const bf16_t *tb) {
+  constexpr int R = C::TM + C::TN;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const int i = t / C::TN, j = t % C::TN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kCopy && t < 4) {
+      if (t < Copier32<A_K, 8>::kInstr) ca.issue_one(t, la, ta);
+      else cb.issue_one(t - Copier32<A_K, 8>::kInstr, lb, tb);
+    }
+    if (kBar && t == 3) {
+      wait_copies8(2);
+      bar_nofence();
+    }
+    if (kRead && t >= 4) {
+#pragma unroll
+      for (int q = (t - 4) * R / 4; q < (t - 3) * R / 4; ++q)
+        read_frag8s<A_K, B_K, C>(q, na, nb, as, bs, wm, wn, kk_next);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <bool A_K, bool B_K, typename C>
+AJ_DEV void mainloop8s(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda,
+                       const bf16_t *B, int64_t ldb, int M, int N, int m0, int n0, int kbeg,
+                       int kend, Smem4s<A_K, B_K> &sm) {
+  static_assert(C::NT == 512 && C::TM * C::TN == 8, "8 waves of 8 MFMA tiles");
+  using TA = Tile32<A_K, 8>;
+  using TB = Tile32<B_K, 8>;
+  using CA = Copier32<A_K, 8>;
+  using CB = Copier32<B_K, 8>;
+  static_assert(CA::kInstr + CB::kInstr == 4, "copies per k-step");
+  constexpr int BK = 32;
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  const int nfull = kend > kbeg ? (kend - kbeg) / BK : 0;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  if (nk == 0) return;
+  CA ca;
+  CB cb;
+  ca.init(lda, m0, M);
+  cb.init(ldb, n0, N);
+  const bf16_t *ta = A + (A_K ? (int64_t)m0 * lda + kbeg : (int64_t)kbeg * lda + m0);
+  const bf16_t *tb = B + (B_K ? (int64_t)n0 * ldb + kbeg : (int64_t)kbeg * ldb + n0);
+  auto copy_step = [&](int kt) {
+    const int st = kt & 3;
+    if (kt < nfull) {
+#pragma unroll
+      for (int q = 0; q < CA::kInstr; ++q) ca.issue_one(q, sm.a[st], ta + kt * ca.step);
+#pragma unroll
+      for (int q = 0; q < CB::kInstr; ++q) cb.issue_one(q, sm.b[st], tb + kt * cb.step);
+    } else {
+      TA::load(sm.a[st], A, lda, m0, M, kbeg + kt * BK, kend);
+      TB::load(sm.b[st], B, ldb, n0, N, kbeg + kt * BK, kend);
+    }
+  };
+  bf16x8_t f0a[C::TM], f0b[C::TN], f1a[C::TM], f1b[C::TN];
+  auto read_first = [&](int kt) {
+    const int st = kt & 3;
+#pragma unroll
+    for (int q = 0; q < C::TM + C::TN; ++q)
+      read_frag8s<A_K, B_K, C>(q, f0a, f0b, sm.a[st], sm.b[st], wm, wn, 0);
+  };
+  const int pro = nk < 3 ? nk : 3;
+  for (int kt = 0; kt < pro; ++kt) copy_step(kt);
+  wait_copies8(pro - 1);
+  bar_nofence();
+  read_first(0);
+  int kt = 0;
+  for (; kt + 3 < nfull; ++kt) {
+    const int st = kt & 3, nx = (kt + 3) & 3;
+    const uint16_t *as = sm.a[st], *bs = sm.b[st];
+    frag_wait(f0a, f0b);
+    slice8s<A_K, B_K, C, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
+                                     sm.a[nx], sm.b[nx], ta + (kt + 3) * ca.step,
+                                     tb + (kt + 3) * cb.step);
+    frag_wait(f1a, f1b);
+    const int s1 = (kt + 1) & 3;
+    slice8s<A_K, B_K, C, false, true, true>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1], wm, wn,
+                                            0, ca, cb, nullptr, nullptr, nullptr, nullptr);
+  }
+  for (; kt < nk; ++kt) {
+    const int st = kt & 3;
+    const uint16_t *as = sm.a[st], *bs = sm.b[st];
+    if (kt + 3 < nk) copy_step(kt + 3);
+    frag_wait(f0a, f0b);
+    slice8s<A_K, B_K, C, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
+                                      nullptr, nullptr, nullptr, nullptr);
+    frag_wait(f1a, f1b);
+    slice8s<A_K, B_K, C, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
+                                       nullptr, nullptr, nullptr, nullptr);
+    wait_copies8((kt + 2 < nk) + (kt + 3 < nk));
     bar_nofence();
     if (kt + 1 < nk) read_first(kt + 1);
   }

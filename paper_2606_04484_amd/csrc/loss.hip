@@ -12,6 +12,7 @@
 // in bfloat16, then dhn += dz W_chunk and dW_chunk += dz^T hn are GEMMs.
 // float32 (the small workload): the same arithmetic with each chunk of logits
 // written to a float32 buffer and reduced by row kernels.
+#include <type_traits>
 #include "ops.h"
 #include "gemm_core.h"
 
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(256) void dz_kernel(const float *z, int n, int cw, 
 // ---------------------------------------------------------------- fused (bfloat16)
 namespace gemm_core = aj::gemm_core;
 using Cfg = gemm_core::CfgWide;
-template <bool A_K, bool B_K> using Smem = gemm_core::Smem<A_K, B_K, Cfg>;
+template <bool A_K, bool B_K> using Smem = gemm_core::Smem4s<A_K, B_K>;
 using gemm_core::f32x16_t;
 constexpr float kLog2e = 1.4426950408889634f;
 // 2^x on the hardware unit (v_exp_f32) for arguments <= 0 or -inf (a
@@ -271,6 +272,28 @@ AJ_DEV float half_sum(float v) {
 #pragma unroll
   for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Reductions over each row of 16 lanes on the DPP network (no LDS traffic):
+// swaps within pairs and quads, then the mirrors of 8 and 16 lanes.  Every
+// lane of the row ends with the result.
+template <int CTRL>
+AJ_DEV float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
+AJ_DEV float row16_max(float v) {
+  v = fmaxf(v, dpp<kQuadXor1>(v));
+  v = fmaxf(v, dpp<kQuadXor2>(v));
+  v = fmaxf(v, dpp<kRowHalfMirror>(v));
+  return fmaxf(v, dpp<kRowMirror>(v));
+}
+AJ_DEV float row16_sum(float v) {
+  v += dpp<kQuadXor1>(v);
+  v += dpp<kQuadXor2>(v);
+  v += dpp<kRowHalfMirror>(v);
+  return v + dpp<kRowMirror>(v);
 }
 
 // logits tile z = hn W^T (rows: targets, columns: 256 vocab ids) reduced in
@@ -290,29 +313,56 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     ttok[threadIdx.x] = m < n ? tok[tpos[m]] : -1;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop<true, true, Cfg>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, true, Cfg>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+  // A row of this wave's 128 columns lives in the 32 lanes of a half-wave, 4
+  // columns each: reduce over 16 lanes by DPP, then across the two rows of
+  // 16 with one exchange per row, issued for all 16 rows of a pass together.
+  const int col0 = n0 + wn * Cfg::WTN + (lane & 31);
+  auto epilogue = [&](auto inside) {
+    constexpr bool kInside = decltype(inside)::value;   // every column < V
 #pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i)
+    for (int i = 0; i < Cfg::TM; ++i) {
+      float mx[16], sm_[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
-      float v[Cfg::TN], mx = -INFINITY;
+      for (int r = 0; r < 16; ++r) {
+        float m = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) {
-        const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
-        v[j] = col < V ? acc[i][j][r] * kLog2e : -INFINITY;
-        mx = fmaxf(mx, v[j]);
-        if (col == ttok[rl] && m0 + rl < n) zt[m0 + rl] = acc[i][j][r];
+        for (int j = 0; j < Cfg::TN; ++j)
+          if (kInside || col0 + 32 * j < V) m = fmaxf(m, acc[i][j][r]);
+        mx[r] = row16_max(m * kLog2e);
       }
-      mx = half_max(mx);
-      float sm_ = 0.f;
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) sm_ += v[j] == -INFINITY ? 0.f : fast_exp2(v[j] - mx);
-      sm_ = half_sum(sm_);
-      if ((lane & 31) == 0) red[wn][rl] = make_float2(mx, sm_);
+      for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], __shfl_xor(mx[r], 16, 64));
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float t = 0.f;
+#pragma unroll
+        for (int j = 0; j < Cfg::TN; ++j)
+          if (kInside || col0 + 32 * j < V) t += fast_exp2(acc[i][j][r] * kLog2e - mx[r]);
+        sm_[r] = row16_sum(t);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sm_[r] += __shfl_xor(sm_[r], 16, 64);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
+        if ((lane & 31) == 0) red[wn][rl] = make_float2(mx[r], sm_[r]);
+        // the target's logit, in the lane that holds its column
+        const int t = ttok[rl] - col0;
+        if (t >= 0 && t < Cfg::TN * 32 && (t & 31) == 0 && m0 + rl < n) {
+          float z = acc[i][0][r];
+#pragma unroll
+          for (int j = 1; j < Cfg::TN; ++j)
+            if (t == 32 * j) z = acc[i][j][r];
+          zt[m0 + rl] = z;
+        }
+      }
     }
+  };
+  if (n0 + Cfg::BN <= V) epilogue(std::true_type{});
+  else epilogue(std::false_type{});
   __syncthreads();
   if (threadIdx.x < Cfg::BM && m0 + (int)threadIdx.x < n) {
     float M = -INFINITY, S = 0.f;
@@ -367,24 +417,76 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     tg[threadIdx.x] = m < n ? g[m] : 0.f;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop<true, true, Cfg>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, true, Cfg>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+  auto dz_of = [&](float a, int rl, int col) {
+    const float p = fast_exp2(a * kLog2e - tl[rl]);
+    return tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p);
+  };
+  if (m0 + Cfg::BM > n || n0 + Cfg::BN > cw || cw % 8 != 0 || ((uintptr_t)dz & 15) != 0) {
+    // edge tile: element by element
 #pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i)
+    for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
+        const int m = m0 + rl;
+        if (m >= n) continue;
+#pragma unroll
+        for (int j = 0; j < Cfg::TN; ++j) {
+          const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
+          if (col >= cw) continue;
+          dz[(int64_t)m * cw + col] = f2bf(dz_of(acc[i][j][r], rl, col));
+        }
+      }
+    return;
+  }
+  // Interior tile: dz staged as bfloat16 rows through LDS (the stage ring is
+  // free once every wave is past the main loop), 128 rows per pass (32 of each
+  // wave row), then written 16 bytes per lane.
+  constexpr int LDH = Cfg::BN + 8;   // bf16 elements per staged row
+  uint16_t *stage = reinterpret_cast<uint16_t *>(&sm);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < Cfg::TM; ++i) {
+    // the pass's per-row values, read before any staging write
+    float rl2[16], rg[16];
+    int rt[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = gemm_core::acc_row<Cfg>(wm, i, r, lane);
-      const int m = m0 + rl;
-      if (m >= n) continue;
+      rl2[r] = tl[rl];
+      rg[r] = tg[rl];
+      rt[r] = ttok[rl] - n0;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ls = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
       for (int j = 0; j < Cfg::TN; ++j) {
-        const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
-        if (col >= cw) continue;
-        const float p = fast_exp2(acc[i][j][r] * kLog2e - tl[rl]);
-        dz[(int64_t)m * cw + col] = f2bf(tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p));
+        const int cl = gemm_core::acc_col<Cfg>(wn, j, lane);
+        const float p = fast_exp2(acc[i][j][r] * kLog2e - rl2[r]);
+        stage[ls * LDH + cl] = f2bf(rg[r] * ((cl == rt[r] ? 1.f : 0.f) - p));
       }
     }
+    __syncthreads();
+    constexpr int Q = 128 * (Cfg::BN / 8) / Cfg::NT;   // 16-byte chunks per thread
+    uint4 v[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int c = threadIdx.x + Cfg::NT * q;
+      v[q] = *reinterpret_cast<const uint4 *>(stage + (c >> 5) * LDH + (c & 31) * 8);
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int c = threadIdx.x + Cfg::NT * q;
+      const int ls = c >> 5;
+      const int m = m0 + (ls >> 5) * Cfg::WTM + 32 * i + (ls & 31);
+      *reinterpret_cast<uint4 *>(dz + (int64_t)m * cw + n0 + (c & 31) * 8) = v[q];
+    }
+    __syncthreads();
+  }
 }
 
 int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
