@@ -27,6 +27,11 @@ struct EpArgs {
 
 using gemm_core::f32x16_t;
 
+// LDS stages of the staged GEMM kernels (128 KB).  A fifth stage (the whole
+// 160 KB, copies four k-steps ahead) measured no faster: the copies are bound
+// by the rate of 64-byte row requests, not by how far ahead they run.
+constexpr int kStages = 4;
+
 // A second reduction segment with the operand layouts of the first:
 // C = A B + A2 B2 over k in [0, K) and [0, K2).
 struct Seg2 {
@@ -116,10 +121,12 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   f32x16_t acc[Cfg::TM][Cfg::TN];
   if constexpr (STAGED && Cfg::NT == 256) {
     static_assert(!SEG2, "the staged loops take one segment");
-    gemm_core::mainloop4s<A_K, B_K>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+    gemm_core::mainloop4s<A_K, B_K, SM::kStages>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend,
+                                                 sm);
   } else if constexpr (STAGED) {
     static_assert(!SEG2, "the staged loops take one segment");
-    gemm_core::mainloop8s<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
+    gemm_core::mainloop8s<A_K, B_K, Cfg, SM::kStages>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg,
+                                                      kend, sm);
   } else {
     static_assert(Cfg::NT == 512, "8-wave tile");
     gemm_core::mainloop<A_K, B_K, Cfg>(acc, A, lda, B, ldb, M, N, m0, n0, kbeg, kend, sm);
@@ -227,7 +234,7 @@ template <bool A_K, bool B_K>
 __global__ __launch_bounds__(gemm_core::Cfg::NT, 1) void gemm_mfma_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K> sm;
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K, kStages> sm;
   gemm_tile<A_K, B_K, gemm_core::Cfg, false, true>(M, N, K, k_per_split, A, lda, B, ldb, ep,
                                                    partial, sm);
 }
@@ -238,7 +245,7 @@ template <bool A_K, bool B_K>
 __global__ __launch_bounds__(gemm_core::Cfg4::NT, 1) void gemm_mfma4s_kernel(
     int M, int N, int K, int k_per_split, const bf16_t *A, int64_t lda, const bf16_t *B,
     int64_t ldb, EpArgs ep, float *partial) {
-  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K> sm;
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<A_K, B_K, kStages> sm;
   gemm_tile<A_K, B_K, gemm_core::Cfg4, false, true>(M, N, K, k_per_split, A, lda, B, ldb, ep,
                                                     partial, sm);
 }

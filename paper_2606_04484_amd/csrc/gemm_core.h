@@ -335,10 +335,13 @@ struct Copier32 {
   }
 };
 
-template <bool A_K, bool B_K>
+// S stages of a 32-wide k-step (16 KB per operand each): four fill the
+// common 128 KB, five the whole 160 KB of a gfx950 CU.
+template <bool A_K, bool B_K, int S = 4>
 struct Smem4s {
-  uint16_t a[4][256 * 32];
-  uint16_t b[4][256 * 32];
+  static constexpr int kStages = S;
+  uint16_t a[S][256 * 32];
+  uint16_t b[S][256 * 32];
 };
 
 // A workgroup barrier without the memory fence of __syncthreads: that fence
@@ -352,12 +355,21 @@ AJ_DEV void bar_nofence() {
   asm volatile("" ::: "memory");
 }
 
-// Waits until at most n k-steps' copies (8 per wave each) are still in flight.
-AJ_DEV void wait_copies(int n) {
-  if (n >= 2) __asm__ volatile("s_waitcnt vmcnt(16)" ::: "memory");
-  else if (n == 1) __asm__ volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  else __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+// Waits until at most n k-steps' copies (PER per wave each, n <= 3) are
+// still in flight.
+template <int PER>
+AJ_DEV void wait_steps(int n) {
+  static_assert(PER == 4 || PER == 8, "copies per wave and k-step");
+  switch (n * PER) {
+    case 24: __asm__ volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+    case 16: __asm__ volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    case 12: __asm__ volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+    case 8: __asm__ volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 4: __asm__ volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    default: __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
 }
+AJ_DEV void wait_copies(int n) { wait_steps<8>(n); }
 
 // Fragment reads of one 16-wide slice, issued one after each of the last 8
 // MFMAs of the slice before, in the order B0 A0 B1 B2 B3 A1 A2 A3, so that
@@ -425,7 +437,7 @@ AJ_DEV void read_frag4s(int q, bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint1
 // the k-step's closing wait and barrier sit after the first 8 MFMAs (this
 // wave's reads of the current stage are all complete by then), so that the
 // reads of the next k-step's first slice, from as / bs, overlap the last 8.
-template <bool A_K, bool B_K, bool kCopy, bool kRead, bool kBar = false>
+template <bool A_K, bool B_K, bool kCopy, bool kRead, bool kBar = false, int kYoung = 2>
 AJ_DEV void slice4s(f32x16_t (&acc)[4][4], bf16x8_t (&fa)[4], bf16x8_t (&fb)[4],
                     bf16x8_t (&na)[4], bf16x8_t (&nb)[4], const uint16_t *as, const uint16_t *bs,
                     int wm, int wn, int kk_next, const Copier32<A_K> &ca,
@@ -448,8 +460,8 @@ AJ_DEV void slice4s(f32x16_t (&acc)[4][4], bf16x8_t (&fa)[4], bf16x8_t (&fb)[4],
       else cb.issue_one(t - Copier32<A_K>::kInstr, lb, tb);
     }
     if (kBar && t == 7) {
-      // the next k-step's copies have landed (those of the two after it may fly)
-      wait_copies(2);
+      // the next k-step's copies have landed (those of the kYoung after it may fly)
+      wait_copies(kYoung);
       bar_nofence();
     }
     if (kRead && t >= 8) read_frag4s<A_K, B_K>(t - 8, na, nb, as, bs, wm, wn, kk_next);
@@ -457,14 +469,15 @@ AJ_DEV void slice4s(f32x16_t (&acc)[4][4], bf16x8_t (&fa)[4], bf16x8_t (&fb)[4],
   }
 }
 
-template <bool A_K, bool B_K>
+template <bool A_K, bool B_K, int S>
 AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, const bf16_t *B,
                        int64_t ldb, int M, int N, int m0, int n0, int kbeg, int kend,
-                       Smem4s<A_K, B_K> &sm) {
+                       Smem4s<A_K, B_K, S> &sm) {
   using TA = Tile32<A_K>;
   using TB = Tile32<B_K>;
   static_assert(Copier32<A_K>::kInstr + Copier32<B_K>::kInstr == 8, "copies per k-step");
-  constexpr int BK = 32;
+  static_assert(S == 4 || S == 5, "stages");
+  constexpr int BK = 32, AHEAD = S - 1;   // copies run AHEAD k-steps before their products
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int nfull = kend > kbeg ? (kend - kbeg) / BK : 0;
   const int wave = threadIdx.x >> 6;
@@ -484,7 +497,7 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
   const bf16_t *tb = B + (B_K ? (int64_t)n0 * ldb + kbeg : (int64_t)kbeg * ldb + n0);
   // all 8 copies of k-step kt (< nk) into its stage
   auto copy_step = [&](int kt) {
-    const int st = kt & 3;
+    const int st = kt % S;
     if (kt < nfull) {
 #pragma unroll
       for (int q = 0; q < Copier32<A_K>::kInstr; ++q) ca.issue_one(q, sm.a[st], ta + kt * ca.step);
@@ -496,39 +509,43 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
     }
   };
   bf16x8_t f0a[4], f0b[4], f1a[4], f1b[4];
-  const int pro = nk < 3 ? nk : 3;
+  const int pro = nk < AHEAD ? nk : AHEAD;
   for (int kt = 0; kt < pro; ++kt) copy_step(kt);
   wait_copies(pro - 1);
   bar_nofence();
-  auto read_first = [&](int kt) {
-    const int st = kt & 3;
+  auto read_first = [&](int st) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) read_frag4s<A_K, B_K>(q, f0a, f0b, sm.a[st], sm.b[st], wm, wn, 0);
   };
   read_first(0);
-  int kt = 0;
-  // steady state: the k-step three ahead is a full one, copied in the first slice
-  for (; kt + 3 < nfull; ++kt) {
-    const int st = kt & 3, nx = (kt + 3) & 3;
+  int kt = 0, st = 0;   // st = kt % S
+  // steady state: the k-step AHEAD on is a full one, copied in the first slice
+  for (; kt + AHEAD < nfull; ++kt) {
+    const int nx = st == 0 ? S - 1 : st - 1;   // (kt + AHEAD) % S
+    const int s1 = st == S - 1 ? 0 : st + 1;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
     slice4s<A_K, B_K, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, sm.a[nx],
-                                  sm.b[nx], ta + (kt + 3) * ca.step, tb + (kt + 3) * cb.step);
-    const int s1 = (kt + 1) & 3;
-    slice4s<A_K, B_K, false, true, true>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1], wm, wn, 0,
-                                         ca, cb, nullptr, nullptr, nullptr, nullptr);
+                                  sm.b[nx], ta + (kt + AHEAD) * ca.step,
+                                  tb + (kt + AHEAD) * cb.step);
+    slice4s<A_K, B_K, false, true, true, AHEAD - 1>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1],
+                                                    wm, wn, 0, ca, cb, nullptr, nullptr, nullptr,
+                                                    nullptr);
+    st = s1;
   }
-  // the last three k-steps (the last may be ragged, its copies bounded)
+  // the last AHEAD k-steps (the last may be ragged, its copies bounded)
   for (; kt < nk; ++kt) {
-    const int st = kt & 3;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
-    if (kt + 3 < nk) copy_step(kt + 3);
+    if (kt + AHEAD < nk) copy_step(kt + AHEAD);
     slice4s<A_K, B_K, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb, nullptr,
                                    nullptr, nullptr, nullptr);
     slice4s<A_K, B_K, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb, nullptr,
                                     nullptr, nullptr, nullptr);
-    wait_copies((kt + 2 < nk) + (kt + 3 < nk));
+    // k-step kt+1 must have landed; those after it (up to kt+AHEAD) may fly
+    const int last = kt + AHEAD < nk - 1 ? kt + AHEAD : nk - 1;
+    wait_copies(last > kt + 1 ? last - kt - 1 : 0);
     bar_nofence();
-    if (kt + 1 < nk) read_first(kt + 1);
+    st = st == S - 1 ? 0 : st + 1;
+    if (kt + 1 < nk) read_first(st);
   }
 }
 
@@ -540,11 +557,7 @@ AJ_DEV void mainloop4s(f32x16_t (&acc)[4][4], const bf16_t *A, int64_t lda, cons
 // closing wait and barrier the 4th MFMA of its second, and the next slice's
 // TM + TN fragment reads are spread over the last 4 (two waves per SIMD cover
 // each other's waits, so the slices wait for their fragments as a whole).
-AJ_DEV void wait_copies8(int n) {   // 4 copies per wave per k-step
-  if (n >= 2) __asm__ volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  else if (n == 1) __asm__ volatile("s_waitcnt vmcnt(4)" ::: "memory");
-  else __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-}
+AJ_DEV void wait_copies8(int n) { wait_steps<4>(n); }   // 4 copies per wave per k-step
 
 template <bool A_K, bool B_K, typename C>
 AJ_DEV void read_frag8s(int q, bf16x8_t (&na)[C::TM], bf16x8_t (&nb)[C::TN], const uint16_t *as,
@@ -553,7 +566,8 @@ AJ_DEV void read_frag8s(int q, bf16x8_t (&na)[C::TM], bf16x8_t (&nb)[C::TN], con
   else nb[q - C::TM] = Tile32<B_K, 8>::frag(bs, wn * C::WTN + (q - C::TM) * 32, kk);
 }
 
-template <bool A_K, bool B_K, typename C, bool kCopy, bool kRead, bool kBar = false>
+template <bool A_K, bool B_K, typename C, bool kCopy, bool kRead, bool kBar = false,
+          int kYoung = 2>
 AJ_DEV void slice8s(f32x16_t (&acc)[C::TM][C::TN], const bf16x8_t (&fa)[C::TM],
                     const bf16x8_t (&fb)[C::TN], bf16x8_t (&na)[C::TM], bf16x8_t (&nb)[C::TN],
                     const uint16_t *as, const uint16_t *bs, int wm, int wn, int kk_next,
@@ -570,7 +584,7 @@ AJ_DEV void slice8s(f32x16_t (&acc)[C::TM][C::TN], const bf16x8_t (&fa)[C::TM],
       else cb.issue_one(t - Copier32<A_K, 8>::kInstr, lb, tb);
     }
     if (kBar && t == 3) {
-      wait_copies8(2);
+      wait_copies8(kYoung);
       bar_nofence();
     }
     if (kRead && t >= 4) {
@@ -582,17 +596,18 @@ AJ_DEV void slice8s(f32x16_t (&acc)[C::TM][C::TN], const bf16x8_t (&fa)[C::TM],
   }
 }
 
-template <bool A_K, bool B_K, typename C>
+template <bool A_K, bool B_K, typename C, int S>
 AJ_DEV void mainloop8s(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t lda,
                        const bf16_t *B, int64_t ldb, int M, int N, int m0, int n0, int kbeg,
-                       int kend, Smem4s<A_K, B_K> &sm) {
+                       int kend, Smem4s<A_K, B_K, S> &sm) {
   static_assert(C::NT == 512 && C::TM * C::TN == 8, "8 waves of 8 MFMA tiles");
+  static_assert(S == 4 || S == 5, "stages");
   using TA = Tile32<A_K, 8>;
   using TB = Tile32<B_K, 8>;
   using CA = Copier32<A_K, 8>;
   using CB = Copier32<B_K, 8>;
   static_assert(CA::kInstr + CB::kInstr == 4, "copies per k-step");
-  constexpr int BK = 32;
+  constexpr int BK = 32, AHEAD = S - 1;
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int nfull = kend > kbeg ? (kend - kbeg) / BK : 0;
   const int wave = threadIdx.x >> 6;
@@ -611,7 +626,7 @@ AJ_DEV void mainloop8s(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t l
   const bf16_t *ta = A + (A_K ? (int64_t)m0 * lda + kbeg : (int64_t)kbeg * lda + m0);
   const bf16_t *tb = B + (B_K ? (int64_t)n0 * ldb + kbeg : (int64_t)kbeg * ldb + n0);
   auto copy_step = [&](int kt) {
-    const int st = kt & 3;
+    const int st = kt % S;
     if (kt < nfull) {
 #pragma unroll
       for (int q = 0; q < CA::kInstr; ++q) ca.issue_one(q, sm.a[st], ta + kt * ca.step);
@@ -623,43 +638,45 @@ AJ_DEV void mainloop8s(f32x16_t (&acc)[C::TM][C::TN], const bf16_t *A, int64_t l
     }
   };
   bf16x8_t f0a[C::TM], f0b[C::TN], f1a[C::TM], f1b[C::TN];
-  auto read_first = [&](int kt) {
-    const int st = kt & 3;
+  auto read_first = [&](int st) {
 #pragma unroll
     for (int q = 0; q < C::TM + C::TN; ++q)
       read_frag8s<A_K, B_K, C>(q, f0a, f0b, sm.a[st], sm.b[st], wm, wn, 0);
   };
-  const int pro = nk < 3 ? nk : 3;
+  const int pro = nk < AHEAD ? nk : AHEAD;
   for (int kt = 0; kt < pro; ++kt) copy_step(kt);
   wait_copies8(pro - 1);
   bar_nofence();
   read_first(0);
-  int kt = 0;
-  for (; kt + 3 < nfull; ++kt) {
-    const int st = kt & 3, nx = (kt + 3) & 3;
+  int kt = 0, st = 0;   // st = kt % S
+  for (; kt + AHEAD < nfull; ++kt) {
+    const int nx = st == 0 ? S - 1 : st - 1;   // (kt + AHEAD) % S
+    const int s1 = st == S - 1 ? 0 : st + 1;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
     frag_wait(f0a, f0b);
     slice8s<A_K, B_K, C, true, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
-                                     sm.a[nx], sm.b[nx], ta + (kt + 3) * ca.step,
-                                     tb + (kt + 3) * cb.step);
+                                     sm.a[nx], sm.b[nx], ta + (kt + AHEAD) * ca.step,
+                                     tb + (kt + AHEAD) * cb.step);
     frag_wait(f1a, f1b);
-    const int s1 = (kt + 1) & 3;
-    slice8s<A_K, B_K, C, false, true, true>(acc, f1a, f1b, f0a, f0b, sm.a[s1], sm.b[s1], wm, wn,
-                                            0, ca, cb, nullptr, nullptr, nullptr, nullptr);
+    slice8s<A_K, B_K, C, false, true, true, AHEAD - 1>(acc, f1a, f1b, f0a, f0b, sm.a[s1],
+                                                       sm.b[s1], wm, wn, 0, ca, cb, nullptr,
+                                                       nullptr, nullptr, nullptr);
+    st = s1;
   }
   for (; kt < nk; ++kt) {
-    const int st = kt & 3;
     const uint16_t *as = sm.a[st], *bs = sm.b[st];
-    if (kt + 3 < nk) copy_step(kt + 3);
+    if (kt + AHEAD < nk) copy_step(kt + AHEAD);
     frag_wait(f0a, f0b);
     slice8s<A_K, B_K, C, false, true>(acc, f0a, f0b, f1a, f1b, as, bs, wm, wn, 16, ca, cb,
                                       nullptr, nullptr, nullptr, nullptr);
     frag_wait(f1a, f1b);
     slice8s<A_K, B_K, C, false, false>(acc, f1a, f1b, f0a, f0b, as, bs, wm, wn, 0, ca, cb,
                                        nullptr, nullptr, nullptr, nullptr);
-    wait_copies8((kt + 2 < nk) + (kt + 3 < nk));
+    const int last = kt + AHEAD < nk - 1 ? kt + AHEAD : nk - 1;
+    wait_copies8(last > kt + 1 ? last - kt - 1 : 0);
     bar_nofence();
-    if (kt + 1 < nk) read_first(kt + 1);
+    st = st == S - 1 ? 0 : st + 1;
+    if (kt + 1 < nk) read_first(st);
   }
 }
 

@@ -313,7 +313,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     ttok[threadIdx.x] = m < n ? tok[tpos[m]] : -1;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop8s<true, true, Cfg>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, true, Cfg, 4>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   // A row of this wave's 128 columns lives in the 32 lanes of a half-wave, 4
@@ -417,7 +417,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     tg[threadIdx.x] = m < n ? g[m] : 0.f;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop8s<true, true, Cfg>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, true, Cfg, 4>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   auto dz_of = [&](float a, int rl, int col) {
