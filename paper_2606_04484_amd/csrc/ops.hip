@@ -210,27 +210,58 @@ __global__ __launch_bounds__(256) void col_reduce_kernel(const float *part, int 
 }
 
 // ---------------------------------------------------------------- RoPE
-// In place on the q and k heads of qkv [n, (Hq+2Hkv)*hd].  Angles are formed
-// in double precision: pos * theta^(-2i/hd) reaches ~7e4 rad.
+// In place on the q and k heads of qkv [n, (Hq+2Hkv)*hd], 4 rotation pairs
+// (i, i + hd/2) per thread.  pos * theta^(-2i/hd) reaches ~1e5 rad, so the
+// angle is formed in double precision as a number of turns and reduced to
+// its fraction, whose sine and cosine are then taken in single precision
+// (|angle| <= pi: error ~2e-7 rad).
+AJ_DEV void load4(const float *p, float (&v)[4]) {
+  const float4 a = *(const float4 *)p;
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+}
+AJ_DEV void load4(const bf16_t *p, float (&v)[4]) {
+  const uint2 u = *(const uint2 *)p;
+  v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+AJ_DEV void store4(float *p, const float (&v)[4]) { *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]); }
+AJ_DEV void store4(bf16_t *p, const float (&v)[4]) {
+  *(uint2 *)p = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kernel(T *qkv, int n, const int32_t *pos, int n_rot_heads,
                                                    int ld, int hd, double log_theta, int inverse) {
-  const int half = hd >> 1;
+  __shared__ double turns_per_pos[64];      // theta^(-2i/hd) / (2 pi), hd <= 128
+  const int half = hd >> 1, q4 = half >> 2;
+  if ((int)threadIdx.x < half)
+    turns_per_pos[threadIdx.x] =
+        exp(-(2.0 * (int)threadIdx.x / hd) * log_theta) * 0.15915494309189535;   // 1 / (2 pi)
+  __syncthreads();
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)n * n_rot_heads * half;
+  const int64_t total = (int64_t)n * n_rot_heads * q4;
   if (idx >= total) return;
-  const int i = (int)(idx % half);
-  const int64_t t = idx / half;
+  const int i0 = (int)(idx % q4) * 4;
+  const int64_t t = idx / q4;
   const int h = (int)(t % n_rot_heads);
   const int row = (int)(t / n_rot_heads);
-  const double ang = (double)pos[row] * exp(-(2.0 * i / hd) * log_theta);
-  double sd, cd;
-  sincos(ang, &sd, &cd);
-  const float c = (float)cd, s = inverse ? -(float)sd : (float)sd;
   T *p = qkv + (int64_t)row * ld + (int64_t)h * hd;
-  const float x1 = ldf(p + i), x2 = ldf(p + i + half);
-  stf(p + i, x1 * c - x2 * s);
-  stf(p + i + half, x2 * c + x1 * s);
+  float x1[4], x2[4], y1[4], y2[4];
+  load4(p + i0, x1);
+  load4(p + i0 + half, x2);
+  const double ps = (double)pos[row];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const double turns = ps * turns_per_pos[i0 + e];
+    const float ang = (float)(turns - rint(turns)) * 6.2831853071795865f;
+    float sn, cs;
+    sincosf(ang, &sn, &cs);
+    if (inverse) sn = -sn;
+    y1[e] = x1[e] * cs - x2[e] * sn;
+    y2[e] = x2[e] * cs + x1[e] * sn;
+  }
+  store4(p + i0, y1);
+  store4(p + i0 + half, y2);
 }
 
 // ---------------------------------------------------------------- SwiGLU
@@ -360,7 +391,7 @@ void rmsnorm_bwd(const float *dy, const T *x, const float *rstd, const T *g, int
 template <typename T>
 void rope(T *qkv, int n, const int32_t *pos, int n_rot_heads, int ld, int hd, float theta,
           bool inverse, hipStream_t s) {
-  const int64_t total = (int64_t)n * n_rot_heads * (hd / 2);
+  const int64_t total = (int64_t)n * n_rot_heads * (hd / 8);   // hd is a multiple of 8
   if (total > 0)
     rope_kernel<T><<<blocks_for(total, 256), 256, 0, s>>>(qkv, n, pos, n_rot_heads, ld, hd,
                                                          log((double)theta), inverse ? 1 : 0);
