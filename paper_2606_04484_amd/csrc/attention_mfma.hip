@@ -211,6 +211,65 @@ AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const uint16_t *tile, const bf1
   }
 }
 
+// Waits until at most n LDS reads (inline assembly, issued in order) are in flight.
+AJ_DEV void lds_wait_n(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt lgkmcnt(2)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
+  }
+}
+
+// One 32-row tile (token rows t0..t0+31) of two staged tiles against the
+// lane's operands: sa += ta rows x ka, sb += tb rows x kb (k = features).
+// Fragments are read two k-steps ahead; each step waits only for its own.
+template <int HD>
+AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, const uint16_t *tb,
+                            int t0, const bf16x8_t (&ka)[HD / 16], const bf16x8_t (&kb)[HD / 16]) {
+  constexpr int KS = HD / 16;
+  bf16x8_t fa[KS], fb[KS];
+#pragma unroll
+  for (int kk = 0; kk < 2 && kk < KS; ++kk) {
+    fa[kk] = TokTile<HD>::row_frag(ta, t0, 16 * kk);
+    fb[kk] = TokTile<HD>::row_frag(tb, t0, 16 * kk);
+  }
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    if (kk + 2 < KS) {
+      fa[kk + 2] = TokTile<HD>::row_frag(ta, t0, 16 * (kk + 2));
+      fb[kk + 2] = TokTile<HD>::row_frag(tb, t0, 16 * (kk + 2));
+    }
+    // reads issued after this step's pair: those of steps kk+1 .. min(kk+2, KS-1)
+    lds_wait_n(2 * ((kk + 2 < KS ? kk + 2 : KS - 1) - kk));
+    asm volatile("" : "+v"(fa[kk]));
+    asm volatile("" : "+v"(fb[kk]));
+    sa = mfma(fa[kk], ka[kk], sa);
+    sb = mfma(fb[kk], kb[kk], sb);
+  }
+}
+
+// acc[i] (features 32i..32i+31) += tile^T x P over tokens t0..t0+31, P given
+// as the two packed accumulator halves of that 32-row tile (pack8 order)
+template <int HD>
+AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const uint16_t *tile, int t0,
+                            const bf16x8_t (&pj)[2]) {
+  constexpr int DT = HD / 32;
+  bf16x8_t f[2][DT];
+#pragma unroll
+  for (int i = 0; i < DT; ++i) f[0][i] = TokTile<HD>::col_frag(tile, 32 * i, t0);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    lds_wait(f[j]);
+    if (j == 0) {
+#pragma unroll
+      for (int i = 0; i < DT; ++i) f[1][i] = TokTile<HD>::col_frag(tile, 32 * i, t0 + 16);
+    }
+#pragma unroll
+    for (int i = 0; i < DT; ++i) acc[i] = mfma(f[j][i], pj[j], acc[i]);
+  }
+}
+
 // ------------------------------------------------------------------ forward
 // One workgroup: 128 queries of one head (4 waves of 32), key tiles of 64
 // double-buffered; a lane owns one query.
@@ -498,60 +557,56 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
     const int buf = it & 1, qb = k0 + kTR * (it % n_qb);
     if (it + 1 < n_it) load_item(it + 1, buf ^ 1);
     if (qb + kTR - 1 >= w_lo && qb <= w_hi) {
-      // S = Q K^T, dP = dO V^T: [64 queries x 32 keys] as two row tiles
-      f32x16_t s[2], dp[2];
+      const bool full = qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke;   // every query sees every key
+      // query rows 32tt..32tt+31 of the tile at a time: S = Q K^T and
+      // dP = dO V^T [32 queries x 32 keys], the softmax terms, then dV^T +=
+      // dO^T P and dK^T += Q^T dS over those 32 queries (not unrolled: one
+      // half's S, dP and softmax terms live at a time)
+#pragma unroll 1
+      for (int tt = 0; tt < 2; ++tt) {
+        f32x16_t s, dp;
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
-      // the lane's 32 query rows: 32tt + 8(r/4) + 4hl + r%4
-      f32x4_t lv[2][4], dl[2][4];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          lv[tt][r4] = lds_read_f4(Ls[buf] + 32 * tt + 8 * r4 + 4 * hl);
-          dl[tt][r4] = lds_read_f4(Dl[buf] + 32 * tt + 8 * r4 + 4 * hl);
-        }
-      // the reads above are inline assembly: wait for them, and pass the
-      // values through empty statements so no use moves above the wait
-      lds_wait();
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+        for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+        // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4
+        f32x4_t lv[4], dl[4];
 #pragma unroll
         for (int r4 = 0; r4 < 4; ++r4) {
-          asm volatile("" : "+v"(lv[tt][r4]));
-          asm volatile("" : "+v"(dl[tt][r4]));
+          lv[r4] = lds_read_f4(Ls[buf] + 32 * tt + 8 * r4 + 4 * hl);
+          dl[r4] = lds_read_f4(Dl[buf] + 32 * tt + 8 * r4 + 4 * hl);
         }
-      rows_times<HD>(s, Qs[buf], kf);
-      rows_times<HD>(dp, Ds[buf], vf);
-      if (qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke) {   // every query sees every key
+        // the reads above are inline assembly: wait for them, and pass the
+        // values through empty statements so no use moves above the wait
+        lds_wait();
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+        for (int r4 = 0; r4 < 4; ++r4) {
+          asm volatile("" : "+v"(lv[r4]));
+          asm volatile("" : "+v"(dl[r4]));
+        }
+        rows_times_pair<HD>(s, dp, Qs[buf], Ds[buf], 32 * tt, kf, vf);
+        if (full) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const float p = fast_exp2(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e);
-            s[tt][r] = p;
-            dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
+            const float p = fast_exp2(s[r] * c - lv[r >> 2][r & 3] * kLog2e);
+            s[r] = p;
+            dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
           }
-      } else {
-        // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
-        const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+        } else {
+          // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
+          const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
             const bool ok = off >= lo && off < hi;
-            const float p = ok ? fast_exp2(s[tt][r] * c - lv[tt][r >> 2][r & 3] * kLog2e) : 0.f;
-            s[tt][r] = p;
-            dp[tt][r] = p * (dp[tt][r] - dl[tt][r >> 2][r & 3]);
+            const float p = ok ? fast_exp2(s[r] * c - lv[r >> 2][r & 3] * kLog2e) : 0.f;
+            s[r] = p;
+            dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
           }
+        }
+        const bf16x8_t pj[2] = {pack8(s, 0), pack8(s, 8)};
+        const bf16x8_t sj[2] = {pack8(dp, 0), pack8(dp, 8)};
+        cols_times_half<HD>(dv, Ds[buf], 32 * tt, pj);       // dV^T += dO^T P
+        cols_times_half<HD>(dk, Qs[buf], 32 * tt, sj);       // dK^T += Q^T dS
       }
-      const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
-      const bf16x8_t sj[4] = {pack8(dp[0], 0), pack8(dp[0], 8), pack8(dp[1], 0), pack8(dp[1], 8)};
-      cols_times<HD>(dv, Ds[buf], pj);                   // dV^T += dO^T P
-      cols_times<HD>(dk, Qs[buf], sj);                   // dK^T += Q^T dS
     }
     lds_wait();
     dma_wait();
