@@ -40,6 +40,7 @@ Saved carve_saved(const aj_block_cfg &c, int n, void *base) {
 struct BwdWs {
   void *dy_t, *ds, *dgu, *dx1_t, *dout, *dqkv;
   float *db, *dx1, *delta, *da, *dg_part, *splitk;
+  size_t splitk_floats;
   size_t bytes;
 };
 
@@ -66,6 +67,7 @@ BwdWs carve_bwd(const aj_block_cfg &c, int n, void *base) {
   sk = std::max(sk, aj::gemm_split_floats((int)d, (int)hq, n));
   sk = std::max(sk, aj::gemm_split_floats((int)q, (int)d, n));
   w.splitk = cv.take<float>(sk > 0 ? sk : 1);
+  w.splitk_floats = sk > 0 ? sk : 1;
   w.bytes = cv.bytes();
   return w;
 }
@@ -96,6 +98,7 @@ struct LoraBwd {
   float *v32;         // [n, r] d_out B
   void *vs;           // [n, r] v
   float *partial;     // split-K partials of dA / dB
+  size_t partial_floats;
 };
 
 int proj_in(const aj_block_cfg &c, int p) {
@@ -147,7 +150,7 @@ size_t carve_lora_bwd(const aj_block_cfg &c, int r, int n, void *base, LoraBwd *
   void *vs = cv.take<char>((int64_t)n * r * es);
   const size_t sk = lora_split_floats(c, r, n);
   float *part = cv.take<float>(sk > 0 ? sk : 1);
-  if (lb) { lb->v32 = v32; lb->vs = vs; lb->partial = part; }
+  if (lb) { lb->v32 = v32; lb->vs = vs; lb->partial = part; lb->partial_floats = sk > 0 ? sk : 1; }
   return cv.bytes();
 }
 
@@ -182,6 +185,7 @@ int lora_grads(const aj_block_cfg &c, const LoraBwd &lb, int p, const T *d_out, 
   g.M = n_out; g.N = r; g.K = n; g.A = d_out; g.lda = n_out; g.a_kmajor = false;
   g.B = lb.u[p]; g.ldb = r; g.b_kmajor = false; g.C = lb.db[p]; g.ldc = r;
   g.out = OUT_ACCUM_F32; g.split_k = lora_split(g.M, g.N, g.K); g.partial = lb.partial;
+  g.partial_cap = lb.partial_floats;
   if ((rc = gemm<T>(g, st))) return rc;
   g = Gemm();   // v [n, r] = (d_out B)_s
   g.M = n; g.N = r; g.K = n_out; g.A = d_out; g.lda = n_out;
@@ -192,6 +196,7 @@ int lora_grads(const aj_block_cfg &c, const LoraBwd &lb, int p, const T *d_out, 
   g.M = r; g.N = k_in; g.K = n; g.A = lb.vs; g.lda = r; g.a_kmajor = false;
   g.B = in; g.ldb = k_in; g.b_kmajor = false; g.C = lb.da[p]; g.ldc = k_in;
   g.out = OUT_ACCUM_F32; g.split_k = lora_split(g.M, g.N, g.K); g.partial = lb.partial;
+  g.partial_cap = lb.partial_floats;
   return gemm<T>(g, st);
 }
 
@@ -286,6 +291,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
     g.M = d; g.N = F; g.K = n; g.A = dy_t; g.lda = d; g.a_kmajor = false;
     g.B = sv.s; g.ldb = F; g.b_kmajor = false; g.C = gr.w_down; g.ldc = F;
     g.out = OUT_ACCUM_F32; g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
+    g.partial_cap = ws.splitk_floats;
     if ((r = gemm<T>(g, st))) return r;
   }
   if (lb && (r = lora_grads<T>(c, *lb, kDown, dy_t, (const T *)sv.s, n, st))) return r;
@@ -301,6 +307,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
     g.M = 2 * F; g.N = d; g.K = n; g.A = ws.dgu; g.lda = 2 * F; g.a_kmajor = false;
     g.B = sv.b; g.ldb = d; g.b_kmajor = false; g.C = gr.w_gate_up; g.ldc = d;
     g.out = OUT_ACCUM_F32; g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
+    g.partial_cap = ws.splitk_floats;
     if ((r = gemm<T>(g, st))) return r;
   }
   if (lb && (r = lora_grads<T>(c, *lb, kGu, (const T *)ws.dgu, (const T *)sv.b, n, st))) return r;
@@ -319,6 +326,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
     g.M = d; g.N = hq; g.K = n; g.A = dx1_t; g.lda = d; g.a_kmajor = false;
     g.B = sv.o; g.ldb = hq; g.b_kmajor = false; g.C = gr.w_o; g.ldc = hq;
     g.out = OUT_ACCUM_F32; g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
+    g.partial_cap = ws.splitk_floats;
     if ((r = gemm<T>(g, st))) return r;
   }
   if (lb && (r = lora_grads<T>(c, *lb, kO, dx1_t, (const T *)sv.o, n, st))) return r;
@@ -337,6 +345,7 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
     g.M = qdim; g.N = d; g.K = n; g.A = ws.dqkv; g.lda = qdim; g.a_kmajor = false;
     g.B = sv.a; g.ldb = d; g.b_kmajor = false; g.C = gr.w_qkv; g.ldc = d;
     g.out = OUT_ACCUM_F32; g.split_k = gemm_split_k(g.M, g.N, g.K); g.partial = ws.splitk;
+    g.partial_cap = ws.splitk_floats;
     if ((r = gemm<T>(g, st))) return r;
   }
   if (lb && (r = lora_grads<T>(c, *lb, kQkv, (const T *)ws.dqkv, (const T *)sv.a, n, st)))

@@ -355,6 +355,9 @@ template <typename T>
 int gemm(const Gemm &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return AJ_OK;
   if (g.split_k > 1 && !g.partial) return fail(AJ_ERR_WORKSPACE, "gemm: split-K without workspace");
+  if (g.split_k > 1 && (size_t)g.split_k * g.M * g.N > g.partial_cap)
+    return fail(AJ_ERR_WORKSPACE, "gemm: split-K %d of %d x %d needs %zu floats, workspace has %zu",
+                g.split_k, g.M, g.N, (size_t)g.split_k * g.M * g.N, g.partial_cap);
   if (g.K2 > 0 && (g.split_k > 1 || !g.A2 || !g.B2))
     return fail(AJ_ERR_UNSUPPORTED, "gemm: a second segment needs its operands and no split-K");
   EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R, 0};

@@ -22,6 +22,7 @@ struct LossWs {
   float *z, *run_m, *run_s, *zt, *part, *g, *dhn, *dg_part;
   float2 *tile_ms;        // fused forward: per (row, 256-column tile) (max, sum of exp), log2 units
   float *splitk;          // split-K partials of the dW_vocab GEMM
+  size_t splitk_floats;
   void *dz;
   int32_t *tpos, *trow;   // targets clamped into the documented range, and their h rows
   size_t bytes;
@@ -46,8 +47,13 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   w.part = cv.take<float>(kFinBlocks * 8);
   w.dhn = cv.take<float>((int64_t)n_tgt * c.d_model);
   w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n_tgt, c.d_model));
-  const size_t sk = aj::gemm_split_floats((int)cw, c.d_model, n_tgt);
+  // the dW_vocab GEMM runs on full chunks and on the last, narrower one:
+  // their split-K factors (tile counts) differ
+  const int64_t last = c.vocab % cw == 0 ? cw : c.vocab % cw;
+  const size_t sk = std::max(aj::gemm_split_floats((int)cw, c.d_model, n_tgt),
+                             aj::gemm_split_floats((int)last, c.d_model, n_tgt));
   w.splitk = cv.take<float>(sk > 0 ? sk : 1);
+  w.splitk_floats = sk > 0 ? sk : 1;
   w.bytes = cv.bytes();
   return w;
 }
@@ -599,6 +605,7 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     g.B = sv.hn; g.ldb = d; g.b_kmajor = false;
     g.C = dwv + (int64_t)c0 * d; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
     g.split_k = aj::gemm_split_k(g.M, g.N, g.K); g.partial = w.splitk;
+    g.partial_cap = w.splitk_floats;
     if ((r = aj::gemm<T>(g, st))) return r;
   }
   aj::rmsnorm_bwd<T>(w.dhn, (const T *)h, sv.rstd, (const T *)gf, n, d, w.trow, 0, 1,

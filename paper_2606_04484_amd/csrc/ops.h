@@ -58,6 +58,7 @@ struct Gemm {
   const void *R = nullptr;     // optional residual, same type/ld as C: C = A B + R
   int split_k = 1;             // > 1: partial sums in `partial`, reduced in fixed order
   float *partial = nullptr;    // split_k * M * N floats (OUT_ACCUM_F32 or c_f32 only)
+  size_t partial_cap = 0;      // floats available at `partial` (checked before any launch)
   bool recompute = false;      // recomputes a forward product: no algorithmic flops
   // optional second reduction segment, same operand layouts, no split-K:
   // C (op) A B + A2 B2 with k in [0, K) and [0, K2)
@@ -68,16 +69,26 @@ struct Gemm {
 template <typename T>
 int gemm(const Gemm &g, hipStream_t s);
 
-// Split-K factor for an M x N output over K: 1 when the 256x256 tiles already
-// cover the 256 CUs, else enough splits for ~1.5-2 waves with K/S >= 4096.
+// Split-K factor for an M x N output over K (K/S >= 4096): with fewer 256x256
+// tiles than CUs, enough splits for ~1.5-2 rounds of 256 workgroups; with
+// more, a split of at most 4 when it fills the last round clearly better
+// (one workgroup per CU: a part-filled round costs a whole one).
 inline int gemm_split_k(int M, int N, int K) {
   const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
-  if (tiles >= 240 || K < 8192) return 1;
-  int S = (448 + tiles - 1) / tiles;
-  const int kmax = K / 4096;
-  if (S > kmax) S = kmax;
-  if (S > 16) S = 16;
-  return S < 1 ? 1 : S;
+  if (K < 8192) return 1;
+  const int kmax = K / 4096 < 16 ? K / 4096 : 16;
+  if (tiles < 240) {
+    const int S = (448 + tiles - 1) / tiles;
+    return S > kmax ? kmax : (S < 1 ? 1 : S);
+  }
+  auto idle = [&](int S) {   // idle fraction of the rounds
+    const long t = (long)tiles * S, slots = (t + 255) / 256 * 256;
+    return (double)(slots - t) / (double)slots;
+  };
+  int best = 1;
+  for (int S = 2; S <= 4 && S <= kmax; ++S)
+    if (idle(S) < idle(best) - 0.08) best = S;
+  return best;
 }
 // Floats of split-K partials gemm() needs for such a GEMM (0 when no split).
 inline size_t gemm_split_floats(int M, int N, int K) {
