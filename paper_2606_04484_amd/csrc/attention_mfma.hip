@@ -169,8 +169,10 @@ AJ_DEV f32x4_t lds_read_f4(const float *p) {
 AJ_DEV void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile) += tile rows x B,
-// B = per-lane operands bv[kk] (k = features 16kk..16kk+15)
-template <int HD>
+// B = per-lane operands bv[kk] (k = features 16kk..16kk+15); with kZero the
+// products start from zero (acc is not read: the first MFMA of each chain
+// takes the constant 0 as its accumulator)
+template <int HD, bool kZero = false>
 AJ_DEV void rows_times(f32x16_t (&acc)[2], const uint16_t *tile, const bf16x8_t (&bv)[HD / 16]) {
   constexpr int KS = HD / 16;
   bf16x8_t f[2][2];
@@ -184,8 +186,9 @@ AJ_DEV void rows_times(f32x16_t (&acc)[2], const uint16_t *tile, const bf16x8_t 
       f[cur ^ 1][0] = TokTile<HD>::row_frag(tile, 0, 16 * (kk + 1));
       f[cur ^ 1][1] = TokTile<HD>::row_frag(tile, 32, 16 * (kk + 1));
     }
-    acc[0] = mfma(f[cur][0], bv[kk], acc[0]);
-    acc[1] = mfma(f[cur][1], bv[kk], acc[1]);
+    const bool fresh = kZero && kk == 0;
+    acc[0] = mfma(f[cur][0], bv[kk], fresh ? f32x16_t{} : acc[0]);
+    acc[1] = mfma(f[cur][1], bv[kk], fresh ? f32x16_t{} : acc[1]);
   }
 }
 
@@ -222,7 +225,8 @@ AJ_DEV void lds_wait_n(int n) {
 }
 
 // One 32-row tile (token rows t0..t0+31) of two staged tiles against the
-// lane's operands: sa += ta rows x ka, sb += tb rows x kb (k = features).
+// lane's operands: sa = ta rows x ka, sb = tb rows x kb (k = features; the
+// incoming sa, sb are not read).
 // Fragments are read two k-steps ahead; each step waits only for its own.
 template <int HD>
 AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, const uint16_t *tb,
@@ -244,8 +248,8 @@ AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, cons
     lds_wait_n(2 * ((kk + 2 < KS ? kk + 2 : KS - 1) - kk));
     asm volatile("" : "+v"(fa[kk]));
     asm volatile("" : "+v"(fb[kk]));
-    sa = mfma(fa[kk], ka[kk], sa);
-    sb = mfma(fb[kk], kb[kk], sb);
+    sa = mfma(fa[kk], ka[kk], kk == 0 ? f32x16_t{} : sa);
+    sb = mfma(fb[kk], kb[kk], kk == 0 ? f32x16_t{} : sb);
   }
 }
 
@@ -327,20 +331,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[tt][r] = 0.f;
-      rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
+      rows_times<HD, true>(s, Ks[buf], qf);              // S^T = K Q^T (unscaled)
       float mx = -INFINITY;
       if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            s[tt][r] *= c;
-            mx = fmaxf(mx, s[tt][r]);
-          }
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[tt][r]);
       } else {
         const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
 #pragma unroll
@@ -348,29 +345,39 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
-            s[tt][r] = (off >= lo && off <= hi) ? s[tt][r] * c : -INFINITY;
+            s[tt][r] = (off >= lo && off <= hi) ? s[tt][r] : -INFINITY;
             mx = fmaxf(mx, s[tt][r]);
           }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m, mx);
-      const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m - mn);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;        // log2 units (c > 0)
+      // The running maximum m moves only when a row's tile maximum exceeds it
+      // by more than 8 (log2 units): the weights exp2(s c - m) then stay
+      // below 2^8, and the rescale of O and the sum runs, for the whole wave,
+      // only when some row needs it.  m is the same stale value in the final
+      // log-sum-exp, so the result is exact.
+      const bool grow = mx > m + 8.f;                      // also when m is still -inf
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float mn = grow ? mx : m;
+        const float alpha = grow ? fast_exp2(m - mn) : 1.f;   // 0 when m was -inf
+#pragma unroll
+        for (int i = 0; i < DT; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+        lsum *= alpha;
+        m = mn;
+      }
       float ls = 0.f;
+      const float nm = -m;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = mn == -INFINITY ? 0.f : fast_exp2(s[tt][r] - mn);
+          const float p = m == -INFINITY ? 0.f : fast_exp2(fmaf(s[tt][r], c, nm));
           s[tt][r] = p;
           ls += p;
         }
       ls += __shfl_xor(ls, 32, 64);
-      lsum = lsum * alpha + ls;
-      m = mn;
-#pragma unroll
-      for (int i = 0; i < DT; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+      lsum += ls;
       const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
       cols_times<HD>(o, Vs[buf], pj);                    // O^T += V^T P^T
     }
@@ -453,12 +460,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2], dp[2];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) { s[tt][r] = 0.f; dp[tt][r] = 0.f; }
-      rows_times<HD>(s, Ks[buf], qf);                    // S^T = K Q^T
-      rows_times<HD>(dp, Vs[buf], df);                   // dP^T = V dO^T
+      rows_times<HD, true>(s, Ks[buf], qf);              // S^T = K Q^T
+      rows_times<HD, true>(dp, Vs[buf], df);             // dP^T = V dO^T
       // key k0 + 4hl + off (off a constant per element) is visible iff
       // lo <= off <= hi
       const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
@@ -564,9 +567,7 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n
       // half's S, dP and softmax terms live at a time)
 #pragma unroll 1
       for (int tt = 0; tt < 2; ++tt) {
-        f32x16_t s, dp;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+        f32x16_t s, dp;   // set by rows_times_pair
         // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4
         f32x4_t lv[4], dl[4];
 #pragma unroll
