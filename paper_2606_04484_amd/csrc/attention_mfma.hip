@@ -444,6 +444,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const float c = a.scale * kLog2e;
   const int w_lo = (int)wave_min_f((float)qs);
   const int w_hi = min(q0 + 32 * w + 31, a.n_tok - 1);
+  const int w_qs = (int)-wave_min_f(-(float)qs);        // latest segment start of the wave
   __syncthreads();
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
@@ -459,22 +460,31 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
       TT::load(Vs[buf ^ 1], vbase, ld, k0 + kTR, kv_hi + 1);
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
-      f32x16_t s[2], dp[2];
-      rows_times<HD, true>(s, Ks[buf], qf);              // S^T = K Q^T
-      rows_times<HD, true>(dp, Vs[buf], df);             // dP^T = V dO^T
-      // key k0 + 4hl + off (off a constant per element) is visible iff
-      // lo <= off <= hi
-      const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
+      const bool full = k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w;   // every key visible to every row
+      // key rows 32tt..32tt+31 of the tile at a time (not unrolled: one
+      // half's S and dP live at a time): S^T = K Q^T, dP^T = V dO^T, the
+      // softmax terms, then dQ^T += K^T dS^T over those 32 keys
+#pragma unroll 1
+      for (int tt = 0; tt < 2; ++tt) {
+        f32x16_t s, dp;   // set by rows_times_pair
+        rows_times_pair<HD>(s, dp, Ks[buf], Vs[buf], 32 * tt, qf, df);
+        if (full) {
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+          for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] - dlt);
+        } else {
+          // key k0 + 4hl + off (off a constant per element) is visible iff
+          // lo <= off <= hi
+          const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
-          const float p = (off >= lo && off <= hi) ? fast_exp2(s[tt][r] * c - lse2) : 0.f;
-          s[tt][r] = p * (dp[tt][r] - dlt);
+          for (int r = 0; r < 16; ++r) {
+            const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+            const float p = (off >= lo && off <= hi) ? fast_exp2(fmaf(s[r], c, -lse2)) : 0.f;
+            s[r] = p * (dp[r] - dlt);
+          }
         }
-      const bf16x8_t sj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
-      cols_times<HD>(acc, Ks[buf], sj);                  // dQ^T += K^T dS^T
+        const bf16x8_t sj[2] = {pack8(s, 0), pack8(s, 8)};
+        cols_times_half<HD>(acc, Ks[buf], 32 * tt, sj);  // dQ^T += K^T dS^T
+      }
     }
     lds_wait();
     dma_wait();
