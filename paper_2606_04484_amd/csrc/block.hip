@@ -297,10 +297,17 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   if (lb && (r = lora_grads<T>(c, *lb, kDown, dy_t, (const T *)sv.s, n, st))) return r;
   g = Gemm();
   g.M = n; g.N = F; g.K = d; g.A = dy_t; g.lda = d;
-  g.B = w.w_down; g.ldb = F; g.b_kmajor = false; g.C = ws.ds; g.ldc = F;
+  g.B = w.w_down; g.ldb = F; g.b_kmajor = false;
   lora_bwd_seg(g, lb, kDown, F);
-  if ((r = gemm<T>(g, st))) return r;
-  swiglu_bwd<T, T>((const T *)ws.ds, (const T *)sv.gu, n, F, (T *)ws.dgu, st);
+  if constexpr (sizeof(T) == 2) {
+    // d gate / d up straight from the float32 d s tile in the GEMM's epilogue
+    g.C = ws.dgu; g.ldc = 2 * F; g.swiglu_gu = sv.gu;
+    if ((r = gemm<T>(g, st))) return r;
+  } else {
+    g.C = ws.ds; g.ldc = F;
+    if ((r = gemm<T>(g, st))) return r;
+    swiglu_bwd<T, T>((const T *)ws.ds, (const T *)sv.gu, n, F, (T *)ws.dgu, st);
+  }
   // gate/up projection
   if (!frozen) {
     g = Gemm();

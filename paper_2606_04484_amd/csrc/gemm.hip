@@ -23,7 +23,15 @@ struct EpArgs {
   int c_f32, accum;
   const void *R;
   int vec;   // 4-column vector stores are aligned (C, R, partial rows)
+  const bf16_t *gu;   // SwiGLU backward: [gate | up] rows (stride ldc), else null
 };
+
+// d gate, d up of one SwiGLU element from d s (float32) and bf16 gate / up
+AJ_DEV void swiglu_grad(float ds, float g, float u, float &dg, float &du) {
+  const float sg = 1.f / (1.f + __expf(-g));
+  dg = ds * u * sg * (1.f + g * (1.f - sg));
+  du = ds * g * sg;
+}
 
 using gemm_core::f32x16_t;
 
@@ -41,7 +49,7 @@ struct Seg2 {
 };
 
 // Output modes of the epilogue's fast path (interior tiles, aligned rows).
-enum { kEpPartial, kEpAccum, kEpF32, kEpF32R, kEpBf16, kEpBf16R };
+enum { kEpPartial, kEpAccum, kEpF32, kEpF32R, kEpBf16, kEpBf16R, kEpSwiglu };
 
 // One pass of the fast epilogue: the 64 staged rows (32 of each wave row)
 // x 256 columns, 4 columns per thread and instruction; every LDS read of the
@@ -73,6 +81,27 @@ AJ_DEV void store_pass(const float *stage, int i, int m0, int n0, int64_t ldo, f
       const float4 w = make_float4(v[q].x + u[q].x, v[q].y + u[q].y, v[q].z + u[q].z,
                                    v[q].w + u[q].w);
       *reinterpret_cast<float4 *>((float *)ep.C + offset(q)) = w;
+    }
+  } else if constexpr (MODE == kEpSwiglu) {
+    uint2 g4[Q], u4[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      g4[q] = *reinterpret_cast<const uint2 *>(ep.gu + offset(q));
+      u4[q] = *reinterpret_cast<const uint2 *>(ep.gu + offset(q) + ep.N);
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const float dsv[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+      const float gv[4] = {__uint_as_float(g4[q].x << 16), __uint_as_float(g4[q].x & 0xffff0000u),
+                           __uint_as_float(g4[q].y << 16), __uint_as_float(g4[q].y & 0xffff0000u)};
+      const float uv[4] = {__uint_as_float(u4[q].x << 16), __uint_as_float(u4[q].x & 0xffff0000u),
+                           __uint_as_float(u4[q].y << 16), __uint_as_float(u4[q].y & 0xffff0000u)};
+      float dg[4], du[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) swiglu_grad(dsv[e], gv[e], uv[e], dg[e], du[e]);
+      bf16_t *cp = (bf16_t *)ep.C + offset(q);
+      *reinterpret_cast<uint2 *>(cp) = make_uint2(f2bf2(dg[0], dg[1]), f2bf2(dg[2], dg[3]));
+      *reinterpret_cast<uint2 *>(cp + ep.N) = make_uint2(f2bf2(du[0], du[1]), f2bf2(du[2], du[3]));
     }
   } else if constexpr (MODE == kEpBf16R) {
     uint2 u[Q];
@@ -148,6 +177,7 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
   const int64_t ldo = partial ? N : ep.ldc;
   const bool fast = ep.vec && m0 + Cfg::BM <= M && n0 + Cfg::BN <= N;
   const int mode = P ? kEpPartial
+                   : ep.gu ? kEpSwiglu
                    : ep.accum ? kEpAccum
                    : ep.c_f32 ? (ep.R ? kEpF32R : kEpF32)
                               : (ep.R ? kEpBf16R : kEpBf16);
@@ -168,6 +198,11 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
         case kEpF32: store_pass<kEpF32, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
         case kEpF32R: store_pass<kEpF32R, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
         case kEpBf16: store_pass<kEpBf16, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
+        case kEpSwiglu:
+          // 8-wave tiles only: in the 4-wave one the extra pass pushes the
+          // epilogue past full unrolling and the accumulator into scratch
+          if constexpr (Cfg::NT == 512) store_pass<kEpSwiglu, Cfg>(stage, i, m0, n0, ldo, P, ep);
+          break;
         default: store_pass<kEpBf16R, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
       }
       __syncthreads();
@@ -181,6 +216,18 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
       if (m >= M || n >= N) continue;
       const float4 v = *reinterpret_cast<const float4 *>(stage + row * LDW + c4);
       const int64_t o = (int64_t)m * ldo + n;
+      if (ep.gu) {
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (n + e >= N) break;
+          float dg, du;
+          swiglu_grad(vv[e], bf2f(ep.gu[o + e]), bf2f(ep.gu[o + e + N]), dg, du);
+          ((bf16_t *)ep.C)[o + e] = f2bf(dg);
+          ((bf16_t *)ep.C)[o + e + N] = f2bf(du);
+        }
+        continue;
+      }
       if (ep.vec && n + 4 <= N) {
         if (P) {
           *reinterpret_cast<float4 *>(P + o) = v;
@@ -321,6 +368,12 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(int M, int N, int K, i
       } else if (ep.c_f32) {
         ((float *)ep.C)[(int64_t)m * ep.ldc + n] =
             v + (ep.R ? ((const float *)ep.R)[(int64_t)m * ep.ldc + n] : 0.f);
+      } else if (ep.gu) {
+        const int64_t o = (int64_t)m * ep.ldc + n;
+        float dg, du;
+        swiglu_grad(v, bf2f(ep.gu[o]), bf2f(ep.gu[o + N]), dg, du);
+        stf((T *)ep.C + o, dg);
+        stf((T *)ep.C + o + N, du);
       } else {
         T *c = (T *)ep.C + (int64_t)m * ep.ldc + n;
         stf(c, v + (ep.R ? ldf((const T *)ep.R + (int64_t)m * ep.ldc + n) : 0.f));
@@ -360,13 +413,19 @@ int gemm(const Gemm &g, hipStream_t s) {
                 g.split_k, g.M, g.N, (size_t)g.split_k * g.M * g.N, g.partial_cap);
   if (g.K2 > 0 && (g.split_k > 1 || !g.A2 || !g.B2))
     return fail(AJ_ERR_UNSUPPORTED, "gemm: a second segment needs its operands and no split-K");
-  EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R, 0};
+  EpArgs ep{g.M, g.N, g.C, g.ldc, g.c_f32 ? 1 : 0, g.out == OUT_ACCUM_F32 ? 1 : 0, g.R, 0,
+            (const bf16_t *)g.swiglu_gu};
+  if (g.swiglu_gu && (sizeof(T) != 2 || g.split_k > 1 || ep.accum || ep.c_f32 || g.R ||
+                      g.ldc < 2 * (int64_t)g.N))
+    return fail(AJ_ERR_UNSUPPORTED, "gemm: SwiGLU epilogue needs bf16 C [n, 2N], no split-K, "
+                "accumulation or residual");
   if (ep.accum) ep.c_f32 = 1;
   {
     const uintptr_t al = ep.c_f32 ? 15 : 7;
     const bool split = g.split_k > 1;
     ep.vec = split ? (g.N % 4 == 0 && ((uintptr_t)g.partial & 15) == 0)
-                   : (g.ldc % 4 == 0 && ((uintptr_t)g.C & al) == 0 && ((uintptr_t)g.R & al) == 0);
+                   : (g.ldc % 4 == 0 && ((uintptr_t)g.C & al) == 0 && ((uintptr_t)g.R & al) == 0 &&
+                      (!g.swiglu_gu || (g.N % 4 == 0 && ((uintptr_t)g.swiglu_gu & 7) == 0)));
   }
   const int S = g.split_k > 1 ? g.split_k : 1;
   int kps = (g.K + S - 1) / S;
@@ -388,7 +447,8 @@ int gemm(const Gemm &g, hipStream_t s) {
     }
   }
   if (mfma) {
-    const bool long_k = kps >= kLongK && g.K2 == 0;   // the second segment runs 8-wave
+    // the second segment and the SwiGLU epilogue run 8-wave
+    const bool long_k = kps >= kLongK && g.K2 == 0 && !g.swiglu_gu;
     int kc = g.a_kmajor ? (g.b_kmajor ? AJ_KC_GEMM_NT : AJ_KC_GEMM_NN) : AJ_KC_GEMM_TN;
     if (long_k) kc += AJ_KC_GEMM4_NT - AJ_KC_GEMM_NT;
     const int tk =

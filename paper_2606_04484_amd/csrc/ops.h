@@ -59,6 +59,11 @@ struct Gemm {
   int split_k = 1;             // > 1: partial sums in `partial`, reduced in fixed order
   float *partial = nullptr;    // split_k * M * N floats (OUT_ACCUM_F32 or c_f32 only)
   size_t partial_cap = 0;      // floats available at `partial` (checked before any launch)
+  // SwiGLU backward in the epilogue (bfloat16 only, no split-K): the product is
+  // d s (N = F columns); with gate g = gu[m][n] and up u = gu[m][F + n] (row
+  // stride ldc = 2F) the epilogue stores d gate = d s u sig(g) (1 + g (1 - sig(g)))
+  // at C[m][n] and d up = d s g sig(g) at C[m][F + n]
+  const void *swiglu_gu = nullptr;
   bool recompute = false;      // recomputes a forward product: no algorithmic flops
   // optional second reduction segment, same operand layouts, no split-K:
   // C (op) A B + A2 B2 with k in [0, K) and [0, K2)
