@@ -41,12 +41,14 @@ def parse():
     return ap.parse_args()
 
 
-# HBM bytes per launch of the dominant kernel, from two rocprofv3 --pmc passes
+# HBM bytes per launch of the dominant kernel (the TN and NN long-reduction
+# GEMMs take nearly the same time per step here, so both are listed), from two rocprofv3 --pmc passes
 # (FETCH_SIZE, WRITE_SIZE) over the same bench command, each scaled by the
 # counter's reading for a plain copy of known size.  Keyed by (kernel class,
 # workload); `sources` are hashed so that a changed kernel reports null.
 TRAFFIC = {
-    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.4e6, "sources": "ad3b1bb9bb792128"},
+    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.7e6, "sources": "7e2861621a20400e"},
+    ("gemm4_nn", "block1.5b-64x8"): {"bytes_per_launch": 5465.2e6, "sources": "7e2861621a20400e"},
 }
 
 

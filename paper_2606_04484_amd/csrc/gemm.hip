@@ -133,6 +133,13 @@ AJ_DEV void store_pass(const float *stage, int i, int m0, int n0, int64_t ldo, f
   }
 }
 
+// LDS writes of the staged rows (or their reads) complete, then a barrier:
+// unlike __syncthreads, the tile's global stores stay in flight.
+AJ_DEV void epi_barrier() {
+  __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  gemm_core::bar_nofence();
+}
+
 // Shared body of the two GEMM kernels: main loop of configuration C (and the
 // second segment's, SEG2), then the epilogue through LDS.
 template <bool A_K, bool B_K, typename Cfg, bool SEG2 = false, bool STAGED = false,
@@ -163,7 +170,7 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
       gemm_core::mainloop<A_K, B_K, Cfg>(acc, s2.A, s2.lda, s2.B, s2.ldb, M, N, m0, n0, 0, s2.K,
                                          sm, false);
   }
-  __syncthreads();
+  epi_barrier();
 
   // Epilogue through LDS, 32 rows of each wave row at a time: the lane's
   // accumulators (column lane%32, rows 8*(r/4) + 4*(lane/32) + r%4 of each
@@ -190,7 +197,7 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
         const int lr = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         stage[lr * LDW + wn * Cfg::WTN + j * 32 + (lane & 31)] = acc[i][j][r];
       }
-    __syncthreads();
+    epi_barrier();
     if (fast) {
       switch (mode) {
         case kEpPartial: store_pass<kEpPartial, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
@@ -205,7 +212,7 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
           break;
         default: store_pass<kEpBf16R, Cfg>(stage, i, m0, n0, ldo, P, ep); break;
       }
-      __syncthreads();
+      epi_barrier();
       continue;
     }
 #pragma unroll 4
@@ -272,7 +279,7 @@ AJ_DEV void gemm_tile(int M, int N, int K, int k_per_split, const bf16_t *A, int
         }
       }
     }
-    __syncthreads();
+    epi_barrier();
   }
 }
 
