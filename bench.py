@@ -193,12 +193,52 @@ def extras(A, merger, cfg, tl, dev, torch, capi, actor, steps):
                     "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
                     "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     del P, G, M1, M2, Pc
+    out["merge_scaled"] = merge_scaled(merger, tl, torch, capi, actor)
     out["text_merge"] = text_merge(A, cfg, torch, capi, actor, steps)
     out["full_model"] = full_model(merger, cfg, torch, capi, actor)
     return out
 
 
 FULL_LAYERS = 28        # decoder blocks of a 1.5B-class model at this block shape
+
+
+def merge_scaled(merger, tl, torch, capi, actor, R=64):
+    """The merge on R copies of the workload's timelines side by side (the
+    episodes are independent, so every count is R times the workload's): at
+    the workload's own size the merge is a chain of short launches whose
+    latency hides its bandwidth; here its bytes dominate."""
+    d0 = merger.tl
+    n_tok, n_tl, n_traj = tl.n_tok, tl.n_tl, tl.n_traj
+    rep = torch.arange(R, device="cuda", dtype=torch.int64)
+    dev = {
+        "traj_tl_off": torch.cat([d0["traj_tl_off"][:1],
+                                  (d0["traj_tl_off"][1:].long()[None, :] + n_tl * rep[:, None])
+                                  .flatten().int()]),
+        "tl_tok_off": torch.cat([d0["tl_tok_off"][:1],
+                                 (d0["tl_tok_off"][1:][None, :] + n_tok * rep[:, None]).flatten()]),
+        "tok": d0["tok"].repeat(R), "flags": d0["flags"].repeat(R),
+        "old_logprob": d0["old_logprob"].repeat(R), "adv": d0["adv"].repeat(R),
+    }
+    big = actor.Merger(dev)
+    for i in range(4):
+        if i == 1:
+            capi.aj_timing_enable(True)
+        big.launch(True)
+    rec = capi.aj_timing_read()
+    capi.aj_timing_enable(False)
+    counts = big.out["counts"].cpu().numpy()
+    base = merger.out["counts"].cpu().numpy()
+    ms = rec["merge"][0] / rec["merge"][1]
+    n_llm = R * int(np.count_nonzero((tl.flags & 3) == 2))
+    mb = 5 * R * n_tok + 8 * n_llm + 17 * int(counts[1]) + 4 * int(counts[2])
+    res = {"copies": R, "unmerged_tokens": R * n_tok, "merged_tokens": int(counts[1]),
+           "counts_match": bool(np.array_equal(counts[:3], R * base[:3])),
+           "ms": round(ms, 4), "algorithmic_MB": round(mb / 1e6, 1),
+           "GB/s": round(mb / (ms * 1e-3) / 1e9, 1),
+           "hbm_frac": round(mb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del big, dev
+    torch.cuda.empty_cache()
+    return res
 
 
 def full_model(merger, cfg, torch, capi, actor):

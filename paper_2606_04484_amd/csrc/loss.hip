@@ -302,6 +302,13 @@ AJ_DEV float row16_sum(float v) {
   return v + dpp<kRowMirror>(v);
 }
 
+// LDS writes (or reads) complete, then a barrier; unlike __syncthreads this
+// does not wait for the workgroup's global stores.
+AJ_DEV void lds_barrier() {
+  __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  gemm_core::bar_nofence();
+}
+
 // logits tile z = hn W^T (rows: targets, columns: 256 vocab ids) reduced in
 // registers: per row, the tile's max and sum of exp (log2 units) and, in the
 // tile that holds it, the target's logit.  Logits never leave the chip.
@@ -369,7 +376,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
   };
   if (n0 + Cfg::BN <= V) epilogue(std::true_type{});
   else epilogue(std::false_type{});
-  __syncthreads();
+  lds_barrier();
   if (threadIdx.x < Cfg::BM && m0 + (int)threadIdx.x < n) {
     float M = -INFINITY, S = 0.f;
 #pragma unroll
@@ -453,7 +460,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
   // wave row), then written 16 bytes per lane.
   constexpr int LDH = Cfg::BN + 8;   // bf16 elements per staged row
   uint16_t *stage = reinterpret_cast<uint16_t *>(&sm);
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i) {
     // the pass's per-row values, read before any staging write
@@ -476,7 +483,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
         stage[ls * LDH + cl] = f2bf(rg[r] * ((cl == rt[r] ? 1.f : 0.f) - p));
       }
     }
-    __syncthreads();
+    lds_barrier();
     constexpr int Q = 128 * (Cfg::BN / 8) / Cfg::NT;   // 16-byte chunks per thread
     uint4 v[Q];
 #pragma unroll
@@ -491,7 +498,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
       const int m = m0 + (ls >> 5) * Cfg::WTM + 32 * i + (ls & 31);
       *reinterpret_cast<uint4 *>(dz + (int64_t)m * cw + n0 + (c & 31) * 8) = v[q];
     }
-    __syncthreads();
+    lds_barrier();
   }
 }
 

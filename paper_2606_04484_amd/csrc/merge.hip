@@ -19,16 +19,18 @@
 //   find_absorber   one workgroup per timeline j: candidates i from the episode's
 //                   last timeline down, prefix compare with early exit
 //   resolve         survivor scan -> segment index, cu_seqlens, counts
-//   claim_fill / claim   llm tokens of absorbed timelines vote (atomicMax of j)
-//                   for the survivor position they land on
-//   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv
+//   claim_fill / claim   llm tokens of absorbed timelines vote (atomicMax of
+//                   their token index, which orders like j) for the survivor
+//                   position they land on (one workgroup per timeline)
+//   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (one
+//                   workgroup per timeline)
 //   tgt_count / tgt_scan / tgt_write / cu_targets   ascending masked targets
 #include "common.h"
 
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kChunk = 1024;          // outputs per workgroup in the target compaction
+constexpr int kChunk = 1024;          // tokens per workgroup in the block-start compaction
 // Offsets that do not tile the input stop the merge (every count 0); bad flag
 // bytes are reported and the token is treated as written (author 3: not llm).
 constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY | AJ_DEVERR_BLOCKS;
@@ -51,7 +53,7 @@ struct MergeArgs {
   // workspace
   int32_t *status;      // [0] error bits seen by this call
   int32_t *tl_seg;      // [n_tl]
-  int32_t *claim;       // [n_tok]
+  int32_t *claim;       // [n_tok] per output position: source token of its log-prob
   int32_t *chunk_cnt;   // [n_chunks]
   int32_t *chunk_off;   // [n_chunks]
   int32_t *user_err;
@@ -76,15 +78,15 @@ AJ_DEV void raise(const MergeArgs &a, int bits) {
   if (a.user_err) atomicOr(a.user_err, bits);
 }
 
-// Largest timeline index i with tl_tok_off[i] <= u (u < n_tok, offsets valid).
-AJ_DEV int find_timeline(const int64_t *off, int n_tl, int64_t u, int lo, int hi) {
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= u) lo = mid; else hi = mid - 1;
-  }
-  // skip empty timelines sharing the offset (none when offsets are valid)
-  while (lo + 1 < n_tl && off[lo + 1] <= u) ++lo;
-  return lo;
+// Timeline handled by workgroup w of a one-per-timeline grid of n.  The
+// hardware deals workgroups round-robin to the 8 XCDs, and episodes have
+// equal turn counts, so w itself would put every episode's last timeline
+// (its survivor) on one XCD; instead each XCD takes a contiguous eighth of
+// the timelines (a bijection on [0, n)).
+AJ_DEV int spread_timeline(int w, int n) {
+  const int per = n / 8, rem = n % 8;
+  const int x = w % 8;
+  return x * per + (x < rem ? x : rem) + w / 8;
 }
 
 // Inclusive block scan of one int per thread; returns the inclusive value, *total
@@ -143,7 +145,7 @@ __global__ void validate_kernel(MergeArgs a) {
 
 // One workgroup per timeline j.
 __global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
-  const int j = blockIdx.x;
+  const int j = spread_timeline(blockIdx.x, a.n_tl);
   if (fatal(a)) {
     if (threadIdx.x == 0) a.absorber[j] = -1;
     return;
@@ -168,13 +170,18 @@ __global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
     bool equal = true;
     for (int64_t base = 0; base < lj; base += 8 * kBlock) {
       int bad = 0;
+      int32_t tj[8], ti[8];
+      uint8_t fj[8], fi[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {   // clamped (lj >= 1): all loads issued together
+        const int64_t p = min(base + r * kBlock + (int64_t)threadIdx.x, lj - 1);
+        tj[r] = a.tok[bj + p]; ti[r] = a.tok[bi + p];
+        fj[r] = a.flags[bj + p]; fi[r] = a.flags[bi + p];
+      }
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
-        int64_t p = base + r * kBlock + threadIdx.x;
-        if (p < lj) {
-          bad |= a.tok[bj + p] != a.tok[bi + p];
-          bad |= ((a.flags[bj + p] ^ a.flags[bi + p]) & AJ_FLAG_BLOCK_START) != 0;
-        }
+        bad |= tj[r] != ti[r];
+        bad |= ((fj[r] ^ fi[r]) & AJ_FLAG_BLOCK_START) != 0;
       }
       if (__syncthreads_or(bad)) { equal = false; break; }
     }
@@ -188,33 +195,45 @@ __global__ void fill_absorber_kernel(MergeArgs a) {
   if (t < a.n_tl) a.absorber[t] = -1;
 }
 
-// Single workgroup of 1024 threads.
+// Single workgroup of 1024 threads, 4 consecutive timelines per thread.
 __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
+  constexpr int kPer = 4;
   __shared__ int carry_seg, carry_tok, carry_max;
   if (threadIdx.x == 0) { carry_seg = 0; carry_tok = 0; carry_max = 0; }
   __syncthreads();
   const bool bad = fatal(a);
-  for (int base = 0; base < a.n_tl; base += 1024) {
-    int i = base + threadIdx.x;
-    int surv = 0, len = 0;
-    if (!bad && i < a.n_tl) {
-      surv = a.absorber[i] < 0;
-      len = surv ? (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]) : 0;
+  for (int base = 0; base < a.n_tl; base += 1024 * kPer) {
+    const int i0 = base + threadIdx.x * kPer;
+    int surv[kPer], len[kPer], ns = 0, nl = 0;
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = i0 + r;
+      surv[r] = 0; len[r] = 0;
+      if (!bad && i < a.n_tl) {
+        surv[r] = a.absorber[i] < 0;
+        len[r] = surv[r] ? (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]) : 0;
+      }
+      ns += surv[r]; nl += len[r];
     }
     int tot_s, tot_l;
-    int is = block_scan_incl<1024>(surv, &tot_s);
-    int il = block_scan_incl<1024>(len, &tot_l);
-    if (i < a.n_tl) {
-      if (surv) {
-        int seg = carry_seg + is - 1;
+    const int is = block_scan_incl<1024>(ns, &tot_s);
+    const int il = block_scan_incl<1024>(nl, &tot_l);
+    int seg = carry_seg + is - ns, tok = carry_tok + il - nl, mx = 0;
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = i0 + r;
+      if (i >= a.n_tl) continue;
+      if (surv[r]) {
         a.tl_seg[i] = seg;
         a.seg_src[seg] = i;
-        a.cu_seqlens[seg] = carry_tok + il - len;
-        atomicMax(&carry_max, len);
+        a.cu_seqlens[seg] = tok;
+        ++seg; tok += len[r];
+        mx = max(mx, len[r]);
       } else {
         a.tl_seg[i] = -1;
       }
     }
+    if (mx) atomicMax(&carry_max, mx);
     __syncthreads();
     if (threadIdx.x == 0) { carry_seg += tot_s; carry_tok += tot_l; }
     __syncthreads();
@@ -229,76 +248,133 @@ __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
 }
 
 __global__ void claim_fill_kernel(MergeArgs a) {
-  int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (o < a.counts[1]) a.claim[o] = -1;
-}
-
-// The WG's tokens span timelines [tl_first, tl_last]; find them once.
-AJ_DEV void wg_timeline_range(const MergeArgs &a, int64_t u0, int *lo, int *hi) {
-  __shared__ int r[2];
-  if (threadIdx.x == 0) {
-    int64_t u1 = u0 + blockDim.x - 1;
-    if (u1 >= a.n_tok) u1 = a.n_tok - 1;
-    r[0] = find_timeline(a.tl_tok_off, a.n_tl, u0, 0, a.n_tl - 1);
-    r[1] = find_timeline(a.tl_tok_off, a.n_tl, u1, r[0], a.n_tl - 1);
+  const int64_t n = a.counts[1];
+  const int64_t o = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (o + 4 <= n && ((uintptr_t)a.claim & 15) == 0) {
+    *reinterpret_cast<int4 *>(a.claim + o) = make_int4(-1, -1, -1, -1);
+  } else {
+    for (int64_t q = o; q < n; ++q) a.claim[q] = -1;
   }
-  __syncthreads();
-  *lo = r[0];
-  *hi = r[1];
 }
 
+// Tokens of timeline i handled by one workgroup, kUnroll per thread at a
+// time (their loads issued together); p is the position in the timeline.
+constexpr int kUnroll = 4;
+
+// One workgroup per timeline: an absorbed timeline's llm tokens vote for the
+// survivor position they land on with their own token index; token offsets
+// grow with the timeline index, so the atomicMax winner is the token of the
+// largest absorbed timeline, the one Algorithm 1 lets write last.  The flag
+// bytes of absorbed timelines are checked here, those of survivors in emit.
 __global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
   if (fatal(a)) return;
-  const int64_t u0 = (int64_t)blockIdx.x * blockDim.x;
-  int lo, hi;
-  wg_timeline_range(a, u0, &lo, &hi);
-  const int64_t u = u0 + threadIdx.x;
-  if (u >= a.n_tok) return;
-  const int i = find_timeline(a.tl_tok_off, a.n_tl, u, lo, hi);
+  const int i = spread_timeline(blockIdx.x, a.n_tl);
   const int s = a.absorber[i];
   if (s < 0) return;
-  if ((a.flags[u] & AJ_AUTHOR_MASK) != AJ_AUTHOR_LLM) return;
-  const int64_t p = u - a.tl_tok_off[i];
-  atomicMax(&a.claim[a.cu_seqlens[a.tl_seg[s]] + p], i);
+  const int64_t b = a.tl_tok_off[i];
+  const int len = (int)(a.tl_tok_off[i + 1] - b);
+  int32_t *dst = a.claim + a.cu_seqlens[a.tl_seg[s]];   // s is a survivor, len_s >= len
+  int bad = 0;
+  for (int p0 = 0; p0 < len; p0 += kUnroll * kBlock) {
+    uint8_t f[kUnroll];
+#pragma unroll
+    for (int r = 0; r < kUnroll; ++r)   // clamped (len >= 1): no branch between the loads
+      f[r] = a.flags[b + min(p0 + r * kBlock + (int)threadIdx.x, len - 1)];
+#pragma unroll
+    for (int r = 0; r < kUnroll; ++r) {
+      const int p = p0 + r * kBlock + (int)threadIdx.x;
+      bad |= p < len && (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
+      if (p < len && (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM) atomicMax(dst + p, (int32_t)(b + p));
+    }
+  }
+  if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
 
+// One workgroup per timeline: a survivor's tokens go to its segment, with
+// the log-prob and advantage of the token that owns each position (its own
+// llm token, else the claim of the largest absorbed timeline).
 __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claims) {
   if (fatal(a)) return;
-  const int64_t u0 = (int64_t)blockIdx.x * blockDim.x;
-  int lo, hi;
-  wg_timeline_range(a, u0, &lo, &hi);
-  const int64_t u = u0 + threadIdx.x;
-  if (u >= a.n_tok) return;
-  const int i = find_timeline(a.tl_tok_off, a.n_tl, u, lo, hi);
-  const uint8_t f = a.flags[u];
-  if ((f & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK) raise(a, AJ_DEVERR_BAD_FLAGS);
+  const int i = spread_timeline(blockIdx.x, a.n_tl);
   if (a.absorber[i] >= 0) return;
-  const int64_t p = u - a.tl_tok_off[i];
-  const int64_t o = a.cu_seqlens[a.tl_seg[i]] + p;
-  int64_t src = -1;
-  if ((f & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM) {
-    src = u;
-  } else if (use_claims) {
-    int c = a.claim[o];
-    if (c >= 0) src = a.tl_tok_off[c] + p;
+  const int64_t b = a.tl_tok_off[i];
+  const int len = (int)(a.tl_tok_off[i + 1] - b);
+  const int64_t o0 = a.cu_seqlens[a.tl_seg[i]];
+  int bad = 0;
+  for (int p0 = 0; p0 < len; p0 += kUnroll * kBlock) {
+    // every load of the step at once: the token's own log-prob and advantage
+    // are read whether or not it is an llm token, so only a claimed position
+    // waits for a second, dependent read
+    uint8_t f[kUnroll];
+    int32_t t[kUnroll], c[kUnroll];
+    float lp[kUnroll], ad[kUnroll];
+#pragma unroll
+    for (int r = 0; r < kUnroll; ++r) {
+      // clamped rather than guarded (len >= 1): no branch between the loads
+      const int p = min(p0 + r * kBlock + (int)threadIdx.x, len - 1);
+      f[r] = a.flags[b + p];
+      t[r] = a.tok[b + p];
+      lp[r] = a.old_logprob[b + p];
+      ad[r] = a.adv[b + p];
+      c[r] = use_claims ? a.claim[o0 + p] : -1;
+    }
+#pragma unroll
+    for (int r = 0; r < kUnroll; ++r) {
+      const int p = p0 + r * kBlock + (int)threadIdx.x;
+      if (p >= len) continue;
+      bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
+      const bool own = (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
+      const bool has = own || c[r] >= 0;
+      if (!own && c[r] >= 0) {
+        lp[r] = a.old_logprob[c[r]];
+        ad[r] = a.adv[c[r]];
+      }
+      const int64_t o = o0 + p;
+      a.otok[o] = t[r];
+      a.opos[o] = p;
+      a.omask[o] = has;
+      a.olp[o] = has ? lp[r] : 0.f;
+      a.oadv[o] = has ? ad[r] : 0.f;
+    }
   }
-  a.otok[o] = a.tok[u];
-  a.opos[o] = (int32_t)p;
-  a.omask[o] = src >= 0;
-  a.olp[o] = src >= 0 ? a.old_logprob[src] : 0.f;
-  a.oadv[o] = src >= 0 ? a.adv[src] : 0.f;
+  if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
 
-AJ_DEV int is_target(const MergeArgs &a, int64_t o, int64_t n_out) {
-  return o < n_out && a.omask[o] && a.opos[o] != 0;
+// Target flags of the kTgtPer outputs from o0 (bit r: output o0 + r is a
+// masked token that is not a segment's first); all loads issued together,
+// 16-byte ones when the outputs are aligned.
+constexpr int kTgtPer = 16;
+constexpr int kTgtChunk = kTgtPer * kBlock;   // outputs per workgroup
+
+AJ_DEV uint32_t target_bits(const MergeArgs &a, int64_t o0, int64_t n_out) {
+  uint32_t bits = 0;
+  if (o0 + kTgtPer <= n_out && ((uintptr_t)a.omask & 15) == 0 && ((uintptr_t)a.opos & 15) == 0) {
+    const uint4 m = *reinterpret_cast<const uint4 *>(a.omask + o0);
+    int4 q[kTgtPer / 4];
+#pragma unroll
+    for (int v = 0; v < kTgtPer / 4; ++v) q[v] = *reinterpret_cast<const int4 *>(a.opos + o0 + 4 * v);
+    const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+    for (int v = 0; v < kTgtPer / 4; ++v) {
+      const int pv[4] = {q[v].x, q[v].y, q[v].z, q[v].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        bits |= (uint32_t)(((mw[v] >> (8 * e)) & 0xff) != 0 && pv[e] != 0) << (4 * v + e);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kTgtPer; ++r) {
+      const int64_t o = o0 + r;
+      if (o < n_out && a.omask[o] && a.opos[o] != 0) bits |= 1u << r;
+    }
+  }
+  return bits;
 }
 
 __global__ __launch_bounds__(kBlock) void tgt_count_kernel(MergeArgs a) {
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
-  const int64_t o0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
-  int c = 0;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) c += is_target(a, o0 + r, n_out);
+  const int64_t o0 = (int64_t)blockIdx.x * kTgtChunk + threadIdx.x * kTgtPer;
+  const int c = __popc(target_bits(a, o0, n_out));
   int tot;
   block_scan_incl<kBlock>(c, &tot);
   if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
@@ -328,16 +404,17 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
 
 __global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
-  const int64_t o0 = (int64_t)blockIdx.x * kChunk + threadIdx.x * 4;
-  int f[4], c = 0;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) { f[r] = is_target(a, o0 + r, n_out); c += f[r]; }
+  const int64_t o0 = (int64_t)blockIdx.x * kTgtChunk + threadIdx.x * kTgtPer;
+  uint32_t bits = target_bits(a, o0, n_out);
+  const int c = __popc(bits);
   int tot;
-  int incl = block_scan_incl<kBlock>(c, &tot);
+  const int incl = block_scan_incl<kBlock>(c, &tot);
   int w = a.chunk_off[blockIdx.x] + incl - c;
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-    if (f[r]) a.targets[w++] = (int32_t)(o0 + r);
+  while (bits) {
+    const int r = __ffs(bits) - 1;
+    a.targets[w++] = (int32_t)(o0 + r);
+    bits &= bits - 1;
+  }
 }
 
 __global__ void cu_targets_kernel(MergeArgs a) {
@@ -672,7 +749,7 @@ MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const 
 
 // The target list and per-segment target offsets, once tok/pos/mask are out.
 void launch_targets(const MergeArgs &a, hipStream_t s) {
-  const int64_t n_chunks = (a.n_tok + kChunk - 1) / kChunk;
+  const int64_t n_chunks = (a.n_tok + kTgtChunk - 1) / kTgtChunk;
   if (a.n_tok > 0) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
   if (a.n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
@@ -704,10 +781,10 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
   if (in->n_tok > 0) {
     const int64_t gtok = (in->n_tok + kBlock - 1) / kBlock;
     if (merge) {
-      claim_fill_kernel<<<gtok, kBlock, 0, s>>>(a);
-      claim_kernel<<<gtok, kBlock, 0, s>>>(a);
+      claim_fill_kernel<<<(gtok + 3) / 4, kBlock, 0, s>>>(a);
+      claim_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
     }
-    emit_kernel<<<gtok, kBlock, 0, s>>>(a, merge ? 1 : 0);
+    emit_kernel<<<in->n_tl, kBlock, 0, s>>>(a, merge ? 1 : 0);
   }
   launch_targets(a, s);
   aj::timing_end(s, tk);

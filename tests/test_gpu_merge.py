@@ -101,3 +101,56 @@ def test_offsets_not_tiling_are_reported():
     from paper_2606_04484_amd.capi import lib  # noqa: F401
     assert m.device_error() & 8
     assert (L.n_seg, L.n_tok, L.n_mask) == (0, 0, 0)
+
+
+def _replicate(tl, R):
+    """R copies of the timelines side by side (host arrays)."""
+    from workloads.gen import Timelines
+    k = np.arange(R, dtype=np.int64)[:, None]
+    traj = np.concatenate([[0], (tl.traj_tl_off[1:][None, :] + k * tl.n_tl).ravel()]).astype(np.int32)
+    tok_off = np.concatenate([[0], (tl.tl_tok_off[1:][None, :] + k * tl.n_tok).ravel()]).astype(np.int64)
+    return Timelines(traj, tok_off, np.tile(tl.tok, R), np.tile(tl.flags, R), np.tile(tl.adv, R),
+                     np.tile(tl.lp_noise, R))
+
+
+def test_replicated_workload():
+    """16 copies of block1.5b-64x8 (19M unmerged tokens): the episodes are
+    independent, so every output is the oracle's merge of one copy, repeated
+    with its offsets shifted; bit-exact."""
+    R = 16
+    base = make_timelines(get_config(1))
+    eps = om.episodes_from_flat(base.traj_tl_off, base.tl_tok_off, base.tok, base.flags,
+                                base.lp_noise, base.adv)
+    ref, absorbers = om.merge_batch(eps)
+    glob = []
+    for e, ab in enumerate(absorbers):
+        b0 = int(base.traj_tl_off[e])
+        glob.extend(a + b0 if a >= 0 else -1 for a in ab)
+    glob = np.asarray(glob, np.int64)
+    tl = _replicate(base, R)
+    print(f"replicated merge: {R} copies, {tl.n_tok} unmerged tokens", flush=True)
+    m, L = _run(tl, tl.lp_noise)
+    o = {k: v.cpu().numpy() for k, v in m.out.items()}
+    k = np.arange(R, dtype=np.int64)[:, None]
+    n_tl, T = base.n_tl, ref.n_tok
+    assert (L.n_seg, L.n_tok) == (R * ref.n_seg, R * T)
+    exp_abs = np.where(glob[None, :] >= 0, glob[None, :] + k * n_tl, -1).ravel()
+    np.testing.assert_array_equal(o["absorber"][:R * n_tl], exp_abs)
+    cu = np.concatenate([(ref.cu_seqlens[:-1][None, :] + k * T).ravel(), [R * T]])
+    np.testing.assert_array_equal(o["cu_seqlens"][:L.n_seg + 1], cu)
+    surv = np.flatnonzero(glob == -1)
+    np.testing.assert_array_equal(o["seg_src"][:L.n_seg], (surv[None, :] + k * n_tl).ravel())
+    n = R * T
+    np.testing.assert_array_equal(o["tok"][:n], np.tile(ref.tok, R))
+    np.testing.assert_array_equal(o["pos"][:n], np.tile(ref.pos, R))
+    np.testing.assert_array_equal(o["mask"][:n], np.tile(ref.mask, R))
+    np.testing.assert_array_equal(o["old_logprob"][:n].astype(np.float64), np.tile(ref.old_logprob, R))
+    np.testing.assert_array_equal(o["adv"][:n].astype(np.float64), np.tile(ref.adv, R))
+    tgt = np.flatnonzero((ref.mask == 1) & (ref.pos != 0))
+    all_t = (tgt[None, :] + k * T).ravel()
+    assert L.n_mask == len(all_t)
+    np.testing.assert_array_equal(o["targets"][:len(all_t)], all_t)
+    np.testing.assert_array_equal(o["cu_targets"][:L.n_seg + 1],
+                                  np.searchsorted(all_t, cu, side="left"))
+    assert L.max_seqlen == int(np.diff(ref.cu_seqlens).max())
+    assert m.device_error() == 0
