@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES three times and exit: the "
                          "reference for scaling the HBM byte counters")
+    ap.add_argument("--merge-scaled-only", action="store_true",
+                    help="only merge the workload and 64 side-by-side copies of it (the "
+                         "merge_scaled extra) and print that record")
     return ap.parse_args()
 
 
@@ -368,6 +371,13 @@ def main():
     m = cfg.model
     torch.cuda.set_device(0)
     tl = make_timelines(cfg)
+    if args.merge_scaled_only:
+        dev = actor.upload_timelines(tl, tl.lp_noise)
+        merger = actor.Merger(dev)
+        merger.launch(True)
+        merger.layout(m.pack_tokens)
+        print(json.dumps({"workload": cfg.name, "merge_scaled": merge_scaled(merger, tl, torch, capi, actor)}))
+        return
     W = make_weights_torch(m, seed=1000, device="cuda")
     # rollout log-probs: the policy's own log-probs (untimed forward of this
     # path on the unmerged layout) plus the generator's N(0, 0.05) noise

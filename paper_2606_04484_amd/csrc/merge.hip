@@ -22,8 +22,8 @@
 //   claim_fill / claim   llm tokens of absorbed timelines vote (atomicMax of
 //                   their token index, which orders like j) for the survivor
 //                   position they land on (one workgroup per timeline)
-//   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (one
-//                   workgroup per timeline)
+//   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (each
+//                   workgroup a range of output positions)
 //   tgt_count / tgt_scan / tgt_write / cu_targets   ascending masked targets
 #include "common.h"
 
@@ -206,13 +206,13 @@ __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
     const int i0 = base + threadIdx.x * kPer;
     int surv[kPer], len[kPer], ns = 0, nl = 0;
 #pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int i = i0 + r;
-      surv[r] = 0; len[r] = 0;
-      if (!bad && i < a.n_tl) {
-        surv[r] = a.absorber[i] < 0;
-        len[r] = surv[r] ? (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]) : 0;
-      }
+    for (int r = 0; r < kPer; ++r) {   // clamped, not guarded: the loads issue together
+      const int i = min(i0 + r, a.n_tl - 1);
+      const bool ok = !bad && i0 + r < a.n_tl;
+      const int ab = a.absorber[i];
+      const int l = (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]);
+      surv[r] = ok && ab < 0;
+      len[r] = surv[r] ? l : 0;
       ns += surv[r]; nl += len[r];
     }
     int tot_s, tot_l;
@@ -290,38 +290,103 @@ __global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
   if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
 
-// One workgroup per timeline: a survivor's tokens go to its segment, with
-// the log-prob and advantage of the token that owns each position (its own
-// llm token, else the claim of the largest absorbed timeline).
+// Largest s in [lo, hi] with cu[s] <= o (cu ascending, cu[lo] <= o), by one
+// wave: 64 probes a step, so a few dependent reads for any segment count.
+AJ_DEV int wave_search(const int32_t *cu, int64_t o, int lo, int hi) {
+  const int lane = threadIdx.x & 63;
+  while (lo < hi) {
+    const int64_t span = (int64_t)hi - lo + 1;
+    const int q = lo + (int)(span * lane / 64);
+    // q ascends with the lane and lane 0 probes lo, so the lanes with
+    // cu[q] <= o are a non-empty prefix
+    const uint64_t m = __ballot(cu[q] <= o);
+    const int l = 63 - __clzll(m);
+    const int nlo = __shfl(q, l, 64);
+    const int nhi = l < 63 ? __shfl(q, l + 1, 64) - 1 : hi;
+    lo = nlo;
+    hi = nhi;
+  }
+  return lo;
+}
+
+// Largest s in [lo, hi] with cu[s] <= o, one thread.
+AJ_DEV int thread_search(const int32_t *cu, int64_t o, int lo, int hi) {
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= o) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Output positions [ob, ob + kEmitSpan) per workgroup step (a grid-stride
+// walk over the merged length, which only the device knows): wave 0 finds
+// the first segment and tabulates the next 64 segments' output and input
+// offsets in LDS; every output then reads its token, the token's own
+// log-prob and advantage and its claim at once, and a claimed position
+// reads the claiming token's.  Work is spread evenly whatever the mix of
+// survivors and absorbed timelines.
+constexpr int kEmitPer = 8;
+constexpr int kEmitSpan = kEmitPer * kBlock;
+constexpr int kEmitWgs = 2048;   // at most 8 workgroups per CU at once
+
 __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claims) {
   if (fatal(a)) return;
-  const int i = spread_timeline(blockIdx.x, a.n_tl);
-  if (a.absorber[i] >= 0) return;
-  const int64_t b = a.tl_tok_off[i];
-  const int len = (int)(a.tl_tok_off[i + 1] - b);
-  const int64_t o0 = a.cu_seqlens[a.tl_seg[i]];
+  const int64_t n_out = a.counts[1];
+  const int n_seg = (int)a.counts[0];
+  __shared__ int32_t seg_cu[65];
+  __shared__ int64_t seg_base[64];
+  __shared__ int seg_first;
+  const int lane = threadIdx.x & 63;
   int bad = 0;
-  for (int p0 = 0; p0 < len; p0 += kUnroll * kBlock) {
-    // every load of the step at once: the token's own log-prob and advantage
-    // are read whether or not it is an llm token, so only a claimed position
-    // waits for a second, dependent read
-    uint8_t f[kUnroll];
-    int32_t t[kUnroll], c[kUnroll];
-    float lp[kUnroll], ad[kUnroll];
+  for (int64_t ob = (int64_t)blockIdx.x * kEmitSpan; ob < n_out;
+       ob += (int64_t)gridDim.x * kEmitSpan) {
+    if (threadIdx.x < 64) {
+      const int s0 = wave_search(a.cu_seqlens, ob, 0, n_seg - 1);
+      const int sl = s0 + lane;
+      seg_cu[lane] = a.cu_seqlens[min(sl, n_seg)];           // cu[n_seg] = n_out
+      if (lane == 0) seg_cu[64] = s0 + 64 <= n_seg ? a.cu_seqlens[s0 + 64] : INT32_MAX;
+      seg_base[lane] = sl < n_seg ? a.tl_tok_off[a.seg_src[sl]] : 0;
+      if (lane == 0) seg_first = s0;
+    }
+    __syncthreads();
+    int64_t u[kEmitPer];
+    int pos[kEmitPer], n_tgt = 0;
 #pragma unroll
-    for (int r = 0; r < kUnroll; ++r) {
-      // clamped rather than guarded (len >= 1): no branch between the loads
-      const int p = min(p0 + r * kBlock + (int)threadIdx.x, len - 1);
-      f[r] = a.flags[b + p];
-      t[r] = a.tok[b + p];
-      lp[r] = a.old_logprob[b + p];
-      ad[r] = a.adv[b + p];
-      c[r] = use_claims ? a.claim[o0 + p] : -1;
+    for (int r = 0; r < kEmitPer; ++r) {
+      const int64_t o = min(ob + r * kBlock + (int64_t)threadIdx.x, n_out - 1);
+      int k;
+      int64_t cs, base;
+      if (o < seg_cu[64]) {
+        k = 0;   // largest k with seg_cu[k] <= o, in LDS
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1)
+          if (k + st < 64 && seg_cu[k + st] <= o) k += st;
+        cs = seg_cu[k];
+        base = seg_base[k];
+      } else {   // more than 64 segments in the span: a search of its own
+        const int sg = thread_search(a.cu_seqlens, o, seg_first + 64, n_seg - 1);
+        cs = a.cu_seqlens[sg];
+        base = a.tl_tok_off[a.seg_src[sg]];
+      }
+      pos[r] = (int)(o - cs);
+      u[r] = base + pos[r];
+    }
+    uint8_t f[kEmitPer];
+    int32_t t[kEmitPer], c[kEmitPer];
+    float lp[kEmitPer], ad[kEmitPer];
+#pragma unroll
+    for (int r = 0; r < kEmitPer; ++r) {
+      const int64_t o = min(ob + r * kBlock + (int64_t)threadIdx.x, n_out - 1);
+      f[r] = a.flags[u[r]];
+      t[r] = a.tok[u[r]];
+      lp[r] = a.old_logprob[u[r]];
+      ad[r] = a.adv[u[r]];
+      c[r] = use_claims ? a.claim[o] : -1;
     }
 #pragma unroll
-    for (int r = 0; r < kUnroll; ++r) {
-      const int p = p0 + r * kBlock + (int)threadIdx.x;
-      if (p >= len) continue;
+    for (int r = 0; r < kEmitPer; ++r) {
+      const int64_t o = ob + r * kBlock + threadIdx.x;
+      if (o >= n_out) continue;
       bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
       const bool own = (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
       const bool has = own || c[r] >= 0;
@@ -329,37 +394,40 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claim
         lp[r] = a.old_logprob[c[r]];
         ad[r] = a.adv[c[r]];
       }
-      const int64_t o = o0 + p;
       a.otok[o] = t[r];
-      a.opos[o] = p;
+      a.opos[o] = pos[r];
       a.omask[o] = has;
       a.olp[o] = has ? lp[r] : 0.f;
       a.oadv[o] = has ? ad[r] : 0.f;
+      n_tgt += has && pos[r] != 0;
     }
+    // the span's target count for the compaction (chunk = span)
+    int tot;
+    block_scan_incl<kBlock>(n_tgt, &tot);
+    if (threadIdx.x == 0) a.chunk_cnt[ob / kEmitSpan] = tot;
   }
   if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
 
 // Target flags of the kTgtPer outputs from o0 (bit r: output o0 + r is a
 // masked token that is not a segment's first); all loads issued together,
-// 16-byte ones when the outputs are aligned.
-constexpr int kTgtPer = 16;
+// vector ones when the outputs are aligned.  kTgtChunk equals emit's span,
+// so emit can count a chunk's targets as it writes them.
+constexpr int kTgtPer = 8;
 constexpr int kTgtChunk = kTgtPer * kBlock;   // outputs per workgroup
+static_assert(kTgtChunk == kEmitSpan, "emit counts the target chunks");
 
 AJ_DEV uint32_t target_bits(const MergeArgs &a, int64_t o0, int64_t n_out) {
   uint32_t bits = 0;
-  if (o0 + kTgtPer <= n_out && ((uintptr_t)a.omask & 15) == 0 && ((uintptr_t)a.opos & 15) == 0) {
-    const uint4 m = *reinterpret_cast<const uint4 *>(a.omask + o0);
-    int4 q[kTgtPer / 4];
+  if (o0 + kTgtPer <= n_out && ((uintptr_t)a.omask & 7) == 0 && ((uintptr_t)a.opos & 15) == 0) {
+    const uint2 m = *reinterpret_cast<const uint2 *>(a.omask + o0);
+    const int4 q0 = *reinterpret_cast<const int4 *>(a.opos + o0);
+    const int4 q1 = *reinterpret_cast<const int4 *>(a.opos + o0 + 4);
+    const int pv[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
 #pragma unroll
-    for (int v = 0; v < kTgtPer / 4; ++v) q[v] = *reinterpret_cast<const int4 *>(a.opos + o0 + 4 * v);
-    const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
-#pragma unroll
-    for (int v = 0; v < kTgtPer / 4; ++v) {
-      const int pv[4] = {q[v].x, q[v].y, q[v].z, q[v].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        bits |= (uint32_t)(((mw[v] >> (8 * e)) & 0xff) != 0 && pv[e] != 0) << (4 * v + e);
+    for (int r = 0; r < 8; ++r) {
+      const uint32_t mb = ((r < 4 ? m.x : m.y) >> (8 * (r & 3))) & 0xff;
+      bits |= (uint32_t)(mb != 0 && pv[r] != 0) << r;
     }
   } else {
 #pragma unroll
@@ -386,12 +454,14 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
   __shared__ int carry;
   if (threadIdx.x == 0) carry = 0;
   __syncthreads();
-  for (int base = 0; base < n_chunks; base += 1024) {
+  // the target compaction counts only chunks that hold outputs
+  const int n_used = blocks ? n_chunks : (int)((a.counts[1] + kTgtChunk - 1) / kTgtChunk);
+  for (int base = 0; base < n_used; base += 1024) {
     int c = base + threadIdx.x;
-    int v = c < n_chunks ? a.chunk_cnt[c] : 0;
+    int v = c < n_used ? a.chunk_cnt[c] : 0;
     int tot;
     int incl = block_scan_incl<1024>(v, &tot);
-    if (c < n_chunks) a.chunk_off[c] = carry + incl - v;
+    if (c < n_used) a.chunk_off[c] = carry + incl - v;
     __syncthreads();
     if (threadIdx.x == 0) carry += tot;
     __syncthreads();
@@ -402,18 +472,22 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
   }
 }
 
+// A grid-stride walk over the chunks that hold outputs (the merged length is
+// known only on the device).
 __global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
-  const int64_t o0 = (int64_t)blockIdx.x * kTgtChunk + threadIdx.x * kTgtPer;
-  uint32_t bits = target_bits(a, o0, n_out);
-  const int c = __popc(bits);
-  int tot;
-  const int incl = block_scan_incl<kBlock>(c, &tot);
-  int w = a.chunk_off[blockIdx.x] + incl - c;
-  while (bits) {
-    const int r = __ffs(bits) - 1;
-    a.targets[w++] = (int32_t)(o0 + r);
-    bits &= bits - 1;
+  for (int64_t ch = blockIdx.x; ch * kTgtChunk < n_out; ch += gridDim.x) {
+    const int64_t o0 = ch * kTgtChunk + threadIdx.x * kTgtPer;
+    uint32_t bits = target_bits(a, o0, n_out);
+    const int c = __popc(bits);
+    int tot;
+    const int incl = block_scan_incl<kBlock>(c, &tot);
+    int w = a.chunk_off[ch] + incl - c;
+    while (bits) {
+      const int r = __ffs(bits) - 1;
+      a.targets[w++] = (int32_t)(o0 + r);
+      bits &= bits - 1;
+    }
   }
 }
 
@@ -748,11 +822,13 @@ MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const 
 }
 
 // The target list and per-segment target offsets, once tok/pos/mask are out.
-void launch_targets(const MergeArgs &a, hipStream_t s) {
+// counted: emit already wrote the per-chunk target counts.
+void launch_targets(const MergeArgs &a, hipStream_t s, bool counted) {
   const int64_t n_chunks = (a.n_tok + kTgtChunk - 1) / kTgtChunk;
-  if (a.n_tok > 0) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  if (a.n_tok > 0 && !counted) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
-  if (a.n_tok > 0) tgt_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
+  if (a.n_tok > 0)
+    tgt_write_kernel<<<(int)(n_chunks < kEmitWgs ? n_chunks : kEmitWgs), kBlock, 0, s>>>(a);
   cu_targets_kernel<<<(a.n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
 }
 
@@ -784,9 +860,10 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
       claim_fill_kernel<<<(gtok + 3) / 4, kBlock, 0, s>>>(a);
       claim_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
     }
-    emit_kernel<<<in->n_tl, kBlock, 0, s>>>(a, merge ? 1 : 0);
+    const int64_t spans = (in->n_tok + kEmitSpan - 1) / kEmitSpan;
+    emit_kernel<<<(int)(spans < kEmitWgs ? spans : kEmitWgs), kBlock, 0, s>>>(a, merge ? 1 : 0);
   }
-  launch_targets(a, s);
+  launch_targets(a, s, true);
   aj::timing_end(s, tk);
   return aj::check_launch(name);
 }
@@ -833,7 +910,7 @@ int run_text(const aj_timelines *in, const aj_block_texts *text, aj_packed *out,
   if (n_blk > 0) place_text_kernel<<<gblk, kBlock, 0, s>>>(a);
   if (in->n_tok > 0)
     emit_text_kernel<<<(in->n_tok + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
-  launch_targets(a, s);
+  launch_targets(a, s, false);
   if (ti && n_blk > 0) ti_kernel<<<n_blk, 64, 0, s>>>(a);
   aj::timing_end(s, tk);
   return aj::check_launch(name);
