@@ -1,8 +1,11 @@
 """GPU merge / flatten against the oracle: bit-exact on every output array.
 
 Covers the hand-worked golden cases, all five seeded workloads at full size
-(merged and unmerged layouts), an empty batch, and offsets that do not tile
-the token range (reported through the device error word, every count 0).
+(merged and unmerged layouts), 16 side-by-side copies of the 1.5B-class
+workload, thousands of episodes whose segments are a few tokens long (many
+segments per output range, several rounds of the survivor scan), an empty
+batch, and offsets that do not tile the token range (reported through the
+device error word, every count 0).
 """
 import numpy as np
 import pytest
@@ -154,3 +157,52 @@ def test_replicated_workload():
                                   np.searchsorted(all_t, cu, side="left"))
     assert L.max_seqlen == int(np.diff(ref.cu_seqlens).max())
     assert m.device_error() == 0
+
+
+def _tiny_timelines(n_ep, seed):
+    """Many episodes of short timelines (1-6 token blocks): merged segments
+    of a few tokens, so one emit range spans far more than 64 segments and
+    the survivor scan runs several rounds; 1 call in 5 rewrites its
+    context."""
+    from workloads.gen import Timelines, FLAG_BLOCK_START
+    rng = np.random.default_rng(seed)
+    traj, tl_off, tok, flags, adv, lp = [0], [0], [], [], [], []
+
+    def block(author):
+        m = int(rng.integers(1, 7))
+        f = np.full(m, author, np.uint8)
+        f[0] |= FLAG_BLOCK_START
+        return list(rng.integers(0, 50, m)), list(f)
+
+    for _ in range(n_ep):
+        n_calls = int(rng.integers(1, 5))
+        ctx_t, ctx_f = block(0)
+        for _c in range(n_calls):
+            if rng.random() < 0.2:
+                ctx_t, ctx_f = block(0)
+            rt, rf = block(2)
+            a = float(rng.normal())
+            tok += ctx_t + rt
+            flags += ctx_f + rf
+            adv += [0.0] * len(ctx_t) + [a] * len(rt)
+            lp += [0.0] * len(ctx_t) + list(rng.normal(-2.0, 0.5, len(rt)))
+            tl_off.append(tl_off[-1] + len(ctx_t) + len(rt))
+            # the next call's context: this one's, its response as context
+            # (author kept), then an observation block
+            ot, of = block(1)
+            ctx_t, ctx_f = ctx_t + rt + ot, ctx_f + rf + of
+        traj.append(traj[-1] + n_calls)
+    tl = Timelines(np.asarray(traj, np.int32), np.asarray(tl_off, np.int64),
+                   np.asarray(tok, np.int32), np.asarray(flags, np.uint8),
+                   np.asarray(adv, np.float32), np.zeros(len(tok), np.float32))
+    return tl, np.asarray(lp, np.float32)
+
+
+@pytest.mark.parametrize("merged", [True, False])
+def test_many_tiny_segments(merged):
+    """~6000 episodes of a few short calls each (segments of ~4-40 tokens,
+    >12000 timelines): bit-exact against the oracle."""
+    tl, lp = _tiny_timelines(6000, seed=7)
+    print(f"tiny segments: {tl.n_traj} episodes, {tl.n_tl} timelines, {tl.n_tok} tokens",
+          flush=True)
+    _check(tl, lp, merged)
