@@ -189,6 +189,10 @@ def test_bf16_text_match():
 BF16_CASES = {
     "hd64_gqa2": dict(hd=64, d=256, hq=4, hkv=2, ff=512, vocab=2000, chunk=768),
     "hd128_gqa3": dict(hd=128, d=384, hq=6, hkv=2, ff=768, vocab=3000, chunk=1024),
+    # d_ff 328: the MLP products end in partial 256-wide tiles (the SwiGLU
+    # backward epilogue on its element-wise edge path) and the down
+    # projection's reduction ends in a ragged 8-wide k-step
+    "hd64_ff328": dict(hd=64, d=256, hq=4, hkv=2, ff=328, vocab=2000, chunk=768),
 }
 
 
