@@ -513,7 +513,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
 // tiles of 64 after the keys, double-buffered (Q, dO and the queries' LSE and
 // delta).
 template <int HD>
-__global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int n_kt) {
+__global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /*n_kt*/) {
   using TT = TokTile<HD>;
   constexpr int KS = HD / 16, DT = HD / 32;
   __shared__ __attribute__((aligned(16))) uint16_t Qs[2][TT::kHalfs];

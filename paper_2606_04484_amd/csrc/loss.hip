@@ -269,17 +269,6 @@ constexpr float kLog2e = 1.4426950408889634f;
 AJ_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float kLn2 = 0.6931471805599453f;
 
-AJ_DEV float half_max(float v) {   // max over the 32 lanes of this half-wave
-#pragma unroll
-  for (int o = 1; o < 32; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-AJ_DEV float half_sum(float v) {
-#pragma unroll
-  for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 // Reductions over each row of 16 lanes on the DPP network (no LDS traffic):
 // swaps within pairs and quads, then the mirrors of 8 and 16 lanes.  Every
 // lane of the row ends with the result.

@@ -56,7 +56,7 @@ AJ_DEV float block_sum(float v, float *red) {
   return s;
 }
 
-__global__ __launch_bounds__(256) void grpo_kernel(int n_groups, const int32_t *off,
+__global__ __launch_bounds__(256) void grpo_kernel(int /*n_groups*/, const int32_t *off,
                                                    const float *reward, float eps, float *adv,
                                                    uint8_t *keep, int32_t *err) {
   __shared__ float red[4];
