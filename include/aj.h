@@ -172,15 +172,38 @@ int aj_merge_timelines_text(const aj_timelines *in, const aj_block_texts *text, 
 int aj_plan_packs(const int32_t *cu_seqlens, int32_t n_seg, int32_t max_tokens,
                   int32_t *pack_seg_off, int32_t *n_packs);
 
-/* ------------------------------------------------------------------ embedding */
-/* x[p] = emb[tok[p]] for p < n_tok; emb [vocab, d], x [n_tok, d] in `dtype`. */
+/* ------------------------------------------------------------------ embedding
+ * The first layer of the policy that scores each sample's tokens (Section 3:
+ * a sample is a token sequence used for policy optimization; Section 4.2,
+ * step (4): the update trains the full model weights, the embedding
+ * included).  The policy's architecture is not given by the paper; the
+ * embedding is the input table of the decoder models it trains (Section 5).
+ */
+/* x[p] = emb[tok[p]] for p < n_tok; emb [vocab, d], x [n_tok, d] in `dtype`.
+ * A token outside [0, vocab) gives a zero row and sets AJ_DEVERR_TOKEN_RANGE
+ * in *err (err may be NULL). */
 int aj_embed_fwd(const int32_t *tok, int32_t n_tok, const void *emb, int32_t d, int32_t vocab,
                  int dtype, void *x, int32_t *err, void *stream);
-/* d_emb[tok[p]] += dx[p] (float32, [vocab, d] and [n_tok, d]). */
+/* Workspace bytes of aj_embed_bwd for n_tok rows of width d. */
+size_t aj_embed_bwd_workspace_bytes(int32_t n_tok, int32_t d);
+/* The embedding gradient: d_emb[v] += sum of dx[p] over the positions p with
+ * tok[p] == v (float32; d_emb [vocab, d], dx [n_tok, d], both 16-byte
+ * aligned, d a multiple of 4, n_tok <= 2^30).  Deterministic: each row of
+ * d_emb receives one addition, the rows of its token summed in ascending
+ * position order (no float atomics), so the result is bit-identical on
+ * every call.  Tokens outside [0, vocab) contribute nothing.  ws: at least
+ * aj_embed_bwd_workspace_bytes(n_tok, d) bytes, else AJ_ERR_WORKSPACE. */
 int aj_embed_bwd(const int32_t *tok, int32_t n_tok, const float *dx, int32_t d, int32_t vocab,
-                 float *d_emb, void *stream);
+                 float *d_emb, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------ 2. block
+ * The policy's forward and backward over the merged samples: Section 4.4.2
+ * (Timeline Merging) merges timelines precisely so that the actor update
+ * does not run the shared prefix of every call again -- each surviving
+ * timeline is one segment, attended causally within itself only -- and
+ * Section 4.2, step (4) then computes the policy-gradient loss and updates
+ * the weights.  The paper trains Qwen-family decoders (Section 5) and gives
+ * no architecture; the block below is that standard decoder layer.
  * One pre-norm decoder block over a pack of segments laid end to end:
  *   a = RMSNorm(x)*g1; q,k,v = a W_qkv^T; rotate-half RoPE on q,k at `pos`
  *   (inverse frequency theta^(-2i/head_dim)); o = causal softmax(q k^T/sqrt(hd)) v
@@ -224,12 +247,21 @@ typedef struct {
 size_t aj_block_saved_bytes(const aj_block_cfg *cfg, int32_t n_tok);
 /* Scratch for either direction. */
 size_t aj_block_workspace_bytes(const aj_block_cfg *cfg, int32_t n_tok, int32_t n_seg);
-/* x, y: [n_tok, d] in cfg->dtype.  `saved` must outlive the matching backward. */
+/* x, y: [n_tok, d] in cfg->dtype.  `saved` (aj_block_saved_bytes) receives
+ * the activations the backward reads and must outlive it; ws: at least
+ * aj_block_workspace_bytes bytes.  Errors: AJ_ERR_NULL for a missing
+ * pointer, AJ_ERR_SHAPE for sizes or offsets out of range or query heads
+ * that do not group evenly over the key/value heads, AJ_ERR_UNSUPPORTED for
+ * a head_dim outside 8..128 (multiple of 8) or another dtype,
+ * AJ_ERR_WORKSPACE for a short workspace. */
 int aj_varlen_block_fwd(const aj_block_cfg *cfg, const aj_block_weights *w, const aj_varlen *vl,
                         const void *x, void *y, void *saved, void *ws, size_t ws_bytes,
                         void *stream);
-/* dy, dx: float32 [n_tok, d] (dx is written, not accumulated; dx may alias dy).
- * x must be the forward's input. */
+/* The gradient of the block: dy, dx float32 [n_tok, d] (dx is written, not
+ * accumulated; dx may alias dy); every weight gradient in g is float32 and
+ * accumulated (+=), summed over tokens in a fixed order (bit-identical on
+ * every call).  x and `saved` must be the forward's.  Errors as the
+ * forward. */
 int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weights *w, const aj_varlen *vl,
                         const void *x, const void *saved, const float *dy, float *dx,
                         const aj_block_grads *g, void *ws, size_t ws_bytes, void *stream);

@@ -198,6 +198,7 @@ class ActorUpdate:
             self.saved = u8(C.aj_lora_saved_bytes(self.bcfg, self.rank, n_tok))
             self.bws = u8(C.aj_lora_workspace_bytes(self.bcfg, self.rank, n_tok))
         self.ckpt = u8(C.aj_stack_ckpt_bytes(self.bcfg, self.n_layers, n_tok))
+        self.ews = u8(C.aj_embed_bwd_workspace_bytes(n_tok, d))
         self.lsaved = u8(C.aj_loss_saved_bytes(self.lcfg, n_tgt))
         self.lws = u8(C.aj_loss_workspace_bytes(self.lcfg, n_tgt))
         self._cap = (n_tok, n_tgt)
@@ -243,7 +244,7 @@ class ActorUpdate:
             if self.lora is None:
                 C.aj_stack_bwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, self.ckpt,
                                self.saved, dh, dh, self.layer_grads, self.bws, base=t0)
-                C.aj_embed_bwd(tok, dh, G["emb"])
+                C.aj_embed_bwd(tok, dh, G["emb"], self.ews)
             else:
                 C.aj_stack_lora_bwd(self.bcfg, self.layers, self.adapters, self.rank, self.scale,
                                     cu, pos, p["max_len"], x, self.ckpt, self.saved, dh, dh,

@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libaj.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["status.cpp", "merge.hip", "ops.hip", "gemm.hip", "attention.hip", "attention_mfma.hip", "block.hip",
+SOURCES = ["status.cpp", "merge.hip", "ops.hip", "embed.hip", "gemm.hip", "attention.hip", "attention_mfma.hip", "block.hip",
            "loss.hip", "update.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-munsafe-fp-atomics",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -114,7 +114,8 @@ EXPORTS = {
                                           C.POINTER(Packed), vp, vp, vp, sz, vp]),
     "aj_plan_packs": (C.c_int, [vp, i32, i32, vp, C.POINTER(i32)]),
     "aj_embed_fwd": (C.c_int, [vp, i32, vp, i32, i32, C.c_int, vp, vp, vp]),
-    "aj_embed_bwd": (C.c_int, [vp, i32, vp, i32, i32, vp, vp]),
+    "aj_embed_bwd_workspace_bytes": (sz, [i32, i32]),
+    "aj_embed_bwd": (C.c_int, [vp, i32, vp, i32, i32, vp, vp, sz, vp]),
     "aj_block_saved_bytes": (sz, [C.POINTER(BlockCfg), i32]),
     "aj_block_workspace_bytes": (sz, [C.POINTER(BlockCfg), i32, i32]),
     "aj_varlen_block_fwd": (C.c_int, [C.POINTER(BlockCfg), C.POINTER(BlockWeights),
@@ -261,9 +262,16 @@ def aj_embed_fwd(tok, emb, x, err=None, stream=None):
            "aj_embed_fwd")
 
 
-def aj_embed_bwd(tok, dx, d_emb, stream=None):
+def aj_embed_bwd_workspace_bytes(n_tok, d):
+    return int(lib().aj_embed_bwd_workspace_bytes(int(n_tok), int(d)))
+
+
+def aj_embed_bwd(tok, dx, d_emb, ws, stream=None):
+    """d_emb[tok[p]] += dx[p] (float32), deterministic; ws: a byte tensor of at least
+    aj_embed_bwd_workspace_bytes(tok.numel(), d) bytes."""
     _check(lib().aj_embed_bwd(ptr(tok), tok.numel(), ptr(dx), d_emb.shape[1], d_emb.shape[0],
-                              ptr(d_emb), stream_handle(stream)), "aj_embed_bwd")
+                              ptr(d_emb), ptr(ws), ws.numel() * ws.element_size(),
+                              stream_handle(stream)), "aj_embed_bwd")
 
 
 # ------------------------------------------------------------------ block

@@ -644,27 +644,3 @@ extern "C" int aj_stack_lora_bwd(const aj_block_cfg *cfg, int32_t n_layers,
   return stack_bwd<float>(*cfg, n_layers, w, *vl, (const float *)x, (float *)ckpt, sv, dy, dx,
                           nullptr, bw, st, lora, g, &la, &lw);
 }
-
-extern "C" int aj_embed_fwd(const int32_t *tok, int32_t n_tok, const void *emb, int32_t d,
-                            int32_t vocab, int dtype, void *x, int32_t *err, void *stream) {
-  AJ_REQUIRE(n_tok >= 0 && d > 0 && vocab > 0, AJ_ERR_SHAPE, "aj_embed_fwd: sizes");
-  if (n_tok == 0) return AJ_OK;
-  AJ_REQUIRE(tok && emb && x, AJ_ERR_NULL, "aj_embed_fwd: null pointer");
-  hipStream_t st = (hipStream_t)stream;
-  if (dtype == AJ_BF16)
-    aj::embed_fwd<bf16_t>(tok, n_tok, (const bf16_t *)emb, d, vocab, (bf16_t *)x, err, st);
-  else if (dtype == AJ_F32)
-    aj::embed_fwd<float>(tok, n_tok, (const float *)emb, d, vocab, (float *)x, err, st);
-  else
-    return aj::fail(AJ_ERR_UNSUPPORTED, "aj_embed_fwd: dtype %d", dtype);
-  return aj::check_launch("aj_embed_fwd");
-}
-
-extern "C" int aj_embed_bwd(const int32_t *tok, int32_t n_tok, const float *dx, int32_t d,
-                            int32_t vocab, float *d_emb, void *stream) {
-  AJ_REQUIRE(n_tok >= 0 && d > 0 && vocab > 0, AJ_ERR_SHAPE, "aj_embed_bwd: sizes");
-  if (n_tok == 0) return AJ_OK;
-  AJ_REQUIRE(tok && dx && d_emb, AJ_ERR_NULL, "aj_embed_bwd: null pointer");
-  aj::embed_bwd(tok, n_tok, dx, d, vocab, d_emb, (hipStream_t)stream);
-  return aj::check_launch("aj_embed_bwd");
-}

@@ -7,8 +7,6 @@ namespace aj {
 template <typename T>
 void embed_fwd(const int32_t *tok, int n, const T *emb, int d, int vocab, T *x, int32_t *err,
                hipStream_t s);
-void embed_bwd(const int32_t *tok, int n, const float *dx, int d, int vocab, float *demb,
-               hipStream_t s);
 
 // out[i] = RMSNorm(x[r]) * g, r = rows ? rows[i] + shift : i; rstd[i] saved.
 template <typename T>

@@ -13,33 +13,6 @@ AJ_DEV float wave_sum(float v) {
   return v;
 }
 
-// ---------------------------------------------------------------- embedding
-template <typename T>
-__global__ __launch_bounds__(256) void embed_fwd_kernel(const int32_t *tok, int n, const T *emb,
-                                                        int d, int vocab, T *x, int32_t *err) {
-  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= n) return;
-  const int t = tok[row];
-  const bool ok = t >= 0 && t < vocab;
-  if (!ok && lane == 0 && err) atomicOr(err, AJ_DEVERR_TOKEN_RANGE);
-  const T *src = emb + (int64_t)(ok ? t : 0) * d;
-  T *dst = x + (int64_t)row * d;
-  for (int c = lane; c < d; c += 64) dst[c] = ok ? src[c] : T(0);
-}
-
-__global__ __launch_bounds__(256) void embed_bwd_kernel(const int32_t *tok, int n, const float *dx,
-                                                        int d, int vocab, float *demb) {
-  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= n) return;
-  const int t = tok[row];
-  if (t < 0 || t >= vocab) return;
-  const float *src = dx + (int64_t)row * d;
-  float *dst = demb + (int64_t)t * d;
-  for (int c = lane; c < d; c += 64) atomicAdd(dst + c, src[c]);
-}
-
 // ---------------------------------------------------------------- RMSNorm
 // One wave per row; lane handles columns 8*(lane + 64*v) + e, v < NV, e < 8,
 // so every access is a 16-byte (bf16) or 32-byte (float) vector.  NV is the
@@ -340,15 +313,6 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 }  // namespace
 
-template <typename T>
-void embed_fwd(const int32_t *tok, int n, const T *emb, int d, int vocab, T *x, int32_t *err,
-               hipStream_t s) {
-  if (n > 0) embed_fwd_kernel<T><<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(tok, n, emb, d, vocab, x, err);
-}
-void embed_bwd(const int32_t *tok, int n, const float *dx, int d, int vocab, float *demb,
-               hipStream_t s) {
-  if (n > 0) embed_bwd_kernel<<<blocks_for(n, kRowsPerBlock), 256, 0, s>>>(tok, n, dx, d, vocab, demb);
-}
 
 // Dispatch on the number of 512-column groups per row (d <= 8192).
 #define AJ_NV_DISPATCH(d, CALL)                      \
@@ -428,8 +392,6 @@ void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumul
 }
 
 #define AJ_INST(T)                                                                              \
-  template void embed_fwd<T>(const int32_t *, int, const T *, int, int, T *, int32_t *,       \
-                             hipStream_t);                                                     \
   template void rmsnorm_fwd<T>(const T *, const T *, int, int, float, const int32_t *, int, T *, \
                                float *, hipStream_t);                                          \
   template void rmsnorm_bwd<T>(const float *, const T *, const float *, const T *, int, int,    \
