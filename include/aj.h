@@ -128,6 +128,22 @@ int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
 int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
                          void *ws, size_t ws_bytes, void *stream);
 
+/* aj_merge_timelines for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  It takes no workspace argument; its workspace is a built-in
+ * device array of aj_merge_noalloc_max_workspace_bytes() bytes (64 MiB), one
+ * per GPU, held until the process ends and reused by every call on that GPU.
+ * Inputs whose aj_merge_workspace_bytes exceeds it are refused with
+ * AJ_ERR_WORKSPACE before anything is enqueued (at most ~16M unmerged tokens).
+ * Outputs, errors and results are those of aj_merge_timelines, bit for bit.
+ * The call allocates nothing (no hipMalloc or hipFree); the first call on a
+ * device looks up that device's copy of the array.  Calls that overlap on
+ * one GPU (several streams or threads at once) share the array and race:
+ * serialise them. */
+size_t aj_merge_noalloc_max_workspace_bytes(void);
+int aj_merge_timelines_noalloc(const aj_timelines *in, aj_packed *out, int32_t *err,
+                               void *stream);
+
 /* ------------------------------------------------------------------ 1b. merge, text-level Match
  * Section 4.4.2, Relaxed Matching Strategies: Match compares the MESSAGE TEXT
  * of aligned blocks instead of their token ids (the paper's default

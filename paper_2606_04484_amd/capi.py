@@ -109,6 +109,8 @@ EXPORTS = {
     "aj_merge_workspace_bytes": (sz, [i32, i32, i64]),
     "aj_merge_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
     "aj_flatten_timelines": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp, sz, vp]),
+    "aj_merge_noalloc_max_workspace_bytes": (sz, []),
+    "aj_merge_timelines_noalloc": (C.c_int, [C.POINTER(Timelines), C.POINTER(Packed), vp, vp]),
     "aj_merge_text_workspace_bytes": (sz, [i32, i32, i64, i32]),
     "aj_merge_timelines_text": (C.c_int, [C.POINTER(Timelines), C.POINTER(BlockTexts),
                                           C.POINTER(Packed), vp, vp, vp, sz, vp]),
@@ -217,6 +219,17 @@ def aj_flatten_timelines(tl, out, err, ws, stream=None):
     _check(lib().aj_flatten_timelines(C.byref(_timelines(tl)), C.byref(_packed(out)), ptr(err),
                                       ptr(ws), ws.numel() * ws.element_size(),
                                       stream_handle(stream)), "aj_flatten_timelines")
+
+
+def aj_merge_noalloc_max_workspace_bytes():
+    return int(lib().aj_merge_noalloc_max_workspace_bytes())
+
+
+def aj_merge_timelines_noalloc(tl, out, err, stream=None):
+    """aj_merge_timelines on the library's built-in per-GPU workspace (no ws argument)."""
+    _check(lib().aj_merge_timelines_noalloc(C.byref(_timelines(tl)), C.byref(_packed(out)),
+                                            ptr(err), stream_handle(stream)),
+           "aj_merge_timelines_noalloc")
 
 
 def aj_merge_text_workspace_bytes(n_traj, n_tl, n_tok, n_blk):

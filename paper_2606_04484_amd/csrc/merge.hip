@@ -25,7 +25,16 @@
 //   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (each
 //                   workgroup a range of output positions)
 //   tgt_count / tgt_scan / tgt_write / cu_targets   ascending masked targets
+#include <mutex>
+
 #include "common.h"
+
+// Workspace of aj_merge_timelines_noalloc: one copy per GPU, held for the
+// life of the process.  Host code never passes this name to a kernel (on
+// the host it is only a stand-in symbol); it uses the device address that
+// hipGetSymbolAddress returns for the current device.
+static constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -943,6 +952,45 @@ extern "C" int aj_merge_timelines(const aj_timelines *in, aj_packed *out, int32_
 extern "C" int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
                                     void *ws, size_t ws_bytes, void *stream) {
   return run(in, out, err, ws, ws_bytes, stream, false);
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on the current device, looked up once per device.
+int scratch_ptr(void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return aj::fail(AJ_ERR_HIP, "aj_merge_timelines_noalloc: no current device (%d)", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return aj::fail(AJ_ERR_HIP, "aj_merge_timelines_noalloc: hipGetSymbolAddress: %s",
+                      hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return AJ_OK;
+}
+}  // namespace
+
+extern "C" size_t aj_merge_noalloc_max_workspace_bytes(void) { return kScratchBytes; }
+
+extern "C" int aj_merge_timelines_noalloc(const aj_timelines *in, aj_packed *out, int32_t *err,
+                                          void *stream) {
+  AJ_REQUIRE(in, AJ_ERR_NULL, "aj_merge_timelines_noalloc: null input");
+  const size_t need = carve(nullptr, in->n_tl, in->n_tok).bytes;
+  AJ_REQUIRE(need <= kScratchBytes, AJ_ERR_WORKSPACE,
+             "aj_merge_timelines_noalloc: %d timelines of %lld tokens need %zu bytes of "
+             "workspace, more than the built-in %zu",
+             in->n_tl, (long long)in->n_tok, need, kScratchBytes);
+  void *ws = nullptr;
+  if (int rc = scratch_ptr(&ws)) return rc;
+  return run(in, out, err, ws, kScratchBytes, stream, true);
 }
 
 extern "C" int aj_plan_packs(const int32_t *cu_seqlens, int32_t n_seg, int32_t max_tokens,
