@@ -6,7 +6,12 @@ timeline merging -> (per pack of <= 131072 tokens) embedding, decoder-block
 forward, fused LM-head / clipped policy-gradient loss forward and backward,
 block backward, embedding backward.  Inputs sit in HBM before timing starts.
 The same batch is also run unmerged (every LLM call its own sample) for the
-merged-vs-unmerged speedup.  Prints one JSON line.
+merged-vs-unmerged speedup.
+
+The headline is the largest workload, long32b-8x60 (the 32B-class block over
+8 episodes of 60 calls); the 1.5B-class, agent-shaped 7B-class and
+multi-agent 7B-class workloads follow as sub-records, merged and unmerged.
+Prints one JSON line on stdout; progress goes to stderr.
 """
 import argparse
 import json
@@ -24,24 +29,40 @@ PEAK_F32_TFLOPS = 157.3        # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
 
 
+HEADLINE = "4"                 # long32b-8x60, the largest single-GPU workload
+SUB_RECORDS = "1,2,3"          # block1.5b-64x8, agent7b-32x10..30, multiagent7b-16x4x12
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="1", help="workload index (0..4) or name")
+    ap.add_argument("--config", default=HEADLINE, help="headline workload index (0..4) or name")
+    ap.add_argument("--unmerged-steps", type=int, default=2,
+                    help="timed unmerged steps of the headline workload (no extra warm-up: the "
+                         "merged run has loaded every kernel)")
+    ap.add_argument("--sub", default=SUB_RECORDS,
+                    help="comma-separated workloads measured as sub-records ('' for none)")
+    ap.add_argument("--sub-steps", type=int, default=2)
+    ap.add_argument("--sub-warmup", type=int, default=1)
     ap.add_argument("--no-unmerged", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the KL / GRPO selection / AdamW measurements")
+                    help="skip the KL / GRPO selection / AdamW / text-merge / full-model / "
+                         "scaled-merge measurements")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES three times and exit: the "
                          "reference for scaling the HBM byte counters")
     ap.add_argument("--merge-scaled-only", action="store_true",
-                    help="only merge the workload and 64 side-by-side copies of it (the "
-                         "merge_scaled extra) and print that record")
+                    help="only run the scaled merge (the agent-shaped workload's 32 episodes "
+                         "repeated to 1024) and print that record")
     return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 # HBM bytes per launch of the dominant kernel (the TN and NN long-reduction
@@ -196,7 +217,6 @@ def extras(A, merger, cfg, tl, dev, torch, capi, actor, steps):
                     "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
                     "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     del P, G, M1, M2, Pc
-    out["merge_scaled"] = merge_scaled(merger, tl, torch, capi, actor)
     out["text_merge"] = text_merge(A, cfg, torch, capi, actor, steps)
     out["full_model"] = full_model(merger, cfg, torch, capi, actor)
     return out
@@ -205,11 +225,13 @@ def extras(A, merger, cfg, tl, dev, torch, capi, actor, steps):
 FULL_LAYERS = 28        # decoder blocks of a 1.5B-class model at this block shape
 
 
-def merge_scaled(merger, tl, torch, capi, actor, R=64):
+def merge_scaled(merger, tl, torch, capi, actor, R=32):
     """The merge on R copies of the workload's timelines side by side (the
     episodes are independent, so every count is R times the workload's): at
-    the workload's own size the merge is a chain of short launches whose
-    latency hides its bandwidth; here its bytes dominate."""
+    a workload's own size the merge is a chain of short launches whose
+    latency hides its bandwidth; here its bytes dominate.  With the
+    agent-shaped 7B-class workload (32 episodes) and R = 32 this is the
+    1024-episode instance of that workload's recipe."""
     d0 = merger.tl
     n_tok, n_tl, n_traj = tl.n_tok, tl.n_tl, tl.n_traj
     rep = torch.arange(R, device="cuda", dtype=torch.int64)
@@ -234,9 +256,11 @@ def merge_scaled(merger, tl, torch, capi, actor, R=64):
     ms = rec["merge"][0] / rec["merge"][1]
     n_llm = R * int(np.count_nonzero((tl.flags & 3) == 2))
     mb = 5 * R * n_tok + 8 * n_llm + 17 * int(counts[1]) + 4 * int(counts[2])
-    res = {"copies": R, "unmerged_tokens": R * n_tok, "merged_tokens": int(counts[1]),
+    res = {"copies": R, "episodes": R * n_traj, "unmerged_tokens": R * n_tok,
+           "merged_tokens": int(counts[1]),
            "counts_match": bool(np.array_equal(counts[:3], R * base[:3])),
-           "ms": round(ms, 4), "algorithmic_MB": round(mb / 1e6, 1),
+           "ms": round(ms, 4), "launches_per_merge": rec["merge"][1] // 3,
+           "algorithmic_MB": round(mb / 1e6, 1),
            "GB/s": round(mb / (ms * 1e-3) / 1e9, 1),
            "hbm_frac": round(mb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     del big, dev
@@ -318,10 +342,23 @@ def text_merge(A, cfg, torch, capi, actor, steps):
     return res
 
 
-def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
-    """The oracle, as is, on a bounded sample of the same workload: the first
-    episode, merged by the oracle, its first `sample_tokens` merged tokens
-    (whole segments, the last one cut)."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, tl, old, W_dev, sample_tokens, all_tl):
+    """The oracle, as is, on a bounded sample of the headline workload: its
+    first episode merged by the oracle, then the float64 actor update on the
+    first `sample_tokens` merged tokens (whole segments, the last one cut);
+    plus the oracle's merge (Algorithm 1, pure Python) timed on every full
+    workload measured in this run."""
     from threadpoolctl import threadpool_info
     from oracle import merge as om
     from oracle import model as M
@@ -329,9 +366,7 @@ def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
     n0 = sub.n_tok
     eps = om.episodes_from_flat(sub.traj_tl_off, sub.tl_tok_off, sub.tok, sub.flags, old[:n0],
                                 sub.adv)
-    t0 = time.perf_counter()
     packed, _ = om.merge_batch(eps)
-    t_merge = time.perf_counter() - t0
     L = min(sample_tokens, packed.n_tok)
     cu = [int(c) for c in packed.cu_seqlens if c < L] + [L]
     cut = om.Packed(cu, packed.tok[:L], packed.mask[:L], packed.old_logprob[:L],
@@ -340,14 +375,161 @@ def cpu_baseline(cfg, tl, old, W_dev, sample_tokens):
     t0 = time.perf_counter()
     M.actor_update(cut, W, cfg.model)
     t_model = time.perf_counter() - t0
+    del W
+    merges = {}
+    for name, t in all_tl.items():
+        e = om.episodes_from_flat(t.traj_tl_off, t.tl_tok_off, t.tok, t.flags, t.lp_noise, t.adv)
+        t0 = time.perf_counter()
+        p, _ = om.merge_batch(e)
+        dt = time.perf_counter() - t0
+        merges[name] = {"unmerged_tokens": int(t.n_tok), "merged_tokens": int(p.n_tok),
+                        "s": round(dt, 3), "unmerged_tokens_per_s": round(t.n_tok / dt, 1)}
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": L / (t_model + t_merge * L / max(n0, 1)), "unit": "tokens/s",
+    return {"value": round(L / t_model, 3), "unit": "tokens/s",
             "cores": int(threads), "kind": "oracle",
-            "sample": f"episode 0 of the same batch merged by the oracle ({n0} unmerged -> "
-                      f"{packed.n_tok} merged tokens, {t_merge:.2f} s), then the float64 actor "
-                      f"update on its first {L} merged tokens ({len(cu) - 1} segments, "
-                      f"{t_model:.1f} s); merge time pro-rated to {L} tokens",
-            "host_cpus": os.cpu_count()}
+            "sample": f"{cfg.name}: episode 0 merged by the oracle ({n0} unmerged -> "
+                      f"{packed.n_tok} merged tokens), then the float64 actor update (forward "
+                      f"+ backward, every gradient) on its first {L} merged tokens "
+                      f"({len(cu) - 1} segments, {t_model:.1f} s)",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "merge_oracle": merges}
+
+
+def rollout_logprobs(A, tl, torch, actor):
+    """Rollout log-probs: the policy's own log-probs (an untimed forward of
+    this path) plus the generator's N(0, 0.05) noise.  The forward runs on the
+    merged layout, whose log-prob of every response token is the unmerged
+    one's; merging with the token index as the log-prob payload carries each
+    target back to its unmerged token."""
+    m = A.m
+    if tl.n_tok < (1 << 24):
+        dev = actor.upload_timelines(tl, np.arange(tl.n_tok, dtype=np.float32))
+        L = actor.merge(dev, merged=True, pack_tokens=m.pack_tokens)
+    else:
+        dev = actor.upload_timelines(tl, np.zeros(tl.n_tok, np.float32))
+        L = actor.merge(dev, merged=False, pack_tokens=m.pack_tokens)
+    cur = A.forward_logprob(L).float().cpu().numpy()
+    tg = L.targets[:L.n_mask].cpu().numpy()
+    src = L.old_logprob[L.targets[:L.n_mask].long()].long().cpu().numpy() \
+        if tl.n_tok < (1 << 24) else tg
+    old = np.zeros(tl.n_tok, np.float32)
+    old[src] = cur + tl.lp_noise[src]
+    return old
+
+
+def measure(cfg, steps, warmup, u_steps, u_warmup, torch, capi, actor, record=False,
+            keep=False):
+    """One workload: merged steps (timed), one recorded step (per-class kernel
+    times), unmerged steps.  Returns the record (and, with keep, the live
+    objects for the extras)."""
+    from workloads import make_timelines, make_weights_torch
+    m = cfg.model
+    tl = make_timelines(cfg)
+    W = make_weights_torch(m, seed=1000, device="cuda")
+    A = actor.ActorUpdate(m, W)
+    old = rollout_logprobs(A, tl, torch, actor)
+    dev = actor.upload_timelines(tl, old)
+    merger = actor.Merger(dev)
+    merger.launch(True)
+    Lm = merger.layout(m.pack_tokens)
+    A.prepare(Lm)
+    log(f"{cfg.name}: {tl.n_tok} -> {Lm.n_tok} tokens, {len(Lm.packs)} packs; "
+        f"{warmup} + {steps} merged steps")
+    Lm, t_m, _ = timed(A, merger, True, steps, warmup, torch, capi)
+    rec = None
+    if record:
+        _, _, rec = timed(A, merger, True, 1, 0, torch, capi, record=True)
+    stats = A.stats.cpu().numpy()
+    blk, lm, att, att_fwd = step_flops(Lm, m)
+    peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_F32_TFLOPS
+    r = {"workload": cfg.name, "merged_tokens": Lm.n_tok, "unmerged_tokens": int(tl.n_tok),
+         "loss_tokens": Lm.n_mask, "segments": Lm.n_seg, "packs": len(Lm.packs),
+         "steps": steps, "warmup": warmup, "ms_per_step": round(t_m * 1e3, 3),
+         "tokens_per_s": round(Lm.n_tok / t_m, 1),
+         "effective_tokens_per_s": round(tl.n_tok / t_m, 1),
+         "loss_tokens_per_s": round(Lm.n_mask / t_m, 1),
+         "mfma_util": round((blk + lm + att) / t_m / 1e12 / peak, 4),
+         "algorithmic_tflop_per_step": {"block": round(blk / 1e12, 3),
+                                        "lm_head": round(lm / 1e12, 3),
+                                        "attention": round(att / 1e12, 3)},
+         "loss": float(stats[0])}
+    if u_steps > 0:
+        mu = actor.Merger(dev)
+        mu.launch(False)
+        Lu = mu.layout(m.pack_tokens)
+        A.prepare(Lu)
+        log(f"{cfg.name}: unmerged {Lu.n_tok} tokens, {len(Lu.packs)} packs; "
+            f"{u_warmup} + {u_steps} steps")
+        Lu, t_u, _ = timed(A, mu, False, u_steps, u_warmup, torch, capi)
+        r["unmerged"] = {"steps": u_steps, "warmup": u_warmup,
+                         "ms_per_step": round(t_u * 1e3, 3), "tokens": Lu.n_tok,
+                         "tokens_per_s": round(Lu.n_tok / t_u, 1), "packs": len(Lu.packs)}
+        r["speedup_vs_unmerged"] = round(t_u / t_m, 3)
+        del mu, Lu
+    log(f"{cfg.name}: merged {t_m * 1e3:.1f} ms/step"
+        + (f", unmerged {r['unmerged']['ms_per_step']:.1f}" if u_steps > 0 else ""))
+    live = dict(tl=tl, W=W, A=A, old=old, dev=dev, merger=merger, Lm=Lm, t_m=t_m, rec=rec,
+                flops=(blk, lm, att, att_fwd), peak=peak)
+    if not keep:
+        for k in ("A", "W", "dev", "merger", "Lm"):
+            live.pop(k)
+        del A, W, dev, merger, Lm
+        torch.cuda.empty_cache()
+    return r, live
+
+
+KERNEL_NAMES = {"gemm_nt": "gemm_mfma_kernel<true, true>",
+                "gemm_nn": "gemm_mfma_kernel<true, false>",
+                "gemm_tn": "gemm_mfma_kernel<false, false>",
+                "gemm4_nt": "gemm_mfma4s_kernel<true, true>",
+                "gemm4_nn": "gemm_mfma4s_kernel<true, false>",
+                "gemm4_tn": "gemm_mfma4s_kernel<false, false>", "attn_fwd": "attn_fwd_mfma_kernel",
+                "lm_fwd": "lm_fwd_fused_kernel", "lm_dz": "lm_dz_fused_kernel"}
+
+
+def roofline(rec, flops, peak, workload):
+    """Per-class kernel times of one step and the dominant kernel against its
+    roofline (HIP events on the launch stream)."""
+    blk, lm, att, att_fwd = flops
+    classes = {}
+    for k, (ms, n, fl) in rec.items():
+        if k == "attn_fwd":
+            fl = att_fwd
+        elif k == "attn_bwd":
+            fl = att - att_fwd
+        classes[k] = dict(ms=ms, launches=n, tflops=(fl / (ms * 1e-3) / 1e12) if ms > 0 else 0.0)
+    # the roofline names one kernel with algorithmic flops: not the multi-kernel
+    # attention backward, not the logits recompute of the LM-head backward
+    dom = max((k for k in classes if k not in ("merge", "attn_bwd", "lm_dz")),
+              key=lambda k: classes[k]["ms"])
+    d = classes[dom]
+    fl_dom = {"attn_fwd": att_fwd}.get(dom, rec[dom][2])
+    roof = {"kernel": KERNEL_NAMES.get(dom, dom), "bound": "mfma",
+            "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(fl_dom / (d["ms"] * 1e-3) / 1e12 / peak, 4),
+            "traffic": None, "launches": d["launches"],
+            "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}
+    tr = TRAFFIC.get((dom, workload))
+    if tr and dom.startswith("gemm") and tr["sources"] == source_hash(GEMM_SOURCES):
+        roof["traffic"] = tr["bytes_per_launch"]
+        roof["traffic_unit"] = "bytes"
+    kc = {k: {kk: round(vv, 4) if isinstance(vv, float) else vv for kk, vv in v.items()}
+          for k, v in classes.items()}
+    return roof, kc
+
+
+def merge_record(rec, tl, Lm):
+    """The merge against HBM: algorithmic bytes = every unmerged token's id and
+    flags, the llm tokens' log-prob and advantage read once; every merged
+    token's id, position, mask, log-prob and advantage and every target written."""
+    if "merge" not in rec or not rec["merge"][1]:
+        return None
+    mms = rec["merge"][0] / rec["merge"][1]
+    n_llm = int(np.count_nonzero((tl.flags & 3) == 2))
+    mb = 5 * tl.n_tok + 8 * n_llm + 17 * Lm.n_tok + 4 * Lm.n_mask
+    return {"ms": round(mms, 4), "algorithmic_MB": round(mb / 1e6, 2),
+            "GB/s": round(mb / (mms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(mb / (mms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def main():
@@ -364,122 +546,90 @@ def main():
     if not os.path.exists(capi.LIB_PATH):
         from paper_2606_04484_amd.build import build
         build()
-    from workloads import get_config, make_timelines, make_weights_torch
+    from workloads import get_config, make_timelines
 
-    key = int(args.config) if args.config.isdigit() else args.config
-    cfg = get_config(key)
-    m = cfg.model
+    key = lambda c: int(c) if c.isdigit() else c
+    cfg = get_config(key(args.config))
     torch.cuda.set_device(0)
-    tl = make_timelines(cfg)
     if args.merge_scaled_only:
+        c = get_config(key(args.config)) if args.config != HEADLINE else get_config(2)
+        tl = make_timelines(c)
         dev = actor.upload_timelines(tl, tl.lp_noise)
         merger = actor.Merger(dev)
         merger.launch(True)
-        merger.layout(m.pack_tokens)
-        print(json.dumps({"workload": cfg.name, "merge_scaled": merge_scaled(merger, tl, torch, capi, actor)}))
+        merger.layout(c.model.pack_tokens)
+        print(json.dumps({"workload": c.name,
+                          "merge_scaled": merge_scaled(merger, tl, torch, capi, actor)}))
         return
-    W = make_weights_torch(m, seed=1000, device="cuda")
-    # rollout log-probs: the policy's own log-probs (untimed forward of this
-    # path on the unmerged layout) plus the generator's N(0, 0.05) noise
-    dev = actor.upload_timelines(tl, np.zeros(tl.n_tok, np.float32))
-    A = actor.ActorUpdate(m, W)
-    Lu = actor.merge(dev, merged=False, pack_tokens=m.pack_tokens)
-    cur = A.forward_logprob(Lu).float().cpu().numpy()
-    tg = Lu.targets[:Lu.n_mask].cpu().numpy()
-    old = np.zeros(tl.n_tok, np.float32)
-    old[tg] = cur + tl.lp_noise[tg]
-    dev["old_logprob"] = torch.from_numpy(old).cuda()
-    del Lu
 
-    merger = actor.Merger(dev)
-    merger.launch(True)
-    Lm = merger.layout(m.pack_tokens)
-    A.prepare(Lm)
-    Lm, t_m, rec = timed(A, merger, True, args.steps, args.warmup, torch, capi, record=False)
-    _, _, rec = timed(A, merger, True, 1, 0, torch, capi, record=True)
-    stats = A.stats.cpu().numpy()
-    res_u = None
-    if not args.no_unmerged:
-        mu = actor.Merger(dev)
-        mu.launch(False)
-        Lu = mu.layout(m.pack_tokens)
-        A.prepare(Lu)
-        Lu, t_u, _ = timed(A, mu, False, max(1, args.steps // 2), 1, torch, capi)
-        res_u = dict(ms_per_step=t_u * 1e3, tokens=Lu.n_tok, tokens_per_s=Lu.n_tok / t_u,
-                     packs=len(Lu.packs))
-
-    blk, lm, att, att_fwd = step_flops(Lm, m)
-    total = blk + lm + att
-    peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_F32_TFLOPS
-    # per-class kernel times of one timed step (HIP events on the launch stream)
-    classes = {}
-    for k, (ms, n, fl) in rec.items():
-        if k == "attn_fwd":
-            fl = att_fwd
-        elif k == "attn_bwd":
-            fl = att - att_fwd
-        classes[k] = dict(ms=ms, launches=n, tflops=(fl / (ms * 1e-3) / 1e12) if ms > 0 else 0.0)
-    # the roofline names one kernel with algorithmic flops: not the multi-kernel
-    # attention backward, not the logits recompute of the LM-head backward
-    dom = max((k for k in classes if k not in ("merge", "attn_bwd", "lm_dz")),
-              key=lambda k: classes[k]["ms"])
-    d = classes[dom]
-    kernel_names = {"gemm_nt": "gemm_mfma_kernel<true, true>", "gemm_nn": "gemm_mfma_kernel<true, false>",
-                    "gemm_tn": "gemm_mfma_kernel<false, false>",
-                    "gemm4_nt": "gemm_mfma4s_kernel<true, true>", "gemm4_nn": "gemm_mfma4s_kernel<true, false>",
-                    "gemm4_tn": "gemm_mfma4s_kernel<false, false>", "attn_fwd": "attn_fwd_mfma_kernel",
-                    "lm_fwd": "lm_fwd_fused_kernel", "lm_dz": "lm_dz_fused_kernel"}
-    fl_dom = {"attn_fwd": att_fwd}.get(dom, rec[dom][2])
-    roof = {"kernel": kernel_names.get(dom, dom), "bound": "mfma", "achieved": round(fl_dom / (d["ms"] * 1e-3) / 1e12, 2),
-            "peak": peak, "unit": "TFLOP/s",
-            "frac": round(fl_dom / (d["ms"] * 1e-3) / 1e12 / peak, 4), "traffic": None,
-            "launches": d["launches"], "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}
-
-    tr = TRAFFIC.get((dom, cfg.name))
-    if tr and dom.startswith("gemm") and tr["sources"] == source_hash(GEMM_SOURCES):
-        roof["traffic"] = tr["bytes_per_launch"]
-        roof["traffic_unit"] = "bytes"
-
+    m = cfg.model
+    head, live = measure(cfg, args.steps, args.warmup,
+                         0 if args.no_unmerged else args.unmerged_steps, 0, torch, capi, actor,
+                         record=True, keep=True)
+    roof, kc = roofline(live["rec"], live["flops"], live["peak"], cfg.name)
+    all_tl = {cfg.name: live["tl"]}
     out = {
         "metric": "merged actor-update tokens/sec/GPU",
-        "value": round(Lm.n_tok / t_m, 1),
+        "value": head["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(t_m * 1e3, 3),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": m.dtype, "data": "synthetic",
-        "config": {"workload": cfg.name, "merged_tokens": Lm.n_tok, "unmerged_tokens": tl.n_tok,
-                   "loss_tokens": Lm.n_mask, "segments": Lm.n_seg, "packs": len(Lm.packs),
-                   "pack_tokens": m.pack_tokens, "d_model": m.d_model, "heads": [m.n_q_heads, m.n_kv_heads],
-                   "head_dim": m.head_dim, "d_ff": m.d_ff, "vocab": m.vocab},
-        "effective_tokens_per_s": round(tl.n_tok / t_m, 1),
-        "loss_tokens_per_s": round(Lm.n_mask / t_m, 1),
-        "mfma_util": round(total / t_m / 1e12 / peak, 4),
-        "algorithmic_tflop_per_step": {"block": round(blk / 1e12, 3), "lm_head": round(lm / 1e12, 3),
-                                       "attention": round(att / 1e12, 3)},
-        "kernel_classes": {k: {kk: round(vv, 4) if isinstance(vv, float) else vv
-                               for kk, vv in v.items()} for k, v in classes.items()},
+        "config": {"workload": cfg.name, "merged_tokens": head["merged_tokens"],
+                   "unmerged_tokens": head["unmerged_tokens"],
+                   "loss_tokens": head["loss_tokens"], "segments": head["segments"],
+                   "packs": head["packs"], "pack_tokens": m.pack_tokens, "d_model": m.d_model,
+                   "heads": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim,
+                   "d_ff": m.d_ff, "vocab": m.vocab, "vocab_chunk": m.vocab_chunk},
+        "effective_tokens_per_s": head["effective_tokens_per_s"],
+        "loss_tokens_per_s": head["loss_tokens_per_s"],
+        "mfma_util": head["mfma_util"],
+        "algorithmic_tflop_per_step": head["algorithmic_tflop_per_step"],
+        "kernel_classes": kc,
         "roofline": roof,
-        "loss": float(stats[0]),
+        "loss": head["loss"],
     }
-    # the merge against HBM: algorithmic bytes = every unmerged token's id and
-    # flags, the llm tokens' log-prob and advantage read once; every merged
-    # token's id, position, mask, log-prob and advantage and every target written
-    if "merge" in rec and rec["merge"][1]:
-        mms = rec["merge"][0] / rec["merge"][1]
-        n_llm = int(np.count_nonzero((tl.flags & 3) == 2))
-        mb = 5 * tl.n_tok + 8 * n_llm + 17 * Lm.n_tok + 4 * Lm.n_mask
-        out["merge"] = {"ms": round(mms, 4), "algorithmic_MB": round(mb / 1e6, 2),
-                        "GB/s": round(mb / (mms * 1e-3) / 1e9, 1),
-                        "hbm_frac": round(mb / (mms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
-    if res_u:
-        out["unmerged"] = {k: round(v, 3) if isinstance(v, float) else v for k, v in res_u.items()}
-        out["speedup_vs_unmerged"] = round(res_u["ms_per_step"] / (t_m * 1e3), 3)
-    if not args.no_extras:
-        out["extras"] = extras(A, merger, cfg, tl, dev, torch, capi, actor, max(1, args.steps // 2))
+    mr = merge_record(live["rec"], live["tl"], live["Lm"])
+    if "unmerged" in head:
+        out["unmerged"] = head["unmerged"]
+        out["speedup_vs_unmerged"] = head["speedup_vs_unmerged"]
+    head_old, head_tl = live["old"], live["tl"]
+    W_head = None if args.no_cpu_baseline else {k: v.cpu() for k, v in live["W"].items()}
+    del live
+    torch.cuda.empty_cache()
+
+    subs = {}
+    for k in [x for x in args.sub.split(",") if x.strip()]:
+        c = get_config(key(k.strip()))
+        if c.name == cfg.name:
+            continue
+        is_b15 = c.name == "block1.5b-64x8"
+        want_extras = not args.no_extras and (is_b15 or c.name == "agent7b-32x10..30")
+        r, lv = measure(c, args.sub_steps, args.sub_warmup,
+                        0 if args.no_unmerged else (2 if is_b15 else 1), 0, torch, capi, actor,
+                        record=True, keep=want_extras)
+        r["roofline"], r["kernel_classes"] = roofline(lv["rec"], lv["flops"], lv["peak"], c.name)
+        if not args.no_extras and is_b15:
+            log("extras on " + c.name)
+            r["extras"] = extras(lv["A"], lv["merger"], c, lv["tl"], lv["dev"], torch, capi,
+                                 actor, 2)
+        if not args.no_extras and c.name == "agent7b-32x10..30":
+            log("scaled merge on " + c.name)
+            r["merge_scaled"] = merge_scaled(lv["merger"], lv["tl"], torch, capi, actor)
+        all_tl[c.name] = lv["tl"]
+        subs[c.name] = r
+        del lv
+        torch.cuda.empty_cache()
+    if subs:
+        out["sub_records"] = subs
+    if mr:
+        out["merge"] = mr
     if not args.no_cpu_baseline:
-        st = args.cpu_sample_tokens or (Lm.n_tok if cfg.name.startswith("tiny") else 4096)
-        out["cpu_baseline"] = cpu_baseline(cfg, tl, old, W, st)
+        log("cpu baseline (oracle)")
+        st = args.cpu_sample_tokens or (head["merged_tokens"] if cfg.name.startswith("tiny")
+                                        else 1024)
+        out["cpu_baseline"] = cpu_baseline(cfg, head_tl, head_old, W_head, st, all_tl)
     print(json.dumps(out), flush=True)
 
 
