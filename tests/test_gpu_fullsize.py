@@ -4,8 +4,9 @@ the full 151936-word LM head, bfloat16, packs of <= 131072 tokens), checked
 where the float64 oracle can follow it one output at a time, and through
 properties that hold at any size.
 
-* Sampled log-probs: for the two shortest merged segments that carry loss
-  tokens, up to 8 target positions each; the oracle computes the block
+* Sampled log-probs: for the two shortest and the two longest merged
+  segments that carry loss tokens (~1.1k to ~4.9k tokens), up to 8 target
+  positions each, spread to the segment's last target; the oracle computes the block
   output at just the rows that predict them (keys and values over the whole
   prefix of the segment) and the LM head at those rows.  Tolerance: the
   bfloat16 log-prob bound, 2e-2 absolute.
@@ -87,8 +88,11 @@ def test_fullsize_sampled_logprobs(full, merged_run):
     np.testing.assert_array_equal(got["targets"], tgt)
     W64 = M.f64_weights(W)
     lens = np.diff(ref.cu_seqlens)
-    cand = [s for s in np.argsort(lens, kind="stable")
-            if np.any((tgt > ref.cu_seqlens[s]) & (tgt < ref.cu_seqlens[s + 1]))][:2]
+    with_t = [s for s in np.argsort(lens, kind="stable")
+              if np.any((tgt > ref.cu_seqlens[s]) & (tgt < ref.cu_seqlens[s + 1]))]
+    # the two shortest and the two longest segments with targets: 8 targets
+    # spread over each, the last of them near the segment's end
+    cand = list(dict.fromkeys(with_t[:2] + with_t[-2:]))
     worst = 0.0
     for s in cand:
         a, b = int(ref.cu_seqlens[s]), int(ref.cu_seqlens[s + 1])

@@ -15,15 +15,20 @@ Checked where the float64 oracle can follow, as for block1.5b-64x8:
 
 * the loss targets of the merged batch are the oracle merge's, exactly;
 * sampled log-probs: in two segments, up to 24 targets among the first 512
-  positions after the segment's first target (the oracle reads only the
-  prefix up to the last sampled row).  At these widths the bfloat16 storage
-  of activations alone moves log-probs by more than the 2e-2 that holds at
-  block1.5b-64x8 (standard deviation ~0.01 at d 3584, ~0.02 at d 5120), so
-  the tolerance is derived per case from that arithmetic: the same rows
-  through the oracle's float64 steps with bfloat16 rounding at each storage
-  point (tests/bf16_model.py) give the error spread the GPU's is held to
-  (RMS within 1.5x + 2e-3, largest within 2x + 5e-3), and its mean must stay
-  within 5e-3 of zero;
+  positions after the segment's first target, and 8 targets in the last
+  tenth of the longest segment (at long32b-8x60 positions past 40k, where
+  RoPE angles are large and most key tiles are far from the query); the
+  oracle reads only the prefix up to the last sampled row.  Two checks:
+  - the stated bfloat16 bound, 2e-2 absolute on every sampled target.  At
+    these widths the bfloat16 storage of activations alone moves log-probs by
+    more than that (standard deviation ~0.01 at d 3584, ~0.02 at d 5120; the
+    storage points that feed the attention scores carry most of it): where
+    the GPU exceeds 2e-2 the case is reported as an expected failure with
+    the measured error;
+  - the error spread of the same rows through the oracle's float64 steps
+    with bfloat16 rounding at each storage point (tests/bf16_model.py): the
+    GPU's RMS within 1.5x + 2e-3 of it, its largest within 2x + 5e-3, and its
+    mean within 5e-3 of zero;
 * the loss equals the oracle's clipped policy-gradient terms of the GPU's
   own log-probs (relative 1e-3);
 * merged = unmerged on the first episode (every trajectory of the long
@@ -73,7 +78,14 @@ def test_large_targets(big):
     assert got["n_tok"] == ref.n_tok and got["n_mask"] == len(tgt)
 
 
-def test_large_sampled_logprobs(big):
+# Worst |d logprob| seen on these rows before the late samples were added; the
+# bfloat16 storage model of the same rows gives 0.033 / 0.040 at d 3584 / 5120.
+EXCEEDS_2E2 = {"agent7b-32x10..30": 0.0327, "multiagent7b-16x4x12": 0.0224,
+               "long32b-8x60": 0.0401}
+
+
+@pytest.fixture(scope="module")
+def sampled(big):
     cfg, m, tl, old, W, ref, got = big
     tgt = got["targets"]
     W64 = {k: np.asarray(W[k], np.float64) for k in M.BLOCK_WEIGHTS + ("emb", "final_norm", "w_vocab")}
@@ -83,18 +95,29 @@ def test_large_sampled_logprobs(big):
         seg_t = tgt[(tgt > a) & (tgt < b)]
         if len(seg_t):
             firsts.append((int(seg_t[0]) - a, s))
-    # the segment whose first target comes earliest, and the shortest one with targets
+    # the segment whose first target comes earliest, and the shortest one with
+    # targets: their first targets; then the longest segment's last tenth
     lens = np.diff(ref.cu_seqlens)
+    picks = {}
     cand = [min(firsts)[1]]
     shortest = min((int(lens[s]), s) for _, s in firsts)[1]
     if shortest not in cand:
         cand.append(shortest)
-    e_gpu, e_model = [], []
     for s in cand:
         a, b = int(ref.cu_seqlens[s]), int(ref.cu_seqlens[s + 1])
         seg_t = tgt[(tgt > a) & (tgt < b)]
         early = seg_t[seg_t < seg_t[0] + 512]
-        pick = early[np.unique(np.linspace(0, len(early) - 1, min(24, len(early))).astype(int))]
+        picks[s] = early[np.unique(np.linspace(0, len(early) - 1, min(24, len(early))).astype(int))]
+    longest = max((int(lens[s]), s) for _, s in firsts)[1]
+    a, b = int(ref.cu_seqlens[longest]), int(ref.cu_seqlens[longest + 1])
+    seg_t = tgt[(tgt > a) & (tgt < b)]
+    late = seg_t[seg_t >= a + int(0.9 * (b - a))]
+    if len(late):
+        late = late[np.unique(np.linspace(0, len(late) - 1, min(8, len(late))).astype(int))]
+        picks[longest] = np.union1d(picks.get(longest, late[:0]), late)
+    e_gpu, e_model, notes = [], [], []
+    for s, pick in picks.items():
+        a, b = int(ref.cu_seqlens[s]), int(ref.cu_seqlens[s + 1])
         x_seg = W64["emb"][ref.tok[a:b]]
         y = M.block_forward_rows(x_seg, ref.pos[a:b], pick - 1 - a, W64, m)
         tok_l = np.concatenate([[0], ref.tok[pick]])
@@ -104,10 +127,26 @@ def test_large_sampled_logprobs(big):
         gpu = got["lp"][np.searchsorted(tgt, pick)]
         e_gpu.append(gpu - lp)
         e_model.append(lp_model - lp)
-        print(f"{cfg.name} segment {s}: {b - a} tokens, {len(pick)} targets in "
-              f"[{pick[0] - a}, {pick[-1] - a}], max |dlogprob| GPU {np.abs(e_gpu[-1]).max():.3g}, "
-              f"bf16 storage model {np.abs(e_model[-1]).max():.3g}", flush=True)
-    e_gpu, e_model = np.concatenate(e_gpu), np.concatenate(e_model)
+        notes.append(f"{cfg.name} segment {s}: {b - a} tokens, {len(pick)} targets at positions "
+                     f"{pick[0] - a}..{pick[-1] - a}, max |dlogprob| GPU "
+                     f"{np.abs(e_gpu[-1]).max():.3g}, bf16 storage model "
+                     f"{np.abs(e_model[-1]).max():.3g}")
+        print(notes[-1], flush=True)
+    return cfg, np.concatenate(e_gpu), np.concatenate(e_model), notes
+
+
+def test_large_sampled_logprobs_stated_bound(sampled):
+    cfg, e_gpu, e_model, notes = sampled
+    print("\n".join(notes), flush=True)
+    worst = float(np.abs(e_gpu).max())
+    if worst > 2e-2 and cfg.name in EXCEEDS_2E2:
+        pytest.xfail(f"{cfg.name}: max |dlogprob| {worst:.4f} > 2e-2 (bf16 storage model of the "
+                     f"same rows: {np.abs(e_model).max():.4f})")
+    assert worst <= 2e-2
+
+
+def test_large_sampled_logprobs_within_bf16_storage_model(sampled):
+    cfg, e_gpu, e_model, notes = sampled
     rms = lambda e: float(np.sqrt(np.mean(e * e)))
     print(f"{cfg.name}: rms GPU {rms(e_gpu):.4f} model {rms(e_model):.4f}, max GPU "
           f"{np.abs(e_gpu).max():.4f} model {np.abs(e_model).max():.4f}, mean GPU "
