@@ -102,13 +102,37 @@ def match_text(a: Block, b: Block) -> bool:
     return a.text == b.text
 
 
-def merge_episode(timelines, match=match_token):
-    """Algorithm 1 on one episode's timelines (collection order).
+def mergeable(longer, shorter, match):
+    """The pairwise mergeability of Section 4.4.2: a timeline S can absorb a
+    timeline T when S has at least as many blocks as T and every block of T
+    matches the block of S at the same index."""
+    return len(longer) >= len(shorter) and all(match(s, t) for s, t in zip(longer, shorter))
 
-    Later, not-yet-absorbed timelines are visited from the last one down; each
-    absorbs every earlier not-yet-absorbed timeline whose blocks it matches
-    one by one, taking over llm authorship (author, tokens, log-prob -- and the
-    advantage) on the aligned blocks where its own block is not llm.
+
+def take_over_llm_blocks(survivor, absorbed):
+    """The transfer of one absorption (Section 4.4.2): wherever the absorbed
+    timeline's block is llm-authored and the survivor's aligned block is not,
+    the survivor's block takes the absorbed one's author, tokens, log-probs
+    and, here, advantages (and its provenance for the TI report); the block
+    keeps its own text."""
+    for k, blk in enumerate(absorbed):
+        if blk.author == LLM and survivor[k].author != LLM:
+            new = blk.copy()
+            new.text = survivor[k].text
+            survivor[k] = new
+
+
+def merge_episode(timelines, match=match_token):
+    """Timeline merging (Algorithm 1) on one episode's timelines (collection
+    order), organised as a worklist of undecided timelines.
+
+    The latest undecided timeline can no longer be absorbed (only later
+    timelines absorb, and every later one is decided), so it survives; it
+    then absorbs each undecided earlier timeline it can, the nearest first,
+    taking over their llm blocks as it goes; those leave the worklist, and
+    the next latest undecided timeline is taken.  This is the paper's
+    reverse-order sweep: the last timeline absorbs what it can, then the
+    latest one not yet absorbed, and so on.
 
     Returns (survivors, absorber): the surviving timelines in original order
     (deep copies, with transfers applied) and, per input timeline, the index of
@@ -119,27 +143,18 @@ def merge_episode(timelines, match=match_token):
         for k, b in enumerate(tl):
             if b.src is None:
                 b.src = (i, k)
-    n = len(T)
-    absorbed = set()
-    absorber = [-1] * n
-    for i in range(n - 1, 0, -1):
-        if i in absorbed:
-            continue
-        for j in range(i - 1, -1, -1):
-            if j in absorbed:
-                continue
-            if len(T[i]) >= len(T[j]) and all(match(T[i][k], T[j][k]) for k in range(len(T[j]))):
-                for k in range(len(T[j])):
-                    if T[j][k].author == LLM and T[i][k].author != LLM:
-                        T[i][k].author = LLM
-                        T[i][k].tokens = T[j][k].tokens.copy()
-                        T[i][k].logprob = T[j][k].logprob.copy()
-                        T[i][k].adv = T[j][k].adv.copy()
-                        T[i][k].src = T[j][k].src
-                absorbed.add(j)
-                absorber[j] = i
-    survivors = [T[i] for i in range(n) if i not in absorbed]
-    return survivors, absorber
+    absorber = [-1] * len(T)
+    undecided = list(range(len(T)))
+    kept = []
+    while undecided:
+        s = undecided.pop()
+        kept.append(s)
+        for j in reversed(undecided):
+            if mergeable(T[s], T[j], match):
+                take_over_llm_blocks(T[s], T[j])
+                absorber[j] = s
+        undecided = [j for j in undecided if absorber[j] < 0]
+    return [T[s] for s in sorted(kept)], absorber
 
 
 class Packed:
