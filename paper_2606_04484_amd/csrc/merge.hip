@@ -14,17 +14,23 @@
 //     first transfer wins, and absorbed timelines arrive in descending j:
 //         payload(s, k) = s's own block if llm, else the block k of the largest
 //                         j absorbed into s whose block k is llm.
-// Kernels:
-//   validate        offsets tile [0, n_tok) and [0, n_tl); first token starts a block
+// Kernels (token-level Match; seven launches):
+//   validate        one workgroup: offsets tile [0, n_tok) and [0, n_tl), every
+//                   timeline starts a block; writes the call's status word
 //   find_absorber   one workgroup per timeline j: candidates i from the episode's
-//                   last timeline down, prefix compare with early exit
-//   resolve         survivor scan -> segment index, cu_seqlens, counts
-//   claim_fill / claim   llm tokens of absorbed timelines vote (atomicMax of
-//                   their token index, which orders like j) for the survivor
-//                   position they land on (one workgroup per timeline)
+//                   last timeline down, prefix compare with early exit; a
+//                   survivor clears the claim slots of its own tokens
+//   claim           llm tokens of absorbed timelines vote (atomicMax of their
+//                   token index, which orders like j) in the claim slot of the
+//                   survivor token they land on (indexed like the input tokens)
+//   resolve         one workgroup: survivor scan -> segment index, cu_seqlens,
+//                   counts
 //   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (each
-//                   workgroup a range of output positions)
-//   tgt_count / tgt_scan / tgt_write / cu_targets   ascending masked targets
+//                   workgroup a range of output positions); counts each range's
+//                   targets and writes their bitmask
+//   tgt_scan        one workgroup: offsets of the per-range target counts
+//   tgt_write       ascending masked targets from the bitmask, and each
+//                   segment's first target (cu_targets)
 #include <mutex>
 
 #include "common.h"
@@ -62,7 +68,8 @@ struct MergeArgs {
   // workspace
   int32_t *status;      // [0] error bits seen by this call
   int32_t *tl_seg;      // [n_tl]
-  int32_t *claim;       // [n_tok] per output position: source token of its log-prob
+  int32_t *claim;       // [n_tok] per survivor input token: source token of its log-prob
+  uint64_t *tbits;      // one bit per output position: a masked target
   int32_t *chunk_cnt;   // [n_chunks]
   int32_t *chunk_off;   // [n_chunks]
   int32_t *user_err;
@@ -128,28 +135,68 @@ AJ_DEV int block_scan_incl(int v, int *total) {
   return res;
 }
 
+// Exclusive scan of the values v[r] (r < K) of one workgroup of NT threads,
+// where thread (wave w, lane l) holds item w*64*K + r*64 + l: loads of
+// consecutive items stay coalesced, the scan runs over the wave's items in
+// order (64-lane scans with a carry), then over the waves.  v[r] becomes
+// carry + the sum of the items before it; returns the total.
+template <int NT, int K>
+AJ_DEV int wave_items_scan(int (&v)[K], int carry) {
+  __shared__ int wtot[NT / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int run = 0;
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    int x = v[r];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    const int tot = __shfl(x, 63, 64);
+    v[r] = run + x - v[r];
+    run += tot;
+  }
+  if (lane == 0) wtot[wid] = run;
+  __syncthreads();
+  int before = carry, all = carry;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    const int t = wtot[w];
+    before += w < wid ? t : 0;
+    all += t;
+  }
+#pragma unroll
+  for (int r = 0; r < K; ++r) v[r] += before;
+  __syncthreads();
+  return all - carry;
+}
+
+AJ_DEV int validate_item(const MergeArgs &a, int t) {
+  int bits = 0;
+  if (t == 0) {
+    if (a.traj_tl_off[0] != 0 || a.traj_tl_off[a.n_traj] != a.n_tl) bits |= AJ_DEVERR_OFFSETS;
+    if (a.tl_tok_off[0] != 0 || a.tl_tok_off[a.n_tl] != a.n_tok) bits |= AJ_DEVERR_OFFSETS;
+  }
+  if (t < a.n_traj && a.traj_tl_off[t] > a.traj_tl_off[t + 1]) bits |= AJ_DEVERR_OFFSETS;
+  if (t < a.n_tl) {
+    const int64_t lo = a.tl_tok_off[t], hi = a.tl_tok_off[t + 1];
+    if (lo < 0 || lo > hi || hi > a.n_tok) bits |= AJ_DEVERR_OFFSETS;
+    else if (lo == hi) bits |= AJ_DEVERR_EMPTY;
+    else if (!(a.flags[lo] & AJ_FLAG_BLOCK_START)) bits |= AJ_DEVERR_BAD_FLAGS;
+  }
+  return bits;
+}
+
 __global__ void init_status_kernel(MergeArgs a) {
   if (threadIdx.x < 4) a.status[threadIdx.x] = 0;
   if (a.ti && threadIdx.x < 2) a.ti[threadIdx.x] = 0;
 }
 
 __global__ void validate_kernel(MergeArgs a) {
-  int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t == 0) {
-    if (a.traj_tl_off[0] != 0 || a.traj_tl_off[a.n_traj] != a.n_tl) raise(a, AJ_DEVERR_OFFSETS);
-    if (a.tl_tok_off[0] != 0 || a.tl_tok_off[a.n_tl] != a.n_tok) raise(a, AJ_DEVERR_OFFSETS);
-  }
-  if (t < a.n_traj && a.traj_tl_off[t] > a.traj_tl_off[t + 1]) raise(a, AJ_DEVERR_OFFSETS);
-  if (t < a.n_tl) {
-    int64_t lo = a.tl_tok_off[t], hi = a.tl_tok_off[t + 1];
-    if (lo < 0 || lo > hi || hi > a.n_tok) {
-      raise(a, AJ_DEVERR_OFFSETS);
-    } else if (lo == hi) {
-      raise(a, AJ_DEVERR_EMPTY);
-    } else if (!(a.flags[lo] & AJ_FLAG_BLOCK_START)) {
-      raise(a, AJ_DEVERR_BAD_FLAGS);
-    }
-  }
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const int bits = validate_item(a, t);
+  if (bits) raise(a, bits);
 }
 
 // One workgroup per timeline j.
@@ -197,6 +244,17 @@ __global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
     if (equal) { result = i; break; }
   }
   if (threadIdx.x == 0) a.absorber[j] = result;
+  // a survivor's tokens are the claim slots its absorbed timelines vote in:
+  // cleared with 16-byte stores between a scalar head and tail
+  if (result < 0 && a.claim) {
+    int32_t *dst = a.claim + bj;
+    const int64_t head = min(lj, (int64_t)((4 - (bj & 3)) & 3));
+    const int64_t n4 = (lj - head) / 4;
+    if (threadIdx.x < head) dst[threadIdx.x] = -1;
+    int4 *d4 = reinterpret_cast<int4 *>(dst + head);
+    for (int64_t q = threadIdx.x; q < n4; q += kBlock) d4[q] = make_int4(-1, -1, -1, -1);
+    for (int64_t p = head + 4 * n4 + threadIdx.x; p < lj; p += kBlock) dst[p] = -1;
+  }
 }
 
 __global__ void fill_absorber_kernel(MergeArgs a) {
@@ -204,65 +262,58 @@ __global__ void fill_absorber_kernel(MergeArgs a) {
   if (t < a.n_tl) a.absorber[t] = -1;
 }
 
-// Single workgroup of 1024 threads, 4 consecutive timelines per thread.
+// One workgroup of 1024 threads; a round covers 1024 * kResPer timelines,
+// wave w the kResPer * 64 consecutive ones from w * 64 * kResPer (lane l
+// holding every 64th), so the loads stay coalesced.
+constexpr int kResPer = 8;
+
 __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
-  constexpr int kPer = 4;
-  __shared__ int carry_seg, carry_tok, carry_max;
-  if (threadIdx.x == 0) { carry_seg = 0; carry_tok = 0; carry_max = 0; }
-  __syncthreads();
+  __shared__ int mx_all;
+  if (threadIdx.x == 0) mx_all = 0;
   const bool bad = fatal(a);
-  for (int base = 0; base < a.n_tl; base += 1024 * kPer) {
-    const int i0 = base + threadIdx.x * kPer;
-    int surv[kPer], len[kPer], ns = 0, nl = 0;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int carry_seg = 0, carry_tok = 0, mx = 0;
+  for (int base = 0; base < a.n_tl; base += 1024 * kResPer) {
+    const int i0 = base + wid * 64 * kResPer + lane;
+    int seg[kResPer], tok[kResPer];
 #pragma unroll
-    for (int r = 0; r < kPer; ++r) {   // clamped, not guarded: the loads issue together
-      const int i = min(i0 + r, a.n_tl - 1);
-      const bool ok = !bad && i0 + r < a.n_tl;
+    for (int r = 0; r < kResPer; ++r) {   // clamped, not guarded: the loads issue together
+      const int i = min(i0 + 64 * r, a.n_tl - 1);
+      const bool ok = !bad && i0 + 64 * r < a.n_tl;
       const int ab = a.absorber[i];
       const int l = (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]);
-      surv[r] = ok && ab < 0;
-      len[r] = surv[r] ? l : 0;
-      ns += surv[r]; nl += len[r];
+      seg[r] = ok && ab < 0;
+      tok[r] = seg[r] ? l : 0;
+      mx = max(mx, tok[r]);
     }
-    int tot_s, tot_l;
-    const int is = block_scan_incl<1024>(ns, &tot_s);
-    const int il = block_scan_incl<1024>(nl, &tot_l);
-    int seg = carry_seg + is - ns, tok = carry_tok + il - nl, mx = 0;
+    uint32_t surv = 0;
 #pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int i = i0 + r;
+    for (int r = 0; r < kResPer; ++r) surv |= (uint32_t)seg[r] << r;
+    const int tot_s = wave_items_scan<1024, kResPer>(seg, carry_seg);
+    const int tot_l = wave_items_scan<1024, kResPer>(tok, carry_tok);
+#pragma unroll
+    for (int r = 0; r < kResPer; ++r) {
+      const int i = i0 + 64 * r;
       if (i >= a.n_tl) continue;
-      if (surv[r]) {
-        a.tl_seg[i] = seg;
-        a.seg_src[seg] = i;
-        a.cu_seqlens[seg] = tok;
-        ++seg; tok += len[r];
-        mx = max(mx, len[r]);
+      if ((surv >> r) & 1) {
+        a.tl_seg[i] = seg[r];
+        a.seg_src[seg[r]] = i;
+        a.cu_seqlens[seg[r]] = tok[r];
       } else {
         a.tl_seg[i] = -1;
       }
     }
-    if (mx) atomicMax(&carry_max, mx);
-    __syncthreads();
-    if (threadIdx.x == 0) { carry_seg += tot_s; carry_tok += tot_l; }
-    __syncthreads();
+    carry_seg += tot_s;
+    carry_tok += tot_l;
   }
+  if (mx) atomicMax(&mx_all, mx);
+  __syncthreads();
   if (threadIdx.x == 0) {
     a.cu_seqlens[carry_seg] = carry_tok;
     a.counts[0] = carry_seg;
     a.counts[1] = carry_tok;
     a.counts[2] = 0;
-    a.counts[3] = carry_max;
-  }
-}
-
-__global__ void claim_fill_kernel(MergeArgs a) {
-  const int64_t n = a.counts[1];
-  const int64_t o = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (o + 4 <= n && ((uintptr_t)a.claim & 15) == 0) {
-    *reinterpret_cast<int4 *>(a.claim + o) = make_int4(-1, -1, -1, -1);
-  } else {
-    for (int64_t q = o; q < n; ++q) a.claim[q] = -1;
+    a.counts[3] = mx_all;
   }
 }
 
@@ -271,10 +322,11 @@ __global__ void claim_fill_kernel(MergeArgs a) {
 constexpr int kUnroll = 4;
 
 // One workgroup per timeline: an absorbed timeline's llm tokens vote for the
-// survivor position they land on with their own token index; token offsets
-// grow with the timeline index, so the atomicMax winner is the token of the
-// largest absorbed timeline, the one Algorithm 1 lets write last.  The flag
-// bytes of absorbed timelines are checked here, those of survivors in emit.
+// survivor token they align with (the same position p in the survivor) with
+// their own token index; token offsets grow with the timeline index, so the
+// atomicMax winner is the token of the largest absorbed timeline, the one
+// Algorithm 1 lets write last.  The flag bytes of absorbed timelines are
+// checked here, those of survivors in emit.
 __global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
   if (fatal(a)) return;
   const int i = spread_timeline(blockIdx.x, a.n_tl);
@@ -282,7 +334,7 @@ __global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
   if (s < 0) return;
   const int64_t b = a.tl_tok_off[i];
   const int len = (int)(a.tl_tok_off[i + 1] - b);
-  int32_t *dst = a.claim + a.cu_seqlens[a.tl_seg[s]];   // s is a survivor, len_s >= len
+  int32_t *dst = a.claim + a.tl_tok_off[s];   // s is a survivor, len_s >= len
   int bad = 0;
   for (int p0 = 0; p0 < len; p0 += kUnroll * kBlock) {
     uint8_t f[kUnroll];
@@ -382,33 +434,47 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claim
     }
     uint8_t f[kEmitPer];
     int32_t t[kEmitPer], c[kEmitPer];
+    int64_t src[kEmitPer];
     float lp[kEmitPer], ad[kEmitPer];
 #pragma unroll
-    for (int r = 0; r < kEmitPer; ++r) {
-      const int64_t o = min(ob + r * kBlock + (int64_t)threadIdx.x, n_out - 1);
+    for (int r = 0; r < kEmitPer; ++r) {   // issued together
       f[r] = a.flags[u[r]];
       t[r] = a.tok[u[r]];
       lp[r] = a.old_logprob[u[r]];
       ad[r] = a.adv[u[r]];
-      c[r] = use_claims ? a.claim[o] : -1;
+      c[r] = use_claims ? a.claim[u[r]] : -1;
     }
+    // the token's own log-prob and advantage (llm), else the claiming token's
 #pragma unroll
     for (int r = 0; r < kEmitPer; ++r) {
-      const int64_t o = ob + r * kBlock + threadIdx.x;
-      if (o >= n_out) continue;
-      bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
       const bool own = (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
-      const bool has = own || c[r] >= 0;
+      src[r] = own ? u[r] : (int64_t)c[r];
       if (!own && c[r] >= 0) {
         lp[r] = a.old_logprob[c[r]];
         ad[r] = a.adv[c[r]];
       }
+      if (src[r] < 0) {
+        lp[r] = 0.f;
+        ad[r] = 0.f;
+      }
+    }
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int r = 0; r < kEmitPer; ++r) {
+      const int64_t o = ob + r * kBlock + threadIdx.x;
+      const bool in = o < n_out;
+      const bool has = in && src[r] >= 0;
+      const bool tgt = has && pos[r] != 0;
+      const uint64_t word = __ballot(tgt);
+      if (lane == 0) a.tbits[ob / 64 + r * (kBlock / 64) + wave] = word;
+      if (!in) continue;
+      bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
       a.otok[o] = t[r];
       a.opos[o] = pos[r];
       a.omask[o] = has;
-      a.olp[o] = has ? lp[r] : 0.f;
-      a.oadv[o] = has ? ad[r] : 0.f;
-      n_tgt += has && pos[r] != 0;
+      a.olp[o] = lp[r];
+      a.oadv[o] = ad[r];
+      n_tgt += tgt;
     }
     // the span's target count for the compaction (chunk = span)
     int tot;
@@ -448,32 +514,43 @@ AJ_DEV uint32_t target_bits(const MergeArgs &a, int64_t o0, int64_t n_out) {
   return bits;
 }
 
+// The text path's target count per chunk (token-level emit counts its own),
+// with the chunk's target bitmask.
 __global__ __launch_bounds__(kBlock) void tgt_count_kernel(MergeArgs a) {
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
   const int64_t o0 = (int64_t)blockIdx.x * kTgtChunk + threadIdx.x * kTgtPer;
-  const int c = __popc(target_bits(a, o0, n_out));
+  const uint32_t bits = target_bits(a, o0, n_out);
+  // 8 bits per thread: thread t holds byte t % 8 of the chunk's word t / 8
+  const int lane = threadIdx.x & 63;
+  uint64_t w = (uint64_t)bits << (8 * (lane & 7));
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) w |= __shfl_xor(w, o, 64);
+  if ((lane & 7) == 0) a.tbits[o0 / 64] = w;
+  const int c = __popc(bits);
   int tot;
   block_scan_incl<kBlock>(c, &tot);
   if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
 }
 
-// Exclusive offsets of the per-chunk counts; the total goes to counts[2] (the
+// Exclusive offsets of the per-chunk counts by one workgroup, 1024 * kScanPer
+// chunks a round; the total goes to counts[2] (the
 // target compaction) or, for the block-start compaction, must equal n_blk.
+constexpr int kScanPer = 16;
+
 __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunks, int blocks) {
-  __shared__ int carry;
-  if (threadIdx.x == 0) carry = 0;
-  __syncthreads();
   // the target compaction counts only chunks that hold outputs
   const int n_used = blocks ? n_chunks : (int)((a.counts[1] + kTgtChunk - 1) / kTgtChunk);
-  for (int base = 0; base < n_used; base += 1024) {
-    int c = base + threadIdx.x;
-    int v = c < n_used ? a.chunk_cnt[c] : 0;
-    int tot;
-    int incl = block_scan_incl<1024>(v, &tot);
-    if (c < n_used) a.chunk_off[c] = carry + incl - v;
-    __syncthreads();
-    if (threadIdx.x == 0) carry += tot;
-    __syncthreads();
+  int carry = 0;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (int base = 0; base < n_used; base += 1024 * kScanPer) {
+    const int c0 = base + wid * 64 * kScanPer + lane;
+    int v[kScanPer];
+#pragma unroll
+    for (int r = 0; r < kScanPer; ++r) v[r] = c0 + 64 * r < n_used ? a.chunk_cnt[c0 + 64 * r] : 0;
+    carry += wave_items_scan<1024, kScanPer>(v, carry);
+#pragma unroll
+    for (int r = 0; r < kScanPer; ++r)
+      if (c0 + 64 * r < n_used) a.chunk_off[c0 + 64 * r] = v[r];
   }
   if (threadIdx.x == 0) {
     if (!blocks) a.counts[2] = carry;
@@ -481,37 +558,47 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
   }
 }
 
+// Targets of chunk ch (kTgtChunk outputs = kTgtChunk / 64 bitmask words), 8
+// outputs (one bitmask byte) per thread.
+AJ_DEV uint32_t chunk_byte(const MergeArgs &a, int64_t ch) {
+  const uint64_t w = a.tbits[ch * (kTgtChunk / 64) + threadIdx.x / 8];
+  return (uint32_t)(w >> (8 * (threadIdx.x & 7))) & 0xffu;
+}
+
 // A grid-stride walk over the chunks that hold outputs (the merged length is
-// known only on the device).
+// known only on the device), then over the segments: cu_targets[s] = the
+// number of targets before the segment's first output.
 __global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
+  const int n_seg = fatal(a) ? 0 : (int)a.counts[0];
   for (int64_t ch = blockIdx.x; ch * kTgtChunk < n_out; ch += gridDim.x) {
-    const int64_t o0 = ch * kTgtChunk + threadIdx.x * kTgtPer;
-    uint32_t bits = target_bits(a, o0, n_out);
+    uint32_t bits = chunk_byte(a, ch);
     const int c = __popc(bits);
     int tot;
     const int incl = block_scan_incl<kBlock>(c, &tot);
     int w = a.chunk_off[ch] + incl - c;
+    const int64_t o0 = ch * kTgtChunk + threadIdx.x * kTgtPer;
     while (bits) {
       const int r = __ffs(bits) - 1;
       a.targets[w++] = (int32_t)(o0 + r);
       bits &= bits - 1;
     }
   }
-}
-
-__global__ void cu_targets_kernel(MergeArgs a) {
-  const int s = blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t n_seg = a.counts[0];
-  if (s > n_seg) return;
   const int n_mask = (int)a.counts[2];
-  const int key = a.cu_seqlens[s];
-  int lo = 0, hi = n_mask;          // first target >= key
-  while (lo < hi) {
-    int mid = (lo + hi) >> 1;
-    if (a.targets[mid] < key) lo = mid + 1; else hi = mid;
+  for (int s = blockIdx.x * kBlock + threadIdx.x; s <= n_seg; s += gridDim.x * kBlock) {
+    const int64_t o = a.cu_seqlens[s];
+    int v = n_mask;
+    if (o < n_out) {
+      const int64_t ch = o / kTgtChunk;
+      v = a.chunk_off[ch];
+      const uint64_t *w = a.tbits + ch * (kTgtChunk / 64);
+      const int64_t full = (o - ch * kTgtChunk) / 64;
+      for (int64_t k = 0; k < full; ++k) v += __popcll(w[k]);
+      const int rem = (int)(o % 64);
+      if (rem) v += __popcll(w[full] & ((1ull << rem) - 1));
+    }
+    a.cu_targets[s] = v;
   }
-  a.cu_targets[s] = lo;
 }
 
 // ---------------------------------------------------------------- text-level Match
@@ -766,6 +853,7 @@ __global__ __launch_bounds__(64) void ti_kernel(MergeArgs a) {
 
 struct MergeWs {
   int32_t *status, *tl_seg, *claim, *chunk_cnt, *chunk_off;
+  uint64_t *tbits;
   int32_t *blk_start, *tl_blk, *blk_tl, *blk_claim, *src_blk, *blk_off, *dst_off, *dst_pos;
   size_t bytes;
 };
@@ -780,6 +868,8 @@ MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok, int32_t n_blk = -1) {
   w.tl_seg = c.take<int32_t>(at_least1(n_tl));
   w.chunk_cnt = c.take<int32_t>(at_least1(n_chunks));
   w.chunk_off = c.take<int32_t>(at_least1(n_chunks));
+  // one target bit per output; emit writes whole 2048-output spans
+  w.tbits = c.take<uint64_t>((n_tok + kTgtChunk - 1) / kTgtChunk * (kTgtChunk / 64) + 1);
   if (n_blk < 0) {
     w.claim = c.take<int32_t>(at_least1(n_tok));
   } else {
@@ -823,22 +913,29 @@ MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const 
   a.cu_targets = out->cu_targets; a.counts = out->counts;
   a.otok = out->tok; a.opos = out->pos; a.omask = out->mask; a.olp = out->old_logprob;
   a.oadv = out->adv; a.targets = out->targets;
-  a.status = w.status; a.tl_seg = w.tl_seg; a.claim = w.claim;
+  a.status = w.status; a.tl_seg = w.tl_seg; a.claim = w.claim; a.tbits = w.tbits;
   a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
   a.blk_start = w.blk_start; a.tl_blk = w.tl_blk; a.blk_tl = w.blk_tl; a.blk_claim = w.blk_claim;
   a.src_blk = w.src_blk; a.blk_off = w.blk_off; a.dst_off = w.dst_off; a.dst_pos = w.dst_pos;
   return a;
 }
 
+// The call's status word, cleared, then the input checks on a grid.
+void launch_validate(const MergeArgs &a, hipStream_t s) {
+  const int n_val = (a.n_tl > a.n_traj ? a.n_tl : a.n_traj) + 1;
+  init_status_kernel<<<1, 64, 0, s>>>(a);
+  validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+}
+
 // The target list and per-segment target offsets, once tok/pos/mask are out.
-// counted: emit already wrote the per-chunk target counts.
+// counted: emit already wrote the per-chunk target counts and the bitmask.
 void launch_targets(const MergeArgs &a, hipStream_t s, bool counted) {
   const int64_t n_chunks = (a.n_tok + kTgtChunk - 1) / kTgtChunk;
   if (a.n_tok > 0 && !counted) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
-  if (a.n_tok > 0)
-    tgt_write_kernel<<<(int)(n_chunks < kEmitWgs ? n_chunks : kEmitWgs), kBlock, 0, s>>>(a);
-  cu_targets_kernel<<<(a.n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  const int64_t segs = ((int64_t)a.n_tl + 1 + kBlock - 1) / kBlock;
+  const int64_t g = n_chunks > segs ? n_chunks : segs;
+  tgt_write_kernel<<<(int)(g < kEmitWgs ? g : kEmitWgs), kBlock, 0, s>>>(a);
 }
 
 int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t ws_bytes,
@@ -853,22 +950,17 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
 
   hipStream_t s = (hipStream_t)stream;
   const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
-  init_status_kernel<<<1, 64, 0, s>>>(a);
-  const int n_val = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
-  validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  launch_validate(a, s);
   if (in->n_tl > 0) {
-    if (merge)
+    if (merge) {
       find_absorber_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
-    else
+      if (in->n_tok > 0) claim_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
+    } else {
       fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+    }
   }
   resolve_kernel<<<1, 1024, 0, s>>>(a);
   if (in->n_tok > 0) {
-    const int64_t gtok = (in->n_tok + kBlock - 1) / kBlock;
-    if (merge) {
-      claim_fill_kernel<<<(gtok + 3) / 4, kBlock, 0, s>>>(a);
-      claim_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
-    }
     const int64_t spans = (in->n_tok + kEmitSpan - 1) / kEmitSpan;
     emit_kernel<<<(int)(spans < kEmitWgs ? spans : kEmitWgs), kBlock, 0, s>>>(a, merge ? 1 : 0);
   }
@@ -900,9 +992,7 @@ int run_text(const aj_timelines *in, const aj_block_texts *text, aj_packed *out,
   const int gblk = (n_blk + kBlock - 1) / kBlock;
   hipStream_t s = (hipStream_t)stream;
   const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
-  init_status_kernel<<<1, 64, 0, s>>>(a);
-  const int n_val = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
-  validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  launch_validate(a, s);
   // blocks: first tokens, first block per timeline, timeline per block
   if (in->n_tok > 0) blk_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 1);
