@@ -303,7 +303,14 @@ template <typename T>
 int attn_bwd(const AttnBwdArgs &a, hipStream_t s) {
   if (a.n_tok <= 0) return AJ_OK;
   if (a.hd > kMaxHd || a.hd % 8) return fail(AJ_ERR_UNSUPPORTED, "attention: head_dim %d", a.hd);
-  if (sizeof(T) == 2 && attn_mfma_supported(a.hd, a.qkv, a.dout, a.dqkv)) return attn_bwd_mfma(a, s);
+  // the matrix-core forward saves its log-sum-exp in log2 units, the plain
+  // kernels in natural ones: the backward must take the forward's path
+  const bool fwd_mfma = sizeof(T) == 2 && attn_mfma_supported(a.hd, a.qkv, a.o, a.o);
+  if (fwd_mfma) {
+    if (!attn_mfma_supported(a.hd, a.qkv, a.dout, a.dqkv))
+      return fail(AJ_ERR_UNSUPPORTED, "attention backward: d out / d qkv not 16-byte aligned");
+    return attn_bwd_mfma(a, s);
+  }
   const int64_t nd = (int64_t)a.n_tok * a.Hq;
   const int tk = timing_begin(s, AJ_KC_ATTN_BWD, 0.0);
   attn_delta_kernel<T><<<(unsigned)((nd + 3) / 4), 256, 0, s>>>(a);

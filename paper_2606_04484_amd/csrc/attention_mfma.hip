@@ -11,10 +11,11 @@
 // lane owns one KEY, and accumulates dV^T = dO^T P and dK^T = Q^T dS the same
 // way.  Segment masking: a query row attends to [segment start, itself].
 //
-// Workgroups: 256 threads, 4 waves of 32 query (or key) rows each.  Query
-// tiles are visited from the end of the pack (the longest rows first) and the
-// head index varies fastest, so the query heads that share a key/value head run
-// side by side on one XCD (ids are dealt round-robin over 8 XCDs) and share its L2.
+// Workgroups: NW waves of 32 query (or key) rows each, all of them reading
+// every staged tile, so that a tile copied into LDS serves 32 * NW rows.
+// Query tiles are visited from the end of the pack (the longest rows first)
+// and the head index varies fastest, so the query heads that share a
+// key/value head run side by side.
 #include "ops.h"
 
 namespace aj {
@@ -100,11 +101,12 @@ AJ_DEV uint32_t lds_addr(const void *p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
 
-template <int HD>
+template <int HD, int NW = 4>
 struct TokTile {
   static constexpr int CPR = HD / 8;                 // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;               // rows per 1 KB wave instruction
-  static constexpr int kInstr = kTR * HD * 2 / 1024 / 4;   // per wave (4 waves)
+  static constexpr int kInstr = kTR * HD * 2 / 1024 / NW;  // per wave (NW waves)
+  static_assert(kInstr >= 1 && kTR * HD * 2 / 1024 % NW == 0, "tile copy split");
   static constexpr int kHalfs = kTR * HD;
 
   AJ_DEV static int swz(int r) {
@@ -259,32 +261,35 @@ AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, cons
 }
 
 // acc[i] (features 32i..32i+31) += tile^T x P over tokens t0..t0+31, P given
-// as the two packed accumulator halves of that 32-row tile (pack8 order)
+// as the two packed accumulator halves of that 32-row tile (pack8 order).
+// One feature block at a time, the next block's two fragments read while the
+// current block's MFMAs issue (four fragments live, not eight).
 template <int HD>
 AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const uint16_t *tile, int t0,
                             const bf16x8_t (&pj)[2]) {
   constexpr int DT = HD / 32;
-  bf16x8_t f[2][DT];
+  bf16x8_t f[2][2];
+  f[0][0] = TokTile<HD>::col_frag(tile, 0, t0);
+  f[0][1] = TokTile<HD>::col_frag(tile, 0, t0 + 16);
 #pragma unroll
-  for (int i = 0; i < DT; ++i) f[0][i] = TokTile<HD>::col_frag(tile, 32 * i, t0);
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    lds_wait(f[j]);
-    if (j == 0) {
-#pragma unroll
-      for (int i = 0; i < DT; ++i) f[1][i] = TokTile<HD>::col_frag(tile, 32 * i, t0 + 16);
+  for (int i = 0; i < DT; ++i) {
+    const int cur = i & 1;
+    lds_wait(f[cur]);
+    if (i + 1 < DT) {
+      f[cur ^ 1][0] = TokTile<HD>::col_frag(tile, 32 * (i + 1), t0);
+      f[cur ^ 1][1] = TokTile<HD>::col_frag(tile, 32 * (i + 1), t0 + 16);
     }
-#pragma unroll
-    for (int i = 0; i < DT; ++i) acc[i] = mfma(f[j][i], pj[j], acc[i]);
+    acc[i] = mfma(f[cur][0], pj[0], acc[i]);
+    acc[i] = mfma(f[cur][1], pj[1], acc[i]);
   }
 }
 
 // ------------------------------------------------------------------ forward
-// One workgroup: 128 queries of one head (4 waves of 32), key tiles of 64
-// double-buffered; a lane owns one query.
-template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n_qt) {
-  using TT = TokTile<HD>;
+// One workgroup: 32 * NW queries of one head (NW waves of 32), key tiles of 64
+// double-buffered and shared by all the waves; a lane owns one query.
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n_qt) {
+  using TT = TokTile<HD, NW>;
   constexpr int KS = HD / 16, DT = HD / 32;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
@@ -294,14 +299,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
   const int g = (h * a.Hkv) / a.Hq;
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hl = lane >> 5, lq = lane & 31;
-  const int q0 = qt * 128;
+  const int q0 = qt * 32 * NW;
   const int q = q0 + 32 * w + lq;
   const bool qv = q < a.n_tok;
   const int qs = qv ? seg_start(a, q) : a.n_tok;
   const bf16_t *qkv = (const bf16_t *)a.qkv;
   if (threadIdx.x == 0) {
     rng[0] = seg_start(a, q0);
-    rng[1] = min(q0 + 127, a.n_tok - 1);
+    rng[1] = min(q0 + 32 * NW - 1, a.n_tok - 1);
   }
   bf16x8_t qf[KS];
 #pragma unroll
@@ -328,15 +333,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
   TT::load(Vs[0], vbase, ld, kv_lo, kv_hi + 1);
   dma_wait();
   __syncthreads();
-  for (int it = 0; it < n_kt; ++it) {
-    const int buf = it & 1, k0 = kv_lo + it * kTR;
+  // tile it reads stage (Kc, Vc) and prefetches tile it + 1 into (Kn, Vn); the
+  // loop runs two tiles per pass so that both stages are fixed LDS addresses
+  auto tile = [&](const int it, uint16_t *Kc, uint16_t *Vc, uint16_t *Kn,
+                  uint16_t *Vn) __attribute__((always_inline)) {
+    const int k0 = kv_lo + it * kTR;
     if (it + 1 < n_kt) {
-      TT::load(Ks[buf ^ 1], kbase, ld, k0 + kTR, kv_hi + 1);
-      TT::load(Vs[buf ^ 1], vbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(Kn, kbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(Vn, vbase, ld, k0 + kTR, kv_hi + 1);
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2];
-      rows_times<HD, true>(s, Ks[buf], qf);              // S^T = K Q^T (unscaled)
+      rows_times<HD, true>(s, Kc, qf);                   // S^T = K Q^T (unscaled)
       float mx = -INFINITY;
       if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
 #pragma unroll
@@ -371,25 +379,31 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
         lsum *= alpha;
         m = mn;
       }
-      float ls = 0.f;
-      const float nm = -m;
+      // m is -inf only while every score the row has seen is -inf (masked):
+      // then exp2(-inf + 0) = 0 without a select per score.  lsum holds this
+      // lane half's keys only (both halves share m); the halves are added
+      // once, after the last tile.
+      const float nm = m == -INFINITY ? 0.f : -m;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = m == -INFINITY ? 0.f : fast_exp2(fmaf(s[tt][r], c, nm));
+          const float p = fast_exp2(fmaf(s[tt][r], c, nm));
           s[tt][r] = p;
-          ls += p;
+          lsum += p;
         }
-      ls += __shfl_xor(ls, 32, 64);
-      lsum += ls;
       const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
-      cols_times<HD>(o, Vs[buf], pj);                    // O^T += V^T P^T
+      cols_times<HD>(o, Vc, pj);                         // O^T += V^T P^T
     }
     lds_wait();
     dma_wait();
     __syncthreads();
+  };
+  for (int it = 0; it < n_kt; it += 2) {
+    tile(it, Ks[0], Vs[0], Ks[1], Vs[1]);
+    if (it + 1 < n_kt) tile(it + 1, Ks[1], Vs[1], Ks[0], Vs[0]);
   }
+  lsum += __shfl_xor(lsum, 32, 64);
   if (!qv) return;
   const float inv = 1.f / lsum;
   bf16_t *out = (bf16_t *)a.o + (int64_t)q * a.Hq * HD + h * HD;
@@ -401,14 +415,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n
       *(u32x2_t *)(out + d) = u32x2_t{pack2(o[i][4 * r4] * inv, o[i][4 * r4 + 1] * inv),
                                       pack2(o[i][4 * r4 + 2] * inv, o[i][4 * r4 + 3] * inv)};
     }
-  if (hl == 0) a.lse[(int64_t)h * a.n_tok + q] = (m + log2f(lsum)) / kLog2e;
+  // log-sum-exp of the scaled scores in log2 units (the backward passes
+  // work in exp2): log2(sum exp2(s c)) = m + log2(lsum)
+  if (hl == 0) a.lse[(int64_t)h * a.n_tok + q] = m + log2f(lsum);
 }
 
 // ------------------------------------------------------------------ dQ
 // Same workgroup shape as the forward; a lane owns one query.
-template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int n_qt) {
-  using TT = TokTile<HD>;
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int n_qt) {
+  using TT = TokTile<HD, NW>;
   constexpr int KS = HD / 16, DT = HD / 32;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
@@ -418,7 +434,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const int g = (h * a.Hkv) / a.Hq;
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hl = lane >> 5, lq = lane & 31;
-  const int q0 = qt * 128;
+  const int q0 = qt * 32 * NW;
   const int q = q0 + 32 * w + lq;
   const bool qv = q < a.n_tok;
   const int qs = qv ? seg_start(a, q) : a.n_tok;
@@ -426,7 +442,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
   const bf16_t *dout = (const bf16_t *)a.dout;
   if (threadIdx.x == 0) {
     rng[0] = seg_start(a, q0);
-    rng[1] = min(q0 + 127, a.n_tok - 1);
+    rng[1] = min(q0 + 32 * NW - 1, a.n_tok - 1);
   }
   bf16x8_t qf[KS], df[KS];
 #pragma unroll
@@ -439,7 +455,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
     qf[kk] = __builtin_bit_cast(bf16x8_t, x);
     df[kk] = __builtin_bit_cast(bf16x8_t, y);
   }
-  const float lse2 = qv ? a.lse[(int64_t)h * a.n_tok + q] * kLog2e : 0.f;
+  const float lse2 = qv ? a.lse[(int64_t)h * a.n_tok + q] : 0.f;       // log2 units
   const float dlt = qv ? a.delta[(int64_t)h * a.n_tok + q] : 0.f;
   f32x16_t acc[DT];
 #pragma unroll
@@ -508,13 +524,13 @@ __global__ __launch_bounds__(256, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int
 }
 
 // ------------------------------------------------------------------ dK, dV
-// One workgroup: 128 keys of one key/value head (4 waves of 32), a lane owns
-// one key; it walks every query head of the group and the segment's query
-// tiles of 64 after the keys, double-buffered (Q, dO and the queries' LSE and
-// delta).
-template <int HD>
-__global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /*n_kt*/) {
-  using TT = TokTile<HD>;
+// One workgroup: 32 * NW keys of one key/value head (NW waves of 32), a lane
+// owns one key; it walks every query head of the group and the segment's
+// query tiles of 64 after the keys, double-buffered (Q, dO and the queries'
+// LSE and delta) and shared by all the waves.
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /*n_kt*/) {
+  using TT = TokTile<HD, NW>;
   constexpr int KS = HD / 16, DT = HD / 32;
   __shared__ __attribute__((aligned(16))) uint16_t Qs[2][TT::kHalfs];
   __shared__ __attribute__((aligned(16))) uint16_t Ds[2][TT::kHalfs];
@@ -525,13 +541,13 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
   const int ldo = a.Hq * HD;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hl = lane >> 5, lq = lane & 31;
-  const int k0 = kt * 128;
+  const int k0 = kt * 32 * NW;
   const int kv = k0 + 32 * w + lq;            // the key row this lane owns
   const bool kvv = kv < a.n_tok;
   const int ke = kvv ? seg_end(a, kv) : 0;    // queries of the key: [kv, ke)
   const bf16_t *qkv = (const bf16_t *)a.qkv;
   const bf16_t *dout = (const bf16_t *)a.dout;
-  if (threadIdx.x == 0) rng[0] = seg_end(a, min(k0 + 127, a.n_tok - 1));
+  if (threadIdx.x == 0) rng[0] = seg_end(a, min(k0 + 32 * NW - 1, a.n_tok - 1));
   bf16x8_t kf[KS], vf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
@@ -558,7 +574,7 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /
   const int n_qb = q_hi > k0 ? (q_hi - k0 + kTR - 1) / kTR : 0;
   const int n_it = group * n_qb;
   // item it: query head g*group + it / n_qb, query tile k0 + 64 * (it % n_qb)
-  auto load_item = [&](int it, int buf) {
+  auto load_item = [&](int it, int buf) __attribute__((always_inline)) {
     const int h = g * group + it / n_qb, qb = k0 + kTR * (it % n_qb);
     TT::load(Qs[buf], qkv + h * HD, ld, qb, q_hi);
     TT::load(Ds[buf], dout + h * HD, ldo, qb, q_hi);
@@ -571,62 +587,72 @@ __global__ __launch_bounds__(256) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /
   if (n_it > 0) load_item(0, 0);
   dma_wait();
   __syncthreads();
-  for (int it = 0; it < n_it; ++it) {
-    const int buf = it & 1, qb = k0 + kTR * (it % n_qb);
-    if (it + 1 < n_it) load_item(it + 1, buf ^ 1);
+  // query rows 32tt..32tt+31 of a staged tile: S = Q K^T and dP = dO V^T
+  // [32 queries x 32 keys], the softmax terms, then dV^T += dO^T P and dK^T
+  // += Q^T dS over those 32 queries
+  auto half = [&](const int tt, const int qb, const bool full, const uint16_t *Qc,
+                  const uint16_t *Dc, const float *Lc,
+                  const float *Dlc) __attribute__((always_inline)) {
+    f32x16_t s, dp;   // set by rows_times_pair
+    rows_times_pair<HD>(s, dp, Qc, Dc, 32 * tt, kf, vf);
+    // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4 (their
+    // LSE in log2 units and delta); read after the products so that they are
+    // not live across them
+    f32x4_t lv[4], dl[4];
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      lv[r4] = lds_read_f4(Lc + 32 * tt + 8 * r4 + 4 * hl);
+      dl[r4] = lds_read_f4(Dlc + 32 * tt + 8 * r4 + 4 * hl);
+    }
+    // the reads above are inline assembly: wait for them, and pass the
+    // values through empty statements so no use moves above the wait
+    lds_wait();
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      asm volatile("" : "+v"(lv[r4]));
+      asm volatile("" : "+v"(dl[r4]));
+    }
+    if (full) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(s[r], c, -lv[r >> 2][r & 3]));
+        s[r] = p;
+        dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
+      }
+    } else {
+      // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
+      const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+        const bool ok = off >= lo && off < hi;
+        const float p = ok ? fast_exp2(fmaf(s[r], c, -lv[r >> 2][r & 3])) : 0.f;
+        s[r] = p;
+        dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
+      }
+    }
+    const bf16x8_t pj[2] = {pack8(s, 0), pack8(s, 8)};
+    const bf16x8_t sj[2] = {pack8(dp, 0), pack8(dp, 8)};
+    cols_times_half<HD>(dv, Dc, 32 * tt, pj);       // dV^T += dO^T P
+    cols_times_half<HD>(dk, Qc, 32 * tt, sj);       // dK^T += Q^T dS
+  };
+  // item it reads stage b and prefetches item it + 1 into the other stage;
+  // two items per pass so that both stages are fixed LDS addresses
+  auto item = [&](const int it, const int b) __attribute__((always_inline)) {
+    const int qb = k0 + kTR * (it % n_qb);
+    if (it + 1 < n_it) load_item(it + 1, b ^ 1);
     if (qb + kTR - 1 >= w_lo && qb <= w_hi) {
       const bool full = qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke;   // every query sees every key
-      // query rows 32tt..32tt+31 of the tile at a time: S = Q K^T and
-      // dP = dO V^T [32 queries x 32 keys], the softmax terms, then dV^T +=
-      // dO^T P and dK^T += Q^T dS over those 32 queries (not unrolled: one
-      // half's S, dP and softmax terms live at a time)
-#pragma unroll 1
-      for (int tt = 0; tt < 2; ++tt) {
-        f32x16_t s, dp;   // set by rows_times_pair
-        // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4
-        f32x4_t lv[4], dl[4];
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          lv[r4] = lds_read_f4(Ls[buf] + 32 * tt + 8 * r4 + 4 * hl);
-          dl[r4] = lds_read_f4(Dl[buf] + 32 * tt + 8 * r4 + 4 * hl);
-        }
-        // the reads above are inline assembly: wait for them, and pass the
-        // values through empty statements so no use moves above the wait
-        lds_wait();
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          asm volatile("" : "+v"(lv[r4]));
-          asm volatile("" : "+v"(dl[r4]));
-        }
-        rows_times_pair<HD>(s, dp, Qs[buf], Ds[buf], 32 * tt, kf, vf);
-        if (full) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float p = fast_exp2(s[r] * c - lv[r >> 2][r & 3] * kLog2e);
-            s[r] = p;
-            dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
-          }
-        } else {
-          // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
-          const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
-            const bool ok = off >= lo && off < hi;
-            const float p = ok ? fast_exp2(s[r] * c - lv[r >> 2][r & 3] * kLog2e) : 0.f;
-            s[r] = p;
-            dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
-          }
-        }
-        const bf16x8_t pj[2] = {pack8(s, 0), pack8(s, 8)};
-        const bf16x8_t sj[2] = {pack8(dp, 0), pack8(dp, 8)};
-        cols_times_half<HD>(dv, Ds[buf], 32 * tt, pj);       // dV^T += dO^T P
-        cols_times_half<HD>(dk, Qs[buf], 32 * tt, sj);       // dK^T += Q^T dS
-      }
+      half(0, qb, full, Qs[b], Ds[b], Ls[b], Dl[b]);
+      half(1, qb, full, Qs[b], Ds[b], Ls[b], Dl[b]);
     }
     lds_wait();
     dma_wait();
     __syncthreads();
+  };
+  for (int it = 0; it < n_it; it += 2) {
+    item(it, 0);
+    if (it + 1 < n_it) item(it + 1, 1);
   }
   if (!kvv) return;
   bf16_t *base = (bf16_t *)a.dqkv + (int64_t)kv * ld;
@@ -665,27 +691,32 @@ bool attn_mfma_supported(int hd, const void *p0, const void *p1, const void *p2)
   return (hd == 64 || hd == 128) && aligned16(p0) && aligned16(p1) && aligned16(p2);
 }
 
+// Waves per workgroup: every wave of a workgroup shares each staged K/V
+// (forward, dQ) or Q/dO (dK/dV) tile.
+constexpr int kFwdWaves = 8, kDqWaves = 8, kDkvWaves = 4;
+
 int attn_fwd_mfma(const AttnArgs &a, hipStream_t s) {
-  const int n_qt = (a.n_tok + 127) / 128;
+  const int n_qt = (a.n_tok + 32 * kFwdWaves - 1) / (32 * kFwdWaves);
   const unsigned grid = (unsigned)n_qt * a.Hq;
   const int tk = timing_begin(s, AJ_KC_ATTN_FWD, 0.0);
-  if (a.hd == 128) attn_fwd_mfma_kernel<128><<<grid, 256, 0, s>>>(a, n_qt);
-  else attn_fwd_mfma_kernel<64><<<grid, 256, 0, s>>>(a, n_qt);
+  if (a.hd == 128) attn_fwd_mfma_kernel<128, kFwdWaves><<<grid, 64 * kFwdWaves, 0, s>>>(a, n_qt);
+  else attn_fwd_mfma_kernel<64, kFwdWaves><<<grid, 64 * kFwdWaves, 0, s>>>(a, n_qt);
   timing_end(s, tk);
   return check_launch("attention forward (mfma)");
 }
 
 int attn_bwd_mfma(const AttnBwdArgs &a, hipStream_t s) {
-  const int n_qt = (a.n_tok + 127) / 128;
+  const int n_qt = (a.n_tok + 32 * kDqWaves - 1) / (32 * kDqWaves);
+  const int n_kt = (a.n_tok + 32 * kDkvWaves - 1) / (32 * kDkvWaves);
   const int64_t nd = (int64_t)a.n_tok * a.Hq;
   const int tk = timing_begin(s, AJ_KC_ATTN_BWD, 0.0);
   attn_delta_bf16_kernel<<<(unsigned)((nd + 3) / 4), 256, 0, s>>>(a);
   if (a.hd == 128) {
-    attn_dq_mfma_kernel<128><<<(unsigned)n_qt * a.Hq, 256, 0, s>>>(a, n_qt);
-    attn_dkv_mfma_kernel<128><<<(unsigned)n_qt * a.Hkv, 256, 0, s>>>(a, n_qt);
+    attn_dq_mfma_kernel<128, kDqWaves><<<(unsigned)n_qt * a.Hq, 64 * kDqWaves, 0, s>>>(a, n_qt);
+    attn_dkv_mfma_kernel<128, kDkvWaves><<<(unsigned)n_kt * a.Hkv, 64 * kDkvWaves, 0, s>>>(a, n_kt);
   } else {
-    attn_dq_mfma_kernel<64><<<(unsigned)n_qt * a.Hq, 256, 0, s>>>(a, n_qt);
-    attn_dkv_mfma_kernel<64><<<(unsigned)n_qt * a.Hkv, 256, 0, s>>>(a, n_qt);
+    attn_dq_mfma_kernel<64, kDqWaves><<<(unsigned)n_qt * a.Hq, 64 * kDqWaves, 0, s>>>(a, n_qt);
+    attn_dkv_mfma_kernel<64, kDkvWaves><<<(unsigned)n_kt * a.Hkv, 64 * kDkvWaves, 0, s>>>(a, n_kt);
   }
   timing_end(s, tk);
   return check_launch("attention backward (mfma)");

@@ -106,7 +106,8 @@ struct AttnArgs {
   const int32_t *cu_seqlens;
   const void *qkv;      // [n_tok, (Hq+2Hkv)*hd], q and k already rotated
   void *o;              // [n_tok, Hq*hd]
-  float *lse;           // [Hq, n_tok]
+  float *lse;           // [Hq, n_tok] log-sum-exp of the scaled scores (log2 units on
+                        // the matrix-core path, natural log on the plain one)
   float scale;
 };
 template <typename T>
