@@ -66,13 +66,15 @@ def log(msg):
 
 
 # HBM bytes per launch of the dominant kernel (the TN and NN long-reduction
-# GEMMs take nearly the same time per step here, so both are listed), from two rocprofv3 --pmc passes
+# GEMMs take nearly the same time per step, so both are listed), from two rocprofv3 --pmc passes
 # (FETCH_SIZE, WRITE_SIZE) over the same bench command, each scaled by the
 # counter's reading for a plain copy of known size.  Keyed by (kernel class,
 # workload); `sources` are hashed so that a changed kernel reports null.
 TRAFFIC = {
     ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.7e6, "sources": "7e2861621a20400e"},
     ("gemm4_nn", "block1.5b-64x8"): {"bytes_per_launch": 5465.2e6, "sources": "7e2861621a20400e"},
+    ("gemm4_tn", "long32b-8x60"): {"bytes_per_launch": 11417.0e6, "sources": "7e2861621a20400e"},
+    ("gemm4_nn", "long32b-8x60"): {"bytes_per_launch": 11233.0e6, "sources": "7e2861621a20400e"},
 }
 
 
