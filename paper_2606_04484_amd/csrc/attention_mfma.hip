@@ -101,6 +101,11 @@ AJ_DEV uint32_t lds_addr(const void *p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
 
+template <int HD>
+AJ_DEV int tok_swz(int r) {
+  return HD == 128 ? ((r & 7) << 1) | ((r >> 3) & 1) : (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+}
+
 template <int HD, int NW = 4>
 struct TokTile {
   static constexpr int CPR = HD / 8;                 // 16-byte chunks per row
@@ -108,10 +113,9 @@ struct TokTile {
   static constexpr int kInstr = kTR * HD * 2 / 1024 / NW;  // per wave (NW waves)
   static_assert(kInstr >= 1 && kTR * HD * 2 / 1024 % NW == 0, "tile copy split");
   static constexpr int kHalfs = kTR * HD;
+  static constexpr int kBytes = kHalfs * 2;
 
-  AJ_DEV static int swz(int r) {
-    return HD == 128 ? ((r & 7) << 1) | ((r >> 3) & 1) : (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
-  }
+  AJ_DEV static int swz(int r) { return tok_swz<HD>(r); }
   // token rows [r0, r0 + 64) of `src` (row stride ld elements); rows at or
   // past `rows` copy row rows - 1 (their products are masked out)
   AJ_DEV static void load(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows) {
@@ -127,30 +131,60 @@ struct TokTile {
                                        16, 0, 0);
     }
   }
-  // MFMA operand: rows = tokens [t0, t0 + 32), k = features [f0, f0 + 16)
-  AJ_DEV static bf16x8_t row_frag(const uint16_t *lds, int t0, int f0) {
-    const int lane = threadIdx.x & 63;
-    const int r = t0 + (lane & 31), c = (f0 >> 3) + (lane >> 5);
-    const uint32_t a = lds_addr(lds + r * HD + 8 * (c ^ swz(r)));
+};
+
+// Per-lane LDS addresses of the fragment reads of TokTile tiles.  Every
+// staged tile of a kernel sits at a fixed byte offset in one __shared__
+// arena; a read passes that offset (plus its token row block's) as the
+// instruction's immediate offset, so that a few address registers serve
+// every tile, stage and row block.  The swizzle depends only on the token
+// row mod 16 (row blocks start at multiples of 16), and a k-slice or a
+// feature block enters the chunk index in bits that the lane's own part
+// leaves free, so it is the lane's base XOR a constant.
+template <int HD>
+struct TileLanes {
+  static constexpr int KS = HD / 16, DT = HD / 32, RB = HD * 2;   // RB: bytes per token row
+  uint32_t row[KS];      // row fragment of k-slice kk
+  uint32_t col[DT][2];   // column fragment of feature block i: token rows r and r + 8
+
+  AJ_DEV void init(const void *arena) {
+    const int lane = threadIdx.x & 63, l = lane & 31, hl = lane >> 5;
+    const int g = lane >> 4, s = lane & 15;
+    const uint32_t base = lds_addr(arena);
+    // row fragments: token row l, chunk 2kk + hl
+    const uint32_t rb = l * RB + 16 * (hl ^ tok_swz<HD>(l));
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) row[kk] = base + (rb ^ (32 * kk));
+    // column fragments (ds_read_b64_tr_b16, see col_frag): source lane s of
+    // 16-lane group g addresses token row r = 4(g/2) + s/4 and features
+    // 32i + 16(g%2) + 4(s%4)..+3, i.e. chunk 4i + c0 at byte 8(s%2) in it;
+    // row r + 8 has the swizzle of row r with bit 0 flipped
+    const int r = 4 * (g >> 1) + (s >> 2), c0 = 2 * (g & 1) + ((s >> 1) & 1);
+    const uint32_t cb = r * RB + 16 * (c0 ^ tok_swz<HD>(r)) + 8 * (s & 1);
+#pragma unroll
+    for (int i = 0; i < DT; ++i) {
+      col[i][0] = base + (cb ^ (64 * i));
+      col[i][1] = base + 8 * RB + (cb ^ (64 * i) ^ 16);
+    }
+  }
+  // MFMA operand: rows = tokens [t0, t0 + 32) of the tile at byte offset off
+  // (t0 * RB included in off), k = features [16kk, 16kk + 16)
+  AJ_DEV bf16x8_t row_frag(const int off, const int kk) const {
     bf16x8_t v;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(row[kk]), "i"(off) : "memory");
     return v;
   }
-  // MFMA operand: rows = features [f0, f0 + 32), k = 8 tokens in the order
+  // MFMA operand: rows = features [32i, 32i + 32), k = 8 tokens in the order
   // the accumulator-to-operand packing (pack8) produces: lane half h holds
-  // tokens t0 + 4h + 0..3 and t0 + 8 + 4h + 0..3.  ds_read_b64_tr_b16: in a
-  // 16-lane group, lane j receives element j%4 of the 4-element run addressed
-  // by lane 4e + j/4; source lane s addresses token row t + s/4, features
-  // fb + 4*(s%4)..+3, so lane j receives feature fb + j at 4 tokens.
-  AJ_DEV static bf16x8_t col_frag(const uint16_t *lds, int f0, int t0) {
-    const int lane = threadIdx.x & 63, g = lane >> 4, s = lane & 15;
-    const int f = f0 + 16 * (g & 1) + 4 * (s & 3);
-    const int r = t0 + 4 * (g >> 1) + (s >> 2);
-    const uint32_t a0 = lds_addr(lds + r * HD + 8 * ((f >> 3) ^ swz(r)) + (f & 7));
-    const uint32_t a1 = lds_addr(lds + (r + 8) * HD + 8 * ((f >> 3) ^ swz(r + 8)) + (f & 7));
+  // tokens t0 + 4h + 0..3 and t0 + 8 + 4h + 0..3 (t0 * RB included in off).
+  // ds_read_b64_tr_b16: in a 16-lane group, lane j receives element j%4 of
+  // the 4-element run addressed by lane 4e + j/4; source lane s addresses
+  // token row t + s/4, features fb + 4*(s%4)..+3, so lane j receives feature
+  // fb + j at 4 tokens.
+  AJ_DEV bf16x8_t col_frag(const int off, const int i) const {
     u32x2_t lo, hi;
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a0) : "memory");
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a1) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(lo) : "v"(col[i][0]), "i"(off) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(hi) : "v"(col[i][1]), "i"(off) : "memory");
     return __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
   }
 };
@@ -166,32 +200,34 @@ AJ_DEV void lds_wait(bf16x8_t (&v)[N]) {
 AJ_DEV void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-// 4 consecutive floats from LDS (inline assembly, like the fragment reads:
-// the tile copies of the next item may still be in flight)
-AJ_DEV f32x4_t lds_read_f4(const float *p) {
+// 4 consecutive floats from LDS at byte address a + off (inline assembly,
+// like the fragment reads: the tile copies of the next item may still be in
+// flight)
+AJ_DEV f32x4_t lds_read_f4(const uint32_t a, const int off) {
   f32x4_t v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(p)) : "memory");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(off) : "memory");
   return v;
 }
 AJ_DEV void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile) += tile rows x B,
-// B = per-lane operands bv[kk] (k = features 16kk..16kk+15); with kZero the
-// products start from zero (acc is not read: the first MFMA of each chain
-// takes the constant 0 as its accumulator)
+// acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile at byte offset off)
+// += tile rows x B, B = per-lane operands bv[kk] (k = features
+// 16kk..16kk+15); with kZero the products start from zero (acc is not read:
+// the first MFMA of each chain takes the constant 0 as its accumulator)
 template <int HD, bool kZero = false>
-AJ_DEV void rows_times(f32x16_t (&acc)[2], const uint16_t *tile, const bf16x8_t (&bv)[HD / 16]) {
-  constexpr int KS = HD / 16;
+AJ_DEV void rows_times(f32x16_t (&acc)[2], const TileLanes<HD> &L, const int off,
+                       const bf16x8_t (&bv)[HD / 16]) {
+  constexpr int KS = HD / 16, RB = HD * 2;
   bf16x8_t f[2][2];
-  f[0][0] = TokTile<HD>::row_frag(tile, 0, 0);
-  f[0][1] = TokTile<HD>::row_frag(tile, 32, 0);
+  f[0][0] = L.row_frag(off, 0);
+  f[0][1] = L.row_frag(off + 32 * RB, 0);
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
     const int cur = kk & 1;
     lds_wait(f[cur]);
     if (kk + 1 < KS) {
-      f[cur ^ 1][0] = TokTile<HD>::row_frag(tile, 0, 16 * (kk + 1));
-      f[cur ^ 1][1] = TokTile<HD>::row_frag(tile, 32, 16 * (kk + 1));
+      f[cur ^ 1][0] = L.row_frag(off, kk + 1);
+      f[cur ^ 1][1] = L.row_frag(off + 32 * RB, kk + 1);
     }
     const bool fresh = kZero && kk == 0;
     acc[0] = mfma(f[cur][0], bv[kk], fresh ? f32x16_t{} : acc[0]);
@@ -199,14 +235,16 @@ AJ_DEV void rows_times(f32x16_t (&acc)[2], const uint16_t *tile, const bf16x8_t 
   }
 }
 
-// acc[i] (features 32i..32i+31) += tile^T x P, P given per 16-token chunk j as
-// packed accumulator halves pj[j] (tokens 32(j/2) + 16(j%2) + pack8 order)
+// acc[i] (features 32i..32i+31) += tile^T x P for the tile at byte offset
+// off, P given per 16-token chunk j as packed accumulator halves pj[j]
+// (tokens 32(j/2) + 16(j%2) + pack8 order)
 template <int HD>
-AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const uint16_t *tile, const bf16x8_t (&pj)[4]) {
-  constexpr int DT = HD / 32;
+AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const int off,
+                       const bf16x8_t (&pj)[4]) {
+  constexpr int DT = HD / 32, RB = HD * 2;
   bf16x8_t f[2][DT];
 #pragma unroll
-  for (int i = 0; i < DT; ++i) f[0][i] = TokTile<HD>::col_frag(tile, 32 * i, 0);
+  for (int i = 0; i < DT; ++i) f[0][i] = L.col_frag(off, i);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int cur = j & 1;
@@ -214,7 +252,7 @@ AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const uint16_t *tile, const bf1
     if (j + 1 < 4) {
 #pragma unroll
       for (int i = 0; i < DT; ++i)
-        f[cur ^ 1][i] = TokTile<HD>::col_frag(tile, 32 * i, 32 * ((j + 1) >> 1) + 16 * ((j + 1) & 1));
+        f[cur ^ 1][i] = L.col_frag(off + (32 * ((j + 1) >> 1) + 16 * ((j + 1) & 1)) * RB, i);
     }
 #pragma unroll
     for (int i = 0; i < DT; ++i) acc[i] = mfma(f[cur][i], pj[j], acc[i]);
@@ -231,25 +269,26 @@ AJ_DEV void lds_wait_n(int n) {
   }
 }
 
-// One 32-row tile (token rows t0..t0+31) of two staged tiles against the
-// lane's operands: sa = ta rows x ka, sb = tb rows x kb (k = features; the
-// incoming sa, sb are not read).
+// One 32-row block (token rows t0..t0+31) of two staged tiles, at byte
+// offsets offa and offb, against the lane's operands: sa = ta rows x ka,
+// sb = tb rows x kb (k = features; the incoming sa, sb are not read).
 // Fragments are read two k-steps ahead; each step waits only for its own.
 template <int HD>
-AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, const uint16_t *tb,
-                            int t0, const bf16x8_t (&ka)[HD / 16], const bf16x8_t (&kb)[HD / 16]) {
-  constexpr int KS = HD / 16;
+AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const TileLanes<HD> &L, const int offa,
+                            const int offb, const int t0, const bf16x8_t (&ka)[HD / 16],
+                            const bf16x8_t (&kb)[HD / 16]) {
+  constexpr int KS = HD / 16, RB = HD * 2;
   bf16x8_t fa[KS], fb[KS];
 #pragma unroll
   for (int kk = 0; kk < 2 && kk < KS; ++kk) {
-    fa[kk] = TokTile<HD>::row_frag(ta, t0, 16 * kk);
-    fb[kk] = TokTile<HD>::row_frag(tb, t0, 16 * kk);
+    fa[kk] = L.row_frag(offa + t0 * RB, kk);
+    fb[kk] = L.row_frag(offb + t0 * RB, kk);
   }
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
     if (kk + 2 < KS) {
-      fa[kk + 2] = TokTile<HD>::row_frag(ta, t0, 16 * (kk + 2));
-      fb[kk + 2] = TokTile<HD>::row_frag(tb, t0, 16 * (kk + 2));
+      fa[kk + 2] = L.row_frag(offa + t0 * RB, kk + 2);
+      fb[kk + 2] = L.row_frag(offb + t0 * RB, kk + 2);
     }
     // reads issued after this step's pair: those of steps kk+1 .. min(kk+2, KS-1)
     lds_wait_n(2 * ((kk + 2 < KS ? kk + 2 : KS - 1) - kk));
@@ -260,24 +299,25 @@ AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const uint16_t *ta, cons
   }
 }
 
-// acc[i] (features 32i..32i+31) += tile^T x P over tokens t0..t0+31, P given
-// as the two packed accumulator halves of that 32-row tile (pack8 order).
-// One feature block at a time, the next block's two fragments read while the
-// current block's MFMAs issue (four fragments live, not eight).
+// acc[i] (features 32i..32i+31) += tile^T x P over tokens t0..t0+31 of the
+// tile at byte offset off, P given as the two packed accumulator halves of
+// that 32-row block (pack8 order).  One feature block at a time, the next
+// block's two fragments read while the current block's MFMAs issue (four
+// fragments live, not eight).
 template <int HD>
-AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const uint16_t *tile, int t0,
-                            const bf16x8_t (&pj)[2]) {
-  constexpr int DT = HD / 32;
+AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const int off,
+                            const int t0, const bf16x8_t (&pj)[2]) {
+  constexpr int DT = HD / 32, RB = HD * 2;
   bf16x8_t f[2][2];
-  f[0][0] = TokTile<HD>::col_frag(tile, 0, t0);
-  f[0][1] = TokTile<HD>::col_frag(tile, 0, t0 + 16);
+  f[0][0] = L.col_frag(off + t0 * RB, 0);
+  f[0][1] = L.col_frag(off + (t0 + 16) * RB, 0);
 #pragma unroll
   for (int i = 0; i < DT; ++i) {
     const int cur = i & 1;
     lds_wait(f[cur]);
     if (i + 1 < DT) {
-      f[cur ^ 1][0] = TokTile<HD>::col_frag(tile, 32 * (i + 1), t0);
-      f[cur ^ 1][1] = TokTile<HD>::col_frag(tile, 32 * (i + 1), t0 + 16);
+      f[cur ^ 1][0] = L.col_frag(off + t0 * RB, i + 1);
+      f[cur ^ 1][1] = L.col_frag(off + (t0 + 16) * RB, i + 1);
     }
     acc[i] = mfma(f[cur][0], pj[0], acc[i]);
     acc[i] = mfma(f[cur][1], pj[1], acc[i]);
@@ -290,10 +330,12 @@ AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const uint16_t *tile, int 
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma_kernel(AttnArgs a, int n_qt) {
   using TT = TokTile<HD, NW>;
-  constexpr int KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
+  constexpr int KS = HD / 16, DT = HD / 32, T = TT::kBytes;
+  // two stages of a K and a V tile: K at 0 and T, V at 2T and 3T (bytes)
+  __shared__ __attribute__((aligned(16))) uint16_t sm[4 * TT::kHalfs];
   __shared__ int rng[2];
+  TileLanes<HD> L;
+  L.init(sm);
   const int t = work_item(blockIdx.x);
   const int h = t % a.Hq, qt = n_qt - 1 - t / a.Hq;
   const int g = (h * a.Hkv) / a.Hq;
@@ -329,22 +371,21 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma_kernel(AttnArgs a, i
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
   const bf16_t *kbase = qkv + (a.Hq + g) * HD, *vbase = qkv + (a.Hq + a.Hkv + g) * HD;
-  TT::load(Ks[0], kbase, ld, kv_lo, kv_hi + 1);
-  TT::load(Vs[0], vbase, ld, kv_lo, kv_hi + 1);
+  TT::load(sm, kbase, ld, kv_lo, kv_hi + 1);
+  TT::load(sm + 2 * TT::kHalfs, vbase, ld, kv_lo, kv_hi + 1);
   dma_wait();
   __syncthreads();
-  // tile it reads stage (Kc, Vc) and prefetches tile it + 1 into (Kn, Vn); the
-  // loop runs two tiles per pass so that both stages are fixed LDS addresses
-  auto tile = [&](const int it, uint16_t *Kc, uint16_t *Vc, uint16_t *Kn,
-                  uint16_t *Vn) __attribute__((always_inline)) {
+  // tile it reads stage st and prefetches tile it + 1 into the other stage;
+  // the loop runs two tiles per pass so that both stages are fixed offsets
+  auto tile = [&](const int it, const int st) __attribute__((always_inline)) {
     const int k0 = kv_lo + it * kTR;
     if (it + 1 < n_kt) {
-      TT::load(Kn, kbase, ld, k0 + kTR, kv_hi + 1);
-      TT::load(Vn, vbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(sm + (st ^ 1) * TT::kHalfs, kbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(sm + (2 + (st ^ 1)) * TT::kHalfs, vbase, ld, k0 + kTR, kv_hi + 1);
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       f32x16_t s[2];
-      rows_times<HD, true>(s, Kc, qf);                   // S^T = K Q^T (unscaled)
+      rows_times<HD, true>(s, L, st * T, qf);            // S^T = K Q^T (unscaled)
       float mx = -INFINITY;
       if (k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w) {   // every key visible to every row
 #pragma unroll
@@ -393,15 +434,15 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma_kernel(AttnArgs a, i
           lsum += p;
         }
       const bf16x8_t pj[4] = {pack8(s[0], 0), pack8(s[0], 8), pack8(s[1], 0), pack8(s[1], 8)};
-      cols_times<HD>(o, Vc, pj);                         // O^T += V^T P^T
+      cols_times<HD>(o, L, (2 + st) * T, pj);            // O^T += V^T P^T
     }
     lds_wait();
     dma_wait();
     __syncthreads();
   };
   for (int it = 0; it < n_kt; it += 2) {
-    tile(it, Ks[0], Vs[0], Ks[1], Vs[1]);
-    if (it + 1 < n_kt) tile(it + 1, Ks[1], Vs[1], Ks[0], Vs[0]);
+    tile(it, 0);
+    if (it + 1 < n_kt) tile(it + 1, 1);
   }
   lsum += __shfl_xor(lsum, 32, 64);
   if (!qv) return;
@@ -425,10 +466,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma_kernel(AttnArgs a, i
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a, int n_qt) {
   using TT = TokTile<HD, NW>;
-  constexpr int KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][TT::kHalfs];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][TT::kHalfs];
+  constexpr int KS = HD / 16, DT = HD / 32, T = TT::kBytes;
+  // two stages of a K and a V tile: K at 0 and T, V at 2T and 3T (bytes)
+  __shared__ __attribute__((aligned(16))) uint16_t sm[4 * TT::kHalfs];
   __shared__ int rng[2];
+  TileLanes<HD> L;
+  L.init(sm);
   const int t = work_item(blockIdx.x);
   const int h = t % a.Hq, qt = n_qt - 1 - t / a.Hq;
   const int g = (h * a.Hkv) / a.Hq;
@@ -470,46 +513,53 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
   const int kv_lo = rng[0], kv_hi = rng[1];
   const int n_kt = (kv_hi - kv_lo + kTR) / kTR;
   const bf16_t *kbase = qkv + (a.Hq + g) * HD, *vbase = qkv + (a.Hq + a.Hkv + g) * HD;
-  TT::load(Ks[0], kbase, ld, kv_lo, kv_hi + 1);
-  TT::load(Vs[0], vbase, ld, kv_lo, kv_hi + 1);
+  TT::load(sm, kbase, ld, kv_lo, kv_hi + 1);
+  TT::load(sm + 2 * TT::kHalfs, vbase, ld, kv_lo, kv_hi + 1);
   dma_wait();
   __syncthreads();
-  for (int it = 0; it < n_kt; ++it) {
-    const int buf = it & 1, k0 = kv_lo + it * kTR;
+  // key rows 32tt..32tt+31 of the tile at stage st: S^T = K Q^T, dP^T =
+  // V dO^T, the softmax terms, then dQ^T += K^T dS^T over those 32 keys
+  auto half = [&](const int tt, const int st, const int k0,
+                  const bool full) __attribute__((always_inline)) {
+    f32x16_t s, dp;   // set by rows_times_pair
+    rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, qf, df);
+    if (full) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] - dlt);
+    } else {
+      // key k0 + 4hl + off (off a constant per element) is visible iff
+      // lo <= off <= hi
+      const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
+        const float p = (off >= lo && off <= hi) ? fast_exp2(fmaf(s[r], c, -lse2)) : 0.f;
+        s[r] = p * (dp[r] - dlt);
+      }
+    }
+    const bf16x8_t sj[2] = {pack8(s, 0), pack8(s, 8)};
+    cols_times_half<HD>(acc, L, st * T, 32 * tt, sj);   // dQ^T += K^T dS^T
+  };
+  // tile it reads stage st and prefetches tile it + 1 into the other stage;
+  // two tiles per pass so that both stages are fixed offsets
+  auto tile = [&](const int it, const int st) __attribute__((always_inline)) {
+    const int k0 = kv_lo + it * kTR;
     if (it + 1 < n_kt) {
-      TT::load(Ks[buf ^ 1], kbase, ld, k0 + kTR, kv_hi + 1);
-      TT::load(Vs[buf ^ 1], vbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(sm + (st ^ 1) * TT::kHalfs, kbase, ld, k0 + kTR, kv_hi + 1);
+      TT::load(sm + (2 + (st ^ 1)) * TT::kHalfs, vbase, ld, k0 + kTR, kv_hi + 1);
     }
     if (k0 <= w_hi && k0 + kTR - 1 >= w_lo) {
       const bool full = k0 >= w_qs && k0 + kTR - 1 <= q0 + 32 * w;   // every key visible to every row
-      // key rows 32tt..32tt+31 of the tile at a time (not unrolled: one
-      // half's S and dP live at a time): S^T = K Q^T, dP^T = V dO^T, the
-      // softmax terms, then dQ^T += K^T dS^T over those 32 keys
-#pragma unroll 1
-      for (int tt = 0; tt < 2; ++tt) {
-        f32x16_t s, dp;   // set by rows_times_pair
-        rows_times_pair<HD>(s, dp, Ks[buf], Vs[buf], 32 * tt, qf, df);
-        if (full) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] - dlt);
-        } else {
-          // key k0 + 4hl + off (off a constant per element) is visible iff
-          // lo <= off <= hi
-          const int lo = qs - k0 - 4 * hl, hi = q - k0 - 4 * hl;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
-            const float p = (off >= lo && off <= hi) ? fast_exp2(fmaf(s[r], c, -lse2)) : 0.f;
-            s[r] = p * (dp[r] - dlt);
-          }
-        }
-        const bf16x8_t sj[2] = {pack8(s, 0), pack8(s, 8)};
-        cols_times_half<HD>(acc, Ks[buf], 32 * tt, sj);  // dQ^T += K^T dS^T
-      }
+      half(0, st, k0, full);
+      half(1, st, k0, full);
     }
     lds_wait();
     dma_wait();
     __syncthreads();
+  };
+  for (int it = 0; it < n_kt; it += 2) {
+    tile(it, 0);
+    if (it + 1 < n_kt) tile(it + 1, 1);
   }
   if (!qv) return;
   bf16_t *out = (bf16_t *)a.dqkv + (int64_t)q * ld + h * HD;
@@ -531,11 +581,15 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /*n_kt*/) {
   using TT = TokTile<HD, NW>;
-  constexpr int KS = HD / 16, DT = HD / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[2][TT::kHalfs];
-  __shared__ __attribute__((aligned(16))) uint16_t Ds[2][TT::kHalfs];
-  __shared__ __attribute__((aligned(16))) float Ls[2][kTR], Dl[2][kTR];
+  constexpr int KS = HD / 16, DT = HD / 32, T = TT::kBytes;
+  // two stages of a Q and a dO tile: Q at 0 and T, dO at 2T and 3T (bytes)
+  __shared__ __attribute__((aligned(16))) uint16_t sm[4 * TT::kHalfs];
+  // two stages of the tile's LSE and delta: LSE at 0 and 256, delta at 512
+  // and 768 (bytes)
+  __shared__ __attribute__((aligned(16))) float ld_sm[4][kTR];
   __shared__ int rng[1];
+  TileLanes<HD> L;
+  L.init(sm);
   const int t = work_item(blockIdx.x);
   const int g = t % a.Hkv, kt = t / a.Hkv;   // early keys of a segment see the most queries
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
@@ -576,33 +630,34 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
   // item it: query head g*group + it / n_qb, query tile k0 + 64 * (it % n_qb)
   auto load_item = [&](int it, int buf) __attribute__((always_inline)) {
     const int h = g * group + it / n_qb, qb = k0 + kTR * (it % n_qb);
-    TT::load(Qs[buf], qkv + h * HD, ld, qb, q_hi);
-    TT::load(Ds[buf], dout + h * HD, ldo, qb, q_hi);
+    TT::load(sm + buf * TT::kHalfs, qkv + h * HD, ld, qb, q_hi);
+    TT::load(sm + (2 + buf) * TT::kHalfs, dout + h * HD, ldo, qb, q_hi);
     if (w < 2) {                // one float per lane: LSE (wave 0), delta (wave 1)
       const float *src = (w == 0 ? a.lse : a.delta) + (int64_t)h * a.n_tok + min(qb + lane, q_hi - 1);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(w == 0 ? Ls[buf] : Dl[buf]),
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)ld_sm[2 * w + buf],
                                        4, 0, 0);
     }
   };
+  // the lane's LSE / delta reads: 4 floats at 16 hl bytes past the offset
+  const uint32_t ld_lane = lds_addr(ld_sm) + 16 * hl;
   if (n_it > 0) load_item(0, 0);
   dma_wait();
   __syncthreads();
   // query rows 32tt..32tt+31 of a staged tile: S = Q K^T and dP = dO V^T
   // [32 queries x 32 keys], the softmax terms, then dV^T += dO^T P and dK^T
   // += Q^T dS over those 32 queries
-  auto half = [&](const int tt, const int qb, const bool full, const uint16_t *Qc,
-                  const uint16_t *Dc, const float *Lc,
-                  const float *Dlc) __attribute__((always_inline)) {
+  auto half = [&](const int tt, const int qb, const bool full,
+                  const int st) __attribute__((always_inline)) {
     f32x16_t s, dp;   // set by rows_times_pair
-    rows_times_pair<HD>(s, dp, Qc, Dc, 32 * tt, kf, vf);
+    rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, kf, vf);
     // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4 (their
     // LSE in log2 units and delta); read after the products so that they are
     // not live across them
     f32x4_t lv[4], dl[4];
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
-      lv[r4] = lds_read_f4(Lc + 32 * tt + 8 * r4 + 4 * hl);
-      dl[r4] = lds_read_f4(Dlc + 32 * tt + 8 * r4 + 4 * hl);
+      lv[r4] = lds_read_f4(ld_lane, st * 256 + (32 * tt + 8 * r4) * 4);
+      dl[r4] = lds_read_f4(ld_lane, (2 + st) * 256 + (32 * tt + 8 * r4) * 4);
     }
     // the reads above are inline assembly: wait for them, and pass the
     // values through empty statements so no use moves above the wait
@@ -633,8 +688,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     }
     const bf16x8_t pj[2] = {pack8(s, 0), pack8(s, 8)};
     const bf16x8_t sj[2] = {pack8(dp, 0), pack8(dp, 8)};
-    cols_times_half<HD>(dv, Dc, 32 * tt, pj);       // dV^T += dO^T P
-    cols_times_half<HD>(dk, Qc, 32 * tt, sj);       // dK^T += Q^T dS
+    cols_times_half<HD>(dv, L, (2 + st) * T, 32 * tt, pj);   // dV^T += dO^T P
+    cols_times_half<HD>(dk, L, st * T, 32 * tt, sj);         // dK^T += Q^T dS
   };
   // item it reads stage b and prefetches item it + 1 into the other stage;
   // two items per pass so that both stages are fixed LDS addresses
@@ -643,8 +698,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     if (it + 1 < n_it) load_item(it + 1, b ^ 1);
     if (qb + kTR - 1 >= w_lo && qb <= w_hi) {
       const bool full = qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke;   // every query sees every key
-      half(0, qb, full, Qs[b], Ds[b], Ls[b], Dl[b]);
-      half(1, qb, full, Qs[b], Ds[b], Ls[b], Dl[b]);
+      half(0, qb, full, b);
+      half(1, qb, full, b);
     }
     lds_wait();
     dma_wait();
