@@ -117,9 +117,13 @@ struct TokTile {
 
   AJ_DEV static int swz(int r) { return tok_swz<HD>(r); }
   // token rows [r0, r0 + 64) of `src` (row stride ld elements); rows at or
-  // past `rows` copy row rows - 1 (their products are masked out)
-  AJ_DEV static void load(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // past `rows` copy row rows - 1 (their products are masked out).  tid is
+  // the thread index (a caller short of registers passes it through an
+  // opaque copy so that the per-lane offsets are recomputed, not kept live)
+  AJ_DEV static void load(uint16_t *lds, const bf16_t *src, int64_t ld, int r0, int rows,
+                          int tid = -1) {
+    const int th = tid < 0 ? (int)threadIdx.x : tid;
+    const int lane = th & 63, wave = th >> 6;
 #pragma unroll
     for (int q = 0; q < kInstr; ++q) {
       const int blk = wave * kInstr + q;
@@ -259,14 +263,36 @@ AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const i
   }
 }
 
-// Waits until at most n LDS reads (inline assembly, issued in order) are in flight.
+// Waits until at most n LDS reads (inline assembly, issued in order) are in
+// flight (n a constant after inlining, 0..15).
 AJ_DEV void lds_wait_n(int n) {
   switch (n) {
-    case 0: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt lgkmcnt(1)" ::: "memory"); break;
     case 2: asm volatile("s_waitcnt lgkmcnt(2)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt lgkmcnt(3)" ::: "memory"); break;
     case 4: asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt lgkmcnt(5)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt lgkmcnt(6)" ::: "memory"); break;
+    case 7: asm volatile("s_waitcnt lgkmcnt(7)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt lgkmcnt(8)" ::: "memory"); break;
+    case 9: asm volatile("s_waitcnt lgkmcnt(9)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt lgkmcnt(10)" ::: "memory"); break;
+    case 11: asm volatile("s_waitcnt lgkmcnt(11)" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt lgkmcnt(12)" ::: "memory"); break;
+    case 13: asm volatile("s_waitcnt lgkmcnt(13)" ::: "memory"); break;
+    case 14: asm volatile("s_waitcnt lgkmcnt(14)" ::: "memory"); break;
     default: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
   }
+}
+
+// A workgroup barrier without the memory fence of __syncthreads (which would
+// also wait for every LDS read and copy in flight); the waits it needs are
+// explicit before it, and the empty statements keep the compiler from moving
+// memory operations across it.
+AJ_DEV void bar_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // One 32-row block (token rows t0..t0+31) of two staged tiles, at byte
@@ -576,20 +602,90 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
 // ------------------------------------------------------------------ dK, dV
 // One workgroup: 32 * NW keys of one key/value head (NW waves of 32), a lane
 // owns one key; it walks every query head of the group and the segment's
-// query tiles of 64 after the keys, double-buffered (Q, dO and the queries'
-// LSE and delta) and shared by all the waves.
+// query tiles of 64 after the keys (items), staged three deep (Q, dO and the
+// queries' LSE and delta) and shared by all the waves.
+//
+// A lane holds its key's K and V rows and its dK, dV accumulators, which
+// leaves room for one wave per SIMD: nothing else on the SIMD covers the
+// wave's waits, so each wave runs a software pipeline over the items'
+// 32-query halves u.  Step u first issues, one MFMA at a time, the products
+// dV^T += dO^T P and dK^T += Q^T dS of half u - 1 and, between them, the
+// vector work of half u's softmax terms (exponentials, masks, bf16 packing of
+// P and dS); then the products S = Q K^T and dP = dO V^T of half u + 1 into
+// the same registers.  The LDS reads of the fragments run a few MFMAs ahead,
+// and those of half u + 1's LSE and delta one step ahead.
+
+template <int V> struct Ci { static constexpr int value = V; };
+
+// fn(Ci<I>{}) for I = B..E-1, each call with its index as a constant
+template <int B, int E>
+struct StaticFor {
+  template <typename Fn> AJ_DEV static void run(Fn &fn) {
+    fn(Ci<B>{});
+    StaticFor<B + 1, E>::run(fn);
+  }
+};
+template <int E>
+struct StaticFor<E, E> {
+  template <typename Fn> AJ_DEV static void run(Fn &) {}
+};
+
+// LDS read schedule of one step: NS MFMA slots, the first NC = NS / 2 the
+// dV/dK products (fragment: two ds_read_b64_tr_b16), the rest the S/dP
+// products (fragment: one ds_read_b128).  Fragment j (the operand of MFMA j)
+// is read D slots ahead, so a step begins with its fragments 0..D-1 in
+// flight (read by the step before, after the LSE and delta of the step's
+// softmax half).  After slot NC the step reads the next half's LSE and delta
+// (8 reads).  In a step with a barrier between the two groups (the next
+// item's tile becomes visible there), the S/dP fragments are read after it.
+template <int NS, int D>
+struct DkvSched {
+  static constexpr int NC = NS / 2;
+  static constexpr int size(int f) { return f % NS < NC ? 2 : 1; }   // f >= NS: next step's
+  // fragments [first, last) read after slot s
+  static constexpr int first(int s, bool bar) {
+    return bar && s < NC - 1 && s + D >= NC ? 0 : bar && s == NC - 1 ? NC : s + D;
+  }
+  static constexpr int last(int s, bool bar) {
+    return bar && s < NC - 1 && s + D >= NC ? 0 : bar && s == NC - 1 ? NC + D : s + D + 1;
+  }
+  // LDS reads still allowed in flight when MFMA j waits for its fragment
+  static constexpr int wait(int j, bool bar) {
+    int cnt = 0, end = -1;
+    for (int f = 0; f < D; ++f) {
+      cnt += size(f);
+      if (f == j) end = cnt;
+    }
+    for (int s = 0; s < j; ++s) {
+      for (int f = first(s, bar); f < last(s, bar); ++f) {
+        cnt += size(f);
+        if (f == j) end = cnt;
+      }
+      if (s == NC) cnt += 8;
+    }
+    return cnt - end;
+  }
+  // slot of the vector work of softmax score r (0..15): spread over the
+  // dV/dK group (the LSE and delta were read before fragment 0)
+  static constexpr int score_slot(int r) { return r * NC / 16; }
+};
+
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, int /*n_kt*/) {
   using TT = TokTile<HD, NW>;
-  constexpr int KS = HD / 16, DT = HD / 32, T = TT::kBytes;
-  // two stages of a Q and a dO tile: Q at 0 and T, dO at 2T and 3T (bytes)
-  __shared__ __attribute__((aligned(16))) uint16_t sm[4 * TT::kHalfs];
-  // two stages of the tile's LSE and delta: LSE at 0 and 256, delta at 512
-  // and 768 (bytes)
-  __shared__ __attribute__((aligned(16))) float ld_sm[4][kTR];
+  constexpr int KS = HD / 16, DT = HD / 32, T = TT::kBytes, RB = HD * 2;
+  constexpr int NS = 8 * DT, NC = NS / 2, D = 3;
+  using Sched = DkvSched<NS, D>;
+  static_assert(Sched::wait(0, false) <= 15 && Sched::wait(NC + 1, false) <= 15, "lgkmcnt range");
+  // three stages of a Q tile (region smq) and a dO tile (region smd) at s*T;
+  // the stages' LSE (rows 0..2) and delta (rows 3..5)
+  __shared__ __attribute__((aligned(16))) uint16_t smq[3 * TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) uint16_t smd[3 * TT::kHalfs];
+  __shared__ __attribute__((aligned(16))) float ld_sm[6][kTR];
   __shared__ int rng[1];
-  TileLanes<HD> L;
-  L.init(sm);
+  TileLanes<HD> LQ, LD;
+  LQ.init(smq);
+  LD.init(smd);
   const int t = work_item(blockIdx.x);
   const int g = t % a.Hkv, kt = t / a.Hkv;   // early keys of a segment see the most queries
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
@@ -612,6 +708,10 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     }
     kf[kk] = __builtin_bit_cast(bf16x8_t, x);
     vf[kk] = __builtin_bit_cast(bf16x8_t, y);
+    // the key and value rows are only ever MFMA operands: keep them in the
+    // accumulation registers (the vector registers are the scarce ones)
+    asm volatile("" : "+a"(kf[kk]));
+    asm volatile("" : "+a"(vf[kk]));
   }
   f32x16_t dk[DT], dv[DT];
 #pragma unroll
@@ -619,95 +719,239 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
 #pragma unroll
     for (int r = 0; r < 16; ++r) { dk[i][r] = 0.f; dv[i][r] = 0.f; }
   const float c = a.scale * kLog2e;
-  const int w_lo = min(k0 + 32 * w, a.n_tok);               // first query any key of the wave sees
-  const int w_hi = (int)-wave_min_f(kvv ? -(float)(ke - 1) : 1.f);   // last one
-  const int w_ke = (int)wave_min_f(kvv ? (float)ke : 0.f);   // earliest segment end (0: a key is past the end)
+  // The products of half -1 (the first step's dV/dK group) read stage 2 with
+  // zero P and dS: clear it so that they add exact zeros.
+  {
+    const u32x4_t z{0, 0, 0, 0};
+    for (int i = threadIdx.x; i < TT::kHalfs / 8; i += 64 * NW) {
+      *(u32x4_t *)(smq + 2 * TT::kHalfs + 8 * i) = z;
+      *(u32x4_t *)(smd + 2 * TT::kHalfs + 8 * i) = z;
+    }
+  }
   __syncthreads();
   const int q_hi = rng[0];    // queries [k0, q_hi)
   const int group = a.Hq / a.Hkv;
   const int n_qb = q_hi > k0 ? (q_hi - k0 + kTR - 1) / kTR : 0;
   const int n_it = group * n_qb;
   // item it: query head g*group + it / n_qb, query tile k0 + 64 * (it % n_qb)
-  auto load_item = [&](int it, int buf) __attribute__((always_inline)) {
+  auto load_item = [&](int it, auto ST) __attribute__((always_inline)) {
+    constexpr int st = decltype(ST)::value;
     const int h = g * group + it / n_qb, qb = k0 + kTR * (it % n_qb);
-    TT::load(sm + buf * TT::kHalfs, qkv + h * HD, ld, qb, q_hi);
-    TT::load(sm + (2 + buf) * TT::kHalfs, dout + h * HD, ldo, qb, q_hi);
+    TT::load(smq + st * TT::kHalfs, qkv + h * HD, ld, qb, q_hi);
+    TT::load(smd + st * TT::kHalfs, dout + h * HD, ldo, qb, q_hi);
     if (w < 2) {                // one float per lane: LSE (wave 0), delta (wave 1)
       const float *src = (w == 0 ? a.lse : a.delta) + (int64_t)h * a.n_tok + min(qb + lane, q_hi - 1);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)ld_sm[2 * w + buf],
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)ld_sm[3 * w + st],
                                        4, 0, 0);
     }
   };
   // the lane's LSE / delta reads: 4 floats at 16 hl bytes past the offset
   const uint32_t ld_lane = lds_addr(ld_sm) + 16 * hl;
-  if (n_it > 0) load_item(0, 0);
-  dma_wait();
-  __syncthreads();
-  // query rows 32tt..32tt+31 of a staged tile: S = Q K^T and dP = dO V^T
-  // [32 queries x 32 keys], the softmax terms, then dV^T += dO^T P and dK^T
-  // += Q^T dS over those 32 queries
-  auto half = [&](const int tt, const int qb, const bool full,
-                  const int st) __attribute__((always_inline)) {
-    f32x16_t s, dp;   // set by rows_times_pair
-    rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, kf, vf);
-    // the lane's 16 query rows of this tile: 32tt + 8(r/4) + 4hl + r%4 (their
-    // LSE in log2 units and delta); read after the products so that they are
-    // not live across them
-    f32x4_t lv[4], dl[4];
+
+  // pipeline state: S, dP of the current half (s, dp: exponentiated in a
+  // step's first group, overwritten by the next half's products in its
+  // second); that half's LSE and delta (lv, dl); packed P, dS of the
+  // previous half (pp, sp) and of the current one (pc, spc)
+  f32x16_t s, dp;
+  f32x4_t lv[4], dl[4];
+  bf16x8_t pp[2], sp[2], pc[2], spc[2];
+  const bf16x8_t zero8 = __builtin_bit_cast(bf16x8_t, u32x4_t{0, 0, 0, 0});
+  pp[0] = pp[1] = sp[0] = sp[1] = zero8;
+  pc[0] = pc[1] = spc[0] = spc[1] = zero8;
+  // LSE (log2 units) and delta of the lane's 16 query rows of half (tt, st):
+  // 32tt + 8(r/4) + 4hl + r%4
+  auto read_ld = [&](const int tt, const int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       lv[r4] = lds_read_f4(ld_lane, st * 256 + (32 * tt + 8 * r4) * 4);
-      dl[r4] = lds_read_f4(ld_lane, (2 + st) * 256 + (32 * tt + 8 * r4) * 4);
+      dl[r4] = lds_read_f4(ld_lane, (3 + st) * 256 + (32 * tt + 8 * r4) * 4);
     }
-    // the reads above are inline assembly: wait for them, and pass the
-    // values through empty statements so no use moves above the wait
-    lds_wait();
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      asm volatile("" : "+v"(lv[r4]));
-      asm volatile("" : "+v"(dl[r4]));
-    }
-    if (full) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(fmaf(s[r], c, -lv[r >> 2][r & 3]));
-        s[r] = p;
-        dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
-      }
-    } else {
-      // query qb + 4hl + off is seen by the lane's key iff lo <= off < hi
-      const int lo = kv - qb - 4 * hl, hi = kvv ? ke - qb - 4 * hl : lo;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
-        const bool ok = off >= lo && off < hi;
-        const float p = ok ? fast_exp2(fmaf(s[r], c, -lv[r >> 2][r & 3])) : 0.f;
-        s[r] = p;
-        dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
-      }
-    }
-    const bf16x8_t pj[2] = {pack8(s, 0), pack8(s, 8)};
-    const bf16x8_t sj[2] = {pack8(dp, 0), pack8(dp, 8)};
-    cols_times_half<HD>(dv, L, (2 + st) * T, 32 * tt, pj);   // dV^T += dO^T P
-    cols_times_half<HD>(dk, L, st * T, 32 * tt, sj);         // dK^T += Q^T dS
   };
-  // item it reads stage b and prefetches item it + 1 into the other stage;
-  // two items per pass so that both stages are fixed LDS addresses
-  auto item = [&](const int it, const int b) __attribute__((always_inline)) {
-    const int qb = k0 + kTR * (it % n_qb);
-    if (it + 1 < n_it) load_item(it + 1, b ^ 1);
-    if (qb + kTR - 1 >= w_lo && qb <= w_hi) {
-      const bool full = qb >= k0 + 32 * w + 31 && qb + kTR - 1 < w_ke;   // every query sees every key
-      half(0, qb, full, b);
-      half(1, qb, full, b);
+
+  // fragment j of a step: dV/dK group (j < NC): dv[i] (j < NC/2, dO tile) or
+  // dk[i] (Q tile), feature block i = j % DT, token rows 32tt + 16((j/DT)%2);
+  // S/dP group: k-slice (j - NC)/2 of the Q (even) or dO (odd) tile rows 32tt
+  auto read_frag = [&](const int j, const int tt_c, const int st_c, const int tt_p,
+                       const int st_p) __attribute__((always_inline)) -> bf16x8_t {
+    if (j < NC) {
+      const int i = j % DT, hb = (j / DT) & 1;
+      const int off = st_c * T + (32 * tt_c + 16 * hb) * RB;
+      return j < NC / 2 ? LD.col_frag(off, i) : LQ.col_frag(off, i);
     }
+    const int kk = (j - NC) >> 1;
+    const int off = st_p * T + 32 * tt_p * RB;
+    return ((j - NC) & 1) ? LD.row_frag(off, kk) : LQ.row_frag(off, kk);
+  };
+
+  // The causal and segment mask enters S as its accumulator's initial value:
+  // 0 where the lane's key sees the query row, -inf where it does not (then
+  // P = exp2(-inf) = 0 and dS = 0).  Most halves are seen whole; the bias is
+  // written only for the others (and cleared after them).  Query row offset
+  // o (past 4hl) of a half is seen iff (unsigned)(o - lo) < span.
+  f32x16_t bias;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) bias[r] = 0.f;
+  bool bias_zero = true;   // uniform
+  auto set_bias = [&](const int lo, const int span) __attribute__((always_inline)) {
+    const bool part = __builtin_amdgcn_ballot_w64(!(lo <= 0 && 27 - lo < span)) != 0;
+    if (part) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        bias[r] = (uint32_t)(8 * (r >> 2) + (r & 3) - lo) < (uint32_t)span ? 0.f : -INFINITY;
+      bias_zero = false;
+    } else if (!bias_zero) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) bias[r] = 0.f;
+      bias_zero = true;
+    }
+  };
+
+  bf16x8_t F[NS];
+  // One step: dV/dK products of half (tt_c, st_c) with pp, sp while the
+  // softmax terms of the current half (s, dp, lv, dl) go into pc, spc; then
+  // the S/dP products of half (tt_p, st_p), masked by (lo_p, span_p), into
+  // s, dp, and that half's LSE and delta into lv, dl.  On entry F[0..D-1]
+  // are in flight, on exit the next step's (its dV/dK group: half
+  // (tt_s, st_s), this step's softmax half).  With BAR, a barrier between
+  // the groups makes the next item's stage visible, then `after` runs.
+  auto step = [&](auto TTC, auto STC, auto TTS, auto STS, auto TTP, auto STP, auto BAR,
+                  const int lo_p, const int span_p, auto after) __attribute__((always_inline)) {
+    constexpr int tt_c = decltype(TTC)::value, st_c = decltype(STC)::value;
+    constexpr int tt_s = decltype(TTS)::value, st_s = decltype(STS)::value;
+    constexpr int tt_p = decltype(TTP)::value, st_p = decltype(STP)::value;
+    constexpr bool bar = decltype(BAR)::value != 0;
+    set_bias(lo_p, span_p);
+    float pv[16], dq[16];
+    auto slot = [&](auto JC) __attribute__((always_inline)) {
+      constexpr int j = decltype(JC)::value;
+      constexpr int wn = Sched::wait(j, bar);
+      constexpr int f0 = Sched::first(j, bar), f1 = Sched::last(j, bar);
+      lds_wait_n(wn);
+      asm volatile("" : "+v"(F[j]));
+      if (j == 0) {
+        // the LSE and delta reads precede fragment 0
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          asm volatile("" : "+v"(lv[r4]));
+          asm volatile("" : "+v"(dl[r4]));
+        }
+      }
+      if (j < NC) {
+        const int i = j % DT, hb = (j / DT) & 1;
+        if (j < NC / 2) dv[i] = mfma(F[j], pp[hb], dv[i]);   // dV^T += dO^T P
+        else dk[i] = mfma(F[j], sp[hb], dk[i]);              // dK^T += Q^T dS
+      } else {
+        const int kk = (j - NC) >> 1;
+        if (((j - NC) & 1) == 0) s = mfma(F[j], kf[kk], kk == 0 ? bias : s);   // S = Q K^T (+ mask)
+        else dp = mfma(F[j], vf[kk], kk == 0 ? f32x16_t{} : dp);                     // dP = dO V^T
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (bar && j == NC - 1) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        bar_nofence();
+        after();
+      }
+#pragma unroll
+      for (int f = f0; f < f1; ++f) {
+        if (f < NS) F[f] = read_frag(f, tt_c, st_c, tt_p, st_p);
+        else F[f - NS] = read_frag(f - NS, tt_s, st_s, 0, 0);
+      }
+      if (j == NC) read_ld(tt_p, st_p);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (j >= NC || Sched::score_slot(r) != j) continue;
+        // the score's inputs and the packed words pass through empty
+        // statements, which keep this vector work in its slot (between the
+        // slot's LDS reads and the next slot's wait) instead of gathered
+        float sr = s[r], dr = dp[r];
+        asm volatile("" : "+v"(sr), "+v"(dr));
+        const float pr = fast_exp2(fmaf(sr, c, -lv[r >> 2][r & 3]));
+        pv[r] = pr;
+        dq[r] = pr * (dr - dl[r >> 2][r & 3]);
+        if (r & 1) {
+          const int h8 = r >> 3, k = (r & 7) >> 1;
+          // the pair (r - 1, r) is word k of the packed half h8
+          uint32_t wp = pack2(pv[r - 1], pv[r]), ws = pack2(dq[r - 1], dq[r]);
+          asm volatile("" : "+v"(wp), "+v"(ws));
+          u32x4_t up = __builtin_bit_cast(u32x4_t, pc[h8]);
+          u32x4_t us = __builtin_bit_cast(u32x4_t, spc[h8]);
+          up[k] = wp;
+          us[k] = ws;
+          pc[h8] = __builtin_bit_cast(bf16x8_t, up);
+          spc[h8] = __builtin_bit_cast(bf16x8_t, us);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    StaticFor<0, NS>::run(slot);
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      pp[x] = pc[x];
+      sp[x] = spc[x];
+    }
+  };
+
+  // One item (query tile of 64, two halves) at stage ST: the even step
+  // exponentiates its first half, the odd one its second and, past the
+  // barrier, stages item it + 2 into the stage item it - 1 used.  The loop
+  // runs whole groups of three items (one per stage, so that every stage
+  // offset is a constant and the loop has a single exit); the items past
+  // n_it stage a copy of the last one and see no query (their P and dS are
+  // zero, so their products add exact zeros).
+  const int span = kvv ? ke - kv : 0;   // the key sees query rows [kv, ke)
+  const int n_it3 = (n_it + 2) / 3 * 3;
+  auto item = [&](const int it, auto ST) __attribute__((always_inline)) {
+    constexpr int st = decltype(ST)::value;
+    // half tt of item i: row offset o is seen iff o - (lo(i) - 32tt) < span(i)
+    const int lo = kv - (k0 + kTR * (min(it, n_it - 1) % n_qb)) - 4 * hl;
+    const int lo1 = kv - (k0 + kTR * (min(it + 1, n_it - 1) % n_qb)) - 4 * hl;
+    step(Ci<1>{}, Ci<(st + 2) % 3>{}, Ci<0>{}, Ci<st>{}, Ci<1>{}, Ci<st>{}, Ci<0>{}, lo - 32,
+         it < n_it ? span : 0, [] {});
+    step(Ci<0>{}, Ci<st>{}, Ci<1>{}, Ci<st>{}, Ci<0>{}, Ci<(st + 1) % 3>{}, Ci<1>{}, lo1,
+         it + 1 < n_it ? span : 0, [&]() __attribute__((always_inline)) {
+           if (it + 2 < n_it3) load_item(min(it + 2, n_it - 1), Ci<(st + 2) % 3>{});
+         });
+  };
+  // the last half's dV/dK products (its first D fragments are in flight)
+  auto tail = [&](auto ST) __attribute__((always_inline)) {
+    constexpr int st = decltype(ST)::value;
+#pragma unroll
+    for (int j = D; j < NC; ++j) F[j] = read_frag(j, 1, st, 0, 0);
     lds_wait();
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      asm volatile("" : "+v"(F[j]));
+      const int i = j % DT, hb = (j / DT) & 1;
+      if (j < NC / 2) dv[i] = mfma(F[j], pp[hb], dv[i]);
+      else dk[i] = mfma(F[j], sp[hb], dk[i]);
+    }
+  };
+  if (n_it > 0) {
+    load_item(0, Ci<0>{});
+    load_item(min(1, n_it - 1), Ci<1>{});
     dma_wait();
     __syncthreads();
-  };
-  for (int it = 0; it < n_it; it += 2) {
-    item(it, 0);
-    if (it + 1 < n_it) item(it + 1, 1);
+    // S, dP, LSE and delta of half 0
+    set_bias(kv - k0 - 4 * hl, span);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      bf16x8_t fq = LQ.row_frag(0, kk), fd = LD.row_frag(0, kk);
+      lds_wait();
+      asm volatile("" : "+v"(fq));
+      asm volatile("" : "+v"(fd));
+      s = mfma(fq, kf[kk], kk == 0 ? bias : s);
+      dp = mfma(fd, vf[kk], kk == 0 ? f32x16_t{} : dp);
+    }
+    read_ld(0, 0);
+    // the first step's dV/dK group: half -1 (stage 2, cleared)
+#pragma unroll
+    for (int f = 0; f < D; ++f) F[f] = read_frag(f, 1, 2, 0, 0);
+    for (int it = 0; it < n_it3; it += 3) {
+      item(it, Ci<0>{});
+      item(it + 1, Ci<1>{});
+      item(it + 2, Ci<2>{});
+    }
+    tail(Ci<2>{});
   }
   if (!kvv) return;
   bf16_t *base = (bf16_t *)a.dqkv + (int64_t)kv * ld;

@@ -209,6 +209,9 @@ BF16_CASES = {
     # chunk (NN, k = 4104; the second chunk is 896 wide), and unmerged the
     # weight gradients (TN, k = 5856 tokens); few output tiles, so split-K
     "hd64_long_k": dict(hd=64, d=256, hq=4, hkv=2, ff=4104, vocab=5000, chunk=4104),
+    # one query head per key/value head: the dK/dV pass walks a single head,
+    # so its item count is often not a multiple of its three LDS stages
+    "hd128_mha": dict(hd=128, d=256, hq=2, hkv=2, ff=512, vocab=2000, chunk=768),
 }
 
 
