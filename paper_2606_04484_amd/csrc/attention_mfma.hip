@@ -785,25 +785,22 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
 
   // The causal and segment mask enters S as its accumulator's initial value:
   // 0 where the lane's key sees the query row, -inf where it does not (then
-  // P = exp2(-inf) = 0 and dS = 0).  Most halves are seen whole; the bias is
-  // written only for the others (and cleared after them).  Query row offset
-  // o (past 4hl) of a half is seen iff (unsigned)(o - lo) < span.
-  f32x16_t bias;
+  // P = exp2(-inf) = 0 and dS = 0).  Most halves are seen whole by every
+  // lane of the wave and start from 0; only the others build the bias.
+  // Query row offset o (past 4hl) of a half is seen iff
+  // (unsigned)(o - lo) < span.
+  auto seen_whole = [&](const int lo, const int span) __attribute__((always_inline)) {
+    return __builtin_amdgcn_ballot_w64(!(lo <= 0 && 27 - lo < span)) == 0;
+  };
+  // first S product of a half: F Q-fragment, K-slice 0
+  auto s_first = [&](const bf16x8_t &fq, const bool whole, const int lo,
+                     const int span) __attribute__((always_inline)) -> f32x16_t {
+    if (whole) return mfma(fq, kf[0], f32x16_t{});
+    f32x16_t bias;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) bias[r] = 0.f;
-  bool bias_zero = true;   // uniform
-  auto set_bias = [&](const int lo, const int span) __attribute__((always_inline)) {
-    const bool part = __builtin_amdgcn_ballot_w64(!(lo <= 0 && 27 - lo < span)) != 0;
-    if (part) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        bias[r] = (uint32_t)(8 * (r >> 2) + (r & 3) - lo) < (uint32_t)span ? 0.f : -INFINITY;
-      bias_zero = false;
-    } else if (!bias_zero) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) bias[r] = 0.f;
-      bias_zero = true;
-    }
+    for (int r = 0; r < 16; ++r)
+      bias[r] = (uint32_t)(8 * (r >> 2) + (r & 3) - lo) < (uint32_t)span ? 0.f : -INFINITY;
+    return mfma(fq, kf[0], bias);
   };
 
   bf16x8_t F[NS];
@@ -820,7 +817,7 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     constexpr int tt_s = decltype(TTS)::value, st_s = decltype(STS)::value;
     constexpr int tt_p = decltype(TTP)::value, st_p = decltype(STP)::value;
     constexpr bool bar = decltype(BAR)::value != 0;
-    set_bias(lo_p, span_p);
+    const bool whole_p = seen_whole(lo_p, span_p);
     float pv[16], dq[16];
     auto slot = [&](auto JC) __attribute__((always_inline)) {
       constexpr int j = decltype(JC)::value;
@@ -842,7 +839,8 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
         else dk[i] = mfma(F[j], sp[hb], dk[i]);              // dK^T += Q^T dS
       } else {
         const int kk = (j - NC) >> 1;
-        if (((j - NC) & 1) == 0) s = mfma(F[j], kf[kk], kk == 0 ? bias : s);   // S = Q K^T (+ mask)
+        if (((j - NC) & 1) == 0)   // S = Q K^T (+ mask)
+          s = kk == 0 ? s_first(F[j], whole_p, lo_p, span_p) : mfma(F[j], kf[kk], s);
         else dp = mfma(F[j], vf[kk], kk == 0 ? f32x16_t{} : dp);                     // dP = dO V^T
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -932,14 +930,14 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     dma_wait();
     __syncthreads();
     // S, dP, LSE and delta of half 0
-    set_bias(kv - k0 - 4 * hl, span);
+    const bool whole0 = seen_whole(kv - k0 - 4 * hl, span);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       bf16x8_t fq = LQ.row_frag(0, kk), fd = LD.row_frag(0, kk);
       lds_wait();
       asm volatile("" : "+v"(fq));
       asm volatile("" : "+v"(fd));
-      s = mfma(fq, kf[kk], kk == 0 ? bias : s);
+      s = kk == 0 ? s_first(fq, whole0, kv - k0 - 4 * hl, span) : mfma(fq, kf[kk], s);
       dp = mfma(fd, vf[kk], kk == 0 ? f32x16_t{} : dp);
     }
     read_ld(0, 0);
