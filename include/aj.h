@@ -345,6 +345,10 @@ int aj_stack_lora_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_
                       size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------ 3. loss
+ * The final norm, the vocab projection, the token log-prob and the clipped
+ * policy-gradient objective of the actor update (Section 3, the GRPO/PPO-style
+ * update the agents are trained with; the merged timelines of Section 4.4.2
+ * are scored through it unchanged).
  * hn = RMSNorm(h) * g_final; for every target position p (targets[i]):
  *   logprob[i] = log softmax(hn[p-1] W_vocab^T)[tok[p]]
  *   r = exp(logprob[i] - old_logprob[p])
@@ -367,6 +371,12 @@ typedef struct {
   float clip_eps;
   float rms_eps;
   int32_t dtype;                /* aj_dtype of h, final_norm, w_vocab */
+  int32_t keep_logits;          /* bfloat16 only: 1 = the forward also writes the float32
+                                   logits of every scored row into `saved` (n_tgt x vocab
+                                   floats, counted by aj_loss_saved_bytes) and the backward
+                                   reads them instead of recomputing the vocab projection;
+                                   the results are bitwise those of the recomputing
+                                   backward.  0 = recompute (saved holds only hn, rstd). */
 } aj_loss_cfg;
 
 typedef struct {
@@ -396,6 +406,8 @@ int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const v
                            float *logprob, float *lse, float *stats, int32_t *err,
                            void *ws, size_t ws_bytes, void *stream);
 /* dh: float32 [n_tok, d], WRITTEN (rows that feed no target become 0).
+ * `saved` must come from the forward of the same call (same cfg, in, h,
+ * weights): with keep_logits it holds that forward's logits. 
  * d_final_norm [d], d_w_vocab [vocab, d]: float32, accumulated; NULL = that
  * weight is frozen and its gradient is not computed. */
 int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *in, const void *h,

@@ -145,17 +145,26 @@ class ActorUpdate:
     """Weights, gradient accumulators and step buffers of the policy: embedding,
     m.n_layers decoder blocks (checkpointed: aj_stack_fwd / aj_stack_bwd), LM head."""
 
-    def __init__(self, m, weights, device="cuda", lora=None, lora_rank=0, lora_scale=1.0):
+    # the share of the free device memory the kept logits of one pack may take
+    KEEP_LOGITS_SHARE = 0.5
+
+    def __init__(self, m, weights, device="cuda", lora=None, lora_rank=0, lora_scale=1.0,
+                 keep_logits=None):
         """lora: optional dict of LoRA matrices keyed by lora_key (storage dtype of the
         weights); then only they train (self.G holds their gradients) and every
-        weight, gain, the embedding and the LM head stay frozen."""
+        weight, gain, the embedding and the LM head stay frozen.
+        keep_logits: the LM-head backward reads the forward's float32 logits
+        instead of recomputing them (bfloat16; bitwise the same result).  None
+        = whenever one pack's logits fit in KEEP_LOGITS_SHARE of the free memory."""
         self.m = m
         self.W = weights
         self.n_layers = getattr(m, "n_layers", 1)
         self.dev = torch.device(device)
         self.dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
         self.bcfg = C.block_cfg(m)
-        self.lcfg = C.loss_cfg(m)
+        self.keep_logits = keep_logits
+        self.lcfg = C.loss_cfg(m)          # the step's (keep_logits decided per capacity)
+        self.lcfg_fwd = C.loss_cfg(m)      # forward-only scoring keeps nothing
         self.lora, self.rank, self.scale = lora, lora_rank, lora_scale
         trained = lora if lora is not None else weights
         self.G = {k: torch.zeros(v.shape, dtype=torch.float32, device=self.dev)
@@ -199,6 +208,13 @@ class ActorUpdate:
             self.bws = u8(C.aj_lora_workspace_bytes(self.bcfg, self.rank, n_tok))
         self.ckpt = u8(C.aj_stack_ckpt_bytes(self.bcfg, self.n_layers, n_tok))
         self.ews = u8(C.aj_embed_bwd_workspace_bytes(n_tok, d))
+        self.lsaved = None
+        keep = self.keep_logits
+        if keep is None:
+            logit_bytes = n_tgt * self.m.vocab * 4
+            keep = self.m.dtype == "bf16" and \
+                logit_bytes <= self.KEEP_LOGITS_SHARE * torch.cuda.mem_get_info(dev)[0]
+        self.lcfg = C.loss_cfg(self.m, keep_logits=bool(keep))
         self.lsaved = u8(C.aj_loss_saved_bytes(self.lcfg, n_tgt))
         self.lws = u8(C.aj_loss_workspace_bytes(self.lcfg, n_tgt))
         self._cap = (n_tok, n_tgt)
@@ -269,8 +285,9 @@ class ActorUpdate:
             C.aj_embed_fwd(L.tok[t0:t1], self.W["emb"], self.x[:n], self.err)
             self._stack_fwd(L.cu_seqlens[s0:s1 + 1], L.pos[t0:t1], p["max_len"], self.x[:n],
                             self.y[:n], t0)
-            C.aj_logprob_pg_loss_fwd(self.lcfg, L.targets[r0:r1], L.tok, L.old_logprob, L.adv,
-                                     inv, self.y[:n], self.W["final_norm"], self.W["w_vocab"],
-                                     self.lsaved, self.logprob[r0:r1], self.lse[r0:r1],
-                                     self.stats, self.lws, self.err, row_base=t0)
+            C.aj_logprob_pg_loss_fwd(self.lcfg_fwd, L.targets[r0:r1], L.tok, L.old_logprob,
+                                     L.adv, inv, self.y[:n], self.W["final_norm"],
+                                     self.W["w_vocab"], self.lsaved, self.logprob[r0:r1],
+                                     self.lse[r0:r1], self.stats, self.lws, self.err,
+                                     row_base=t0)
         return self.logprob[:L.n_mask]

@@ -93,7 +93,7 @@ class Varlen(C.Structure):
 
 class LossCfg(C.Structure):
     _fields_ = [("d_model", i32), ("vocab", i32), ("vocab_chunk", i32), ("clip_eps", f32),
-                ("rms_eps", f32), ("dtype", i32)]
+                ("rms_eps", f32), ("dtype", i32), ("keep_logits", i32)]
 
 
 class LossIn(C.Structure):
@@ -405,9 +405,9 @@ def aj_stack_lora_bwd(cfg, layers, adapters, rank, scale, cu_seqlens, pos, max_s
 
 # ------------------------------------------------------------------ loss
 
-def loss_cfg(m):
+def loss_cfg(m, keep_logits=False):
     return LossCfg(m.d_model, m.vocab, m.vocab_chunk, m.clip_eps, m.rms_eps,
-                   AJ_BF16 if m.dtype == "bf16" else AJ_F32)
+                   AJ_BF16 if m.dtype == "bf16" else AJ_F32, 1 if keep_logits else 0)
 
 
 def aj_loss_saved_bytes(cfg, n_tgt):

@@ -5,11 +5,15 @@
 // reads no other logits).
 // bfloat16: the forward is one MFMA GEMM over the whole vocab whose epilogue
 // reduces each 256-column logit tile to a per-row (max, sum of exp) partial
-// and picks up the target's logit, so logits never reach memory; a small
-// kernel then combines the partials into the log-sum-exp.  The backward
-// recomputes each vocab_chunk-wide slab of logits and its epilogue writes
+// and picks up the target's logit; a small kernel then combines the partials
+// into the log-sum-exp.  The backward recomputes each vocab_chunk-wide slab of
+// logits and its epilogue writes
 //   dz = g * (onehot(target) - softmax)        g = d loss / d logprob
 // in bfloat16, then dhn += dz W_chunk and dW_chunk += dz^T hn are GEMMs.
+// With keep_logits the forward epilogue also stores its float32 logits (the
+// same values the recomputation would produce: same tiles, same reduction
+// order) and the backward forms dz from them element by element, trading the
+// second vocab projection for ~3 x 4 bytes of HBM traffic per logit.
 // float32 (the small workload): the same arithmetic with each chunk of logits
 // written to a float32 buffer and reduced by row kernels.
 #include <type_traits>
@@ -61,8 +65,11 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
 struct LossSaved {
   void *hn;
   float *rstd;
+  float *z;               // keep_logits: [n_tgt, vocab] float32 logits, else null
   size_t bytes;
 };
+
+bool keeps_logits(const aj_loss_cfg &c) { return c.keep_logits != 0 && c.dtype == AJ_BF16; }
 
 LossSaved carve_saved(const aj_loss_cfg &c, int n_tgt, void *base) {
   const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
@@ -70,6 +77,7 @@ LossSaved carve_saved(const aj_loss_cfg &c, int n_tgt, void *base) {
   LossSaved s;
   s.hn = cv.take<char>((int64_t)n_tgt * c.d_model * es);
   s.rstd = cv.take<float>(n_tgt);
+  s.z = keeps_logits(c) ? cv.take<float>((int64_t)n_tgt * c.vocab) : nullptr;
   s.bytes = cv.bytes();
   return s;
 }
@@ -303,7 +311,7 @@ AJ_DEV void lds_barrier() {
 // tile that holds it, the target's logit.  Logits never leave the chip.
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     int n, int V, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
-    const int32_t *tok, float2 *tile_ms, float *zt) {
+    const int32_t *tok, float2 *tile_ms, float *zt, float *zkeep) {
   __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
   __shared__ int ttok[Cfg::BM];
   __shared__ float2 red[Cfg::WN][Cfg::BM];
@@ -322,6 +330,21 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
   // columns each: reduce over 16 lanes by DPP, then across the two rows of
   // 16 with one exchange per row, issued for all 16 rows of a pass together.
   const int col0 = n0 + wn * Cfg::WTN + (lane & 31);
+  if (zkeep) {
+    // the tile's logits for the backward: per accumulator row, the 32 lanes
+    // of a half-wave store 32 consecutive columns
+#pragma unroll
+    for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + gemm_core::acc_row<Cfg>(wm, i, r, lane);
+        if (m >= n) continue;
+        float *zr = zkeep + (int64_t)m * V;
+#pragma unroll
+        for (int j = 0; j < Cfg::TN; ++j)
+          if (col0 + 32 * j < V) zr[col0 + 32 * j] = acc[i][j][r];
+      }
+  }
   auto epilogue = [&](auto inside) {
     constexpr bool kInside = decltype(inside)::value;   // every column < V
 #pragma unroll
@@ -401,6 +424,45 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(int n, int n_tiles, con
   }
 }
 
+// d logit of logit z in a row with log-sum-exp tl (log2 units) and loss
+// gradient g: g (onehot - softmax).  One definition for the recomputing and
+// the logit-keeping backward, so that both round identically.
+AJ_DEV float dz_value(float z, float tl, float g, bool target) {
+  const float p = fast_exp2(fmaf(z, kLog2e, -tl));
+  return g * ((target ? 1.f : 0.f) - p);
+}
+
+// dz from the kept logits of vocab columns [c0, c0 + cw): 8 columns per
+// thread (V, c0 and cw multiples of 8, 16-byte aligned rows) or, on the
+// general path, one.
+template <bool kVec>
+__global__ __launch_bounds__(256) void lm_dz_kept_kernel(int n, int cw, int c0, int V,
+                                                         const float *zkeep, const int32_t *tpos,
+                                                         const int32_t *tok, const float *lse,
+                                                         const float *g, bf16_t *dz) {
+  constexpr int E = kVec ? 8 : 1;
+  const int per_row = cw / E;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)n * per_row) return;
+  const int m = (int)(idx / per_row), cb = (int)(idx % per_row) * E;
+  const float tl = lse[m] * kLog2e, gm = g[m];
+  const int tt = tok[tpos[m]] - c0;
+  const float *zr = zkeep + (int64_t)m * V + c0 + cb;
+  if (kVec) {
+    const float4 a = *reinterpret_cast<const float4 *>(zr);
+    const float4 b = *reinterpret_cast<const float4 *>(zr + 4);
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = f2bf2(dz_value(v[2 * e], tl, gm, cb + 2 * e == tt),
+                   dz_value(v[2 * e + 1], tl, gm, cb + 2 * e + 1 == tt));
+    *reinterpret_cast<uint4 *>(dz + (int64_t)m * cw + cb) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    dz[(int64_t)m * cw + cb] = f2bf(dz_value(zr[0], tl, gm, cb == tt));
+  }
+}
+
 // dz = g (onehot(target) - softmax) for vocab columns [c0, c0 + cw), from the
 // recomputed logits, straight to bfloat16.
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
@@ -422,10 +484,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
   gemm_core::mainloop8s<true, true, Cfg, 4>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
-  auto dz_of = [&](float a, int rl, int col) {
-    const float p = fast_exp2(a * kLog2e - tl[rl]);
-    return tg[rl] * ((col == ttok[rl] ? 1.f : 0.f) - p);
-  };
+  auto dz_of = [&](float a, int rl, int col) { return dz_value(a, tl[rl], tg[rl], col == ttok[rl]); };
   if (m0 + Cfg::BM > n || n0 + Cfg::BN > cw || cw % 8 != 0 || ((uintptr_t)dz & 15) != 0) {
     // edge tile: element by element
 #pragma unroll
@@ -468,8 +527,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
 #pragma unroll
       for (int j = 0; j < Cfg::TN; ++j) {
         const int cl = gemm_core::acc_col<Cfg>(wn, j, lane);
-        const float p = fast_exp2(acc[i][j][r] * kLog2e - rl2[r]);
-        stage[ls * LDH + cl] = f2bf(rg[r] * ((cl == rt[r] ? 1.f : 0.f) - p));
+        stage[ls * LDH + cl] = f2bf(dz_value(acc[i][j][r], rl2[r], rg[r], cl == rt[r]));
       }
     }
     lds_barrier();
@@ -535,7 +593,7 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     const int tk = aj::timing_begin(st, AJ_KC_LM_FWD, 2.0 * n * (double)c.vocab * d);
     lm_fwd_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, c.vocab, d, (const bf16_t *)sv.hn,
                                                    (const bf16_t *)w_vocab, w.tpos, in.tok,
-                                                   w.tile_ms, w.zt);
+                                                   w.tile_ms, w.zt, sv.z);
     aj::timing_end(st, tk);
     lm_combine_kernel<<<(n + 3) / 4, 256, 0, st>>>(n, tiles_n, w.tile_ms, w.zt, lse, logprob);
     token_check_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, in.tok, c.vocab, err);
@@ -577,7 +635,20 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
   for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
     const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
     int r;
-    if (sizeof(T) == 2) {
+    if (sizeof(T) == 2 && sv.z) {
+      const bool vec = c.vocab % 8 == 0 && c0 % 8 == 0 && cw % 8 == 0 &&
+                       ((uintptr_t)sv.z & 15) == 0 && ((uintptr_t)w.dz & 15) == 0;
+      const int64_t work = (int64_t)n * (vec ? cw / 8 : cw);
+      const unsigned blocks = (unsigned)((work + 255) / 256);
+      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);
+      if (vec)
+        lm_dz_kept_kernel<true><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos, in.tok,
+                                                        lse, w.g, (bf16_t *)w.dz);
+      else
+        lm_dz_kept_kernel<false><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos, in.tok,
+                                                         lse, w.g, (bf16_t *)w.dz);
+      aj::timing_end(st, tk);
+    } else if (sizeof(T) == 2) {
       const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
       const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
       lm_dz_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, cw, c0, d, (const bf16_t *)sv.hn,

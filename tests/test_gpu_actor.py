@@ -23,14 +23,16 @@ GRADS = ("emb", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down", 
          "w_vocab")
 
 
-def run_gpu(case, merged=True, pack_tokens=131072, ref_pos=None, kl_coef=0.0, record=False):
+def run_gpu(case, merged=True, pack_tokens=131072, ref_pos=None, kl_coef=0.0, record=False,
+            keep_logits=None):
     """ref_pos: optional reference log-probs per merged position (host array);
-    record: also return the library's per-class kernel launch record of the step."""
+    record: also return the library's per-class kernel launch record of the step;
+    keep_logits: the LM-head backward from kept logits (None: the actor's choice)."""
     from paper_2606_04484_amd import actor, capi
     dev = actor.upload_timelines(case.tl, case.old)
     L = actor.merge(dev, merged=merged, pack_tokens=pack_tokens, text=merged and case.text)
     if case.lora is None:
-        A = actor.ActorUpdate(case.m, case.device_weights())
+        A = actor.ActorUpdate(case.m, case.device_weights(), keep_logits=keep_logits)
     else:
         A = actor.ActorUpdate(case.m, case.device_weights(), lora=case.device_weights(which=case.lora),
                               lora_rank=next(v for k, v in case.lora.items()
@@ -283,6 +285,23 @@ def test_merged_equals_unmerged_on_gpu():
     assert abs(a["loss"] - b["loss"]) <= 1e-2 * max(abs(b["loss"]), 1e-3)
     for k in GRADS:
         assert rel_l2(a["grads"][k], b["grads"][k]) < 1e-2, k
+
+
+@pytest.mark.parametrize("name", ["hd128_gqa3", "hd64_long_k", "vocab_2003"])
+def test_kept_logits_equal_recomputed(name):
+    """The LM-head backward that forms d logits from the forward's kept float32
+    logits gives bitwise the log-probs, loss and gradients of the backward that
+    recomputes the vocab projection (same tiles, same reduction order, one
+    formula for d logits); vocab 2003 takes the element-by-element path."""
+    kw = dict(hd=64, d=256, hq=4, hkv=2, ff=512, vocab=2003, chunk=768) \
+        if name == "vocab_2003" else BF16_CASES[name]
+    m = bf16_case_model(**kw)
+    case = Case(workload(m), noise_std=0.3, margin=0.05)
+    a, b = run_gpu(case, keep_logits=True), run_gpu(case, keep_logits=False)
+    assert a["err"] == 0 and b["err"] == 0
+    assert np.array_equal(a["lp"], b["lp"]) and a["loss"] == b["loss"]
+    for k in GRADS:
+        assert np.array_equal(a["grads"][k], b["grads"][k]), k
 
 
 def test_deterministic():
