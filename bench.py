@@ -593,6 +593,22 @@ def main():
         "loss": head["loss"],
     }
     mr = merge_record(live["rec"], live["tl"], live["Lm"])
+    if not args.no_extras:
+        # The LM-head backward reading the forward's kept float32 logits instead
+        # of recomputing the vocab projection (bitwise the same step): an
+        # option that trades ~4 bytes of HBM per logit of a pack for the
+        # second projection; the headline keeps the streaming design, which
+        # never materialises the logits.
+        log("kept-logits variant on " + cfg.name)
+        A = live["A"]
+        A.set_keep_logits(True)
+        A.prepare(live["Lm"])
+        _, t_k, _ = timed(A, live["merger"], True, 2, 1, torch, capi)
+        out["kept_logits"] = {"steps": 2, "warmup": 1, "ms_per_step": round(t_k * 1e3, 3),
+                              "tokens_per_s": round(live["Lm"].n_tok / t_k, 1),
+                              "vs_streaming": round(head["ms_per_step"] / (t_k * 1e3), 3)}
+        A.set_keep_logits(False)
+        del A
     if "unmerged" in head:
         out["unmerged"] = head["unmerged"]
         out["speedup_vs_unmerged"] = head["speedup_vs_unmerged"]

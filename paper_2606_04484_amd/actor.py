@@ -149,13 +149,16 @@ class ActorUpdate:
     KEEP_LOGITS_SHARE = 0.5
 
     def __init__(self, m, weights, device="cuda", lora=None, lora_rank=0, lora_scale=1.0,
-                 keep_logits=None):
+                 keep_logits=False):
         """lora: optional dict of LoRA matrices keyed by lora_key (storage dtype of the
         weights); then only they train (self.G holds their gradients) and every
         weight, gain, the embedding and the LM head stay frozen.
-        keep_logits: the LM-head backward reads the forward's float32 logits
-        instead of recomputing them (bfloat16; bitwise the same result).  None
-        = whenever one pack's logits fit in KEEP_LOGITS_SHARE of the free memory."""
+        keep_logits: False (the default) streams the vocab projection and the
+        LM-head backward recomputes it, so the logits are never materialised;
+        True makes the backward read the forward's float32 logits instead
+        (bfloat16; bitwise the same result, ~4 bytes per logit of a pack in
+        HBM); None = True whenever one pack's logits fit in KEEP_LOGITS_SHARE of
+        the free memory."""
         self.m = m
         self.W = weights
         self.n_layers = getattr(m, "n_layers", 1)
@@ -185,6 +188,14 @@ class ActorUpdate:
                         for l in range(self.n_layers)]
             self.adapters = fields(lora)
             self.layer_grads = fields(self.G)
+
+    def set_keep_logits(self, keep):
+        """Switches the LM-head backward between recomputing and kept logits
+        (the step buffers are sized again by the next prepare)."""
+        self.keep_logits = keep
+        self._cap = (0, 0)
+        if hasattr(self, "logprob"):
+            del self.logprob
 
     def zero_grads(self):
         for g in self.G.values():
