@@ -214,55 +214,6 @@ AJ_DEV f32x4_t lds_read_f4(const uint32_t a, const int off) {
 }
 AJ_DEV void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile at byte offset off)
-// += tile rows x B, B = per-lane operands bv[kk] (k = features
-// 16kk..16kk+15); with kZero the products start from zero (acc is not read:
-// the first MFMA of each chain takes the constant 0 as its accumulator)
-template <int HD, bool kZero = false>
-AJ_DEV void rows_times(f32x16_t (&acc)[2], const TileLanes<HD> &L, const int off,
-                       const bf16x8_t (&bv)[HD / 16]) {
-  constexpr int KS = HD / 16, RB = HD * 2;
-  bf16x8_t f[2][2];
-  f[0][0] = L.row_frag(off, 0);
-  f[0][1] = L.row_frag(off + 32 * RB, 0);
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
-    const int cur = kk & 1;
-    lds_wait(f[cur]);
-    if (kk + 1 < KS) {
-      f[cur ^ 1][0] = L.row_frag(off, kk + 1);
-      f[cur ^ 1][1] = L.row_frag(off + 32 * RB, kk + 1);
-    }
-    const bool fresh = kZero && kk == 0;
-    acc[0] = mfma(f[cur][0], bv[kk], fresh ? f32x16_t{} : acc[0]);
-    acc[1] = mfma(f[cur][1], bv[kk], fresh ? f32x16_t{} : acc[1]);
-  }
-}
-
-// acc[i] (features 32i..32i+31) += tile^T x P for the tile at byte offset
-// off, P given per 16-token chunk j as packed accumulator halves pj[j]
-// (tokens 32(j/2) + 16(j%2) + pack8 order)
-template <int HD>
-AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const int off,
-                       const bf16x8_t (&pj)[4]) {
-  constexpr int DT = HD / 32, RB = HD * 2;
-  bf16x8_t f[2][DT];
-#pragma unroll
-  for (int i = 0; i < DT; ++i) f[0][i] = L.col_frag(off, i);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int cur = j & 1;
-    lds_wait(f[cur]);
-    if (j + 1 < 4) {
-#pragma unroll
-      for (int i = 0; i < DT; ++i)
-        f[cur ^ 1][i] = L.col_frag(off + (32 * ((j + 1) >> 1) + 16 * ((j + 1) & 1)) * RB, i);
-    }
-#pragma unroll
-    for (int i = 0; i < DT; ++i) acc[i] = mfma(f[cur][i], pj[j], acc[i]);
-  }
-}
-
 // Waits until at most n LDS reads (inline assembly, issued in order) are in
 // flight (n a constant after inlining, 0..15).
 AJ_DEV void lds_wait_n(int n) {
@@ -282,6 +233,57 @@ AJ_DEV void lds_wait_n(int n) {
     case 13: asm volatile("s_waitcnt lgkmcnt(13)" ::: "memory"); break;
     case 14: asm volatile("s_waitcnt lgkmcnt(14)" ::: "memory"); break;
     default: asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); break;
+  }
+}
+
+// acc[t] (t = 0, 1: token rows 32t..32t+31 of the tile at byte offset off)
+// += tile rows x B, B = per-lane operands bv[kk] (k = features
+// 16kk..16kk+15); with kZero the products start from zero (acc is not read:
+// the first MFMA of each chain takes the constant 0 as its accumulator).
+// Fragment q = 2kk + t feeds MFMA q and is read kAhead MFMAs ahead.
+template <int HD, bool kZero = false>
+AJ_DEV void rows_times(f32x16_t (&acc)[2], const TileLanes<HD> &L, const int off,
+                       const bf16x8_t (&bv)[HD / 16]) {
+  constexpr int KS = HD / 16, RB = HD * 2, NQ = 2 * KS, kAhead = 4;
+  bf16x8_t f[NQ];
+  auto read = [&](const int q) __attribute__((always_inline)) {
+    f[q] = L.row_frag(off + (q & 1) * 32 * RB, q >> 1);
+  };
+#pragma unroll
+  for (int q = 0; q < kAhead; ++q) read(q);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + kAhead < NQ) read(q + kAhead);
+    // one read per fragment; those issued after fragment q may stay in flight
+    lds_wait_n((q + kAhead < NQ ? q + kAhead : NQ - 1) - q);
+    asm volatile("" : "+v"(f[q]));
+    const int kk = q >> 1, t = q & 1;
+    const bool fresh = kZero && kk == 0;
+    acc[t] = mfma(f[q], bv[kk], fresh ? f32x16_t{} : acc[t]);
+  }
+}
+
+// acc[i] (features 32i..32i+31) += tile^T x P for the tile at byte offset
+// off, P given per 16-token chunk j as packed accumulator halves pj[j]
+// (tokens 32(j/2) + 16(j%2) + pack8 order).  Fragment q = j DT + i feeds
+// MFMA q and is read kAhead MFMAs ahead (two LDS reads per fragment).
+template <int HD>
+AJ_DEV void cols_times(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const int off,
+                       const bf16x8_t (&pj)[4]) {
+  constexpr int DT = HD / 32, RB = HD * 2, NQ = 4 * DT, kAhead = 4;
+  bf16x8_t f[NQ];
+  auto read = [&](const int q) __attribute__((always_inline)) {
+    const int j = q / DT;
+    f[q] = L.col_frag(off + (32 * (j >> 1) + 16 * (j & 1)) * RB, q % DT);
+  };
+#pragma unroll
+  for (int q = 0; q < kAhead; ++q) read(q);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + kAhead < NQ) read(q + kAhead);
+    lds_wait_n(2 * ((q + kAhead < NQ ? q + kAhead : NQ - 1) - q));
+    asm volatile("" : "+v"(f[q]));
+    acc[q % DT] = mfma(f[q], pj[q / DT], acc[q % DT]);
   }
 }
 
@@ -327,26 +329,24 @@ AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const TileLanes<HD> &L, 
 
 // acc[i] (features 32i..32i+31) += tile^T x P over tokens t0..t0+31 of the
 // tile at byte offset off, P given as the two packed accumulator halves of
-// that 32-row block (pack8 order).  One feature block at a time, the next
-// block's two fragments read while the current block's MFMAs issue (four
-// fragments live, not eight).
+// that 32-row block (pack8 order).  Fragment q = 2i + h (token rows
+// t0 + 16h) feeds MFMA q and is read kAhead MFMAs ahead.
 template <int HD>
 AJ_DEV void cols_times_half(f32x16_t (&acc)[HD / 32], const TileLanes<HD> &L, const int off,
                             const int t0, const bf16x8_t (&pj)[2]) {
-  constexpr int DT = HD / 32, RB = HD * 2;
-  bf16x8_t f[2][2];
-  f[0][0] = L.col_frag(off + t0 * RB, 0);
-  f[0][1] = L.col_frag(off + (t0 + 16) * RB, 0);
+  constexpr int DT = HD / 32, RB = HD * 2, NQ = 2 * DT, kAhead = 3;
+  bf16x8_t f[NQ];
+  auto read = [&](const int q) __attribute__((always_inline)) {
+    f[q] = L.col_frag(off + (t0 + 16 * (q & 1)) * RB, q >> 1);
+  };
 #pragma unroll
-  for (int i = 0; i < DT; ++i) {
-    const int cur = i & 1;
-    lds_wait(f[cur]);
-    if (i + 1 < DT) {
-      f[cur ^ 1][0] = L.col_frag(off + t0 * RB, i + 1);
-      f[cur ^ 1][1] = L.col_frag(off + (t0 + 16) * RB, i + 1);
-    }
-    acc[i] = mfma(f[cur][0], pj[0], acc[i]);
-    acc[i] = mfma(f[cur][1], pj[1], acc[i]);
+  for (int q = 0; q < kAhead && q < NQ; ++q) read(q);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (q + kAhead < NQ) read(q + kAhead);
+    lds_wait_n(2 * ((q + kAhead < NQ ? q + kAhead : NQ - 1) - q));
+    asm volatile("" : "+v"(f[q]));
+    acc[q >> 1] = mfma(f[q], pj[q & 1], acc[q >> 1]);
   }
 }
 
