@@ -82,6 +82,19 @@ def test_host_validation_needs_no_gpu():
     assert L.aj_logprob_pg_loss_fwd(C.byref(lc), C.byref(li), *([None] * 9), 0, None) == 2
 
 
+def test_loss_saved_bytes_with_kept_logits():
+    """keep_logits adds the float32 logits of every scored row to the loss's
+    saved buffer, in bfloat16 only (the float32 path ignores it)."""
+    capi = _lib()
+    for dtype, grows in ((capi.AJ_BF16, True), (capi.AJ_F32, False)):
+        base = capi.aj_loss_saved_bytes(capi.LossCfg(256, 5000, 1024, 0.2, 1e-6, dtype, 0), 300)
+        kept = capi.aj_loss_saved_bytes(capi.LossCfg(256, 5000, 1024, 0.2, 1e-6, dtype, 1), 300)
+        if grows:
+            assert 300 * 5000 * 4 <= kept - base <= 300 * 5000 * 4 + 256, (base, kept)
+        else:
+            assert kept == base
+
+
 def test_text_merge_host_validation():
     """aj_merge_timelines_text: argument errors return before any HIP call."""
     capi = _lib()
