@@ -134,7 +134,8 @@ int aj_flatten_timelines(const aj_timelines *in, aj_packed *out, int32_t *err,
  * device array of aj_merge_noalloc_max_workspace_bytes() bytes (64 MiB), one
  * per GPU, held until the process ends and reused by every call on that GPU.
  * Inputs whose aj_merge_workspace_bytes exceeds it are refused with
- * AJ_ERR_WORKSPACE before anything is enqueued (at most ~16M unmerged tokens).
+ * AJ_ERR_WORKSPACE before anything is enqueued (about 470M unmerged tokens in
+ * few timelines; each timeline also takes ~60 bytes).
  * Outputs, errors and results are those of aj_merge_timelines, bit for bit.
  * The call allocates nothing (no hipMalloc or hipFree); the first call on a
  * device looks up that device's copy of the array.  Calls that overlap on

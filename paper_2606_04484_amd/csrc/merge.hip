@@ -14,20 +14,31 @@
 //     first transfer wins, and absorbed timelines arrive in descending j:
 //         payload(s, k) = s's own block if llm, else the block k of the largest
 //                         j absorbed into s whose block k is llm.
-// Kernels (token-level Match; seven launches):
-//   validate        one workgroup: offsets tile [0, n_tok) and [0, n_tl), every
-//                   timeline starts a block; writes the call's status word
-//   find_absorber   one workgroup per timeline j: candidates i from the episode's
-//                   last timeline down, prefix compare with early exit; a
-//                   survivor clears the claim slots of its own tokens
-//   claim           llm tokens of absorbed timelines vote (atomicMax of their
-//                   token index, which orders like j) in the claim slot of the
-//                   survivor token they land on (indexed like the input tokens)
-//   resolve         one workgroup: survivor scan -> segment index, cu_seqlens,
-//                   counts
+// Every token of a timeline is read by one pass that needs it: the prefix
+// compare reads the tokens of every timeline that has a candidate absorber,
+// the output pass the survivors'.  The compare splits each timeline into
+// items of kCmpChunk tokens, so a long timeline is many short, evenly sized
+// work items, and records each item's runs of llm tokens; the output pass
+// takes a survivor's transferred log-probs from its absorbed timelines' runs
+// (pulled, so nothing is cleared, voted into or read back per token).
+// Kernels (token-level Match):
+//   init_status     the call's status word
+//   setup           offsets tile [0, n_tok) and [0, n_tl), every timeline starts
+//                   a block; episode bounds per timeline; compare items per
+//                   timeline
+//   filter          one wavefront per timeline j: the first candidate, from the
+//                   episode's last timeline down, that can hold T_j as a prefix
+//                   (length, block boundary at |T_j|, first and last 64 tokens)
+//   compare         one workgroup per kCmpChunk tokens of T_j: full compare with
+//                   that candidate (a difference marks j), llm runs of the item
+//   finalize        absorber = the candidate, or for a marked j the candidates
+//                   below it compared in full (Algorithm 1's order)
+//   resolve         one workgroup: survivor scan -> cu_seqlens, counts
 //   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (each
-//                   workgroup a range of output positions); counts each range's
-//                   targets and writes their bitmask
+//                   workgroup a range of output positions); a survivor's non-llm
+//                   token takes the log-prob of the largest absorbed timeline
+//                   whose run covers its position; counts each range's targets
+//                   and writes their bitmask
 //   tgt_scan        one workgroup: offsets of the per-range target counts
 //   tgt_write       ascending masked targets from the bitmask, and each
 //                   segment's first target (cu_targets)
@@ -46,6 +57,9 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kChunk = 1024;          // tokens per workgroup in the block-start compaction
+constexpr int kCmpChunk = 4096;       // tokens per compare item: 64 rows of 64
+constexpr int kRuns = 4;              // llm runs kept per compare item (more: marked kRuns + 1)
+static_assert(kCmpChunk == 64 * 64, "one 64-bit llm row per lane of a wavefront");
 // Offsets that do not tile the input stop the merge (every count 0); bad flag
 // bytes are reported and the token is treated as written (author 3: not llm).
 constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY | AJ_DEVERR_BLOCKS;
@@ -68,11 +82,25 @@ struct MergeArgs {
   // workspace
   int32_t *status;      // [0] error bits seen by this call
   int32_t *tl_seg;      // [n_tl]
-  int32_t *claim;       // [n_tok] per survivor input token: source token of its log-prob
+  int32_t *seg_base;    // [n_tl] first input token of each segment's survivor
+  int32_t *range_rec;   // [n_ranges][kRecInts] per output range: first segment, transfer entries
   uint64_t *tbits;      // one bit per output position: a masked target
   int32_t *chunk_cnt;   // [n_chunks]
   int32_t *chunk_off;   // [n_chunks]
   int32_t *user_err;
+  // token-level Match only.  Compare item (j, k) covers positions
+  // [k * kCmpChunk, (k + 1) * kCmpChunk) of T_j and is slot
+  // tl_tok_off[j] / kCmpChunk + j + k: the slots of consecutive timelines
+  // never overlap, and n_tok / kCmpChunk + n_tl slots hold them all.
+  int32_t n_slots;
+  int32_t *ep_first;          // [n_tl] first timeline of the timeline's episode
+  int32_t *ep_last;           // [n_tl] last timeline of the timeline's episode
+  int32_t *cand;              // [n_tl] first candidate passing the filter, -1: none
+  int32_t *miss;              // [n_tl] nonzero: the full compare with cand found a difference
+  int4 *slot_rec;             // [n_slots] item: {j, first token of T_j, first token of the
+                              // candidate (-1: no item), positions | k << 13}
+  int32_t *rcnt;              // [n_slots] llm runs of the item (kRuns + 1: more than kRuns)
+  int32_t *runs;              // [n_slots][kRuns][2] [first, end) positions in the timeline
   // text-level Match only
   int32_t n_blk;
   const uint64_t *blk_text;   // [n_blk] text key per block
@@ -199,25 +227,205 @@ __global__ void validate_kernel(MergeArgs a) {
   if (bits) raise(a, bits);
 }
 
-// One workgroup per timeline j.
-__global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
-  const int j = spread_timeline(blockIdx.x, a.n_tl);
-  if (fatal(a)) {
-    if (threadIdx.x == 0) a.absorber[j] = -1;
-    return;
+// The checks of validate, then the token merge's per-timeline tables:
+// episode bounds and a cleared difference mark.  Tables are written only from
+// offsets that are in range; if any are not, every later kernel stops.
+__global__ __launch_bounds__(kBlock) void setup_kernel(MergeArgs a) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const int bits = validate_item(a, t);
+  if (bits) raise(a, bits);
+  if (t < a.n_traj) {
+    const int lo = a.traj_tl_off[t], hi = a.traj_tl_off[t + 1];
+    if (0 <= lo && lo <= hi && hi <= a.n_tl)
+      for (int i = lo; i < hi; ++i) {
+        a.ep_first[i] = lo;
+        a.ep_last[i] = hi - 1;
+      }
   }
-  // episode of j: largest e with traj_tl_off[e] <= j
-  int lo = 0, hi = a.n_traj - 1;
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (a.traj_tl_off[mid] <= j) lo = mid; else hi = mid - 1;
+  if (t < a.n_tl) a.miss[t] = 0;
+}
+
+// One wavefront per timeline j: the first candidate i (from the episode's
+// last timeline down, Algorithm 1's order) that passes the necessary
+// conditions of T_j <= T_i on a few tokens: |T_i| >= |T_j|, a block starts in
+// T_i right after T_j ends (or both end together), and the first and last 64
+// positions of T_j agree in token id and block-start bit.  Candidates above
+// the result fail a necessary condition, so they cannot absorb j.  Then the
+// records of j's compare slots (and of the unused slots up to j + 1's first):
+// everything a compare workgroup needs, in one load.
+__global__ __launch_bounds__(kBlock) void filter_kernel(MergeArgs a) {
+  const int j = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (j >= a.n_tl) return;
+  const bool bad = fatal(a);
+  int c = -1;
+  if (!bad) {
+    const int last = a.ep_last[j];
+    const int64_t bj = a.tl_tok_off[j], lj = a.tl_tok_off[j + 1] - bj;
+    const int64_t q1 = min((int64_t)lane, lj - 1), q2 = max(lj - 1 - lane, (int64_t)0);
+    const int32_t t0 = a.tok[bj], tj1 = a.tok[bj + q1], tj2 = a.tok[bj + q2];
+    const int fj1 = a.flags[bj + q1] & AJ_FLAG_BLOCK_START;
+    const int fj2 = a.flags[bj + q2] & AJ_FLAG_BLOCK_START;
+    for (int ib = last; ib > j && c < 0; ib -= 64) {
+      const int i = ib - lane;   // lane 0 holds the nearest the episode's end
+      bool ok = false;
+      int64_t bi = 0;
+      if (i > j) {
+        bi = a.tl_tok_off[i];
+        const int64_t li = a.tl_tok_off[i + 1] - bi;
+        ok = li >= lj && a.tok[bi] == t0 &&
+             (li == lj || (a.flags[bi + lj] & AJ_FLAG_BLOCK_START) != 0);
+      }
+      uint64_t m = __ballot(ok);
+      while (m) {
+        const int l = __ffsll((unsigned long long)m) - 1;
+        m &= m - 1;
+        const int64_t b = __shfl(bi, l, 64);
+        const bool eq = a.tok[b + q1] == tj1 && a.tok[b + q2] == tj2 &&
+                        (a.flags[b + q1] & AJ_FLAG_BLOCK_START) == fj1 &&
+                        (a.flags[b + q2] & AJ_FLAG_BLOCK_START) == fj2;
+        if (__ballot(!eq) == 0) {
+          c = ib - l;
+          break;
+        }
+      }
+    }
   }
-  while (lo + 1 < a.n_traj && a.traj_tl_off[lo + 1] <= j) ++lo;
-  const int last = a.traj_tl_off[lo + 1] - 1;
+  if (lane == 0) a.cand[j] = c;
+  if (bad) return;
+  const int64_t bj = a.tl_tok_off[j], ej = a.tl_tok_off[j + 1];
+  const int64_t bc = c >= 0 ? a.tl_tok_off[c] : 0;
+  // floor(b/C) + ceil((e-b)/C) <= floor(e/C) + 1: the slots of j end at or
+  // before the first slot of j + 1
+  const int s0 = (int)(bj / kCmpChunk) + j;
+  const int s1 = (int)(ej / kCmpChunk) + j + 1;
+  const int nk = (int)((ej - bj + kCmpChunk - 1) / kCmpChunk);
+  for (int g = s0 + lane; g < s1; g += 64) {
+    const int k = g - s0;
+    int4 r = make_int4(-1, 0, -1, 0);
+    if (k < nk && c >= 0) {
+      const int p0 = k * kCmpChunk;
+      r = make_int4(j, (int)(bj + p0), (int)(bc + p0),
+                    (int)((uint32_t)min((int64_t)kCmpChunk, ej - bj - p0) | ((uint32_t)k << 13)));
+    }
+    a.slot_rec[g] = r;
+  }
+}
+
+// Compare rounds per item: each thread takes 4 consecutive positions a round.
+constexpr int kCmpRounds = kCmpChunk / (4 * kBlock);
+// Four token ids from a dword-aligned address (multi-dword global loads need
+// only dword alignment).
+typedef int32_t i32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
+// Four consecutive flag bytes from any byte address, by aligned dword reads:
+// the dword holding the first byte and, when that is not its first byte, the
+// next one, which then holds the fourth (so neither read leaves the pages of
+// the bytes asked for).
+AJ_DEV uint32_t load_flags4(const uint8_t *p) {
+  const uintptr_t addr = reinterpret_cast<uintptr_t>(p);
+  const uint32_t *w = reinterpret_cast<const uint32_t *>(addr & ~(uintptr_t)3);
+  const uint32_t sh = (uint32_t)(addr & 3);
+  const uint32_t lo = w[0];
+  const uint32_t hi = sh ? w[1] : 0u;
+  return __builtin_amdgcn_alignbyte(hi, lo, sh);
+}
+
+// One workgroup per compare slot: positions [p0, p0 + kCmpChunk) of T_j
+// against the same positions of its candidate (token id and block-start
+// bit); a difference marks j.  The llm tokens of the item, as 64 rows of 64
+// bits in LDS, become its runs [first, end), kRuns at most (more: the item is
+// marked and the output pass reads its flags instead).  Each thread takes 4
+// consecutive positions a round: 16-byte token loads and 4 flag bytes per
+// dword.  Slots are dealt to the XCDs in contiguous ranges, so the items of
+// one episode -- which read the same candidate -- share an L2.
+__global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
+  const int g = spread_timeline(blockIdx.x, a.n_slots);
+  const int4 rc = a.slot_rec[g];
+  if (fatal(a) || rc.z < 0) return;
+  const int j = rc.x;
+  const int32_t uj = rc.y, uc = rc.z;   // first tokens of the item in T_j and its candidate
+  const int n = (int)((uint32_t)rc.w & 8191u);           // positions, 1..kCmpChunk
+  const int p0 = (int)((uint32_t)rc.w >> 13) * kCmpChunk;
+  __shared__ uint64_t rows[kCmpChunk / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  i32x4_a4 tj[kCmpRounds], tc[kCmpRounds];
+  uint32_t fj[kCmpRounds], fc[kCmpRounds];
+#pragma unroll
+  for (int r = 0; r < kCmpRounds; ++r) {
+    const int q = r * 4 * kBlock + 4 * (int)threadIdx.x;
+    if (q + 4 <= n) {
+      tj[r] = *reinterpret_cast<const i32x4_a4 *>(a.tok + uj + q);
+      tc[r] = *reinterpret_cast<const i32x4_a4 *>(a.tok + uc + q);
+      fj[r] = load_flags4(a.flags + uj + q);
+      fc[r] = load_flags4(a.flags + uc + q);
+    } else {   // the item's ragged end: clamped single reads
+      uint32_t xj = 0, xc = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int qq = min(q + e, n - 1);
+        tj[r][e] = a.tok[uj + qq];
+        tc[r][e] = a.tok[uc + qq];
+        xj |= (uint32_t)a.flags[uj + qq] << (8 * e);
+        xc |= (uint32_t)a.flags[uc + qq] << (8 * e);
+      }
+      fj[r] = xj;
+      fc[r] = xc;
+    }
+  }
+  int diff = 0, bad = 0;
+#pragma unroll
+  for (int r = 0; r < kCmpRounds; ++r) {
+    const int q = r * 4 * kBlock + 4 * (int)threadIdx.x;
+    const int n_in = max(0, min(4, n - q));                     // positions of the group in the item
+    const uint32_t in = n_in == 4 ? 0xffffffffu : (1u << (8 * n_in)) - 1u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) diff |= e < n_in && tj[r][e] != tc[r][e];
+    diff |= ((fj[r] ^ fc[r]) & in & 0x04040404u) != 0;
+    bad |= (fj[r] & (fj[r] >> 1) & in & 0x01010101u) != 0;     // author 3
+    const uint32_t llm = (fj[r] >> 1) & ~fj[r] & in & 0x01010101u;   // author 2
+    const uint32_t n4 = (llm & 1u) | ((llm >> 7) & 2u) | ((llm >> 14) & 4u) | ((llm >> 21) & 8u);
+    // the wave's 256 positions are 4 rows of 64, 16 lanes x 4 positions each:
+    // a row is its 16 lanes' nibbles side by side (an OR over the group)
+    uint64_t row = (uint64_t)n4 << (4 * (lane & 15));
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) row |= __shfl_xor(row, o, 64);
+    if ((lane & 15) == 0) rows[r * (kBlock / 16) + wave * 4 + (lane >> 4)] = row;   // bit = position % 64
+  }
+  if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
+  if (__syncthreads_or(diff) && threadIdx.x == 0) atomicOr(a.miss + j, 1);
+  if (wave != 0) return;
+  // runs: a start is an llm position whose predecessor in the item is not,
+  // an end one whose successor is not; the k-th start pairs with the k-th end
+  const uint64_t m = rows[lane];
+  const uint64_t prev = lane > 0 ? rows[lane - 1] >> 63 : 0;
+  const uint64_t next = lane < 63 ? rows[lane + 1] & 1 : 0;
+  uint64_t st = m & ~((m << 1) | prev);
+  uint64_t en = m & ~((m >> 1) | (next << 63));
+  int xs = __popcll(st), xe = __popcll(en);
+  const int ns = xs, ne = xe;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int ys = __shfl_up(xs, o, 64), ye = __shfl_up(xe, o, 64);
+    if (lane >= o) { xs += ys; xe += ye; }
+  }
+  const int total = __shfl(xs, 63, 64);
+  int32_t *dst = a.runs + (int64_t)g * (2 * kRuns);
+  for (int r = xs - ns; st && r < kRuns; ++r, st &= st - 1)
+    dst[2 * r] = p0 + 64 * lane + __ffsll((unsigned long long)st) - 1;
+  for (int r = xe - ne; en && r < kRuns; ++r, en &= en - 1)
+    dst[2 * r + 1] = p0 + 64 * lane + __ffsll((unsigned long long)en);
+  if (lane == 0) a.rcnt[g] = total > kRuns ? kRuns + 1 : total;
+}
+
+// Algorithm 1's answer for j from the candidates i = from, from - 1, ..., j + 1
+// (every candidate above `from` is known not to hold T_j as a prefix): the
+// first whose block-aligned prefix equals T_j, compared in full by the whole
+// workgroup with early exit; -1 if none.
+AJ_DEV int search_absorber(const MergeArgs &a, int j, int from) {
   const int64_t bj = a.tl_tok_off[j];
   const int64_t lj = a.tl_tok_off[j + 1] - bj;
-  int result = -1;
-  for (int i = last; i > j; --i) {
+  for (int i = from; i > j; --i) {
     const int64_t bi = a.tl_tok_off[i];
     const int64_t li = a.tl_tok_off[i + 1] - bi;
     if (li < lj) continue;
@@ -241,19 +449,35 @@ __global__ __launch_bounds__(kBlock) void find_absorber_kernel(MergeArgs a) {
       }
       if (__syncthreads_or(bad)) { equal = false; break; }
     }
-    if (equal) { result = i; break; }
+    if (equal) return i;
   }
-  if (threadIdx.x == 0) a.absorber[j] = result;
-  // a survivor's tokens are the claim slots its absorbed timelines vote in:
-  // cleared with 16-byte stores between a scalar head and tail
-  if (result < 0 && a.claim) {
-    int32_t *dst = a.claim + bj;
-    const int64_t head = min(lj, (int64_t)((4 - (bj & 3)) & 3));
-    const int64_t n4 = (lj - head) / 4;
-    if (threadIdx.x < head) dst[threadIdx.x] = -1;
-    int4 *d4 = reinterpret_cast<int4 *>(dst + head);
-    for (int64_t q = threadIdx.x; q < n4; q += kBlock) d4[q] = make_int4(-1, -1, -1, -1);
-    for (int64_t p = head + 4 * n4 + threadIdx.x; p < lj; p += kBlock) dst[p] = -1;
+  return -1;
+}
+
+// Timelines per finalize workgroup.
+constexpr int kFinPer = 64;
+
+// absorber[j] = the candidate when the full compare found no difference;
+// for a marked j the workgroup searches the candidates below it (the rare
+// case: a prefix that agrees at both ends and differs inside).
+__global__ __launch_bounds__(kBlock) void finalize_kernel(MergeArgs a) {
+  __shared__ int todo[kFinPer];
+  __shared__ int n_todo;
+  if (threadIdx.x == 0) n_todo = 0;
+  __syncthreads();
+  const bool bad = fatal(a);
+  const int j = blockIdx.x * kFinPer + (int)threadIdx.x;
+  if (threadIdx.x < kFinPer && j < a.n_tl) {
+    const int c = bad ? -1 : a.cand[j];
+    if (c >= 0 && a.miss[j] != 0) todo[atomicAdd(&n_todo, 1)] = j;
+    else a.absorber[j] = c;
+  }
+  __syncthreads();
+  const int n = n_todo;
+  for (int f = 0; f < n; ++f) {
+    const int jj = todo[f];
+    const int r = search_absorber(a, jj, a.cand[jj] - 1);
+    if (threadIdx.x == 0) a.absorber[jj] = r;
   }
 }
 
@@ -298,6 +522,7 @@ __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
       if ((surv >> r) & 1) {
         a.tl_seg[i] = seg[r];
         a.seg_src[seg[r]] = i;
+        a.seg_base[seg[r]] = (int32_t)a.tl_tok_off[i];
         a.cu_seqlens[seg[r]] = tok[r];
       } else {
         a.tl_seg[i] = -1;
@@ -315,40 +540,6 @@ __global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
     a.counts[2] = 0;
     a.counts[3] = mx_all;
   }
-}
-
-// Tokens of timeline i handled by one workgroup, kUnroll per thread at a
-// time (their loads issued together); p is the position in the timeline.
-constexpr int kUnroll = 4;
-
-// One workgroup per timeline: an absorbed timeline's llm tokens vote for the
-// survivor token they align with (the same position p in the survivor) with
-// their own token index; token offsets grow with the timeline index, so the
-// atomicMax winner is the token of the largest absorbed timeline, the one
-// Algorithm 1 lets write last.  The flag bytes of absorbed timelines are
-// checked here, those of survivors in emit.
-__global__ __launch_bounds__(kBlock) void claim_kernel(MergeArgs a) {
-  if (fatal(a)) return;
-  const int i = spread_timeline(blockIdx.x, a.n_tl);
-  const int s = a.absorber[i];
-  if (s < 0) return;
-  const int64_t b = a.tl_tok_off[i];
-  const int len = (int)(a.tl_tok_off[i + 1] - b);
-  int32_t *dst = a.claim + a.tl_tok_off[s];   // s is a survivor, len_s >= len
-  int bad = 0;
-  for (int p0 = 0; p0 < len; p0 += kUnroll * kBlock) {
-    uint8_t f[kUnroll];
-#pragma unroll
-    for (int r = 0; r < kUnroll; ++r)   // clamped (len >= 1): no branch between the loads
-      f[r] = a.flags[b + min(p0 + r * kBlock + (int)threadIdx.x, len - 1)];
-#pragma unroll
-    for (int r = 0; r < kUnroll; ++r) {
-      const int p = p0 + r * kBlock + (int)threadIdx.x;
-      bad |= p < len && (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
-      if (p < len && (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM) atomicMax(dst + p, (int32_t)(b + p));
-    }
-  }
-  if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
 
 // Largest s in [lo, hi] with cu[s] <= o (cu ascending, cu[lo] <= o), by one
@@ -379,102 +570,257 @@ AJ_DEV int thread_search(const int32_t *cu, int64_t o, int lo, int hi) {
   return lo;
 }
 
-// Output positions [ob, ob + kEmitSpan) per workgroup step (a grid-stride
-// walk over the merged length, which only the device knows): wave 0 finds
-// the first segment and tabulates the next 64 segments' output and input
-// offsets in LDS; every output then reads its token, the token's own
-// log-prob and advantage and its claim at once, and a claimed position
-// reads the claiming token's.  Work is spread evenly whatever the mix of
-// survivors and absorbed timelines.
+// Output positions [ob, ob + kEmitSpan) per range.  A first pass (range,
+// one wavefront per range) finds the range's first segment and, for token
+// Match, its transfer entries; the output pass (emit) then needs one record
+// load before its bulk reads.  Transfers: the candidates j of a segment's
+// survivor s are the earlier timelines of its episode with absorber[j] == s;
+// their llm runs that fall inside the range become entries [lo, hi) of output
+// positions with the distance to the source token.  A non-llm survivor token
+// takes the largest source among the entries that cover it (source token
+// indices grow with the timeline index, so that is the largest absorbed j,
+// the transfer Algorithm 1 keeps).
 constexpr int kEmitPer = 8;
 constexpr int kEmitSpan = kEmitPer * kBlock;
-constexpr int kEmitWgs = 2048;   // at most 8 workgroups per CU at once
+constexpr int kEmitWgs = 2048;   // grid of the stride loops when the occupancy query fails
+constexpr int kRangeEnt = 8;     // transfer entries per range record (more: every output walks)
+constexpr int kRecInts = 32;     // {first segment, entries or -1 (walk), kRangeEnt x {lo, hi, dl}}
+static_assert(2 + 3 * kRangeEnt <= kRecInts && kRecInts <= 64, "one record per wavefront load");
+static_assert(kEmitSpan <= kCmpChunk, "a range meets at most two compare items of a timeline");
+
+// Source token of position p of survivor s (whose own token there is not
+// llm): the token at p of the largest j absorbed into s whose token there is
+// llm, or -1.  One thread, candidates from the nearest down; used for ranges
+// a record cannot describe (more than 64 segments or kRangeEnt entries).
+AJ_DEV int64_t claim_walk(const MergeArgs &a, int s, int p) {
+  for (int j = s - 1; j >= a.ep_first[s]; --j) {
+    if (a.absorber[j] != s) continue;
+    const int64_t bj = a.tl_tok_off[j];
+    if (p >= a.tl_tok_off[j + 1] - bj) continue;
+    const int g = (int)(bj / kCmpChunk) + j + p / kCmpChunk;
+    const int n = a.rcnt[g];
+    bool hit = false;
+    if (n > kRuns) {
+      hit = (a.flags[bj + p] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
+    } else {
+      const int32_t *rr = a.runs + (int64_t)g * (2 * kRuns);
+      for (int r = 0; r < n; ++r) hit |= p >= rr[2 * r] && p < rr[2 * r + 1];
+    }
+    if (hit) return bj + p;
+  }
+  return -1;
+}
+
+// One wavefront per output range: the first segment (64 probes a step) and,
+// with use_claims, the transfer entries of the range's segments -- lanes
+// take (segment, candidate) pairs, each pair's runs in the range's positions
+// become entries (an item whose runs overflowed gives one entry whose flag
+// bytes are checked per output).
+__global__ __launch_bounds__(kBlock) void range_kernel(MergeArgs a, int use_claims) {
+  __shared__ int n_ent[kBlock / 64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * (kBlock / 64) + wave;
+  if (fatal(a)) return;
+  const int64_t n_out = a.counts[1];
+  const int n_seg = (int)a.counts[0];
+  const int64_t ob = (int64_t)r * kEmitSpan;
+  if (ob >= n_out) return;
+  const int64_t oe = min(ob + kEmitSpan, n_out);
+  const int s0 = wave_search(a.cu_seqlens, ob, 0, n_seg - 1);
+  int32_t *rec = a.range_rec + (int64_t)r * kRecInts;
+  int ne = 0;
+  if (use_claims) {
+    if (lane == 0) n_ent[wave] = 0;
+    const int sl = s0 + lane;
+    const int cs = a.cu_seqlens[min(sl, n_seg)];
+    const int c64 = a.cu_seqlens[min(s0 + 64, n_seg)];
+    const bool in = sl < n_seg && cs < oe;
+    const int sv = in ? a.seg_src[sl] : 0;
+    const int ce = in ? a.cu_seqlens[sl + 1] : 0;
+    const int np = in ? sv - a.ep_first[sv] : 0;
+    int excl = np;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(excl, o, 64);
+      if (lane >= o) excl += y;
+    }
+    const int total = __shfl(excl, 63, 64);
+    excl -= np;
+    if (s0 + 64 < n_seg && c64 < oe) ne = -1;   // more than 64 segments: walk
+    for (int pb = 0; pb < total && ne >= 0; pb += 64) {
+      const int idx = pb + lane;
+      int k = 0;   // the lane whose pair range holds idx
+#pragma unroll
+      for (int st = 32; st > 0; st >>= 1) {
+        const int v = __shfl(excl, min(k + st, 63), 64);
+        if (k + st < 64 && v <= idx) k += st;
+      }
+      const int svk = __shfl(sv, k, 64), csk = __shfl(cs, k, 64), cek = __shfl(ce, k, 64);
+      const int j = svk - 1 - (idx - __shfl(excl, k, 64));
+      if (idx < total && a.absorber[j] == svk) {
+        const int64_t bj = a.tl_tok_off[j];
+        const int lj = (int)(a.tl_tok_off[j + 1] - bj);
+        const int q0 = (int)(max(ob, (int64_t)csk) - csk);
+        const int q1 = (int)min(min(oe, (int64_t)cek) - csk, (int64_t)lj);
+        const int dl = (int)(bj - csk);   // source token = output position + dl
+        for (int kk = q0 / kCmpChunk; kk * kCmpChunk < q1; ++kk) {
+          const int g = (int)(bj / kCmpChunk) + j + kk;
+          const int nr = a.rcnt[g];
+          const int32_t *rr = a.runs + (int64_t)g * (2 * kRuns);
+          for (int x = 0; x < (nr > kRuns ? 1 : nr); ++x) {
+            int lo, hi;
+            uint32_t ovf = 0;
+            if (nr > kRuns) {
+              lo = max(q0, kk * kCmpChunk);
+              hi = min(q1, (kk + 1) * kCmpChunk);
+              ovf = 0x80000000u;
+            } else {
+              lo = max(rr[2 * x], q0);
+              hi = min(rr[2 * x + 1], q1);
+            }
+            if (lo >= hi) continue;
+            const int e = atomicAdd(&n_ent[wave], 1);
+            if (e < kRangeEnt) {
+              rec[2 + 3 * e] = csk + lo;
+              rec[3 + 3 * e] = (int32_t)((uint32_t)(csk + hi) | ovf);
+              rec[4 + 3 * e] = dl;
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      ne = n_ent[wave];
+      if (ne > kRangeEnt) ne = -1;
+    }
+  }
+  if (lane == 0) {
+    rec[0] = s0;
+    rec[1] = ne;
+  }
+}
+
+// One output of a range the record cannot describe (more than 64 segments
+// or kRangeEnt transfer entries): its segment by search, its transfer by
+// walking the candidates.  Writes the output; returns 1 for a target, 0 for
+// a masked token without one, -1 for an unmasked token.
+AJ_DEV int emit_one(const MergeArgs &a, int32_t o, int n_seg, int use_claims, int *bad) {
+  const int sg = thread_search(a.cu_seqlens, o, 0, n_seg - 1);
+  const int32_t pos = o - a.cu_seqlens[sg];
+  const int32_t u = a.seg_base[sg] + pos;
+  const uint8_t f = a.flags[u];
+  int64_t src = (f & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM ? (int64_t)u : -1;
+  if (src < 0 && use_claims) src = claim_walk(a, a.seg_src[sg], pos);
+  *bad |= (f & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
+  a.otok[o] = a.tok[u];
+  a.opos[o] = pos;
+  a.omask[o] = src >= 0;
+  a.olp[o] = src >= 0 ? a.old_logprob[src] : 0.f;
+  a.oadv[o] = src >= 0 ? a.adv[src] : 0.f;
+  return src < 0 ? -1 : (pos != 0 ? 1 : 0);
+}
 
 __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claims) {
   if (fatal(a)) return;
   const int64_t n_out = a.counts[1];
   const int n_seg = (int)a.counts[0];
   __shared__ int32_t seg_cu[65];
-  __shared__ int64_t seg_base[64];
-  __shared__ int seg_first;
-  const int lane = threadIdx.x & 63;
+  __shared__ int32_t seg_base[64];
+  __shared__ int n_ent;
+  __shared__ int32_t ent[3 * kRangeEnt];   // {lo, hi | overflow << 31, dl}
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int bad = 0;
   for (int64_t ob = (int64_t)blockIdx.x * kEmitSpan; ob < n_out;
        ob += (int64_t)gridDim.x * kEmitSpan) {
+    const int64_t oe = min(ob + kEmitSpan, n_out);
     if (threadIdx.x < 64) {
-      const int s0 = wave_search(a.cu_seqlens, ob, 0, n_seg - 1);
+      const int32_t *rec = a.range_rec + ob / kEmitSpan * kRecInts;
+      const int v = lane < kRecInts ? rec[lane] : 0;
+      const int s0 = __shfl(v, 0, 64), ne = __shfl(v, 1, 64);
+      if (lane >= 2 && lane < 2 + 3 * kRangeEnt) ent[lane - 2] = v;
       const int sl = s0 + lane;
-      seg_cu[lane] = a.cu_seqlens[min(sl, n_seg)];           // cu[n_seg] = n_out
+      seg_cu[lane] = a.cu_seqlens[min(sl, n_seg)];            // cu[n_seg] = n_out
       if (lane == 0) seg_cu[64] = s0 + 64 <= n_seg ? a.cu_seqlens[s0 + 64] : INT32_MAX;
-      seg_base[lane] = sl < n_seg ? a.tl_tok_off[a.seg_src[sl]] : 0;
-      if (lane == 0) seg_first = s0;
+      seg_base[lane] = sl < n_seg ? a.seg_base[sl] : 0;
+      if (lane == 0) n_ent = use_claims ? ne : 0;
     }
     __syncthreads();
-    int64_t u[kEmitPer];
-    int pos[kEmitPer], n_tgt = 0;
+    const int ne = n_ent;
+    int n_tgt = 0;
+    if (ne >= 0 && seg_cu[64] >= oe) {
+      // every output in a table segment, transfers as entries: token indices
+      // and output positions fit in 32 bits (n_tok < 2^31)
+      int32_t u[kEmitPer], pos[kEmitPer];
 #pragma unroll
-    for (int r = 0; r < kEmitPer; ++r) {
-      const int64_t o = min(ob + r * kBlock + (int64_t)threadIdx.x, n_out - 1);
-      int k;
-      int64_t cs, base;
-      if (o < seg_cu[64]) {
-        k = 0;   // largest k with seg_cu[k] <= o, in LDS
+      for (int r = 0; r < kEmitPer; ++r) {
+        const int32_t o = (int32_t)min(ob + r * kBlock + (int64_t)threadIdx.x, n_out - 1);
+        int k = 0;   // largest k with seg_cu[k] <= o, in LDS
 #pragma unroll
         for (int st = 32; st > 0; st >>= 1)
           if (k + st < 64 && seg_cu[k + st] <= o) k += st;
-        cs = seg_cu[k];
-        base = seg_base[k];
-      } else {   // more than 64 segments in the span: a search of its own
-        const int sg = thread_search(a.cu_seqlens, o, seg_first + 64, n_seg - 1);
-        cs = a.cu_seqlens[sg];
-        base = a.tl_tok_off[a.seg_src[sg]];
+        pos[r] = o - seg_cu[k];
+        u[r] = seg_base[k] + pos[r];
       }
-      pos[r] = (int)(o - cs);
-      u[r] = base + pos[r];
-    }
-    uint8_t f[kEmitPer];
-    int32_t t[kEmitPer], c[kEmitPer];
-    int64_t src[kEmitPer];
-    float lp[kEmitPer], ad[kEmitPer];
+      uint8_t f[kEmitPer];
+      int32_t t[kEmitPer];
 #pragma unroll
-    for (int r = 0; r < kEmitPer; ++r) {   // issued together
-      f[r] = a.flags[u[r]];
-      t[r] = a.tok[u[r]];
-      lp[r] = a.old_logprob[u[r]];
-      ad[r] = a.adv[u[r]];
-      c[r] = use_claims ? a.claim[u[r]] : -1;
-    }
-    // the token's own log-prob and advantage (llm), else the claiming token's
-#pragma unroll
-    for (int r = 0; r < kEmitPer; ++r) {
-      const bool own = (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM;
-      src[r] = own ? u[r] : (int64_t)c[r];
-      if (!own && c[r] >= 0) {
-        lp[r] = a.old_logprob[c[r]];
-        ad[r] = a.adv[c[r]];
+      for (int r = 0; r < kEmitPer; ++r) {   // issued together
+        f[r] = a.flags[u[r]];
+        t[r] = a.tok[u[r]];
       }
-      if (src[r] < 0) {
+      int32_t src[kEmitPer];
+#pragma unroll
+      for (int r = 0; r < kEmitPer; ++r) {
+        const int32_t o = (int32_t)(ob + r * kBlock + threadIdx.x);
+        src[r] = -1;
+        if ((f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_LLM) {   // the survivor's own llm token
+          src[r] = u[r];
+          continue;
+        }
+        for (int e = 0; e < ne; ++e) {
+          const uint32_t hi = (uint32_t)ent[3 * e + 1];
+          if (o < ent[3 * e] || (uint32_t)o >= (hi & 0x7fffffffu)) continue;
+          const int32_t s = o + ent[3 * e + 2];
+          if ((hi >> 31) && (a.flags[s] & AJ_AUTHOR_MASK) != AJ_AUTHOR_LLM) continue;
+          src[r] = max(src[r], s);
+        }
+      }
+      float lp[kEmitPer], ad[kEmitPer];
+#pragma unroll
+      for (int r = 0; r < kEmitPer; ++r) {   // only tokens that carry a log-prob
         lp[r] = 0.f;
         ad[r] = 0.f;
+        if (src[r] >= 0) {
+          lp[r] = a.old_logprob[src[r]];
+          ad[r] = a.adv[src[r]];
+        }
       }
-    }
-    const int wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int r = 0; r < kEmitPer; ++r) {
-      const int64_t o = ob + r * kBlock + threadIdx.x;
-      const bool in = o < n_out;
-      const bool has = in && src[r] >= 0;
-      const bool tgt = has && pos[r] != 0;
-      const uint64_t word = __ballot(tgt);
-      if (lane == 0) a.tbits[ob / 64 + r * (kBlock / 64) + wave] = word;
-      if (!in) continue;
-      bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
-      a.otok[o] = t[r];
-      a.opos[o] = pos[r];
-      a.omask[o] = has;
-      a.olp[o] = lp[r];
-      a.oadv[o] = ad[r];
-      n_tgt += tgt;
+      for (int r = 0; r < kEmitPer; ++r) {
+        const int64_t o = ob + r * kBlock + threadIdx.x;
+        const bool in = o < n_out;
+        const bool has = in && src[r] >= 0;
+        const bool tgt = has && pos[r] != 0;
+        const uint64_t word = __ballot(tgt);
+        if (lane == 0) a.tbits[ob / 64 + r * (kBlock / 64) + wave] = word;
+        if (!in) continue;
+        bad |= (f[r] & AJ_AUTHOR_MASK) == AJ_AUTHOR_MASK;
+        a.otok[o] = t[r];
+        a.opos[o] = pos[r];
+        a.omask[o] = has;
+        a.olp[o] = lp[r];
+        a.oadv[o] = ad[r];
+        n_tgt += tgt;
+      }
+    } else {
+#pragma unroll 1
+      for (int r = 0; r < kEmitPer; ++r) {
+        const int64_t o = ob + r * kBlock + threadIdx.x;
+        const int res = o < n_out ? emit_one(a, (int32_t)o, n_seg, use_claims, &bad) : -1;
+        const uint64_t word = __ballot(res > 0);
+        if (lane == 0) a.tbits[ob / 64 + r * (kBlock / 64) + wave] = word;
+        n_tgt += res > 0;
+      }
     }
     // the span's target count for the compaction (chunk = span)
     int tot;
@@ -852,8 +1198,12 @@ __global__ __launch_bounds__(64) void ti_kernel(MergeArgs a) {
 }
 
 struct MergeWs {
-  int32_t *status, *tl_seg, *claim, *chunk_cnt, *chunk_off;
+  int32_t *status, *tl_seg, *chunk_cnt, *chunk_off;
   uint64_t *tbits;
+  int32_t n_slots;
+  int32_t *ep_first, *ep_last, *cand, *miss, *rcnt, *runs;
+  int4 *slot_rec;
+  int32_t *seg_base, *range_rec;
   int32_t *blk_start, *tl_blk, *blk_tl, *blk_claim, *src_blk, *blk_off, *dst_off, *dst_pos;
   size_t bytes;
 };
@@ -870,8 +1220,18 @@ MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok, int32_t n_blk = -1) {
   w.chunk_off = c.take<int32_t>(at_least1(n_chunks));
   // one target bit per output; emit writes whole 2048-output spans
   w.tbits = c.take<uint64_t>((n_tok + kTgtChunk - 1) / kTgtChunk * (kTgtChunk / 64) + 1);
+  w.seg_base = c.take<int32_t>(at_least1(n_tl));
+  w.range_rec = c.take<int32_t>(at_least1((n_tok + kEmitSpan - 1) / kEmitSpan) * kRecInts);
   if (n_blk < 0) {
-    w.claim = c.take<int32_t>(at_least1(n_tok));
+    // compare items: n_tok / kCmpChunk + n_tl slots (n_tok < 2^31)
+    w.n_slots = (int32_t)(n_tok / kCmpChunk + n_tl);
+    w.ep_first = c.take<int32_t>(at_least1(n_tl));
+    w.ep_last = c.take<int32_t>(at_least1(n_tl));
+    w.cand = c.take<int32_t>(at_least1(n_tl));
+    w.miss = c.take<int32_t>(at_least1(n_tl));
+    w.slot_rec = c.take<int4>(at_least1(w.n_slots));
+    w.rcnt = c.take<int32_t>(at_least1(w.n_slots));
+    w.runs = c.take<int32_t>(at_least1((int64_t)w.n_slots * 2 * kRuns));
   } else {
     w.blk_start = c.take<int32_t>(n_blk + 1);
     w.tl_blk = c.take<int32_t>((int64_t)n_tl + 1);
@@ -913,7 +1273,10 @@ MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const 
   a.cu_targets = out->cu_targets; a.counts = out->counts;
   a.otok = out->tok; a.opos = out->pos; a.omask = out->mask; a.olp = out->old_logprob;
   a.oadv = out->adv; a.targets = out->targets;
-  a.status = w.status; a.tl_seg = w.tl_seg; a.claim = w.claim; a.tbits = w.tbits;
+  a.status = w.status; a.tl_seg = w.tl_seg; a.tbits = w.tbits;
+  a.n_slots = w.n_slots; a.ep_first = w.ep_first; a.ep_last = w.ep_last; a.cand = w.cand;
+  a.miss = w.miss; a.slot_rec = w.slot_rec; a.rcnt = w.rcnt; a.runs = w.runs;
+  a.seg_base = w.seg_base; a.range_rec = w.range_rec;
   a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
   a.blk_start = w.blk_start; a.tl_blk = w.tl_blk; a.blk_tl = w.blk_tl; a.blk_claim = w.blk_claim;
   a.src_blk = w.src_blk; a.blk_off = w.blk_off; a.dst_off = w.dst_off; a.dst_pos = w.dst_pos;
@@ -927,6 +1290,27 @@ void launch_validate(const MergeArgs &a, hipStream_t s) {
   validate_kernel<<<(n_val + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
 }
 
+// Workgroups of kBlock threads of a grid-stride kernel that are resident on
+// the current device at once (its occupancy times the CU count), so the
+// stride loop runs in one round; looked up once per device and kernel.
+constexpr int kMaxDev = 64;
+int resident_wgs(const void *kernel, int slot) {
+  static std::mutex mu;
+  static int cache[kMaxDev][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return kEmitWgs;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!cache[dev][slot]) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kBlock, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        per_cu <= 0 || cus <= 0)
+      return kEmitWgs;
+    cache[dev][slot] = per_cu * cus;
+  }
+  return cache[dev][slot];
+}
+
 // The target list and per-segment target offsets, once tok/pos/mask are out.
 // counted: emit already wrote the per-chunk target counts and the bitmask.
 void launch_targets(const MergeArgs &a, hipStream_t s, bool counted) {
@@ -935,7 +1319,8 @@ void launch_targets(const MergeArgs &a, hipStream_t s, bool counted) {
   tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
   const int64_t segs = ((int64_t)a.n_tl + 1 + kBlock - 1) / kBlock;
   const int64_t g = n_chunks > segs ? n_chunks : segs;
-  tgt_write_kernel<<<(int)(g < kEmitWgs ? g : kEmitWgs), kBlock, 0, s>>>(a);
+  const int64_t gw = resident_wgs(reinterpret_cast<const void *>(tgt_write_kernel), 1);
+  tgt_write_kernel<<<(int)(g < gw ? g : gw), kBlock, 0, s>>>(a);
 }
 
 int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t ws_bytes,
@@ -950,19 +1335,26 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
 
   hipStream_t s = (hipStream_t)stream;
   const int tk = aj::timing_begin(s, AJ_KC_MERGE, 0.0);
-  launch_validate(a, s);
-  if (in->n_tl > 0) {
-    if (merge) {
-      find_absorber_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
-      if (in->n_tok > 0) claim_kernel<<<in->n_tl, kBlock, 0, s>>>(a);
-    } else {
-      fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+  if (merge) {
+    // the checks and the per-timeline tables, then Algorithm 1 in closed form
+    const int n_set = (in->n_tl > in->n_traj ? in->n_tl : in->n_traj) + 1;
+    init_status_kernel<<<1, 64, 0, s>>>(a);
+    setup_kernel<<<(n_set + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
+    if (in->n_tl > 0) {
+      filter_kernel<<<(in->n_tl + kBlock / 64 - 1) / (kBlock / 64), kBlock, 0, s>>>(a);
+      if (a.n_slots > 0) compare_kernel<<<a.n_slots, kBlock, 0, s>>>(a);
+      finalize_kernel<<<(in->n_tl + kFinPer - 1) / kFinPer, kBlock, 0, s>>>(a);
     }
+  } else {
+    launch_validate(a, s);
+    if (in->n_tl > 0) fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
   }
   resolve_kernel<<<1, 1024, 0, s>>>(a);
   if (in->n_tok > 0) {
     const int64_t spans = (in->n_tok + kEmitSpan - 1) / kEmitSpan;
-    emit_kernel<<<(int)(spans < kEmitWgs ? spans : kEmitWgs), kBlock, 0, s>>>(a, merge ? 1 : 0);
+    range_kernel<<<(int)((spans + kBlock / 64 - 1) / (kBlock / 64)), kBlock, 0, s>>>(a, merge ? 1 : 0);
+    const int64_t gw = resident_wgs(reinterpret_cast<const void *>(emit_kernel), 0);
+    emit_kernel<<<(int)(spans < gw ? spans : gw), kBlock, 0, s>>>(a, merge ? 1 : 0);
   }
   launch_targets(a, s, true);
   aj::timing_end(s, tk);

@@ -148,4 +148,7 @@ def test_workspace_queries_grow_with_size():
     assert 0 < a < b
     # ~150 KB of saved activations per token at the 7B block shape
     assert 140e3 < b / 2000 < 160e3
-    assert capi.aj_merge_workspace_bytes(4, 32, 5000) > 5000 * 4
+    # per-token (target bits, range counts), per-item and per-timeline tables
+    w = capi.aj_merge_workspace_bytes(4, 32, 5000)
+    assert capi.aj_merge_workspace_bytes(4, 32, 500000) > w > 0
+    assert capi.aj_merge_workspace_bytes(4, 3200, 5000) > w

@@ -68,7 +68,7 @@ def test_noalloc_merge_matches_workspace_merge_twice():
 def test_noalloc_merge_refuses_inputs_beyond_its_workspace():
     from paper_2606_04484_amd import capi
     cap = capi.aj_merge_noalloc_max_workspace_bytes()
-    n_tok = cap // 4 + 4096          # the per-token array alone no longer fits
+    n_tok = 2 ** 31 - 1              # the largest input: its per-token tables alone do not fit
     assert capi.aj_merge_workspace_bytes(1, 1, n_tok) > cap
     tl = capi.Timelines(1, 1, n_tok, None, None, None, None, None, None)
     out = capi.Packed(*([None] * 11))
