@@ -323,9 +323,8 @@ typedef int32_t i32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 // next one, which then holds the fourth (so neither read leaves the pages of
 // the bytes asked for).
 AJ_DEV uint32_t load_flags4(const uint8_t *p) {
-  const uintptr_t addr = reinterpret_cast<uintptr_t>(p);
-  const uint32_t *w = reinterpret_cast<const uint32_t *>(addr & ~(uintptr_t)3);
-  const uint32_t sh = (uint32_t)(addr & 3);
+  const uint32_t sh = (uint32_t)(reinterpret_cast<uintptr_t>(p) & 3);
+  const uint32_t *w = reinterpret_cast<const uint32_t *>(p - sh);   // stays a global pointer
   const uint32_t lo = w[0];
   const uint32_t hi = sh ? w[1] : 0u;
   return __builtin_amdgcn_alignbyte(hi, lo, sh);
@@ -343,10 +342,15 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
   const int g = spread_timeline(blockIdx.x, a.n_slots);
   const int4 rc = a.slot_rec[g];
   if (fatal(a) || rc.z < 0) return;
-  const int j = rc.x;
-  const int32_t uj = rc.y, uc = rc.z;   // first tokens of the item in T_j and its candidate
-  const int n = (int)((uint32_t)rc.w & 8191u);           // positions, 1..kCmpChunk
-  const int p0 = (int)((uint32_t)rc.w >> 13) * kCmpChunk;
+  // the record is the workgroup's: its fields live in scalar registers
+  const int j = __builtin_amdgcn_readfirstlane(rc.x);
+  const int32_t uj = __builtin_amdgcn_readfirstlane(rc.y);   // first token of the item in T_j
+  const int32_t uc = __builtin_amdgcn_readfirstlane(rc.z);   // ... and in the candidate
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(rc.w);
+  const int n = (int)(w & 8191u);                           // positions, 1..kCmpChunk
+  const int p0 = (int)(w >> 13) * kCmpChunk;
+  const int32_t *tj0 = a.tok + uj, *tc0 = a.tok + uc;
+  const uint8_t *fj0 = a.flags + uj, *fc0 = a.flags + uc;
   __shared__ uint64_t rows[kCmpChunk / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   i32x4_a4 tj[kCmpRounds], tc[kCmpRounds];
@@ -355,19 +359,19 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
   for (int r = 0; r < kCmpRounds; ++r) {
     const int q = r * 4 * kBlock + 4 * (int)threadIdx.x;
     if (q + 4 <= n) {
-      tj[r] = *reinterpret_cast<const i32x4_a4 *>(a.tok + uj + q);
-      tc[r] = *reinterpret_cast<const i32x4_a4 *>(a.tok + uc + q);
-      fj[r] = load_flags4(a.flags + uj + q);
-      fc[r] = load_flags4(a.flags + uc + q);
+      tj[r] = *reinterpret_cast<const i32x4_a4 *>(tj0 + (uint32_t)q);
+      tc[r] = *reinterpret_cast<const i32x4_a4 *>(tc0 + (uint32_t)q);
+      fj[r] = load_flags4(fj0 + (uint32_t)q);
+      fc[r] = load_flags4(fc0 + (uint32_t)q);
     } else {   // the item's ragged end: clamped single reads
       uint32_t xj = 0, xc = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int qq = min(q + e, n - 1);
-        tj[r][e] = a.tok[uj + qq];
-        tc[r][e] = a.tok[uc + qq];
-        xj |= (uint32_t)a.flags[uj + qq] << (8 * e);
-        xc |= (uint32_t)a.flags[uc + qq] << (8 * e);
+        const uint32_t qq = (uint32_t)min(q + e, n - 1);
+        tj[r][e] = tj0[qq];
+        tc[r][e] = tc0[qq];
+        xj |= (uint32_t)fj0[qq] << (8 * e);
+        xc |= (uint32_t)fc0[qq] << (8 * e);
       }
       fj[r] = xj;
       fc[r] = xc;
