@@ -57,9 +57,13 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kChunk = 1024;          // tokens per workgroup in the block-start compaction
-constexpr int kCmpChunk = 4096;       // tokens per compare item: 64 rows of 64
+constexpr int kCmpChunk = 2048;       // tokens per compare item: 32 rows of 64
+constexpr int kRows = kCmpChunk / 64;                  // llm rows of 64 positions per item
+constexpr int kRowsPerLane = (kRows + 63) / 64;        // rows per lane of a wavefront
+constexpr int kCntBits = 14;          // item records hold positions (<= kCmpChunk) in 14 bits
 constexpr int kRuns = 4;              // llm runs kept per compare item (more: marked kRuns + 1)
-static_assert(kCmpChunk == 64 * 64, "one 64-bit llm row per lane of a wavefront");
+static_assert(kCmpChunk % 1024 == 0 && kCmpChunk < (1 << kCntBits) &&
+              (kRows <= 64 || kRows % 64 == 0), "item shape");
 // Offsets that do not tile the input stop the merge (every count 0); bad flag
 // bytes are reported and the token is treated as written (author 3: not llm).
 constexpr int kFatal = AJ_DEVERR_OFFSETS | AJ_DEVERR_EMPTY | AJ_DEVERR_BLOCKS;
@@ -98,7 +102,7 @@ struct MergeArgs {
   int32_t *cand;              // [n_tl] first candidate passing the filter, -1: none
   int32_t *miss;              // [n_tl] nonzero: the full compare with cand found a difference
   int4 *slot_rec;             // [n_slots] item: {j, first token of T_j, first token of the
-                              // candidate (-1: no item), positions | k << 13}
+                              // candidate (-1: no item), positions | k << kCntBits}
   int32_t *rcnt;              // [n_slots] llm runs of the item (kRuns + 1: more than kRuns)
   int32_t *runs;              // [n_slots][kRuns][2] [first, end) positions in the timeline
   // text-level Match only
@@ -306,7 +310,7 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(MergeArgs a) {
     if (k < nk && c >= 0) {
       const int p0 = k * kCmpChunk;
       r = make_int4(j, (int)(bj + p0), (int)(bc + p0),
-                    (int)((uint32_t)min((int64_t)kCmpChunk, ej - bj - p0) | ((uint32_t)k << 13)));
+                    (int)((uint32_t)min((int64_t)kCmpChunk, ej - bj - p0) | ((uint32_t)k << kCntBits)));
     }
     a.slot_rec[g] = r;
   }
@@ -332,7 +336,7 @@ AJ_DEV uint32_t load_flags4(const uint8_t *p) {
 
 // One workgroup per compare slot: positions [p0, p0 + kCmpChunk) of T_j
 // against the same positions of its candidate (token id and block-start
-// bit); a difference marks j.  The llm tokens of the item, as 64 rows of 64
+// bit); a difference marks j.  The llm tokens of the item, as rows of 64
 // bits in LDS, become its runs [first, end), kRuns at most (more: the item is
 // marked and the output pass reads its flags instead).  Each thread takes 4
 // consecutive positions a round: 16-byte token loads and 4 flag bytes per
@@ -347,8 +351,8 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
   const int32_t uj = __builtin_amdgcn_readfirstlane(rc.y);   // first token of the item in T_j
   const int32_t uc = __builtin_amdgcn_readfirstlane(rc.z);   // ... and in the candidate
   const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(rc.w);
-  const int n = (int)(w & 8191u);                           // positions, 1..kCmpChunk
-  const int p0 = (int)(w >> 13) * kCmpChunk;
+  const int n = (int)(w & ((1u << kCntBits) - 1));          // positions, 1..kCmpChunk
+  const int p0 = (int)(w >> kCntBits) * kCmpChunk;
   const int32_t *tj0 = a.tok + uj, *tc0 = a.tok + uc;
   const uint8_t *fj0 = a.flags + uj, *fc0 = a.flags + uc;
   __shared__ uint64_t rows[kCmpChunk / 64];
@@ -401,12 +405,24 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
   if (wave != 0) return;
   // runs: a start is an llm position whose predecessor in the item is not,
   // an end one whose successor is not; the k-th start pairs with the k-th end
-  const uint64_t m = rows[lane];
-  const uint64_t prev = lane > 0 ? rows[lane - 1] >> 63 : 0;
-  const uint64_t next = lane < 63 ? rows[lane + 1] & 1 : 0;
-  uint64_t st = m & ~((m << 1) | prev);
-  uint64_t en = m & ~((m >> 1) | (next << 63));
-  int xs = __popcll(st), xe = __popcll(en);
+  // lane l holds rows kRowsPerLane * l ... (positions 64 * row + bit)
+  constexpr int RL = kRowsPerLane;
+  const int nl = kRows / RL;   // lanes holding rows
+  uint64_t m[RL], st[RL], en[RL];
+#pragma unroll
+  for (int i = 0; i < RL; ++i) m[i] = lane < nl ? rows[RL * lane + i] : 0;
+  const uint64_t before = lane > 0 && lane < nl ? rows[RL * lane - 1] >> 63 : 0;
+  const uint64_t after = lane < nl - 1 ? rows[RL * (lane + 1)] & 1 : 0;
+  int xs = 0, xe = 0;
+#pragma unroll
+  for (int i = 0; i < RL; ++i) {
+    const uint64_t prev = i == 0 ? before : m[i - 1] >> 63;
+    const uint64_t next = i == RL - 1 ? after : m[i + 1] & 1;
+    st[i] = m[i] & ~((m[i] << 1) | prev);
+    en[i] = m[i] & ~((m[i] >> 1) | (next << 63));
+    xs += __popcll(st[i]);
+    xe += __popcll(en[i]);
+  }
   const int ns = xs, ne = xe;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -415,10 +431,15 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(MergeArgs a) {
   }
   const int total = __shfl(xs, 63, 64);
   int32_t *dst = a.runs + (int64_t)g * (2 * kRuns);
-  for (int r = xs - ns; st && r < kRuns; ++r, st &= st - 1)
-    dst[2 * r] = p0 + 64 * lane + __ffsll((unsigned long long)st) - 1;
-  for (int r = xe - ne; en && r < kRuns; ++r, en &= en - 1)
-    dst[2 * r + 1] = p0 + 64 * lane + __ffsll((unsigned long long)en);
+  int rs = xs - ns, re = xe - ne;
+#pragma unroll
+  for (int i = 0; i < RL; ++i) {
+    const int base = p0 + 64 * (RL * lane + i);
+    for (; st[i] && rs < kRuns; ++rs, st[i] &= st[i] - 1)
+      dst[2 * rs] = base + __ffsll((unsigned long long)st[i]) - 1;
+    for (; en[i] && re < kRuns; ++re, en[i] &= en[i] - 1)
+      dst[2 * re + 1] = base + __ffsll((unsigned long long)en[i]);
+  }
   if (lane == 0) a.rcnt[g] = total > kRuns ? kRuns + 1 : total;
 }
 
