@@ -520,6 +520,25 @@ def roofline(rec, flops, peak, workload):
     return roof, kc
 
 
+def ceilings(torch, capi):
+    """What this chip sustains, measured on it (the roofline lines keep the
+    published peaks): the bf16 MFMA rate from registers with random and with
+    constant operands, no memory traffic (the random-operand rate is the
+    ceiling for products of random or trained weights: the matrix cores draw
+    more power when their inputs toggle), and the HBM rates of a streaming
+    copy and a read-only stream."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    scratch = torch.empty(2 * cus * 256, dtype=torch.float32, device="cuda")
+    rnd = capi.aj_ceiling_mfma_bf16(True, scratch)
+    const = capi.aj_ceiling_mfma_bf16(False, scratch)
+    buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    copy, read = capi.aj_ceiling_copy(buf)
+    del scratch, buf
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_random_tflops": round(rnd, 1), "mfma_bf16_constant_tflops": round(const, 1),
+            "hbm_copy_gbps": round(copy, 1), "hbm_read_gbps": round(read, 1), "cus": cus}
+
+
 def merge_record(rec, tl, Lm):
     """The merge against HBM: algorithmic bytes = every unmerged token's id and
     flags, the llm tokens' log-prob and advantage read once; every merged
@@ -560,8 +579,10 @@ def main():
         merger = actor.Merger(dev)
         merger.launch(True)
         merger.layout(c.model.pack_tokens)
-        print(json.dumps({"workload": c.name,
-                          "merge_scaled": merge_scaled(merger, tl, torch, capi, actor)}))
+        ms = merge_scaled(merger, tl, torch, capi, actor)
+        ceil = ceilings(torch, capi)
+        ms["frac_of_copy"] = round(ms["GB/s"] / ceil["hbm_copy_gbps"], 4)
+        print(json.dumps({"workload": c.name, "merge_scaled": ms, "ceilings": ceil}))
         return
 
     m = cfg.model
@@ -616,6 +637,10 @@ def main():
     W_head = None if args.no_cpu_baseline else {k: v.cpu() for k, v in live["W"].items()}
     del live
     torch.cuda.empty_cache()
+    ceil = ceilings(torch, capi)
+    if roof and roof.get("unit") == "TFLOP/s":
+        ceil["roofline_frac_of_random_mfma"] = round(roof["achieved"] / ceil["mfma_bf16_random_tflops"], 4)
+    out["ceilings"] = ceil
 
     subs = {}
     for k in [x for x in args.sub.split(",") if x.strip()]:
@@ -641,6 +666,9 @@ def main():
         torch.cuda.empty_cache()
     if subs:
         out["sub_records"] = subs
+        scaled = subs.get("agent7b-32x10..30", {}).get("merge_scaled")
+        if scaled:
+            scaled["frac_of_copy"] = round(scaled["GB/s"] / ceil["hbm_copy_gbps"], 4)
     if mr:
         out["merge"] = mr
     if not args.no_cpu_baseline:

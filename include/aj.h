@@ -496,6 +496,26 @@ int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */
 int aj_timing_read(double *ms, int64_t *launches, double *flops);
 
+/* Measured ceilings of the current device, for reading the rooflines against
+ * what the chip sustains as well as its published peaks (bench reporting;
+ * nothing on the path calls them).  Both wait for their kernels.
+ *   aj_ceiling_mfma_bf16: v_mfma_f32_32x32x16_bf16 from registers only, 8
+ *     independent accumulators per wave, two waves per SIMD, with random
+ *     bfloat16 operands (random_operands != 0: every product's inputs
+ *     toggle, as with trained or random weights) or constant ones; *tflops
+ *     is the best of 3 runs.  out: device scratch of at least
+ *     2 * CUs * 256 floats (AJ_ERR_WORKSPACE otherwise).
+ *   aj_ceiling_copy: a streaming copy of bytes / 2 from the first half of
+ *     buf (device, 16-byte aligned, at least 64 bytes per thread of a grid of
+ *     8 workgroups of 256 per CU) to the second, 16-byte loads and stores,
+ *     then a read-only stream of the first half; *gbps counts read + write
+ *     bytes of the copy, *read_gbps the bytes read; best of 3 runs each after
+ *     a first one.
+ * Errors: AJ_ERR_NULL, AJ_ERR_SHAPE, AJ_ERR_HIP. */
+int aj_ceiling_mfma_bf16(int random_operands, void *out, size_t out_bytes, void *stream,
+                         double *tflops);
+int aj_ceiling_copy(void *buf, size_t bytes, void *stream, double *gbps, double *read_gbps);
+
 #ifdef __cplusplus
 }
 #endif

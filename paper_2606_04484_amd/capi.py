@@ -152,6 +152,8 @@ EXPORTS = {
                                 C.c_int, vp]),
     "aj_timing_enable": (C.c_int, [C.c_int]),
     "aj_timing_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
+    "aj_ceiling_mfma_bf16": (C.c_int, [C.c_int, vp, sz, vp, C.POINTER(C.c_double)]),
+    "aj_ceiling_copy": (C.c_int, [vp, sz, vp, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
 }
 
 KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd", "lm_fwd", "lm_dz",
@@ -499,3 +501,23 @@ def aj_timing_read():
     ms, cnt, fl = (C.c_double * n)(), (i64 * n)(), (C.c_double * n)()
     _check(lib().aj_timing_read(ms, cnt, fl), "aj_timing_read")
     return {k: (ms[i], int(cnt[i]), fl[i]) for i, k in enumerate(KCLASSES)}
+
+
+# ------------------------------------------------------------------ ceilings
+
+def aj_ceiling_mfma_bf16(random_operands, out, stream=None):
+    """TFLOP/s of the register-only bf16 MFMA loop; out: float32 device scratch."""
+    r = C.c_double()
+    _check(lib().aj_ceiling_mfma_bf16(1 if random_operands else 0, ptr(out),
+                                      out.numel() * out.element_size(), stream_handle(stream),
+                                      C.byref(r)), "aj_ceiling_mfma_bf16")
+    return r.value
+
+
+def aj_ceiling_copy(buf, stream=None):
+    """(copy GB/s counting read + write, read-only GB/s) of streams over buf."""
+    r, rd = C.c_double(), C.c_double()
+    _check(lib().aj_ceiling_copy(ptr(buf), buf.numel() * buf.element_size(),
+                                 stream_handle(stream), C.byref(r), C.byref(rd)),
+           "aj_ceiling_copy")
+    return r.value, rd.value
