@@ -506,11 +506,10 @@ int aj_timing_read(double *ms, int64_t *launches, double *flops);
  *     is the best of 3 runs.  out: device scratch of at least
  *     2 * CUs * 256 floats (AJ_ERR_WORKSPACE otherwise).
  *   aj_ceiling_copy: a streaming copy of bytes / 2 from the first half of
- *     buf (device, 16-byte aligned, at least 64 bytes per thread of a grid of
- *     8 workgroups of 256 per CU) to the second, 16-byte loads and stores,
- *     then a read-only stream of the first half; *gbps counts read + write
- *     bytes of the copy, *read_gbps the bytes read; best of 3 runs each after
- *     a first one.
+ *     buf (device, 16-byte aligned, 32 bytes to 1 TiB) to the second, one
+ *     16-byte item per thread, then a read-only stream of the first half;
+ *     *gbps counts read + write bytes of the copy, *read_gbps the bytes read;
+ *     best of 3 runs each after a first one.
  * Errors: AJ_ERR_NULL, AJ_ERR_SHAPE, AJ_ERR_HIP. */
 int aj_ceiling_mfma_bf16(int random_operands, void *out, size_t out_bytes, void *stream,
                          double *tflops);
