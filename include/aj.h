@@ -244,6 +244,17 @@ typedef struct {
   const void *mlp_norm;         /* [d] */
   const void *w_gate_up;        /* [2*d_ff, d] */
   const void *w_down;           /* [d, d_ff] */
+  /* Optional, bfloat16 only: the same four projection weights stored
+   * transposed, [in][out] -- all four or none (NULL).  When given, the
+   * forward's projections read these: their rows reach the matrix cores
+   * faster than those of the [out][in] copies (3-6 % on the 32B-class
+   * shapes).  The caller keeps them equal to the weights above
+   * (aj_transpose_bf16 after every update); the backward, the float32 path
+   * and the LoRA stack read only the weights above. */
+  const void *w_qkv_t;          /* [d, (Hq+2Hkv)*hd] */
+  const void *w_o_t;            /* [Hq*hd, d] */
+  const void *w_gate_up_t;      /* [d, 2*d_ff] */
+  const void *w_down_t;         /* [d_ff, d] */
 } aj_block_weights;
 
 typedef struct {                /* float32, accumulated */
@@ -393,6 +404,12 @@ typedef struct {
   float inv_n_mask;             /* 1 / (loss-masked tokens of the WHOLE batch) */
   const float *ref_logprob;     /* [n_tgt] reference-policy log-prob of each target, or NULL */
   float kl_coef;                /* KL penalty weight; no KL term when 0 or ref_logprob NULL */
+  const void *w_vocab_t;        /* optional: w_vocab transposed, [d, vocab], equal to
+                                   w_vocab (vocab a multiple of 8, else AJ_ERR_SHAPE); the
+                                   bfloat16 vocab projections of the forward and of the
+                                   backward's recompute then read it (faster rows, as for
+                                   aj_block_weights); the float32 path ignores it.  NULL =
+                                   w_vocab only */
 } aj_loss_in;
 
 size_t aj_loss_saved_bytes(const aj_loss_cfg *cfg, int32_t n_tgt);
@@ -495,6 +512,11 @@ enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
 int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */
 int aj_timing_read(double *ms, int64_t *launches, double *flops);
+
+/* dst[c][r] = src[r][c] for a row-major bfloat16 matrix src [rows, cols]
+ * (device pointers, no overlap): the transposed weight copies above.
+ * Errors: AJ_ERR_NULL, AJ_ERR_SHAPE (rows or cols < 1). */
+int aj_transpose_bf16(const void *src, int32_t rows, int32_t cols, void *dst, void *stream);
 
 /* Measured ceilings of the current device, for reading the rooflines against
  * what the chip sustains as well as its published peaks (bench reporting;

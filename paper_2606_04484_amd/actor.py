@@ -149,7 +149,7 @@ class ActorUpdate:
     KEEP_LOGITS_SHARE = 0.5
 
     def __init__(self, m, weights, device="cuda", lora=None, lora_rank=0, lora_scale=1.0,
-                 keep_logits=False):
+                 keep_logits=False, transposed_weights=True):
         """lora: optional dict of LoRA matrices keyed by lora_key (storage dtype of the
         weights); then only they train (self.G holds their gradients) and every
         weight, gain, the embedding and the LM head stay frozen.
@@ -158,7 +158,11 @@ class ActorUpdate:
         True makes the backward read the forward's float32 logits instead
         (bfloat16; bitwise the same result, ~4 bytes per logit of a pack in
         HBM); None = True whenever one pack's logits fit in KEEP_LOGITS_SHARE of
-        the free memory."""
+        the free memory.
+        transposed_weights: bfloat16 full training keeps [in][out] copies of the
+        four projection weights of every block and of the LM head, refreshed at
+        the start of every step (so they follow any weight update), which the
+        forward's projections read faster than the [out][in] weights."""
         self.m = m
         self.W = weights
         self.n_layers = getattr(m, "n_layers", 1)
@@ -178,6 +182,17 @@ class ActorUpdate:
         self._cap = (0, 0)
         self.layers = [{k: weights[layer_key(k, l)] for k in BLOCK_NAMES}
                        for l in range(self.n_layers)]
+        self.WT = None
+        if transposed_weights and self.dt == torch.bfloat16 and lora is None:
+            self.WT = {}
+            for l, lw in enumerate(self.layers):
+                for k in ("w_qkv", "w_o", "w_gate_up", "w_down"):
+                    t = torch.empty(lw[k].shape[1], lw[k].shape[0], dtype=self.dt, device=self.dev)
+                    self.WT[layer_key(k, l)] = t
+                    lw[k + "_t"] = t
+            if m.vocab % 8 == 0:
+                self.WT["w_vocab"] = torch.empty(m.d_model, m.vocab, dtype=self.dt,
+                                                 device=self.dev)
         if lora is None:
             self.layer_grads = [{k: self.G[layer_key(k, l)] for k in BLOCK_NAMES}
                                 for l in range(self.n_layers)]
@@ -196,6 +211,16 @@ class ActorUpdate:
         self._cap = (0, 0)
         if hasattr(self, "logprob"):
             del self.logprob
+
+    def refresh_transposed(self):
+        """The [in][out] weight copies from the current weights (part of each step)."""
+        if self.WT is None:
+            return
+        for k, t in self.WT.items():
+            C.aj_transpose_bf16(self.W[k], t)
+
+    def _w_vocab_t(self):
+        return None if self.WT is None else self.WT.get("w_vocab")
 
     def zero_grads(self):
         for g in self.G.values():
@@ -248,6 +273,8 @@ class ActorUpdate:
             self.prepare(L)
         W, G = self.W, self.G
         inv = 1.0 / L.n_mask if L.n_mask else 0.0
+        self.refresh_transposed()
+        wvt = self._w_vocab_t()
         for p in L.packs:
             t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
             n = t1 - t0
@@ -262,12 +289,14 @@ class ActorUpdate:
             C.aj_logprob_pg_loss_fwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
                                      self.logprob[r0:r1], self.lse[r0:r1], self.stats, self.lws,
-                                     self.err, row_base=t0, ref_logprob=ref, kl_coef=kl_coef)
+                                     self.err, row_base=t0, ref_logprob=ref, kl_coef=kl_coef,
+                                     w_vocab_t=wvt)
             C.aj_logprob_pg_loss_bwd(self.lcfg, tg, L.tok, L.old_logprob, L.adv, inv, y,
                                      W["final_norm"], W["w_vocab"], self.lsaved,
                                      self.logprob[r0:r1], self.lse[r0:r1], dh,
                                      G.get("final_norm"), G.get("w_vocab"), self.lws,
-                                     row_base=t0, ref_logprob=ref, kl_coef=kl_coef)
+                                     row_base=t0, ref_logprob=ref, kl_coef=kl_coef,
+                                     w_vocab_t=wvt)
             if self.lora is None:
                 C.aj_stack_bwd(self.bcfg, self.layers, cu, pos, p["max_len"], x, self.ckpt,
                                self.saved, dh, dh, self.layer_grads, self.bws, base=t0)
@@ -290,6 +319,7 @@ class ActorUpdate:
         """Log-probs of every target under the current weights (forward only)."""
         self.prepare(L)
         inv = 1.0 / L.n_mask if L.n_mask else 0.0
+        self.refresh_transposed()
         for p in L.packs:
             t0, t1, s0, s1, r0, r1 = p["t0"], p["t1"], p["s0"], p["s1"], p["r0"], p["r1"]
             n = t1 - t0
@@ -300,5 +330,5 @@ class ActorUpdate:
                                      L.adv, inv, self.y[:n], self.W["final_norm"],
                                      self.W["w_vocab"], self.lsaved, self.logprob[r0:r1],
                                      self.lse[r0:r1], self.stats, self.lws, self.err,
-                                     row_base=t0)
+                                     row_base=t0, w_vocab_t=self._w_vocab_t())
         return self.logprob[:L.n_mask]

@@ -67,8 +67,12 @@ class BlockCfg(C.Structure):
                 ("d_ff", i32), ("rms_eps", f32), ("rope_theta", f32), ("dtype", i32)]
 
 
+BLOCK_TRANSPOSED = ("w_qkv_t", "w_o_t", "w_gate_up_t", "w_down_t")
+
+
 class BlockWeights(C.Structure):
-    _fields_ = [(n, vp) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+    _fields_ = [(n, vp) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+                + BLOCK_TRANSPOSED]
 
 
 class BlockGrads(C.Structure):
@@ -99,7 +103,7 @@ class LossCfg(C.Structure):
 class LossIn(C.Structure):
     _fields_ = [("n_tok", i32), ("n_tgt", i32), ("row_base", i32), ("targets", vp), ("tok", vp),
                 ("old_logprob", vp), ("adv", vp), ("inv_n_mask", f32), ("ref_logprob", vp),
-                ("kl_coef", f32)]
+                ("kl_coef", f32), ("w_vocab_t", vp)]
 
 
 EXPORTS = {
@@ -152,6 +156,7 @@ EXPORTS = {
                                 C.c_int, vp]),
     "aj_timing_enable": (C.c_int, [C.c_int]),
     "aj_timing_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
+    "aj_transpose_bf16": (C.c_int, [vp, i32, i32, vp, vp]),
     "aj_ceiling_mfma_bf16": (C.c_int, [C.c_int, vp, sz, vp, C.POINTER(C.c_double)]),
     "aj_ceiling_copy": (C.c_int, [vp, sz, vp, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
 }
@@ -309,8 +314,7 @@ def _varlen(n_tok, n_seg, max_seqlen, base, cu_seqlens, pos):
 
 
 def _bw(w):
-    return BlockWeights(*[ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm",
-                                              "w_gate_up", "w_down")])
+    return _layers([w], BlockWeights)[0]
 
 
 def aj_varlen_block_fwd(cfg, w, cu_seqlens, pos, max_seqlen, x, y, saved, ws=None, stream=None,
@@ -340,9 +344,12 @@ def aj_stack_ckpt_bytes(cfg, n_layers, n_tok):
 
 
 def _layers(ws, kind, names=("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")):
+    """Per-layer structs; weight dicts may also hold the optional transposed
+    projection weights (BLOCK_TRANSPOSED keys, all four or none)."""
     arr = (kind * len(ws))()
     for i, w in enumerate(ws):
-        arr[i] = kind(*[ptr(w[k]) for k in names])
+        extra = BLOCK_TRANSPOSED if kind is BlockWeights else ()
+        arr[i] = kind(*[ptr(w[k]) for k in names], *[ptr(w.get(k)) for k in extra])
     return arr
 
 
@@ -420,16 +427,17 @@ def aj_loss_workspace_bytes(cfg, n_tgt):
     return int(lib().aj_loss_workspace_bytes(C.byref(cfg), n_tgt))
 
 
-def _loss_in(n_tok, row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob, kl_coef):
+def _loss_in(n_tok, row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob, kl_coef,
+             w_vocab_t=None):
     return LossIn(n_tok, targets.numel(), row_base, ptr(targets), ptr(tok), ptr(old_logprob),
-                  ptr(adv), float(inv_n_mask), ptr(ref_logprob), float(kl_coef))
+                  ptr(adv), float(inv_n_mask), ptr(ref_logprob), float(kl_coef), ptr(w_vocab_t))
 
 
 def aj_logprob_pg_loss_fwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
                            w_vocab, saved, logprob, lse, stats, ws, err=None, stream=None,
-                           row_base=0, ref_logprob=None, kl_coef=0.0):
+                           row_base=0, ref_logprob=None, kl_coef=0.0, w_vocab_t=None):
     li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob,
-                  kl_coef)
+                  kl_coef, w_vocab_t)
     _check(lib().aj_logprob_pg_loss_fwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
                                         ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
                                         ptr(stats), ptr(err), ptr(ws),
@@ -439,9 +447,10 @@ def aj_logprob_pg_loss_fwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, f
 
 def aj_logprob_pg_loss_bwd(cfg, targets, tok, old_logprob, adv, inv_n_mask, h, final_norm,
                            w_vocab, saved, logprob, lse, dh, d_final_norm, d_w_vocab, ws,
-                           stream=None, row_base=0, ref_logprob=None, kl_coef=0.0):
+                           stream=None, row_base=0, ref_logprob=None, kl_coef=0.0,
+                           w_vocab_t=None):
     li = _loss_in(h.shape[0], row_base, targets, tok, old_logprob, adv, inv_n_mask, ref_logprob,
-                  kl_coef)
+                  kl_coef, w_vocab_t)
     _check(lib().aj_logprob_pg_loss_bwd(C.byref(cfg), C.byref(li), ptr(h), ptr(final_norm),
                                         ptr(w_vocab), ptr(saved), ptr(logprob), ptr(lse),
                                         ptr(dh), ptr(d_final_norm), ptr(d_w_vocab), ptr(ws),
@@ -521,3 +530,12 @@ def aj_ceiling_copy(buf, stream=None):
                                  stream_handle(stream), C.byref(r), C.byref(rd)),
            "aj_ceiling_copy")
     return r.value, rd.value
+
+
+def aj_transpose_bf16(src, dst, stream=None):
+    """dst (cols x rows) = src (rows x cols)^T, both bfloat16 device tensors."""
+    rows, cols = src.shape
+    if dst.shape != (cols, rows) or src.dtype != torch.bfloat16 or dst.dtype != torch.bfloat16:
+        raise ValueError("aj_transpose_bf16: dst must be the bfloat16 [cols, rows] of src")
+    _check(lib().aj_transpose_bf16(ptr(src), rows, cols, ptr(dst), stream_handle(stream)),
+           "aj_transpose_bf16")

@@ -236,10 +236,17 @@ int block_fwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   const int n = v.n_tok, d = c.d_model, hd = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
   const int qdim = (Hq + 2 * Hkv) * hd, F = c.d_ff;
   int r;
+  // the projections read the transposed ([in][out]) weights when given
+  const bool tw = sizeof(T) == 2 && !lf && w.w_qkv_t;
+  auto weight = [&](Gemm &g, const void *w_kmajor, const void *w_t) {
+    g.B = tw ? w_t : w_kmajor;
+    g.ldb = tw ? g.N : g.K;
+    g.b_kmajor = !tw;
+  };
   rmsnorm_fwd<T>(x, (const T *)w.attn_norm, n, d, c.rms_eps, nullptr, 0, (T *)sv.a, sv.rstd1, st);
   Gemm g;
   g.M = n; g.N = qdim; g.K = d;
-  g.A = sv.a; g.lda = d; g.B = w.w_qkv; g.ldb = d; g.C = sv.qkv; g.ldc = qdim;
+  g.A = sv.a; g.lda = d; weight(g, w.w_qkv, w.w_qkv_t); g.C = sv.qkv; g.ldc = qdim;
   if (lf && (r = lora_u<T>(c, *lf, kQkv, (const T *)sv.a, n, st))) return r;
   lora_fwd_seg(g, lf, kQkv);
   if ((r = gemm<T>(g, st))) return r;
@@ -249,7 +256,7 @@ int block_fwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
   if ((r = attn_fwd<T>(at, st))) return r;
   g = Gemm();
   g.M = n; g.N = d; g.K = Hq * hd;
-  g.A = sv.o; g.lda = Hq * hd; g.B = w.w_o; g.ldb = Hq * hd; g.C = sv.x1; g.ldc = d; g.R = x;
+  g.A = sv.o; g.lda = Hq * hd; weight(g, w.w_o, w.w_o_t); g.C = sv.x1; g.ldc = d; g.R = x;
   if (lf && (r = lora_u<T>(c, *lf, kO, (const T *)sv.o, n, st))) return r;
   lora_fwd_seg(g, lf, kO);
   if ((r = gemm<T>(g, st))) return r;
@@ -257,14 +264,14 @@ int block_fwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
                  sv.rstd2, st);
   g = Gemm();
   g.M = n; g.N = 2 * F; g.K = d;
-  g.A = sv.b; g.lda = d; g.B = w.w_gate_up; g.ldb = d; g.C = sv.gu; g.ldc = 2 * F;
+  g.A = sv.b; g.lda = d; weight(g, w.w_gate_up, w.w_gate_up_t); g.C = sv.gu; g.ldc = 2 * F;
   if (lf && (r = lora_u<T>(c, *lf, kGu, (const T *)sv.b, n, st))) return r;
   lora_fwd_seg(g, lf, kGu);
   if ((r = gemm<T>(g, st))) return r;
   swiglu_fwd<T>((const T *)sv.gu, n, F, (T *)sv.s, st);
   g = Gemm();
   g.M = n; g.N = d; g.K = F;
-  g.A = sv.s; g.lda = F; g.B = w.w_down; g.ldb = F; g.C = y; g.ldc = d; g.R = sv.x1;
+  g.A = sv.s; g.lda = F; weight(g, w.w_down, w.w_down_t); g.C = y; g.ldc = d; g.R = sv.x1;
   if (lf && (r = lora_u<T>(c, *lf, kDown, (const T *)sv.s, n, st))) return r;
   lora_fwd_seg(g, lf, kDown);
   if ((r = gemm<T>(g, st))) return r;
@@ -370,6 +377,9 @@ int block_bwd(const aj_block_cfg &c, const aj_block_weights &w, const aj_varlen 
 int check_weights(const aj_block_weights *w, const char *name) {
   AJ_REQUIRE(w && w->attn_norm && w->w_qkv && w->w_o && w->mlp_norm && w->w_gate_up && w->w_down,
              AJ_ERR_NULL, "%s: null weight", name);
+  const int nt = !!w->w_qkv_t + !!w->w_o_t + !!w->w_gate_up_t + !!w->w_down_t;
+  AJ_REQUIRE(nt == 0 || nt == 4, AJ_ERR_NULL, "%s: %d of the 4 transposed weights given", name,
+             nt);
   return AJ_OK;
 }
 
@@ -470,6 +480,15 @@ int check_lora(const aj_lora *lo, const aj_lora_grads *lg, int nl, const char *n
 }
 
 }  // namespace
+
+extern "C" int aj_transpose_bf16(const void *src, int32_t rows, int32_t cols, void *dst,
+                                 void *stream) {
+  AJ_REQUIRE(src && dst, AJ_ERR_NULL, "aj_transpose_bf16: null pointer");
+  AJ_REQUIRE(rows > 0 && cols > 0 && (int64_t)((rows + 63) / 64) * ((cols + 63) / 64) < (1ll << 31),
+             AJ_ERR_SHAPE, "aj_transpose_bf16: %d x %d", rows, cols);
+  aj::transpose16(src, rows, cols, dst, (hipStream_t)stream);
+  return aj::check_launch("aj_transpose_bf16");
+}
 
 extern "C" size_t aj_block_saved_bytes(const aj_block_cfg *cfg, int32_t n_tok) {
   if (!cfg || n_tok < 0) return 0;

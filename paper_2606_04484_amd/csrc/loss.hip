@@ -309,10 +309,12 @@ AJ_DEV void lds_barrier() {
 // logits tile z = hn W^T (rows: targets, columns: 256 vocab ids) reduced in
 // registers: per row, the tile's max and sum of exp (log2 units) and, in the
 // tile that holds it, the target's logit.  Logits never leave the chip.
+// B_K: the vocab weights as stored, [V][d] (k-major) or transposed [d][V].
+template <bool B_K>
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
-    int n, int V, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
+    int n, int V, int d, const bf16_t *hn, const bf16_t *wv, int ldw, const int32_t *tpos,
     const int32_t *tok, float2 *tile_ms, float *zt, float *zkeep) {
-  __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<true, B_K, 4> sm;
   __shared__ int ttok[Cfg::BM];
   __shared__ float2 red[Cfg::WN][Cfg::BM];
   const int tiles_m = (n + Cfg::BM - 1) / Cfg::BM, tiles_n = (V + Cfg::BN - 1) / Cfg::BN;
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_fwd_fused_kernel(
     ttok[threadIdx.x] = m < n ? tok[tpos[m]] : -1;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop8s<true, true, Cfg, 4>(acc, hn, d, wv, d, n, V, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, B_K, Cfg, 4>(acc, hn, d, wv, ldw, n, V, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   // A row of this wave's 128 columns lives in the 32 lanes of a half-wave, 4
@@ -465,10 +467,16 @@ __global__ __launch_bounds__(256) void lm_dz_kept_kernel(int n, int cw, int c0, 
 
 // dz = g (onehot(target) - softmax) for vocab columns [c0, c0 + cw), from the
 // recomputed logits, straight to bfloat16.
+// wc: the chunk's vocab weights, [cw][d] (B_K) or columns of the transposed
+// [d][V] copy, row stride ldw.
+template <bool B_K>
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
-    int n, int cw, int c0, int d, const bf16_t *hn, const bf16_t *wv, const int32_t *tpos,
-    const int32_t *tok, const float *lse, const float *g, bf16_t *dz) {
-  __shared__ __attribute__((aligned(16))) Smem<true, true> sm;
+    int n, int cw, int c0, int d, const bf16_t *hn, const bf16_t *wc, int ldw,
+    const int32_t *tpos, const int32_t *tok, const float *lse, const float *g, bf16_t *dz) {
+  // The body is device code only: this compiler's host pass rejects the
+  // main-loop call of the B_K = true instance (its device pass accepts both).
+#if defined(__HIP_DEVICE_COMPILE__)
+  __shared__ __attribute__((aligned(16))) gemm_core::Smem4s<true, B_K, 4> sm;
   __shared__ int ttok[Cfg::BM];
   __shared__ float tl[Cfg::BM], tg[Cfg::BM];
   const int tiles_m = (n + Cfg::BM - 1) / Cfg::BM, tiles_n = (cw + Cfg::BN - 1) / Cfg::BN;
@@ -481,7 +489,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     tg[threadIdx.x] = m < n ? g[m] : 0.f;
   }
   f32x16_t acc[Cfg::TM][Cfg::TN];
-  gemm_core::mainloop8s<true, true, Cfg, 4>(acc, hn, d, wv + (int64_t)c0 * d, d, n, cw, m0, n0, 0, d, sm);
+  gemm_core::mainloop8s<true, B_K, Cfg, 4>(acc, hn, d, wc, ldw, n, cw, m0, n0, 0, d, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   auto dz_of = [&](float a, int rl, int col) { return dz_value(a, tl[rl], tg[rl], col == ttok[rl]); };
@@ -547,6 +555,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     }
     lds_barrier();
   }
+#endif
 }
 
 int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
@@ -559,6 +568,8 @@ int check_cfg(const aj_loss_cfg *c, const aj_loss_in *in, const char *name) {
   AJ_REQUIRE(c->clip_eps >= 0 && c->rms_eps > 0, AJ_ERR_SHAPE, "%s: eps", name);
   AJ_REQUIRE(in->n_tok >= 0 && in->n_tgt >= 0 && in->n_tgt <= in->n_tok, AJ_ERR_SHAPE,
              "%s: n_tok %d n_tgt %d", name, in->n_tok, in->n_tgt);
+  AJ_REQUIRE(!in->w_vocab_t || c->vocab % 8 == 0, AJ_ERR_SHAPE,
+             "%s: the transposed vocab weights need vocab %% 8 == 0 (vocab %d)", name, c->vocab);
   AJ_REQUIRE(in->n_tgt == 0 || (in->targets && in->tok && in->old_logprob && in->adv),
              AJ_ERR_NULL, "%s: null input arrays", name);
   return AJ_OK;
@@ -591,9 +602,14 @@ int loss_fwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     const int tiles_n = (c.vocab + Cfg::BN - 1) / Cfg::BN;
     const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * tiles_n;
     const int tk = aj::timing_begin(st, AJ_KC_LM_FWD, 2.0 * n * (double)c.vocab * d);
-    lm_fwd_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, c.vocab, d, (const bf16_t *)sv.hn,
-                                                   (const bf16_t *)w_vocab, w.tpos, in.tok,
-                                                   w.tile_ms, w.zt, sv.z);
+    if (in.w_vocab_t)
+      lm_fwd_fused_kernel<false><<<tiles, Cfg::NT, 0, st>>>(
+          n, c.vocab, d, (const bf16_t *)sv.hn, (const bf16_t *)in.w_vocab_t, c.vocab, w.tpos,
+          in.tok, w.tile_ms, w.zt, sv.z);
+    else
+      lm_fwd_fused_kernel<true><<<tiles, Cfg::NT, 0, st>>>(
+          n, c.vocab, d, (const bf16_t *)sv.hn, (const bf16_t *)w_vocab, d, w.tpos, in.tok,
+          w.tile_ms, w.zt, sv.z);
     aj::timing_end(st, tk);
     lm_combine_kernel<<<(n + 3) / 4, 256, 0, st>>>(n, tiles_n, w.tile_ms, w.zt, lse, logprob);
     token_check_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, w.tpos, in.tok, c.vocab, err);
@@ -651,9 +667,14 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
     } else if (sizeof(T) == 2) {
       const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
       const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
-      lm_dz_fused_kernel<<<tiles, Cfg::NT, 0, st>>>(n, cw, c0, d, (const bf16_t *)sv.hn,
-                                                    (const bf16_t *)w_vocab, w.tpos, in.tok, lse,
-                                                    w.g, (bf16_t *)w.dz);
+      if (in.w_vocab_t)
+        lm_dz_fused_kernel<false><<<tiles, Cfg::NT, 0, st>>>(
+            n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)in.w_vocab_t + c0, c.vocab,
+            w.tpos, in.tok, lse, w.g, (bf16_t *)w.dz);
+      else
+        lm_dz_fused_kernel<true><<<tiles, Cfg::NT, 0, st>>>(
+            n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)w_vocab + (int64_t)c0 * d, d,
+            w.tpos, in.tok, lse, w.g, (bf16_t *)w.dz);
       aj::timing_end(st, tk);
     } else {
       if ((r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true))) return r;

@@ -39,6 +39,8 @@ void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s);
 template <typename T>
 void scale_cast(const float *in, int64_t n, float scale, T *out, T *lo, hipStream_t s);
 void fill_f32(float *p, int64_t n, float v, hipStream_t s);
+// dst[c][r] = src[r][c] for a row-major [rows, cols] matrix of 16-bit elements.
+void transpose16(const void *src, int rows, int cols, void *dst, hipStream_t s);
 void splitk_reduce(const float *part, int S, int64_t n, float *out, bool accumulate, hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM

@@ -311,6 +311,48 @@ __global__ void splitk_reduce_kernel(const float *part, int S, int64_t n, float 
 
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
+// ---------------------------------------------------------------- transpose
+// dst[c][r] = src[r][c], 16-bit elements, 64 x 64 tiles through LDS: a tile's
+// rows are read as 16-byte chunks (8 per row, 2 per thread) and written out
+// as 16-byte chunks of its columns; tiles past the matrix edge go element by
+// element.  The padding of 8 elements per LDS row spreads a column's reads
+// over the banks.
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *src, int rows, int cols,
+                                                          uint16_t *dst) {
+  __shared__ __attribute__((aligned(16))) uint16_t t[64][64 + 8];
+  const int tiles_c = (cols + 63) / 64;
+  const int r0 = (int)(blockIdx.x / tiles_c) * 64, c0 = (int)(blockIdx.x % tiles_c) * 64;
+  const bool full = r0 + 64 <= rows && c0 + 64 <= cols && cols % 8 == 0 && rows % 8 == 0 &&
+                    (((uintptr_t)src | (uintptr_t)dst) & 15) == 0;
+  if (full) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = threadIdx.x + 256 * h, r = q >> 3, c = (q & 7) * 8;
+      const uint4 v = *reinterpret_cast<const uint4 *>(src + (int64_t)(r0 + r) * cols + c0 + c);
+      *reinterpret_cast<uint4 *>(&t[r][c]) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = threadIdx.x + 256 * h, c = q >> 3, r = (q & 7) * 8;
+      uint16_t e[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) e[k] = t[r + k][c];
+      uint4 v;
+      v.x = e[0] | (uint32_t)e[1] << 16;
+      v.y = e[2] | (uint32_t)e[3] << 16;
+      v.z = e[4] | (uint32_t)e[5] << 16;
+      v.w = e[6] | (uint32_t)e[7] << 16;
+      *reinterpret_cast<uint4 *>(dst + (int64_t)(c0 + c) * rows + r0 + r) = v;
+    }
+    return;
+  }
+  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
+    const int r = r0 + (q >> 6), c = c0 + (q & 63);
+    if (r < rows && c < cols) dst[(int64_t)c * rows + r] = src[(int64_t)r * cols + c];
+  }
+}
+
 }  // namespace
 
 
@@ -381,6 +423,13 @@ void cast_from_f32(const float *in, int64_t n, T *out, hipStream_t s) {
 template <typename T>
 void scale_cast(const float *in, int64_t n, float scale, T *out, T *lo, hipStream_t s) {
   if (n > 0) scale_cast_kernel<T><<<blocks_for(n, 256), 256, 0, s>>>(in, n, scale, out, lo);
+}
+
+void transpose16(const void *src, int rows, int cols, void *dst, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return;
+  const int64_t tiles = (int64_t)((rows + 63) / 64) * ((cols + 63) / 64);
+  transpose16_kernel<<<(unsigned)tiles, 256, 0, s>>>((const uint16_t *)src, rows, cols,
+                                                     (uint16_t *)dst);
 }
 
 void fill_f32(float *p, int64_t n, float v, hipStream_t s) {

@@ -80,6 +80,20 @@ def test_host_validation_needs_no_gpu():
     lc = capi.LossCfg(128, 1024, 1024, 0.2, 1e-6, 0)
     li = capi.LossIn(10, 11, 0, None, None, None, None, 1.0)      # n_tgt > n_tok
     assert L.aj_logprob_pg_loss_fwd(C.byref(lc), C.byref(li), *([None] * 9), 0, None) == 2
+    # transposed weights: all four projections or none; a vocab the transposed
+    # LM-head copy cannot hold in 16-byte rows
+    cfg = capi.BlockCfg(128, 4, 4, 32, 512, 1e-6, 1e6, 1)
+    w = capi.BlockWeights(*[C.c_void_p(16)] * 6, C.c_void_p(16), C.c_void_p(16))
+    assert L.aj_varlen_block_fwd(C.byref(cfg), C.byref(w), C.byref(vl), None, None, None, None,
+                                 0, None) == 1
+    assert b"transposed" in L.aj_last_error()
+    w = capi.BlockWeights(*[C.c_void_p(16)] * 10)
+    assert L.aj_varlen_block_fwd(C.byref(cfg), C.byref(w), C.byref(vl), None, None, None, None,
+                                 0, None) == 0                     # empty pack: nothing to do
+    lc = capi.LossCfg(128, 1001, 1024, 0.2, 1e-6, 1)
+    li = capi.LossIn(10, 5, 0, None, None, None, None, 1.0, None, 0.0, C.c_void_p(16))
+    assert L.aj_logprob_pg_loss_fwd(C.byref(lc), C.byref(li), *([None] * 9), 0, None) == 2
+    assert b"vocab" in L.aj_last_error()
 
 
 def test_loss_saved_bytes_with_kept_logits():

@@ -24,15 +24,17 @@ GRADS = ("emb", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down", 
 
 
 def run_gpu(case, merged=True, pack_tokens=131072, ref_pos=None, kl_coef=0.0, record=False,
-            keep_logits=None):
+            keep_logits=None, transposed_weights=True):
     """ref_pos: optional reference log-probs per merged position (host array);
     record: also return the library's per-class kernel launch record of the step;
-    keep_logits: the LM-head backward from kept logits (None: the actor's choice)."""
+    keep_logits: the LM-head backward from kept logits (None: the actor's choice);
+    transposed_weights: the bf16 forward projections read [in][out] copies."""
     from paper_2606_04484_amd import actor, capi
     dev = actor.upload_timelines(case.tl, case.old)
     L = actor.merge(dev, merged=merged, pack_tokens=pack_tokens, text=merged and case.text)
     if case.lora is None:
-        A = actor.ActorUpdate(case.m, case.device_weights(), keep_logits=keep_logits)
+        A = actor.ActorUpdate(case.m, case.device_weights(), keep_logits=keep_logits,
+                              transposed_weights=transposed_weights)
     else:
         A = actor.ActorUpdate(case.m, case.device_weights(), lora=case.device_weights(which=case.lora),
                               lora_rank=next(v for k, v in case.lora.items()
@@ -106,6 +108,37 @@ def test_bf16_two_layers_small_packs():
     got = run_gpu(case, True, pack_tokens=700)
     assert len(got["L"].packs) > 3
     check(case, got, True, 2e-2, 1e-2, 1e-2, 0.999)
+
+
+def test_transposed_weights_bitwise_equal():
+    """The bf16 forward projections and vocab products reading the [in][out]
+    weight copies feed every MFMA the same operands in the same order as the
+    [out][in] path: log-probs, loss and every gradient bit for bit, over
+    several packs and two layers (the checkpoint recompute reads them too);
+    and both meet the oracle at the bf16 bounds."""
+    m = dataclasses.replace(bf16_case_model(**BF16_CASES["hd64_gqa2"]), n_layers=2)
+    case = Case(workload(m), noise_std=0.3, margin=0.05)
+    a = run_gpu(case, True, pack_tokens=700, transposed_weights=True)
+    b = run_gpu(case, True, pack_tokens=700, transposed_weights=False)
+    assert len(a["L"].packs) > 3
+    np.testing.assert_array_equal(a["lp"], b["lp"])
+    assert a["loss"] == b["loss"]
+    for k in a["grads"]:
+        np.testing.assert_array_equal(a["grads"][k], b["grads"][k], err_msg=k)
+    check(case, b, True, 2e-2, 1e-2, 1e-2, 0.999)
+
+
+@pytest.mark.parametrize("shape", [(64, 64), (1000, 200), (70, 130), (5120, 8), (3, 1)])
+def test_transpose_bf16(shape):
+    """aj_transpose_bf16 against torch's transpose, bit for bit: whole 64x64
+    tiles, ragged edges, one-column and tiny matrices."""
+    from paper_2606_04484_amd import capi
+    g = torch.Generator(device="cuda").manual_seed(11)
+    src = torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16)
+    dst = torch.full((shape[1], shape[0]), 7.0, dtype=torch.bfloat16, device="cuda")
+    capi.aj_transpose_bf16(src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src.t().contiguous())
 
 
 def test_tiny_f32_lora():
@@ -230,10 +263,13 @@ def test_bf16(name, merged):
 def test_bf16_long_reductions_reach_the_4wave_kernels(merged):
     """The long-reduction case at the bf16 bounds, with the launch record showing
     that the 4-wave NN and NT kernels ran (and TN on the unmerged layout, whose
-    5856 tokens are the weight gradients' reduction)."""
+    5856 tokens are the weight gradients' reduction).  The forward projections
+    read the [out][in] weights here, so that they run the NT layout (with the
+    transposed copies they run NN, as test_transposed_weights_bitwise_equal
+    checks)."""
     m = bf16_case_model(**BF16_CASES["hd64_long_k"])
     case = Case(workload(m), noise_std=0.3, margin=0.05)
-    got = run_gpu(case, merged, record=True)
+    got = run_gpu(case, merged, record=True, transposed_weights=False)
     rec = got["rec"]
     print("launches: " + ", ".join(f"{k} {v[1]}" for k, v in rec.items() if v[1]), flush=True)
     assert rec["gemm4_nn"][1] > 0 and rec["gemm4_nt"][1] > 0

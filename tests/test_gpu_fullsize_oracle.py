@@ -10,9 +10,12 @@ host) and large enough that every long-reduction GEMM layout runs the way it
 does in the benchmark:
   * NN, 4 waves: d h = d z W_chunk (reduction = the 32768-wide vocab chunk)
     and the gate/up input gradient (reduction 2 d_ff = 17920);
-  * NT, 4 waves: the down projection forward (reduction d_ff = 8960);
+  * NN, 4 waves, also the down projection forward (reduction d_ff = 8960),
+    whose weight the step reads from its transposed [in][out] copy;
   * TN, 4 waves: every block weight gradient (reduction = 7147 tokens);
-the test asserts that each of these kernel classes actually launched.
+the test asserts that each of these kernel classes actually launched (the
+NT layout, which the forward runs on the [out][in] weights, is compared with
+the oracle at small shapes in tests/test_gpu_actor.py).
 
 Checked (Section 4.2 step (4): the update; Section 4.4.2: on merged
 timelines): every target's log-prob (absolute 2e-2), the loss (relative
@@ -95,9 +98,14 @@ def gpu_run(case):
 
 
 def test_long_reduction_layouts_ran(gpu_run):
+    """The step as the actor runs it: the forward projections read the
+    transposed weight copies, so every long reduction runs the 4-wave NN or TN
+    layout (the NT one is compared with the oracle at small shapes, with the
+    [out][in] weights)."""
     rec = gpu_run["rec"]
-    for k in ("gemm4_nn", "gemm4_nt", "gemm4_tn", "lm_fwd", "lm_dz", "attn_fwd", "attn_bwd"):
+    for k in ("gemm4_nn", "gemm4_tn", "lm_fwd", "lm_dz", "attn_fwd", "attn_bwd"):
         assert rec[k][1] > 0, k
+    assert rec["gemm4_nt"][1] == 0 and rec["gemm_nt"][1] == 0
 
 
 def test_targets_and_logprobs(case, gpu_run):
