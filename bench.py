@@ -65,16 +65,19 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-# HBM bytes per launch of the dominant kernel (the TN and NN long-reduction
-# GEMMs take nearly the same time per step, so both are listed), from two rocprofv3 --pmc passes
-# (FETCH_SIZE, WRITE_SIZE) over the same bench command, each scaled by the
-# counter's reading for a plain copy of known size.  Keyed by (kernel class,
-# workload); `sources` are hashed so that a changed kernel reports null.
+# HBM bytes per launch of the dominant kernel class, from two rocprofv3 --pmc
+# passes (FETCH_SIZE, WRITE_SIZE) over the same bench command, each scaled by
+# the counter's reading for a plain copy of known size.  Keyed by (kernel
+# class, workload); an entry holds while the GEMM sources hash to `sources`
+# and a step launches the class `launches` times (the same mix of products),
+# otherwise the line reports null.
 TRAFFIC = {
-    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.4e6, "sources": "c74b4918568820ba"},
-    ("gemm4_nn", "block1.5b-64x8"): {"bytes_per_launch": 5478.4e6, "sources": "c74b4918568820ba"},
-    ("gemm4_tn", "long32b-8x60"): {"bytes_per_launch": 10932.2e6, "sources": "c74b4918568820ba"},
-    ("gemm4_nn", "long32b-8x60"): {"bytes_per_launch": 11196.4e6, "sources": "c74b4918568820ba"},
+    ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.4e6, "launches": 27,
+                                     "sources": "c74b4918568820ba"},
+    ("gemm4_tn", "long32b-8x60"): {"bytes_per_launch": 10932.2e6, "launches": 92,
+                                   "sources": "c74b4918568820ba"},
+    ("gemm4_nn", "long32b-8x60"): {"bytes_per_launch": 15834.5e6, "launches": 104,
+                                   "sources": "c74b4918568820ba"},
 }
 
 
@@ -512,7 +515,8 @@ def roofline(rec, flops, peak, workload):
             "traffic": None, "launches": d["launches"],
             "avg_launch_ms": round(d["ms"] / max(d["launches"], 1), 4)}
     tr = TRAFFIC.get((dom, workload))
-    if tr and dom.startswith("gemm") and tr["sources"] == source_hash(GEMM_SOURCES):
+    if (tr and dom.startswith("gemm") and tr["launches"] == d["launches"]
+            and tr["sources"] == source_hash(GEMM_SOURCES)):
         roof["traffic"] = tr["bytes_per_launch"]
         roof["traffic_unit"] = "bytes"
     kc = {k: {kk: round(vv, 4) if isinstance(vv, float) else vv for kk, vv in v.items()}
