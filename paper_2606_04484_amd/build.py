@@ -18,12 +18,20 @@ SOURCES = ["status.cpp", "merge.hip", "ops.hip", "embed.hip", "gemm.hip", "atten
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-munsafe-fp-atomics",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]
+# Per-source code generation options.  The dK/dV attention kernel keeps the
+# key and value rows in the accumulation registers, which makes the compiler
+# give every matrix instruction of the file accumulation-register results;
+# its score accumulators then need a register move per element before the
+# softmax arithmetic.  The option keeps matrix results in vector registers
+# (the K and V operands stay where they are): the pass issues fewer
+# instructions and runs ~3.5 % faster on the 32B-class workload.
+FILE_FLAGS = {"attention_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src):
     out = os.path.join(OBJ, src + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", out]
+    cmd = [HIPCC, *FLAGS, *FILE_FLAGS.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
