@@ -522,7 +522,7 @@ int aj_transpose_bf16(const void *src, int32_t rows, int32_t cols, void *dst, vo
  * what the chip sustains as well as its published peaks (bench reporting;
  * nothing on the path calls them).  Both wait for their kernels.
  *   aj_ceiling_mfma_bf16: v_mfma_f32_32x32x16_bf16 from registers only, 8
- *     independent accumulators per wave, two waves per SIMD, with random
+ *     independent accumulators per wave, one wave per SIMD, with random
  *     bfloat16 operands (random_operands != 0: every product's inputs
  *     toggle, as with trained or random weights) or constant ones; *tflops
  *     is the best of 3 runs.  out: device scratch of at least

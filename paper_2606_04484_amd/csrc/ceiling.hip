@@ -1,9 +1,10 @@
 // Measured ceilings of the device, for reading the rooflines against what the
 // chip sustains rather than its published peaks alone:
 //   * the bf16 matrix-core rate with no memory traffic at all: every wave runs
-//     v_mfma_f32_32x32x16_bf16 on 8 independent accumulators from registers,
-//     two waves per SIMD, with random operands (every product's inputs
-//     toggle, as in a GEMM over trained or random weights) or constant ones;
+//     v_mfma_f32_32x32x16_bf16 on 8 independent accumulators from registers
+//     (one wave per SIMD: the kernel holds 260 registers per lane), with
+//     random operands (every product's inputs toggle, as in a GEMM over
+//     trained or random weights) or constant ones;
 //   * the HBM rates of a streaming copy and of a read-only stream (16-byte
 //     loads and stores, a grid over the whole buffer).
 #include "common.h"
@@ -90,6 +91,25 @@ __global__ __launch_bounds__(256) void read_ceiling_kernel(const u32x4_t *src, i
   if (x == 0x9e3779b9u) out[0] = x;
 }
 
+// Two timing events, destroyed on every return path.
+struct Events {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  Events() {
+    if (hipEventCreate(&e0) != hipSuccess) e0 = nullptr;
+    if (hipEventCreate(&e1) != hipSuccess) e1 = nullptr;
+  }
+  ~Events() {
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+  }
+  bool ok() const { return e0 && e1; }
+  // records e1 on s after the work since e0, waits for it, the time between
+  bool elapsed(hipStream_t s, float *ms) {
+    return hipEventRecord(e1, s) == hipSuccess && hipEventSynchronize(e1) == hipSuccess &&
+           hipEventElapsedTime(ms, e0, e1) == hipSuccess;
+  }
+};
+
 }  // namespace
 
 extern "C" int aj_ceiling_mfma_bf16(int random_operands, void *out, size_t out_bytes, void *stream,
@@ -100,31 +120,28 @@ extern "C" int aj_ceiling_mfma_bf16(int random_operands, void *out, size_t out_b
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus <= 0)
     return aj::fail(AJ_ERR_HIP, "aj_ceiling_mfma_bf16: no device");
-  const int wgs = 2 * cus;   // 2 workgroups of 4 waves per CU: 2 waves per SIMD
+  const int wgs = 2 * cus;   // two rounds of one 4-wave workgroup per CU
   AJ_REQUIRE(out_bytes >= (size_t)wgs * 256 * sizeof(float), AJ_ERR_WORKSPACE,
              "aj_ceiling_mfma_bf16: out holds %zu bytes, needs %zu", out_bytes,
              (size_t)wgs * 256 * sizeof(float));
   hipStream_t s = (hipStream_t)stream;
-  hipEvent_t e0, e1;
-  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
-    return aj::fail(AJ_ERR_HIP, "aj_ceiling_mfma_bf16: event");
+  Events ev;
+  if (!ev.ok()) return aj::fail(AJ_ERR_HIP, "aj_ceiling_mfma_bf16: event");
   double best = 0.0;
   for (int rep = 0; rep < 3; ++rep) {
-    hipEventRecord(e0, s);
+    if (hipEventRecord(ev.e0, s) != hipSuccess)
+      return aj::fail(AJ_ERR_HIP, "aj_ceiling_mfma_bf16: event record");
     if (random_operands)
       mfma_ceiling_kernel<true><<<wgs, 256, 0, s>>>((float *)out, kMfmaIters);
     else
       mfma_ceiling_kernel<false><<<wgs, 256, 0, s>>>((float *)out, kMfmaIters);
-    hipEventRecord(e1, s);
     float ms = 0.f;
-    if (hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+    if (!ev.elapsed(s, &ms))
       return aj::fail(AJ_ERR_HIP, "aj_ceiling_mfma_bf16: %s", hipGetErrorString(hipGetLastError()));
     const double flops = (double)wgs * 4 * kMfmaIters * 64 * (2.0 * 32 * 32 * 16);
     const double r = flops / (ms * 1e-3) / 1e12;
     if (r > best) best = r;
   }
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
   *tflops = best;
   return aj::check_launch("aj_ceiling_mfma_bf16");
 }
@@ -139,26 +156,23 @@ extern "C" int aj_ceiling_copy(void *buf, size_t bytes, void *stream, double *gb
   const u32x4_t *src = (const u32x4_t *)buf;
   u32x4_t *dst = (u32x4_t *)buf + n;
   hipStream_t s = (hipStream_t)stream;
-  hipEvent_t e0, e1;
-  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
-    return aj::fail(AJ_ERR_HIP, "aj_ceiling_copy: event");
+  Events ev;
+  if (!ev.ok()) return aj::fail(AJ_ERR_HIP, "aj_ceiling_copy: event");
   double best = 0.0, best_r = 0.0;
   for (int rep = 0; rep < 8; ++rep) {
     const bool rd = rep >= 4;   // the read-only stream writes its words over dst
-    hipEventRecord(e0, s);
+    if (hipEventRecord(ev.e0, s) != hipSuccess)
+      return aj::fail(AJ_ERR_HIP, "aj_ceiling_copy: event record");
     if (rd) read_ceiling_kernel<<<(int)((n + 1023) / 1024), 256, 0, s>>>(src, n, (uint32_t *)dst);
     else copy_ceiling_kernel<<<(int)((n + 255) / 256), 256, 0, s>>>(src, dst, n);
-    hipEventRecord(e1, s);
     float ms = 0.f;
-    if (hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+    if (!ev.elapsed(s, &ms))
       return aj::fail(AJ_ERR_HIP, "aj_ceiling_copy: %s", hipGetErrorString(hipGetLastError()));
     const double r = (rd ? 1.0 : 2.0) * 16 * n / (ms * 1e-3) / 1e9;
     if (rep == 0 || rep == 4) continue;   // the first run of each pages the buffer in
     if (rd) best_r = r > best_r ? r : best_r;
     else best = r > best ? r : best;
   }
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
   *gbps = best;
   *read_gbps = best_r;
   return aj::check_launch("aj_ceiling_copy");

@@ -96,6 +96,24 @@ def test_host_validation_needs_no_gpu():
     assert b"vocab" in L.aj_last_error()
 
 
+def test_ceiling_and_transpose_host_validation():
+    """The measurement and transpose entry points check their arguments before
+    any device call."""
+    capi = _lib()
+    L = capi.lib()
+    d, d2 = C.c_double(), C.c_double()
+    assert L.aj_ceiling_copy(None, 64, None, C.byref(d), C.byref(d2)) == 1
+    assert L.aj_ceiling_copy(C.c_void_p(4096), 64, None, None, C.byref(d2)) == 1
+    assert L.aj_ceiling_copy(C.c_void_p(4096), 16, None, C.byref(d), C.byref(d2)) == 2
+    assert L.aj_ceiling_copy(C.c_void_p(4104), 64, None, C.byref(d), C.byref(d2)) == 2
+    assert b"16-byte aligned" in L.aj_last_error()
+    assert L.aj_ceiling_mfma_bf16(1, None, 1 << 20, None, C.byref(d)) == 1
+    assert L.aj_ceiling_mfma_bf16(1, C.c_void_p(4096), 1 << 20, None, None) == 1
+    assert L.aj_transpose_bf16(None, 4, 4, C.c_void_p(16), None) == 1
+    assert L.aj_transpose_bf16(C.c_void_p(16), 0, 4, C.c_void_p(16), None) == 2
+    assert L.aj_transpose_bf16(C.c_void_p(16), 4, -1, C.c_void_p(16), None) == 2
+
+
 def test_loss_saved_bytes_with_kept_logits():
     """keep_logits adds the float32 logits of every scored row to the loss's
     saved buffer, in bfloat16 only (the float32 path ignores it)."""
