@@ -525,7 +525,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
     df[kk] = __builtin_bit_cast(bf16x8_t, y);
   }
   const float lse2 = qv ? a.lse[(int64_t)h * a.n_tok + q] : 0.f;       // log2 units
-  const float dlt = qv ? a.delta[(int64_t)h * a.n_tok + q] : 0.f;
+  const float ndlt = qv ? a.delta[(int64_t)h * a.n_tok + q] : 0.f;   // -delta
   f32x16_t acc[DT];
 #pragma unroll
   for (int i = 0; i < DT; ++i)
@@ -551,7 +551,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
     rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, qf, df);
     if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] - dlt);
+      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] + ndlt);
     } else {
       // key k0 + 4hl + off (off a constant per element) is visible iff
       // lo <= off <= hi
@@ -560,7 +560,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
       for (int r = 0; r < 16; ++r) {
         const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
         const float p = (off >= lo && off <= hi) ? fast_exp2(fmaf(s[r], c, -lse2)) : 0.f;
-        s[r] = p * (dp[r] - dlt);
+        s[r] = p * (dp[r] + ndlt);
       }
     }
     const bf16x8_t sj[2] = {pack8(s, 0), pack8(s, 8)};
@@ -666,8 +666,23 @@ struct DkvSched {
     return cnt - end;
   }
   // slot of the vector work of softmax score r (0..15): spread over the
-  // dV/dK group (the LSE and delta were read before fragment 0)
+  // dV/dK group (the LSE was read before fragment 0)
   static constexpr int score_slot(int r) { return r * NC / 16; }
+  // Order of the S/dP group's products (KS k-slices each): position u is S
+  // (Q fragment) or dP (dO fragment) of k-slice kk(u).  The first dP product
+  // comes at u = 4: its accumulator starts from the half's negated delta,
+  // read from LDS right after the group's first MFMA, so fragment 4's reads,
+  // issued after the delta's, have landed by then and the delta with them
+  // (LDS returns in order).  S and dP alternate after that, so that few
+  // products wait on the one before.
+  static constexpr int KS = NS / 4;
+  static_assert(KS >= 4, "the first dP product at position 4");
+  static constexpr bool is_s(int u) { return u < 4 || (u - 4 < 2 * (KS - 4) && ((u - 4) & 1)); }
+  static constexpr int kk(int u) {
+    return u < 4 ? u
+           : u - 4 < 2 * (KS - 4) ? (((u - 4) & 1) ? 4 + (u - 4) / 2 : (u - 4) / 2)
+                                  : u - 4 - (KS - 4);
+  }
 };
 
 template <int HD, int NW>
@@ -748,10 +763,11 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
   // the lane's LSE / delta reads: 4 floats at 16 hl bytes past the offset
   const uint32_t ld_lane = lds_addr(ld_sm) + 16 * hl;
 
-  // pipeline state: S, dP of the current half (s, dp: exponentiated in a
-  // step's first group, overwritten by the next half's products in its
-  // second); that half's LSE and delta (lv, dl); packed P, dS of the
-  // previous half (pp, sp) and of the current one (pc, spc)
+  // pipeline state: S, dP - delta of the current half (s, dp: exponentiated
+  // in a step's first group, overwritten by the next half's products in its
+  // second); that half's LSE (lv) and the next half's negated delta (dl, the
+  // initial value of its dP); packed P, dS of the previous half (pp, sp) and
+  // of the current one (pc, spc)
   f32x16_t s, dp;
   f32x4_t lv[4], dl[4];
   bf16x8_t pp[2], sp[2], pc[2], spc[2];
@@ -767,10 +783,17 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
       dl[r4] = lds_read_f4(ld_lane, (3 + st) * 256 + (32 * tt + 8 * r4) * 4);
     }
   };
+  // the negated delta of the lane's 16 query rows as an accumulator
+  auto delta_init = [&]() __attribute__((always_inline)) -> f32x16_t {
+    f32x16_t v;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) v[r] = dl[r >> 2][r & 3];
+    return v;
+  };
 
   // fragment j of a step: dV/dK group (j < NC): dv[i] (j < NC/2, dO tile) or
   // dk[i] (Q tile), feature block i = j % DT, token rows 32tt + 16((j/DT)%2);
-  // S/dP group: k-slice (j - NC)/2 of the Q (even) or dO (odd) tile rows 32tt
+  // S/dP group: k-slice Sched::kk(j - NC) of the Q or dO tile rows 32tt
   auto read_frag = [&](const int j, const int tt_c, const int st_c, const int tt_p,
                        const int st_p) __attribute__((always_inline)) -> bf16x8_t {
     if (j < NC) {
@@ -778,9 +801,9 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
       const int off = st_c * T + (32 * tt_c + 16 * hb) * RB;
       return j < NC / 2 ? LD.col_frag(off, i) : LQ.col_frag(off, i);
     }
-    const int kk = (j - NC) >> 1;
     const int off = st_p * T + 32 * tt_p * RB;
-    return ((j - NC) & 1) ? LD.row_frag(off, kk) : LQ.row_frag(off, kk);
+    return Sched::is_s(j - NC) ? LQ.row_frag(off, Sched::kk(j - NC))
+                               : LD.row_frag(off, Sched::kk(j - NC));
   };
 
   // The causal and segment mask enters S as its accumulator's initial value:
@@ -826,22 +849,25 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
       lds_wait_n(wn);
       asm volatile("" : "+v"(F[j]));
       if (j == 0) {
-        // the LSE and delta reads precede fragment 0
+        // the LSE reads precede fragment 0
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          asm volatile("" : "+v"(lv[r4]));
-          asm volatile("" : "+v"(dl[r4]));
-        }
+        for (int r4 = 0; r4 < 4; ++r4) asm volatile("" : "+v"(lv[r4]));
       }
       if (j < NC) {
         const int i = j % DT, hb = (j / DT) & 1;
         if (j < NC / 2) dv[i] = mfma(F[j], pp[hb], dv[i]);   // dV^T += dO^T P
         else dk[i] = mfma(F[j], sp[hb], dk[i]);              // dK^T += Q^T dS
       } else {
-        const int kk = (j - NC) >> 1;
-        if (((j - NC) & 1) == 0)   // S = Q K^T (+ mask)
+        constexpr int kk = Sched::kk(j - NC);
+        if constexpr (Sched::is_s(j - NC)) {   // S = Q K^T (+ mask)
           s = kk == 0 ? s_first(F[j], whole_p, lo_p, span_p) : mfma(F[j], kf[kk], s);
-        else dp = mfma(F[j], vf[kk], kk == 0 ? f32x16_t{} : dp);                     // dP = dO V^T
+        } else if constexpr (kk == 0) {    // dP - delta = dO V^T - delta
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) asm volatile("" : "+v"(dl[r4]));
+          dp = mfma(F[j], vf[0], delta_init());
+        } else {
+          dp = mfma(F[j], vf[kk], dp);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
       if (bar && j == NC - 1) {
@@ -865,7 +891,7 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
         asm volatile("" : "+v"(sr), "+v"(dr));
         const float pr = fast_exp2(fmaf(sr, c, -lv[r >> 2][r & 3]));
         pv[r] = pr;
-        dq[r] = pr * (dr - dl[r >> 2][r & 3]);
+        dq[r] = pr * dr;
         if (r & 1) {
           const int h8 = r >> 3, k = (r & 7) >> 1;
           // the pair (r - 1, r) is word k of the packed half h8
@@ -929,18 +955,22 @@ __global__ __launch_bounds__(64 * NW) void attn_dkv_mfma_kernel(AttnBwdArgs a, i
     load_item(min(1, n_it - 1), Ci<1>{});
     dma_wait();
     __syncthreads();
-    // S, dP, LSE and delta of half 0
+    // LSE and delta, then S and dP - delta of half 0
     const bool whole0 = seen_whole(kv - k0 - 4 * hl, span);
+    read_ld(0, 0);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       bf16x8_t fq = LQ.row_frag(0, kk), fd = LD.row_frag(0, kk);
       lds_wait();
       asm volatile("" : "+v"(fq));
       asm volatile("" : "+v"(fd));
+      if (kk == 0) {
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) asm volatile("" : "+v"(dl[r4]));
+      }
       s = kk == 0 ? s_first(fq, whole0, kv - k0 - 4 * hl, span) : mfma(fq, kf[kk], s);
-      dp = mfma(fd, vf[kk], kk == 0 ? f32x16_t{} : dp);
+      dp = mfma(fd, vf[kk], kk == 0 ? delta_init() : dp);
     }
-    read_ld(0, 0);
     // the first step's dV/dK group: half -1 (stage 2, cleared)
 #pragma unroll
     for (int f = 0; f < D; ++f) F[f] = read_frag(f, 1, 2, 0, 0);
@@ -977,7 +1007,9 @@ __global__ __launch_bounds__(256) void attn_delta_bf16_kernel(AttnBwdArgs a) {
   for (int c = lane; c < a.hd; c += 64) s += bf2f(o[c]) * bf2f(d[c]);
 #pragma unroll
   for (int w = 32; w > 0; w >>= 1) s += __shfl_xor(s, w, 64);
-  if (lane == 0) a.delta[(int64_t)h * a.n_tok + row] = s;
+  // stored negated: the dK/dV pass starts its dP accumulators from it, so
+  // that dP - delta costs no vector instruction
+  if (lane == 0) a.delta[(int64_t)h * a.n_tok + row] = -s;
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
