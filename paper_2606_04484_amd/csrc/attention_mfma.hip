@@ -299,12 +299,12 @@ AJ_DEV void bar_nofence() {
 
 // One 32-row block (token rows t0..t0+31) of two staged tiles, at byte
 // offsets offa and offb, against the lane's operands: sa = ta rows x ka,
-// sb = tb rows x kb (k = features; the incoming sa, sb are not read).
+// sb = sb0 + tb rows x kb (k = features; the incoming sa, sb are not read).
 // Fragments are read two k-steps ahead; each step waits only for its own.
 template <int HD>
 AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const TileLanes<HD> &L, const int offa,
                             const int offb, const int t0, const bf16x8_t (&ka)[HD / 16],
-                            const bf16x8_t (&kb)[HD / 16]) {
+                            const bf16x8_t (&kb)[HD / 16], const f32x16_t &sb0) {
   constexpr int KS = HD / 16, RB = HD * 2;
   bf16x8_t fa[KS], fb[KS];
 #pragma unroll
@@ -323,7 +323,7 @@ AJ_DEV void rows_times_pair(f32x16_t &sa, f32x16_t &sb, const TileLanes<HD> &L, 
     asm volatile("" : "+v"(fa[kk]));
     asm volatile("" : "+v"(fb[kk]));
     sa = mfma(fa[kk], ka[kk], kk == 0 ? f32x16_t{} : sa);
-    sb = mfma(fb[kk], kb[kk], kk == 0 ? f32x16_t{} : sb);
+    sb = mfma(fb[kk], kb[kk], kk == 0 ? sb0 : sb);
   }
 }
 
@@ -525,7 +525,11 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
     df[kk] = __builtin_bit_cast(bf16x8_t, y);
   }
   const float lse2 = qv ? a.lse[(int64_t)h * a.n_tok + q] : 0.f;       // log2 units
-  const float ndlt = qv ? a.delta[(int64_t)h * a.n_tok + q] : 0.f;   // -delta
+  // the lane's query keeps one negated delta: every dP^T element starts from it
+  const float ndlt = qv ? a.delta[(int64_t)h * a.n_tok + q] : 0.f;
+  f32x16_t dp0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dp0[r] = ndlt;
   f32x16_t acc[DT];
 #pragma unroll
   for (int i = 0; i < DT; ++i)
@@ -547,11 +551,11 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
   // V dO^T, the softmax terms, then dQ^T += K^T dS^T over those 32 keys
   auto half = [&](const int tt, const int st, const int k0,
                   const bool full) __attribute__((always_inline)) {
-    f32x16_t s, dp;   // set by rows_times_pair
-    rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, qf, df);
+    f32x16_t s, dp;   // S^T and dP^T - delta, set by rows_times_pair
+    rows_times_pair<HD>(s, dp, L, st * T, (2 + st) * T, 32 * tt, qf, df, dp0);
     if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * (dp[r] + ndlt);
+      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], c, -lse2)) * dp[r];
     } else {
       // key k0 + 4hl + off (off a constant per element) is visible iff
       // lo <= off <= hi
@@ -560,7 +564,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
       for (int r = 0; r < 16; ++r) {
         const int off = 32 * tt + 8 * (r >> 2) + (r & 3);
         const float p = (off >= lo && off <= hi) ? fast_exp2(fmaf(s[r], c, -lse2)) : 0.f;
-        s[r] = p * (dp[r] + ndlt);
+        s[r] = p * dp[r];
       }
     }
     const bf16x8_t sj[2] = {pack8(s, 0), pack8(s, 8)};
