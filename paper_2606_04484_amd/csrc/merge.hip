@@ -22,7 +22,7 @@
 // takes a survivor's transferred log-probs from its absorbed timelines' runs
 // (pulled, so nothing is cleared, voted into or read back per token).
 // Kernels (token-level Match):
-//   init_status     the call's status word
+//   init_status     the call's status word and the scans' per-workgroup tallies
 //   setup           offsets tile [0, n_tok) and [0, n_tl), every timeline starts
 //                   a block; episode bounds per timeline; compare items per
 //                   timeline
@@ -32,14 +32,20 @@
 //   compare         one workgroup per kCmpChunk tokens of T_j: full compare with
 //                   that candidate (a difference marks j), llm runs of the item
 //   finalize        absorber = the candidate, or for a marked j the candidates
-//                   below it compared in full (Algorithm 1's order)
-//   resolve         one workgroup: survivor scan -> cu_seqlens, counts
+//                   below it compared in full (Algorithm 1's order); adds each
+//                   wavefront's survivors and their tokens to the tally of the
+//                   survivor-scan workgroup that holds them
+//   resolve         one workgroup per kResSpan timelines, each starting from the
+//                   tallies before it: survivor scan -> cu_seqlens, counts
 //   emit            survivor tokens -> packed tok/pos/mask/old_logprob/adv (each
 //                   workgroup a range of output positions); a survivor's non-llm
 //                   token takes the log-prob of the largest absorbed timeline
 //                   whose run covers its position; counts each range's targets
-//                   and writes their bitmask
-//   tgt_scan        one workgroup: offsets of the per-range target counts
+//                   and writes their bitmask; adds them to the tally of the
+//                   offset-scan workgroup that holds the range
+//   tgt_offsets     one workgroup per kTgtScanSpan ranges, each starting from
+//                   the tallies before it: offsets of the per-range target
+//                   counts
 //   tgt_write       ascending masked targets from the bitmask, and each
 //                   segment's first target (cu_targets)
 #include <mutex>
@@ -62,6 +68,10 @@ constexpr int kRows = kCmpChunk / 64;                  // llm rows of 64 positio
 constexpr int kRowsPerLane = (kRows + 63) / 64;        // rows per lane of a wavefront
 constexpr int kCntBits = 14;          // item records hold positions (<= kCmpChunk) in 14 bits
 constexpr int kRuns = 4;              // llm runs kept per compare item (more: marked kRuns + 1)
+constexpr int kResPer = 8;            // timelines per thread of the survivor scan
+constexpr int kResSpan = kResPer * 256;   // timelines per survivor-scan workgroup
+constexpr int kTgtScanPer = 16;       // target chunks per thread of the target-offset scan
+constexpr int kTgtScanSpan = kTgtScanPer * 256;   // target chunks per scan workgroup
 static_assert(kCmpChunk % 1024 == 0 && kCmpChunk < (1 << kCntBits) &&
               (kRows <= 64 || kRows % 64 == 0), "item shape");
 // Offsets that do not tile the input stop the merge (every count 0); bad flag
@@ -91,6 +101,12 @@ struct MergeArgs {
   uint64_t *tbits;      // one bit per output position: a masked target
   int32_t *chunk_cnt;   // [n_chunks]
   int32_t *chunk_off;   // [n_chunks]
+  int32_t *rblk;        // [n_rblk][4] per kResSpan timelines: survivors, their tokens, the
+                        // longest (added up by the absorber pass), unused
+  int32_t n_rblk;
+  int32_t *tblk;        // [n_tblk] targets per kTgtScanSpan target chunks (added up by the
+                        // passes that count each chunk's targets)
+  int32_t n_tblk;
   int32_t *user_err;
   // token-level Match only.  Compare item (j, k) covers positions
   // [k * kCmpChunk, (k + 1) * kCmpChunk) of T_j and is slot
@@ -223,6 +239,28 @@ AJ_DEV int validate_item(const MergeArgs &a, int t) {
 __global__ void init_status_kernel(MergeArgs a) {
   if (threadIdx.x < 4) a.status[threadIdx.x] = 0;
   if (a.ti && threadIdx.x < 2) a.ti[threadIdx.x] = 0;
+  for (int i = threadIdx.x; i < 4 * a.n_rblk; i += blockDim.x) a.rblk[i] = 0;
+  for (int i = threadIdx.x; i < a.n_tblk; i += blockDim.x) a.tblk[i] = 0;
+}
+
+// Adds one wavefront's survivors (surv: 0/1, len: the survivor's length) to
+// the tally of the survivor-scan workgroup that holds timeline j (every lane's
+// timeline lies in the same kResSpan-aligned range).  Integer sums and a
+// maximum: the result does not depend on the order of the atomics.
+AJ_DEV void tally_survivors(const MergeArgs &a, int j, int surv, int len) {
+  int mx = len;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    surv += __shfl_xor(surv, o, 64);
+    len += __shfl_xor(len, o, 64);
+    mx = max(mx, __shfl_xor(mx, o, 64));
+  }
+  if ((threadIdx.x & 63) == 0 && surv > 0) {
+    int32_t *t = a.rblk + 4 * (j / kResSpan);
+    atomicAdd(t, surv);
+    atomicAdd(t + 1, len);
+    atomicMax(t + 2, mx);
+  }
 }
 
 __global__ void validate_kernel(MergeArgs a) {
@@ -486,84 +524,126 @@ constexpr int kFinPer = 64;
 // for a marked j the workgroup searches the candidates below it (the rare
 // case: a prefix that agrees at both ends and differs inside).
 __global__ __launch_bounds__(kBlock) void finalize_kernel(MergeArgs a) {
-  __shared__ int todo[kFinPer];
+  static_assert(kFinPer == 64 && kResSpan % kFinPer == 0, "one wavefront of timelines");
+  __shared__ int todo[kFinPer], found[kFinPer];
   __shared__ int n_todo;
   if (threadIdx.x == 0) n_todo = 0;
   __syncthreads();
   const bool bad = fatal(a);
   const int j = blockIdx.x * kFinPer + (int)threadIdx.x;
+  int ab = -1, slot = -1;
   if (threadIdx.x < kFinPer && j < a.n_tl) {
-    const int c = bad ? -1 : a.cand[j];
-    if (c >= 0 && a.miss[j] != 0) todo[atomicAdd(&n_todo, 1)] = j;
-    else a.absorber[j] = c;
+    ab = bad ? -1 : a.cand[j];
+    if (ab >= 0 && a.miss[j] != 0) todo[slot = atomicAdd(&n_todo, 1)] = j;
+    else a.absorber[j] = ab;
   }
   __syncthreads();
   const int n = n_todo;
   for (int f = 0; f < n; ++f) {
     const int jj = todo[f];
     const int r = search_absorber(a, jj, a.cand[jj] - 1);
-    if (threadIdx.x == 0) a.absorber[jj] = r;
+    if (threadIdx.x == 0) {
+      a.absorber[jj] = r;
+      found[f] = r;
+    }
+  }
+  __syncthreads();
+  // the survivors among the workgroup's timelines, for the survivor scan
+  if (threadIdx.x < kFinPer && !bad) {
+    if (slot >= 0) ab = found[slot];
+    const bool surv = j < a.n_tl && ab < 0;
+    tally_survivors(a, j, surv ? 1 : 0, surv ? (int)(a.tl_tok_off[j + 1] - a.tl_tok_off[j]) : 0);
   }
 }
 
-__global__ void fill_absorber_kernel(MergeArgs a) {
-  int t = blockIdx.x * blockDim.x + threadIdx.x;
+// No merge: every timeline survives.
+__global__ __launch_bounds__(kBlock) void fill_absorber_kernel(MergeArgs a) {
+  const int t = blockIdx.x * kBlock + threadIdx.x;
+  const bool surv = t < a.n_tl && !fatal(a);
   if (t < a.n_tl) a.absorber[t] = -1;
+  tally_survivors(a, t, surv ? 1 : 0, surv ? (int)(a.tl_tok_off[t + 1] - a.tl_tok_off[t]) : 0);
 }
 
-// One workgroup of 1024 threads; a round covers 1024 * kResPer timelines,
-// wave w the kResPer * 64 consecutive ones from w * 64 * kResPer (lane l
-// holding every 64th), so the loads stay coalesced.
-constexpr int kResPer = 8;
-
-__global__ __launch_bounds__(1024) void resolve_kernel(MergeArgs a) {
-  __shared__ int mx_all;
-  if (threadIdx.x == 0) mx_all = 0;
+// The survivors' scan, one workgroup per kResSpan timelines: wave w of
+// workgroup b holds the kResPer * 64 consecutive timelines from
+// b * kResSpan + w * 64 * kResPer (lane l every 64th), so the loads stay
+// coalesced.  A workgroup's offsets start from the tallies of the workgroups
+// before it (written by the absorber pass); the last one writes the totals.
+__global__ __launch_bounds__(kBlock) void resolve_kernel(MergeArgs a) {
+  static_assert(kResSpan == kResPer * kBlock, "timelines per workgroup");
+  __shared__ int red[3][kBlock / 64];
   const bool bad = fatal(a);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  int carry_seg = 0, carry_tok = 0, mx = 0;
-  for (int base = 0; base < a.n_tl; base += 1024 * kResPer) {
-    const int i0 = base + wid * 64 * kResPer + lane;
-    int seg[kResPer], tok[kResPer];
+  const int b = blockIdx.x;
+  const bool last = b == (int)gridDim.x - 1;
+  // survivors and tokens before this workgroup's timelines; the longest
+  // survivor of all (the last workgroup only)
+  int ps = 0, pt = 0, pm = 0;
+  for (int i = threadIdx.x; i < (last ? a.n_rblk : b); i += kBlock) {
+    if (i < b) {
+      ps += a.rblk[4 * i];
+      pt += a.rblk[4 * i + 1];
+    }
+    pm = max(pm, a.rblk[4 * i + 2]);
+  }
 #pragma unroll
-    for (int r = 0; r < kResPer; ++r) {   // clamped, not guarded: the loads issue together
+  for (int o = 1; o < 64; o <<= 1) {
+    ps += __shfl_xor(ps, o, 64);
+    pt += __shfl_xor(pt, o, 64);
+    pm = max(pm, __shfl_xor(pm, o, 64));
+  }
+  if (lane == 0) {
+    red[0][wid] = ps;
+    red[1][wid] = pt;
+    red[2][wid] = pm;
+  }
+  __syncthreads();
+  ps = pt = pm = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) {
+    ps += red[0][w];
+    pt += red[1][w];
+    pm = max(pm, red[2][w]);
+  }
+  if (bad) ps = pt = pm = 0;
+  const int i0 = b * kResSpan + wid * 64 * kResPer + lane;
+  int seg[kResPer], tok[kResPer];
+#pragma unroll
+  for (int r = 0; r < kResPer; ++r) {
+    seg[r] = tok[r] = 0;
+    if (a.n_tl > 0) {   // clamped, not guarded: the loads issue together
       const int i = min(i0 + 64 * r, a.n_tl - 1);
       const bool ok = !bad && i0 + 64 * r < a.n_tl;
       const int ab = a.absorber[i];
       const int l = (int)(a.tl_tok_off[i + 1] - a.tl_tok_off[i]);
       seg[r] = ok && ab < 0;
       tok[r] = seg[r] ? l : 0;
-      mx = max(mx, tok[r]);
     }
-    uint32_t surv = 0;
-#pragma unroll
-    for (int r = 0; r < kResPer; ++r) surv |= (uint32_t)seg[r] << r;
-    const int tot_s = wave_items_scan<1024, kResPer>(seg, carry_seg);
-    const int tot_l = wave_items_scan<1024, kResPer>(tok, carry_tok);
-#pragma unroll
-    for (int r = 0; r < kResPer; ++r) {
-      const int i = i0 + 64 * r;
-      if (i >= a.n_tl) continue;
-      if ((surv >> r) & 1) {
-        a.tl_seg[i] = seg[r];
-        a.seg_src[seg[r]] = i;
-        a.seg_base[seg[r]] = (int32_t)a.tl_tok_off[i];
-        a.cu_seqlens[seg[r]] = tok[r];
-      } else {
-        a.tl_seg[i] = -1;
-      }
-    }
-    carry_seg += tot_s;
-    carry_tok += tot_l;
   }
-  if (mx) atomicMax(&mx_all, mx);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    a.cu_seqlens[carry_seg] = carry_tok;
-    a.counts[0] = carry_seg;
-    a.counts[1] = carry_tok;
+  uint32_t surv = 0;
+#pragma unroll
+  for (int r = 0; r < kResPer; ++r) surv |= (uint32_t)seg[r] << r;
+  const int tot_s = wave_items_scan<kBlock, kResPer>(seg, ps);
+  const int tot_l = wave_items_scan<kBlock, kResPer>(tok, pt);
+#pragma unroll
+  for (int r = 0; r < kResPer; ++r) {
+    const int i = i0 + 64 * r;
+    if (i >= a.n_tl) continue;
+    if ((surv >> r) & 1) {
+      a.tl_seg[i] = seg[r];
+      a.seg_src[seg[r]] = i;
+      a.seg_base[seg[r]] = (int32_t)a.tl_tok_off[i];
+      a.cu_seqlens[seg[r]] = tok[r];
+    } else {
+      a.tl_seg[i] = -1;
+    }
+  }
+  if (last && threadIdx.x == 0) {
+    a.cu_seqlens[ps + tot_s] = pt + tot_l;
+    a.counts[0] = ps + tot_s;
+    a.counts[1] = pt + tot_l;
     a.counts[2] = 0;
-    a.counts[3] = mx_all;
+    a.counts[3] = pm;
   }
 }
 
@@ -850,7 +930,10 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(MergeArgs a, int use_claim
     // the span's target count for the compaction (chunk = span)
     int tot;
     block_scan_incl<kBlock>(n_tgt, &tot);
-    if (threadIdx.x == 0) a.chunk_cnt[ob / kEmitSpan] = tot;
+    if (threadIdx.x == 0) {
+      a.chunk_cnt[ob / kEmitSpan] = tot;
+      if (tot) atomicAdd(&a.tblk[ob / kEmitSpan / kTgtScanSpan], tot);
+    }
   }
   if (bad) raise(a, AJ_DEVERR_BAD_FLAGS);
 }
@@ -900,17 +983,49 @@ __global__ __launch_bounds__(kBlock) void tgt_count_kernel(MergeArgs a) {
   const int c = __popc(bits);
   int tot;
   block_scan_incl<kBlock>(c, &tot);
-  if (threadIdx.x == 0) a.chunk_cnt[blockIdx.x] = tot;
+  if (threadIdx.x == 0) {
+    a.chunk_cnt[blockIdx.x] = tot;
+    if (tot) atomicAdd(&a.tblk[blockIdx.x / kTgtScanSpan], tot);
+  }
+}
+
+// Exclusive offsets of the per-chunk target counts, one workgroup per
+// kTgtScanSpan chunks, starting from the tallies of the chunks before it; the
+// workgroup holding the last chunk with outputs (or workgroup 0, when there
+// are none) writes the total to counts[2].
+__global__ __launch_bounds__(kBlock) void tgt_offsets_kernel(MergeArgs a) {
+  static_assert(kTgtScanSpan == kTgtScanPer * kBlock, "chunks per workgroup");
+  __shared__ int red[kBlock / 64];
+  const int n_used = (int)((a.counts[1] + kTgtChunk - 1) / kTgtChunk);
+  const int b = blockIdx.x;
+  if (b > 0 && b * kTgtScanSpan >= n_used) return;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int p = 0;
+  for (int i = threadIdx.x; i < b; i += kBlock) p += a.tblk[i];
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) p += __shfl_xor(p, o, 64);
+  if (lane == 0) red[wid] = p;
+  __syncthreads();
+  p = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) p += red[w];
+  const int c0 = b * kTgtScanSpan + wid * 64 * kTgtScanPer + lane;
+  int v[kTgtScanPer];
+#pragma unroll
+  for (int r = 0; r < kTgtScanPer; ++r) v[r] = c0 + 64 * r < n_used ? a.chunk_cnt[c0 + 64 * r] : 0;
+  const int tot = wave_items_scan<kBlock, kTgtScanPer>(v, p);
+#pragma unroll
+  for (int r = 0; r < kTgtScanPer; ++r)
+    if (c0 + 64 * r < n_used) a.chunk_off[c0 + 64 * r] = v[r];
+  if (threadIdx.x == 0 && b == (n_used > 0 ? (n_used - 1) / kTgtScanSpan : 0)) a.counts[2] = p + tot;
 }
 
 // Exclusive offsets of the per-chunk counts by one workgroup, 1024 * kScanPer
-// chunks a round; the total goes to counts[2] (the
-// target compaction) or, for the block-start compaction, must equal n_blk.
+// chunks a round: the block-start compaction, whose total must equal n_blk.
 constexpr int kScanPer = 16;
 
-__global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunks, int blocks) {
-  // the target compaction counts only chunks that hold outputs
-  const int n_used = blocks ? n_chunks : (int)((a.counts[1] + kTgtChunk - 1) / kTgtChunk);
+__global__ __launch_bounds__(1024) void blk_scan_kernel(MergeArgs a, int n_chunks) {
+  const int n_used = n_chunks;
   int carry = 0;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   for (int base = 0; base < n_used; base += 1024 * kScanPer) {
@@ -923,10 +1038,7 @@ __global__ __launch_bounds__(1024) void tgt_scan_kernel(MergeArgs a, int n_chunk
     for (int r = 0; r < kScanPer; ++r)
       if (c0 + 64 * r < n_used) a.chunk_off[c0 + 64 * r] = v[r];
   }
-  if (threadIdx.x == 0) {
-    if (!blocks) a.counts[2] = carry;
-    else if (!fatal(a) && carry != a.n_blk) raise(a, AJ_DEVERR_BLOCKS);
-  }
+  if (threadIdx.x == 0 && !fatal(a) && carry != a.n_blk) raise(a, AJ_DEVERR_BLOCKS);
 }
 
 // Targets of chunk ch (kTgtChunk outputs = kTgtChunk / 64 bitmask words), 8
@@ -1223,7 +1335,8 @@ __global__ __launch_bounds__(64) void ti_kernel(MergeArgs a) {
 }
 
 struct MergeWs {
-  int32_t *status, *tl_seg, *chunk_cnt, *chunk_off;
+  int32_t *status, *tl_seg, *chunk_cnt, *chunk_off, *rblk, *tblk;
+  int32_t n_rblk, n_tblk;
   uint64_t *tbits;
   int32_t n_slots;
   int32_t *ep_first, *ep_last, *cand, *miss, *rcnt, *runs;
@@ -1240,6 +1353,10 @@ MergeWs carve(void *ws, int32_t n_tl, int64_t n_tok, int32_t n_blk = -1) {
   int64_t n_chunks = (n_tok + kChunk - 1) / kChunk;
   auto at_least1 = [](int64_t n) { return n > 0 ? n : 1; };
   w.status = c.take<int32_t>(4);
+  w.n_rblk = (int32_t)((n_tl + kResSpan - 1) / kResSpan);
+  w.rblk = c.take<int32_t>(4 * at_least1(w.n_rblk));
+  w.n_tblk = (int32_t)(((n_tok + kTgtChunk - 1) / kTgtChunk + kTgtScanSpan - 1) / kTgtScanSpan);
+  w.tblk = c.take<int32_t>(at_least1(w.n_tblk));
   w.tl_seg = c.take<int32_t>(at_least1(n_tl));
   w.chunk_cnt = c.take<int32_t>(at_least1(n_chunks));
   w.chunk_off = c.take<int32_t>(at_least1(n_chunks));
@@ -1303,6 +1420,7 @@ MergeArgs make_args(const aj_timelines *in, aj_packed *out, int32_t *err, const 
   a.miss = w.miss; a.slot_rec = w.slot_rec; a.rcnt = w.rcnt; a.runs = w.runs;
   a.seg_base = w.seg_base; a.range_rec = w.range_rec;
   a.chunk_cnt = w.chunk_cnt; a.chunk_off = w.chunk_off; a.user_err = err;
+  a.rblk = w.rblk; a.n_rblk = w.n_rblk; a.tblk = w.tblk; a.n_tblk = w.n_tblk;
   a.blk_start = w.blk_start; a.tl_blk = w.tl_blk; a.blk_tl = w.blk_tl; a.blk_claim = w.blk_claim;
   a.src_blk = w.src_blk; a.blk_off = w.blk_off; a.dst_off = w.dst_off; a.dst_pos = w.dst_pos;
   return a;
@@ -1341,7 +1459,7 @@ int resident_wgs(const void *kernel, int slot) {
 void launch_targets(const MergeArgs &a, hipStream_t s, bool counted) {
   const int64_t n_chunks = (a.n_tok + kTgtChunk - 1) / kTgtChunk;
   if (a.n_tok > 0 && !counted) tgt_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
-  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 0);
+  tgt_offsets_kernel<<<a.n_tblk > 0 ? a.n_tblk : 1, kBlock, 0, s>>>(a);
   const int64_t segs = ((int64_t)a.n_tl + 1 + kBlock - 1) / kBlock;
   const int64_t g = n_chunks > segs ? n_chunks : segs;
   const int64_t gw = resident_wgs(reinterpret_cast<const void *>(tgt_write_kernel), 1);
@@ -1374,7 +1492,7 @@ int run(const aj_timelines *in, aj_packed *out, int32_t *err, void *ws, size_t w
     launch_validate(a, s);
     if (in->n_tl > 0) fill_absorber_kernel<<<(in->n_tl + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
   }
-  resolve_kernel<<<1, 1024, 0, s>>>(a);
+  resolve_kernel<<<a.n_rblk > 0 ? a.n_rblk : 1, kBlock, 0, s>>>(a);
   if (in->n_tok > 0) {
     const int64_t spans = (in->n_tok + kEmitSpan - 1) / kEmitSpan;
     range_kernel<<<(int)((spans + kBlock / 64 - 1) / (kBlock / 64)), kBlock, 0, s>>>(a, merge ? 1 : 0);
@@ -1412,7 +1530,7 @@ int run_text(const aj_timelines *in, const aj_block_texts *text, aj_packed *out,
   launch_validate(a, s);
   // blocks: first tokens, first block per timeline, timeline per block
   if (in->n_tok > 0) blk_count_kernel<<<n_chunks, kBlock, 0, s>>>(a);
-  tgt_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks, 1);
+  blk_scan_kernel<<<1, 1024, 0, s>>>(a, (int)n_chunks);
   if (in->n_tok > 0) blk_write_kernel<<<n_chunks, kBlock, 0, s>>>(a);
   tl_blk_kernel<<<(in->n_tl + 1 + kBlock - 1) / kBlock, kBlock, 0, s>>>(a);
   if (n_blk > 0) blk_tl_kernel<<<gblk, kBlock, 0, s>>>(a);
