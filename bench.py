@@ -505,7 +505,8 @@ def roofline(rec, flops, peak, workload):
         classes[k] = dict(ms=ms, launches=n, tflops=(fl / (ms * 1e-3) / 1e12) if ms > 0 else 0.0)
     # the roofline names one kernel with algorithmic flops: not the multi-kernel
     # attention backward, not the logits recompute of the LM-head backward
-    dom = max((k for k in classes if k not in ("merge", "attn_bwd", "lm_dz")),
+    dom = max((k for k in classes
+               if k not in ("merge", "attn_bwd", "lm_dz") and not k.startswith("stage_")),
               key=lambda k: classes[k]["ms"])
     d = classes[dom]
     fl_dom = {"attn_fwd": att_fwd}.get(dom, rec[dom][2])
@@ -541,6 +542,33 @@ def ceilings(torch, capi):
     torch.cuda.empty_cache()
     return {"mfma_bf16_random_tflops": round(rnd, 1), "mfma_bf16_constant_tflops": round(const, 1),
             "hbm_copy_gbps": round(copy, 1), "hbm_read_gbps": round(read, 1), "cus": cus}
+
+
+def stage_records(rec, flops, peak, n_tok, n_mask, n_packs, m):
+    """The decoder-block and LM-head/loss stages of one step (whole library
+    calls, HIP events on the launch stream) against the MFMA roofline, and
+    the loss stage's algorithmic HBM traffic for completeness: the hidden
+    states of the scored rows read by the forward and the backward, d hidden
+    written in float32 for every token, the vocab matrix read by both, and
+    its float32 gradient read and written once per pack."""
+    blk, lm, att, _ = flops
+    out = {}
+    ms, n, _ = rec.get("stage_block", (0.0, 0, 0.0))
+    if n:
+        tf = (blk + att) / (ms * 1e-3) / 1e12
+        out["block"] = {"ms": round(ms, 3), "calls": n, "tflops": round(tf, 1),
+                        "mfma_frac": round(tf / peak, 4)}
+    ms, n, _ = rec.get("stage_loss", (0.0, 0, 0.0))
+    if n:
+        es = 2 if m.dtype == "bf16" else 4
+        d, V = m.d_model, m.vocab
+        nb = 2 * n_mask * d * es + n_tok * d * 4 + n_packs * (2 * V * d * es + 8 * V * d)
+        tf = lm / (ms * 1e-3) / 1e12
+        out["loss"] = {"ms": round(ms, 3), "calls": n, "tflops": round(tf, 1),
+                       "mfma_frac": round(tf / peak, 4), "algorithmic_GB": round(nb / 1e9, 2),
+                       "GB/s": round(nb / (ms * 1e-3) / 1e9, 1),
+                       "hbm_frac": round(nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    return out
 
 
 def merge_record(rec, tl, Lm):
@@ -618,6 +646,10 @@ def main():
         "loss": head["loss"],
     }
     mr = merge_record(live["rec"], live["tl"], live["Lm"])
+    out["stages"] = stage_records(live["rec"], live["flops"], live["peak"], head["merged_tokens"],
+                                  head["loss_tokens"], head["packs"], m)
+    if mr:
+        out["stages"]["merge"] = mr
     if not args.no_extras:
         # The LM-head backward reading the forward's kept float32 logits instead
         # of recomputing the vocab projection (bitwise the same step): an
@@ -657,6 +689,8 @@ def main():
                         0 if args.no_unmerged else (2 if is_b15 else 1), 0, torch, capi, actor,
                         record=True, keep=want_extras)
         r["roofline"], r["kernel_classes"] = roofline(lv["rec"], lv["flops"], lv["peak"], c.name)
+        r["stages"] = stage_records(lv["rec"], lv["flops"], lv["peak"], r["merged_tokens"],
+                                    r["loss_tokens"], r["packs"], c.model)
         if not args.no_extras and is_b15:
             log("extras on " + c.name)
             r["extras"] = extras(lv["A"], lv["merger"], c, lv["tl"], lv["dev"], torch, capi,

@@ -501,13 +501,18 @@ int aj_adamw_step(int64_t n, float *param, const float *grad, float *m, float *v
  *   AJ_KC_LM_DZ      the fused logits-recompute + d logits kernel (one per chunk)
  *   AJ_KC_ADAMW      one aj_adamw_step call
  *   AJ_KC_SELECT     one aj_grpo_advantages or aj_select_episodes call
- * `flops` accumulates algorithmic flops where the library knows them
- * (2*M*N*K per GEMM and LM_FWD launch; 0 for LM_DZ, which recomputes a
- * forward product, and for the other classes). */
+ *   AJ_KC_STAGE_BLOCK  one whole aj_varlen_block_* / aj_stack_* call (the
+ *                    decoder-block stage, forward or backward)
+ *   AJ_KC_STAGE_LOSS one whole aj_logprob_pg_loss_fwd / _bwd call (the LM
+ *                    head and loss stage)
+ * The two stage classes span every launch of their call, so they overlap
+ * the kernel classes above.  `flops` accumulates algorithmic flops where the
+ * library knows them (2*M*N*K per GEMM and LM_FWD launch; 0 for LM_DZ, which
+ * recomputes a forward product, and for the other classes). */
 enum { AJ_KC_MERGE = 0, AJ_KC_GEMM_NT = 1, AJ_KC_GEMM_NN = 2, AJ_KC_GEMM_TN = 3,
        AJ_KC_ATTN_FWD = 4, AJ_KC_ATTN_BWD = 5, AJ_KC_LM_FWD = 6, AJ_KC_LM_DZ = 7,
        AJ_KC_GEMM4_NT = 8, AJ_KC_GEMM4_NN = 9, AJ_KC_GEMM4_TN = 10, AJ_KC_ADAMW = 11,
-       AJ_KC_SELECT = 12, AJ_KC_COUNT = 13 };
+       AJ_KC_SELECT = 12, AJ_KC_STAGE_BLOCK = 13, AJ_KC_STAGE_LOSS = 14, AJ_KC_COUNT = 15 };
 /* on != 0 starts recording (clearing any earlier record); 0 stops. */
 int aj_timing_enable(int on);
 /* Waits for every recorded event; fills ms, launches and flops, each [AJ_KC_COUNT]. */

@@ -162,7 +162,7 @@ EXPORTS = {
 }
 
 KCLASSES = ("merge", "gemm_nt", "gemm_nn", "gemm_tn", "attn_fwd", "attn_bwd", "lm_fwd", "lm_dz",
-            "gemm4_nt", "gemm4_nn", "gemm4_tn", "adamw", "select")
+            "gemm4_nt", "gemm4_nn", "gemm4_tn", "adamw", "select", "stage_block", "stage_loss")
 
 
 def _declare(L):

@@ -513,6 +513,7 @@ extern "C" int aj_varlen_block_fwd(const aj_block_cfg *cfg, const aj_block_weigh
   AJ_REQUIRE(x && y && saved, AJ_ERR_NULL, "%s: null x/y/saved", name);
   Saved sv = carve_saved(*cfg, vl->n_tok, saved);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return block_fwd<bf16_t>(*cfg, *w, *vl, (const bf16_t *)x, (bf16_t *)y, sv, st);
   return block_fwd<float>(*cfg, *w, *vl, (const float *)x, (float *)y, sv, st);
@@ -534,6 +535,7 @@ extern "C" int aj_varlen_block_bwd(const aj_block_cfg *cfg, const aj_block_weigh
              bw.bytes);
   Saved sv = carve_saved(*cfg, vl->n_tok, const_cast<void *>(saved));
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return block_bwd<bf16_t>(*cfg, *w, *vl, (const bf16_t *)x, sv, dy, dx, *g, bw, st);
   return block_bwd<float>(*cfg, *w, *vl, (const float *)x, sv, dy, dx, *g, bw, st);
@@ -560,6 +562,7 @@ extern "C" int aj_stack_fwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_
              "%s: null x/y/ckpt/saved", name);
   Saved sv = carve_saved(*cfg, vl->n_tok, saved);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return stack_fwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)y,
                              (bf16_t *)ckpt, sv, st);
@@ -586,6 +589,7 @@ extern "C" int aj_stack_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_
              bw.bytes);
   Saved sv = carve_saved(*cfg, vl->n_tok, saved);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return stack_bwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)ckpt, sv, dy, dx,
                              g, bw, st);
@@ -624,6 +628,7 @@ extern "C" int aj_stack_lora_fwd(const aj_block_cfg *cfg, int32_t n_layers,
   LoraFwd la{};
   carve_lora_saved(*cfg, lora[0].rank, vl->n_tok, (char *)saved + sv.bytes, &la);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return stack_fwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)y,
                              (bf16_t *)ckpt, sv, st, lora, &la);
@@ -657,6 +662,7 @@ extern "C" int aj_stack_lora_bwd(const aj_block_cfg *cfg, int32_t n_layers,
   LoraFwd la{};
   carve_lora_saved(*cfg, rank, vl->n_tok, (char *)saved + sv.bytes, &la);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_BLOCK);
   if (cfg->dtype == AJ_BF16)
     return stack_bwd<bf16_t>(*cfg, n_layers, w, *vl, (const bf16_t *)x, (bf16_t *)ckpt, sv, dy, dx,
                              nullptr, bw, st, lora, g, &la, &lw);

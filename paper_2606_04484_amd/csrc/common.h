@@ -40,6 +40,17 @@ int check_launch(const char *what);
 // Benchmark timing (aj_timing_enable): returns a record index or -1 when off.
 int timing_begin(hipStream_t s, int kclass, double flops);
 void timing_end(hipStream_t s, int idx);
+// Brackets every launch of one library call (a stage of the path) for the
+// benchmark timing: the end event is recorded when the span leaves scope,
+// after the call's last launch.
+struct StageSpan {
+  hipStream_t s;
+  int idx;
+  StageSpan(hipStream_t s_, int kc) : s(s_), idx(timing_begin(s_, kc, 0.0)) {}
+  ~StageSpan() { timing_end(s, idx); }
+  StageSpan(const StageSpan &) = delete;
+  StageSpan &operator=(const StageSpan &) = delete;
+};
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

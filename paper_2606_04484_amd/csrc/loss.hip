@@ -729,6 +729,7 @@ extern "C" int aj_logprob_pg_loss_fwd(const aj_loss_cfg *cfg, const aj_loss_in *
              w.bytes);
   LossSaved sv = carve_saved(*cfg, in->n_tgt, saved);
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_LOSS);
   if (cfg->dtype == AJ_BF16)
     return loss_fwd<bf16_t>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, stats, err, w, st);
   return loss_fwd<float>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, stats, err, w, st);
@@ -751,6 +752,7 @@ extern "C" int aj_logprob_pg_loss_bwd(const aj_loss_cfg *cfg, const aj_loss_in *
              name, ws_bytes, w.bytes);
   LossSaved sv = carve_saved(*cfg, in->n_tgt, const_cast<void *>(saved));
   hipStream_t st = (hipStream_t)stream;
+  const aj::StageSpan span(st, AJ_KC_STAGE_LOSS);
   if (cfg->dtype == AJ_BF16)
     return loss_bwd<bf16_t>(*cfg, *in, h, final_norm, w_vocab, sv, logprob, lse, dh, d_final_norm,
                             d_w_vocab, w, st);
