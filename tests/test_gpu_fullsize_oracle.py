@@ -106,6 +106,13 @@ def test_long_reduction_layouts_ran(gpu_run):
     for k in ("gemm4_nn", "gemm4_tn", "lm_fwd", "lm_dz", "attn_fwd", "attn_bwd"):
         assert rec[k][1] > 0, k
     assert rec["gemm4_nt"][1] == 0 and rec["gemm_nt"][1] == 0
+    # one block forward and backward and one loss forward and backward per pack,
+    # each bracketing the kernels it launched
+    n = gpu_run["packs"]
+    assert rec["stage_block"][1] == 2 * n and rec["stage_loss"][1] == 2 * n
+    inner = sum(rec[k][0] for k in ("attn_fwd", "attn_bwd"))
+    assert rec["stage_block"][0] > inner > 0
+    assert rec["stage_loss"][0] > rec["lm_fwd"][0] + rec["lm_dz"][0] > 0
 
 
 def test_targets_and_logprobs(case, gpu_run):
