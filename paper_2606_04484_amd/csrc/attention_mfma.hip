@@ -615,9 +615,10 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_dq_mfma_kernel(AttnBwdArgs a,
 // 32-query halves u.  Step u first issues, one MFMA at a time, the products
 // dV^T += dO^T P and dK^T += Q^T dS of half u - 1 and, between them, the
 // vector work of half u's softmax terms (exponentials, masks, bf16 packing of
-// P and dS); then the products S = Q K^T and dP = dO V^T of half u + 1 into
+// P and dS); then the products S = Q K^T and dP - delta = dO V^T - delta of
+// half u + 1 (its dP accumulators start from the half's negated delta) into
 // the same registers.  The LDS reads of the fragments run a few MFMAs ahead,
-// and those of half u + 1's LSE and delta one step ahead.
+// and those of half u + 1's LSE one step ahead of its softmax.
 
 template <int V> struct Ci { static constexpr int value = V; };
 
@@ -1011,8 +1012,8 @@ __global__ __launch_bounds__(256) void attn_delta_bf16_kernel(AttnBwdArgs a) {
   for (int c = lane; c < a.hd; c += 64) s += bf2f(o[c]) * bf2f(d[c]);
 #pragma unroll
   for (int w = 32; w > 0; w >>= 1) s += __shfl_xor(s, w, 64);
-  // stored negated: the dK/dV pass starts its dP accumulators from it, so
-  // that dP - delta costs no vector instruction
+  // stored negated: the dK/dV and dQ passes start their dP accumulators from
+  // it, so that dP - delta costs no vector instruction
   if (lane == 0) a.delta[(int64_t)h * a.n_tok + row] = -s;
 }
 
