@@ -1041,31 +1041,63 @@ __global__ __launch_bounds__(1024) void blk_scan_kernel(MergeArgs a, int n_chunk
   if (threadIdx.x == 0 && !fatal(a) && carry != a.n_blk) raise(a, AJ_DEVERR_BLOCKS);
 }
 
-// Targets of chunk ch (kTgtChunk outputs = kTgtChunk / 64 bitmask words), 8
-// outputs (one bitmask byte) per thread.
-AJ_DEV uint32_t chunk_byte(const MergeArgs &a, int64_t ch) {
-  const uint64_t w = a.tbits[ch * (kTgtChunk / 64) + threadIdx.x / 8];
-  return (uint32_t)(w >> (8 * (threadIdx.x & 7))) & 0xffu;
+// A grid-stride walk over the chunks that hold outputs (the merged length is
+// known only on the device), one wavefront per chunk: lane l takes outputs
+// [32 l, 32 l + 32) (half a bitmask word), a wavefront scan of the lanes'
+// target counts places them in the wavefront's LDS row, which is then stored
+// contiguously; one round trip of loads per chunk, no wavefront waits on
+// another.  Then a walk over the segments: cu_targets[s] = the number of
+// targets before the segment's first output.
+AJ_DEV void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
 }
 
-// A grid-stride walk over the chunks that hold outputs (the merged length is
-// known only on the device), then over the segments: cu_targets[s] = the
-// number of targets before the segment's first output.
 __global__ __launch_bounds__(kBlock) void tgt_write_kernel(MergeArgs a) {
+  static_assert(kTgtChunk == 64 * 32, "32 outputs per lane of a wavefront");
+  __shared__ int32_t row[kBlock / 64][kTgtChunk];
   const int64_t n_out = fatal(a) ? 0 : a.counts[1];
   const int n_seg = fatal(a) ? 0 : (int)a.counts[0];
-  for (int64_t ch = blockIdx.x; ch * kTgtChunk < n_out; ch += gridDim.x) {
-    uint32_t bits = chunk_byte(a, ch);
+  const int lane = threadIdx.x & 63;
+  int32_t *wr = row[threadIdx.x >> 6];
+  const int64_t n_ch = (n_out + kTgtChunk - 1) / kTgtChunk;
+  const int64_t nw = (int64_t)gridDim.x * (kBlock / 64);
+  // the next chunk's bitmask half and offset are loaded while this one's
+  // targets are placed and stored
+  int64_t ch = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  uint64_t word = 0;
+  int32_t off = 0;
+  if (ch < n_ch) {
+    word = a.tbits[ch * (kTgtChunk / 64) + lane / 2];
+    off = a.chunk_off[ch];
+  }
+  for (; ch < n_ch; ch += nw) {
+    uint64_t next_word = 0;
+    int32_t next_off = 0;
+    if (ch + nw < n_ch) {
+      next_word = a.tbits[(ch + nw) * (kTgtChunk / 64) + lane / 2];
+      next_off = a.chunk_off[ch + nw];
+    }
+    uint32_t bits = (uint32_t)(word >> (32 * (lane & 1)));
     const int c = __popc(bits);
-    int tot;
-    const int incl = block_scan_incl<kBlock>(c, &tot);
-    int w = a.chunk_off[ch] + incl - c;
-    const int64_t o0 = ch * kTgtChunk + threadIdx.x * kTgtPer;
+    int x = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    const int total = __shfl(x, 63, 64);
+    const int32_t o0 = (int32_t)(ch * kTgtChunk + 32 * lane);
+    int k = x - c;
     while (bits) {
-      const int r = __ffs(bits) - 1;
-      a.targets[w++] = (int32_t)(o0 + r);
+      wr[k++] = o0 + __ffs(bits) - 1;
       bits &= bits - 1;
     }
+    wave_lds_sync();
+    for (int i = lane; i < total; i += 64) a.targets[off + i] = wr[i];
+    wave_lds_sync();
+    word = next_word;
+    off = next_off;
   }
   const int n_mask = (int)a.counts[2];
   for (int s = blockIdx.x * kBlock + threadIdx.x; s <= n_seg; s += gridDim.x * kBlock) {
