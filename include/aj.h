@@ -366,8 +366,10 @@ int aj_stack_lora_bwd(const aj_block_cfg *cfg, int32_t n_layers, const aj_block_
  *   r = exp(logprob[i] - old_logprob[p])
  *   loss += -min(r A, clip(r, 1-eps, 1+eps) A) * inv_n_mask,   A = adv[p]
  * The vocab projection is streamed: logits never reach memory in the forward
- * (unless cfg->keep_logits asks for them); the backward materialises one
- * vocab_chunk-wide slab of d logits at a time.
+ * (unless cfg->keep_logits asks for them); the backward forms d logits one
+ * vocab_chunk-wide slab per launch and keeps at most two slabs (bfloat16
+ * chunks of up to 16384 columns, paired so that the d hidden and d W_vocab
+ * products run once per pair; otherwise one).
  * d loss / d logprob = -A r inv_n_mask where the unclipped branch is active
  * ((A > 0 and r <= 1+eps) or (A < 0 and r >= 1-eps)), else 0.
  * Optional KL penalty against a reference policy (the low-variance KL the

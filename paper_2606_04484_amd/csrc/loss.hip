@@ -34,14 +34,34 @@ struct LossWs {
 
 constexpr int kFinBlocks = 256;
 
+// Vocab chunks per group of the backward's d hidden and d W products: the d
+// logits of a group's chunks sit side by side in one [n_tgt, group width]
+// buffer, so each product runs once per group.  bfloat16 chunks of up to
+// 16384 columns go in pairs (a 32768-wide buffer at most); wider ones, and
+// float32, one at a time.
+int chunk_group(const aj_loss_cfg &c) {
+  return c.dtype == AJ_BF16 && c.vocab_chunk <= 16384 ? 2 : 1;
+}
+
+// Widths of the groups: full groups, and the last one (narrower when the
+// vocab is not a multiple of the group's width).
+void group_widths(const aj_loss_cfg &c, int64_t *full, int64_t *last) {
+  const int64_t cw = c.vocab_chunk < c.vocab ? c.vocab_chunk : c.vocab;
+  const int64_t gw = cw * chunk_group(c);
+  *full = gw < c.vocab ? gw : c.vocab;
+  *last = c.vocab % *full == 0 ? *full : c.vocab % *full;
+}
+
 LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   const size_t es = c.dtype == AJ_BF16 ? 2 : 4;
   const int64_t cw = c.vocab_chunk < c.vocab ? c.vocab_chunk : c.vocab;
+  int64_t gfull, glast;
+  group_widths(c, &gfull, &glast);
   aj::Carver cv(base);
   LossWs w;
   w.z = cv.take<float>(c.dtype == AJ_BF16 ? 1 : (int64_t)n_tgt * cw);
   w.tile_ms = cv.take<float2>(c.dtype == AJ_BF16 ? (int64_t)n_tgt * ((c.vocab + 255) / 256) : 1);
-  w.dz = cv.take<char>((int64_t)n_tgt * cw * es);
+  w.dz = cv.take<char>((int64_t)n_tgt * gfull * es);
   w.run_m = cv.take<float>(n_tgt);
   w.run_s = cv.take<float>(n_tgt);
   w.zt = cv.take<float>(n_tgt);
@@ -51,11 +71,10 @@ LossWs carve_ws(const aj_loss_cfg &c, int n_tgt, void *base) {
   w.part = cv.take<float>(kFinBlocks * 8);
   w.dhn = cv.take<float>((int64_t)n_tgt * c.d_model);
   w.dg_part = cv.take<float>(aj::rmsnorm_bwd_part_floats(n_tgt, c.d_model));
-  // the dW_vocab GEMM runs on full chunks and on the last, narrower one:
+  // the dW_vocab GEMM runs on full groups and on the last, narrower one:
   // their split-K factors (tile counts) differ
-  const int64_t last = c.vocab % cw == 0 ? cw : c.vocab % cw;
-  const size_t sk = std::max(aj::gemm_split_floats((int)cw, c.d_model, n_tgt),
-                             aj::gemm_split_floats((int)last, c.d_model, n_tgt));
+  const size_t sk = std::max(aj::gemm_split_floats((int)gfull, c.d_model, n_tgt),
+                             aj::gemm_split_floats((int)glast, c.d_model, n_tgt));
   w.splitk = cv.take<float>(sk > 0 ? sk : 1);
   w.splitk_floats = sk > 0 ? sk : 1;
   w.bytes = cv.bytes();
@@ -441,7 +460,7 @@ template <bool kVec>
 __global__ __launch_bounds__(256) void lm_dz_kept_kernel(int n, int cw, int c0, int V,
                                                          const float *zkeep, const int32_t *tpos,
                                                          const int32_t *tok, const float *lse,
-                                                         const float *g, bf16_t *dz) {
+                                                         const float *g, bf16_t *dz, int ldz) {
   constexpr int E = kVec ? 8 : 1;
   const int per_row = cw / E;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -459,9 +478,9 @@ __global__ __launch_bounds__(256) void lm_dz_kept_kernel(int n, int cw, int c0, 
     for (int e = 0; e < 4; ++e)
       w[e] = f2bf2(dz_value(v[2 * e], tl, gm, cb + 2 * e == tt),
                    dz_value(v[2 * e + 1], tl, gm, cb + 2 * e + 1 == tt));
-    *reinterpret_cast<uint4 *>(dz + (int64_t)m * cw + cb) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4 *>(dz + (int64_t)m * ldz + cb) = make_uint4(w[0], w[1], w[2], w[3]);
   } else {
-    dz[(int64_t)m * cw + cb] = f2bf(dz_value(zr[0], tl, gm, cb == tt));
+    dz[(int64_t)m * ldz + cb] = f2bf(dz_value(zr[0], tl, gm, cb == tt));
   }
 }
 
@@ -472,7 +491,8 @@ __global__ __launch_bounds__(256) void lm_dz_kept_kernel(int n, int cw, int c0, 
 template <bool B_K>
 __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
     int n, int cw, int c0, int d, const bf16_t *hn, const bf16_t *wc, int ldw,
-    const int32_t *tpos, const int32_t *tok, const float *lse, const float *g, bf16_t *dz) {
+    const int32_t *tpos, const int32_t *tok, const float *lse, const float *g, bf16_t *dz,
+    int ldz) {
   // The body is device code only: this compiler's host pass rejects the
   // main-loop call of the B_K = true instance (its device pass accepts both).
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -493,7 +513,8 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   auto dz_of = [&](float a, int rl, int col) { return dz_value(a, tl[rl], tg[rl], col == ttok[rl]); };
-  if (m0 + Cfg::BM > n || n0 + Cfg::BN > cw || cw % 8 != 0 || ((uintptr_t)dz & 15) != 0) {
+  if (m0 + Cfg::BM > n || n0 + Cfg::BN > cw || cw % 8 != 0 || ldz % 8 != 0 ||
+      ((uintptr_t)dz & 15) != 0) {
     // edge tile: element by element
 #pragma unroll
     for (int i = 0; i < Cfg::TM; ++i)
@@ -506,7 +527,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
         for (int j = 0; j < Cfg::TN; ++j) {
           const int col = n0 + gemm_core::acc_col<Cfg>(wn, j, lane);
           if (col >= cw) continue;
-          dz[(int64_t)m * cw + col] = f2bf(dz_of(acc[i][j][r], rl, col));
+          dz[(int64_t)m * ldz + col] = f2bf(dz_of(acc[i][j][r], rl, col));
         }
       }
     return;
@@ -551,7 +572,7 @@ __global__ __launch_bounds__(Cfg::NT, 1) void lm_dz_fused_kernel(
       const int c = threadIdx.x + Cfg::NT * q;
       const int ls = c >> 5;
       const int m = m0 + (ls >> 5) * Cfg::WTM + 32 * i + (ls & 31);
-      *reinterpret_cast<uint4 *>(dz + (int64_t)m * cw + n0 + (c & 31) * 8) = v[q];
+      *reinterpret_cast<uint4 *>(dz + (int64_t)m * ldz + n0 + (c & 31) * 8) = v[q];
     }
     lds_barrier();
   }
@@ -648,50 +669,60 @@ int loss_bwd(const aj_loss_cfg &c, const aj_loss_in &in, const void *h, const vo
                                                     c.clip_eps, in.inv_n_mask, ref, in.kl_coef,
                                                     w.g);
   aj::fill_f32(w.dhn, (int64_t)n * d, 0.f, st);
-  for (int c0 = 0; c0 < c.vocab; c0 += c.vocab_chunk) {
-    const int cw = c.vocab - c0 < c.vocab_chunk ? c.vocab - c0 : c.vocab_chunk;
+  // groups of chunk_group(c) vocab chunks: the chunks' d logits (one launch
+  // each, as in the forward) side by side in w.dz, then one d hidden and one
+  // d W product over the whole group
+  const int G = chunk_group(c);
+  for (int g0 = 0; g0 < c.vocab; g0 += G * c.vocab_chunk) {
+    const int gw = c.vocab - g0 < G * c.vocab_chunk ? c.vocab - g0 : G * c.vocab_chunk;
     int r;
-    if (sizeof(T) == 2 && sv.z) {
-      const bool vec = c.vocab % 8 == 0 && c0 % 8 == 0 && cw % 8 == 0 &&
-                       ((uintptr_t)sv.z & 15) == 0 && ((uintptr_t)w.dz & 15) == 0;
-      const int64_t work = (int64_t)n * (vec ? cw / 8 : cw);
-      const unsigned blocks = (unsigned)((work + 255) / 256);
-      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);
-      if (vec)
-        lm_dz_kept_kernel<true><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos, in.tok,
-                                                        lse, w.g, (bf16_t *)w.dz);
-      else
-        lm_dz_kept_kernel<false><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos, in.tok,
-                                                         lse, w.g, (bf16_t *)w.dz);
-      aj::timing_end(st, tk);
-    } else if (sizeof(T) == 2) {
-      const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
-      const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
-      if (in.w_vocab_t)
-        lm_dz_fused_kernel<false><<<tiles, Cfg::NT, 0, st>>>(
-            n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)in.w_vocab_t + c0, c.vocab,
-            w.tpos, in.tok, lse, w.g, (bf16_t *)w.dz);
-      else
-        lm_dz_fused_kernel<true><<<tiles, Cfg::NT, 0, st>>>(
-            n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)w_vocab + (int64_t)c0 * d, d,
-            w.tpos, in.tok, lse, w.g, (bf16_t *)w.dz);
-      aj::timing_end(st, tk);
-    } else {
-      if ((r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true))) return r;
-      const int64_t tot = (int64_t)n * cw;
-      dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos, in.tok,
-                                                                  lse, w.g, (T *)w.dz);
+    for (int c0 = g0; c0 < g0 + gw; c0 += c.vocab_chunk) {
+      const int cw = g0 + gw - c0 < c.vocab_chunk ? g0 + gw - c0 : c.vocab_chunk;
+      if (sizeof(T) == 2 && sv.z) {
+        bf16_t *dz = (bf16_t *)w.dz + (c0 - g0);
+        const bool vec = c.vocab % 8 == 0 && c0 % 8 == 0 && cw % 8 == 0 && gw % 8 == 0 &&
+                         (c0 - g0) % 8 == 0 && ((uintptr_t)sv.z & 15) == 0 &&
+                         ((uintptr_t)w.dz & 15) == 0;
+        const int64_t work = (int64_t)n * (vec ? cw / 8 : cw);
+        const unsigned blocks = (unsigned)((work + 255) / 256);
+        const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);
+        if (vec)
+          lm_dz_kept_kernel<true><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos,
+                                                          in.tok, lse, w.g, dz, gw);
+        else
+          lm_dz_kept_kernel<false><<<blocks, 256, 0, st>>>(n, cw, c0, c.vocab, sv.z, w.tpos,
+                                                           in.tok, lse, w.g, dz, gw);
+        aj::timing_end(st, tk);
+      } else if (sizeof(T) == 2) {
+        bf16_t *dz = (bf16_t *)w.dz + (c0 - g0);
+        const int tiles = ((n + Cfg::BM - 1) / Cfg::BM) * ((cw + Cfg::BN - 1) / Cfg::BN);
+        const int tk = aj::timing_begin(st, AJ_KC_LM_DZ, 0.0);   // recomputes the forward product
+        if (in.w_vocab_t)
+          lm_dz_fused_kernel<false><<<tiles, Cfg::NT, 0, st>>>(
+              n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)in.w_vocab_t + c0, c.vocab,
+              w.tpos, in.tok, lse, w.g, dz, gw);
+        else
+          lm_dz_fused_kernel<true><<<tiles, Cfg::NT, 0, st>>>(
+              n, cw, c0, d, (const bf16_t *)sv.hn, (const bf16_t *)w_vocab + (int64_t)c0 * d, d,
+              w.tpos, in.tok, lse, w.g, dz, gw);
+        aj::timing_end(st, tk);
+      } else {   // float32: one chunk per group
+        if ((r = chunk_logits<T>(c, n, sv.hn, w_vocab, c0, cw, w.z, st, true))) return r;
+        const int64_t tot = (int64_t)n * cw;
+        dz_kernel<T><<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(w.z, n, cw, c0, w.tpos,
+                                                                    in.tok, lse, w.g, (T *)w.dz);
+      }
     }
-    aj::Gemm g;   // dhn += dz W_chunk
-    g.M = n; g.N = d; g.K = cw; g.A = w.dz; g.lda = cw;
-    g.B = (const T *)w_vocab + (int64_t)c0 * d; g.ldb = d; g.b_kmajor = false;
+    aj::Gemm g;   // dhn += dz W_group
+    g.M = n; g.N = d; g.K = gw; g.A = w.dz; g.lda = gw;
+    g.B = (const T *)w_vocab + (int64_t)g0 * d; g.ldb = d; g.b_kmajor = false;
     g.C = w.dhn; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
     if ((r = aj::gemm<T>(g, st))) return r;
     if (!dwv) continue;   // frozen LM head
-    g = aj::Gemm();   // dW_chunk += dz^T hn
-    g.M = cw; g.N = d; g.K = n; g.A = w.dz; g.lda = cw; g.a_kmajor = false;
+    g = aj::Gemm();   // dW_group += dz^T hn
+    g.M = gw; g.N = d; g.K = n; g.A = w.dz; g.lda = gw; g.a_kmajor = false;
     g.B = sv.hn; g.ldb = d; g.b_kmajor = false;
-    g.C = dwv + (int64_t)c0 * d; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
+    g.C = dwv + (int64_t)g0 * d; g.ldc = d; g.out = aj::OUT_ACCUM_F32;
     g.split_k = aj::gemm_split_k(g.M, g.N, g.K); g.partial = w.splitk;
     g.partial_cap = w.splitk_floats;
     if ((r = aj::gemm<T>(g, st))) return r;

@@ -3,7 +3,8 @@
 // LM-head shapes of every workload and reduction lengths up to the
 // workspace's capacity, the split-K factor gemm() is given never needs more
 // partial floats than the carved workspace holds (block: the four
-// weight-gradient products; LM head: the full and the last vocab chunk).
+// weight-gradient products; LM head: the full and the last group of vocab
+// chunks, the width its weight-gradient product runs on).
 // Built with the library sources included (host compilation only; nothing
 // is launched).  Exit status 1 on a violation.
 #include <cstdio>
@@ -35,7 +36,8 @@ int main() {
     const size_t blk = carve_bwd(b, c.cap, nullptr).splitk_floats;
     const size_t los = carve_ws(l, c.cap, nullptr).splitk_floats;
     const int q = (c.Hq + 2 * c.Hkv) * c.hd, hq = c.Hq * c.hd;
-    const int last = c.V % c.chunk == 0 ? c.chunk : c.V % c.chunk;
+    int64_t gfull = 0, glast = 0;
+    group_widths(l, &gfull, &glast);
     for (int K = 1; K <= c.cap; K += (K < 20000 ? 7 : 61)) {
       const int shp[4][2] = {{c.d, c.F}, {2 * c.F, c.d}, {c.d, hq}, {q, c.d}};
       for (auto &s : shp) {
@@ -44,7 +46,7 @@ int main() {
           if (++bad < 10) printf("block %s %dx%d K=%d S=%d\n", c.name, s[0], s[1], K, S);
         }
       }
-      for (int cw : {std::min(c.chunk, c.V), last}) {
+      for (int cw : {(int)gfull, (int)glast}) {
         const int S = gemm_split_k(cw, c.d, K);
         if (S > 1 && (size_t)S * cw * c.d > los) {
           if (++bad < 10) printf("loss %s %dx%d K=%d S=%d\n", c.name, cw, c.d, K, S);
