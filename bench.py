@@ -74,9 +74,9 @@ def log(msg):
 TRAFFIC = {
     ("gemm4_tn", "block1.5b-64x8"): {"bytes_per_launch": 4840.4e6, "launches": 27,
                                      "sources": "c74b4918568820ba"},
-    ("gemm4_tn", "long32b-8x60"): {"bytes_per_launch": 10932.2e6, "launches": 92,
+    ("gemm4_tn", "long32b-8x60"): {"bytes_per_launch": 17968.3e6, "launches": 56,
                                    "sources": "c74b4918568820ba"},
-    ("gemm4_nn", "long32b-8x60"): {"bytes_per_launch": 15834.5e6, "launches": 104,
+    ("gemm4_nn", "long32b-8x60"): {"bytes_per_launch": 23618.3e6, "launches": 68,
                                    "sources": "c74b4918568820ba"},
 }
 
